@@ -1,0 +1,169 @@
+/*
+ * polyglot.h -- C ABI of the MI355X (gfx950) library for the minibatch SGD
+ * step of the Polyglot window-ranking language model.
+ *
+ * Method.  Kulkarni, Al-Rfou, Perozzi, Skiena, "Exploring the power of GPU's
+ * for training Polyglot language models" (arXiv:1404.1521).  The paper trains
+ * the Polyglot model, a SENNA-like ranking language model (§1 Introduction),
+ * with minibatch SGD (batch size discussion, §4.6), and finds that the
+ * embedding-gradient update -- the "advanced indexing" increment that adds
+ * row k of Y to row I[k] of W for every k (§4.2, Table 1:
+ * GpuAdvancedIncSubtensor1) -- dominates training time; §4.3 replaces it
+ * with a parallel kernel.  The paper does not write the model out; this
+ * library implements the SENNA-style window ranker:
+ *
+ *   x     = concat(E[w_0] .. E[w_{win-1}])          K = win*d values
+ *   x~    = x with block c = win/2 replaced by E[corrupt]
+ *   s(x)  = w2 . tanh(W1 x + b1) + b2
+ *   loss  = (1/B) sum_b max(0, 1 - s(x_b) + s(x~_b))
+ *
+ * and one SGD step P <- P - lr * dloss/dP over E, W1, b1, w2, b2, all
+ * gradients taken at the pre-step parameters.  The hinge derivative at a
+ * margin of exactly 0 is taken as 0.  A corrupt id equal to the true centre
+ * is used as drawn (its gradient cancels).
+ *
+ * Conventions for every entry point.
+ *   - All tensor arguments are DEVICE pointers (hipMalloc / torch CUDA
+ *     tensors on the device the context was created on), C-contiguous,
+ *     row-major, float32 or int32, owned by the caller.  The library never
+ *     frees or retains them after the call returns.
+ *   - Work is enqueued asynchronously on the context's HIP stream; the
+ *     caller must synchronise that stream before reading results on the
+ *     host or touching the buffers from another stream.
+ *   - Return value: POLYGLOT_OK (0) or a negative POLYGLOT_E* code.  Errors
+ *     that the host can detect (bad sizes, NULL pointers, non-finite lr,
+ *     batch above the configured maximum) are returned before anything is
+ *     enqueued.  Ids outside [0, V) are detected on the device: the step
+ *     then modifies no parameter, writes NaN to its loss slot, and raises a
+ *     sticky flag that polyglot_status() reports as POLYGLOT_EID.
+ *   - A context is not thread-safe and must be used from one host thread
+ *     and one stream at a time.
+ *
+ * Layouts (int32 ids, float32 values):
+ *   E[V][d]  W1[H][win*d]  b1[H]  w2[H]  b2[1]
+ *   windows[B][win] (centre at win/2)  corrupt[B]
+ */
+#ifndef POLYGLOT_H
+#define POLYGLOT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define POLYGLOT_OK 0
+#define POLYGLOT_EINVAL -1 /* bad dimension, even window, non-finite lr, bad mode */
+#define POLYGLOT_ENULL -2  /* a required pointer is NULL */
+#define POLYGLOT_EBATCH -3 /* B or N <= 0, or above the context's maximum */
+#define POLYGLOT_EHIP -4   /* HIP runtime error; text in polyglot_last_error() */
+#define POLYGLOT_EID -5    /* an id was outside [0, V) (reported by polyglot_status) */
+#define POLYGLOT_ESTATE -6 /* call not valid in the context's current state */
+
+/* How the embedding-gradient rows are added into the table (§4.3). */
+#define POLYGLOT_SCATTER_SORTED 0 /* stable radix sort by row id, segmented sum: deterministic */
+#define POLYGLOT_SCATTER_ATOMIC 1 /* one float atomic add per (entry, column): order-dependent rounding */
+
+typedef struct polyglot_ctx polyglot_ctx;
+
+typedef struct {
+  int32_t V;            /* vocabulary rows of E, >= 1 */
+  int32_t d;            /* embedding width, multiple of 16, 16..256 */
+  int32_t win;          /* window length, odd, 1..31 */
+  int32_t H;            /* hidden units, 1..64 */
+  int32_t max_batch;    /* largest B accepted by train_step / score / gather */
+  int32_t scatter_mode; /* POLYGLOT_SCATTER_SORTED or POLYGLOT_SCATTER_ATOMIC */
+  int32_t max_scatter;  /* largest N accepted by polyglot_scatter_add (0: no workspace) */
+  int32_t max_rows;     /* largest table row count for polyglot_scatter_add */
+} polyglot_config;
+
+/* Creates a context on the current HIP device.  `stream` is a hipStream_t
+ * (NULL = the legacy default stream).  All workspace is allocated here, once,
+ * sized for cfg->max_batch and cfg->max_scatter; no call below allocates.
+ * On success *out receives the context; on error *out is left NULL. */
+int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out);
+
+/* Waits for the context's stream, frees its workspace and the context. */
+int polyglot_destroy(polyglot_ctx* ctx);
+
+/* Replaces the stream the context enqueues on (hipStream_t, NULL = default). */
+int polyglot_set_stream(polyglot_ctx* ctx, void* stream);
+
+/* One SGD step of the window-ranking model (model above; the embedding
+ * update is the row scatter-add of §4.2/§4.3), in place on E, W1, b1, w2,
+ * b2.  windows[B][win] and corrupt[B] are int32 ids in [0, V).  lr is the
+ * SGD learning rate.  loss_dev, if not NULL, is a device float that
+ * receives the mean hinge loss at the pre-step parameters (NaN if an id was
+ * out of range).  1 <= B <= max_batch. */
+int polyglot_train_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
+                        const int32_t* windows, const int32_t* corrupt, int32_t B, float lr,
+                        float* loss_dev);
+
+/* S consecutive SGD steps, step s using windows + s*B*win and corrupt + s*B,
+ * exactly as S calls of polyglot_train_step.  losses_dev[S] (device, may be
+ * NULL) receives each step's loss.  The launches of the S steps are recorded
+ * once into a HIP graph that the context caches (keyed on every argument)
+ * and replays, which removes per-kernel host launch cost. */
+int polyglot_train_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2,
+                         float* b2, const int32_t* windows, const int32_t* corrupt, int32_t S,
+                         int32_t B, float lr, float* losses_dev);
+
+/* Scores s(x) = w2 . tanh(W1 x + b1) + b2 of the B windows into
+ * scores_dev[B] (NaN for a window holding an out-of-range id). */
+int polyglot_score(polyglot_ctx* ctx, const float* E, const float* W1, const float* b1,
+                   const float* w2, const float* b2, const int32_t* windows, int32_t B,
+                   float* scores_dev);
+
+/* The window gather on its own: X[B][win*d] = concat_j E[windows[b][j]] and
+ * Xc[B][d] = E[corrupt[b]] (bit-exact copies; a row with an out-of-range id
+ * is written as NaN and raises the sticky flag). */
+int polyglot_gather(polyglot_ctx* ctx, const float* E, const int32_t* windows,
+                    const int32_t* corrupt, int32_t B, float* X, float* Xc);
+
+/* The advanced-indexing increment of §4.2/§4.3: for every k in [0, N),
+ * table[idx[k]] += alpha * Y[k], where repeated indices accumulate.
+ * table[rows][d], idx[N] int32 in [0, rows), Y[N][d].  mode selects the
+ * sorted-segment or the atomic algorithm.  N <= max_scatter,
+ * rows <= max_rows, d a multiple of 4 up to 256.  Out-of-range indices
+ * leave the table untouched and raise the sticky flag. */
+int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t d,
+                         const int32_t* idx, const float* Y, int32_t N, float alpha,
+                         int32_t mode);
+
+/* Host copy of the sorted distinct row ids touched by the last sorted-mode
+ * train step (ids of the windows and the corrupt ids).  Synchronises the
+ * stream.  Writes at most cap ids to ids_host and the total to *count.
+ * POLYGLOT_ESTATE if no sorted-mode step has run. */
+int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int32_t* count);
+
+/* Kernel ids reported by polyglot_kernel_times. */
+#define POLYGLOT_K_FWDBWD 0   /* fused gather + forward + hinge + backward (+ sort start) */
+#define POLYGLOT_K_SORT 1     /* radix passes of the entry sort (large batches) */
+#define POLYGLOT_K_UPDATE 2   /* embedding segmented update + dense SGD */
+#define POLYGLOT_K_GATHER 3   /* polyglot_gather */
+#define POLYGLOT_K_SCATTER 4  /* polyglot_scatter_add (all of its launches) */
+#define POLYGLOT_K_SCORE 5    /* polyglot_score */
+#define POLYGLOT_NKERNELS 6
+
+/* Per-kernel timing for measurement.  With enable != 0 every later launch of
+ * this context (outside graph capture) is bracketed by two HIP events
+ * recorded on the context stream; polyglot_kernel_times() synchronises the
+ * stream, writes the summed elapsed milliseconds and the launch count of
+ * each kernel id into ms[POLYGLOT_NKERNELS] and launches[POLYGLOT_NKERNELS]
+ * (host arrays), and resets the sums.  Timing costs two event records per
+ * launch on the host. */
+int polyglot_set_timing(polyglot_ctx* ctx, int enable);
+int polyglot_kernel_times(polyglot_ctx* ctx, double* ms, int32_t* launches);
+
+/* Synchronises the stream and returns the sticky device error
+ * (POLYGLOT_OK or POLYGLOT_EID), then clears it. */
+int polyglot_status(polyglot_ctx* ctx);
+
+/* Text of the last error recorded on this context ("" if none). */
+const char* polyglot_last_error(const polyglot_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* POLYGLOT_H */

@@ -1,0 +1,595 @@
+// Host side of the C ABI declared in include/polyglot.h: argument checks,
+// workspace, launch sequencing, graph replay of multi-step calls, per-kernel
+// event timing.
+#include "polyglot.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "launch.h"
+
+using namespace pg;
+
+namespace {
+
+struct GraphKey {
+  const void* p[7];
+  const void* losses;
+  int S, B;
+  float lr;
+  hipStream_t stream;
+  bool operator==(const GraphKey& o) const {
+    return std::memcmp(p, o.p, sizeof(p)) == 0 && losses == o.losses && S == o.S && B == o.B &&
+           std::memcmp(&lr, &o.lr, sizeof(float)) == 0 && stream == o.stream;
+  }
+};
+
+}  // namespace
+
+struct polyglot_ctx {
+  polyglot_config cfg{};
+  hipStream_t stream = nullptr;
+  int device = 0;
+  int Hp = 0, NT = 0, K = 0, c = 0, cpw = 0;
+  int max_entries = 0, max_tiles = 0, max_groups = 0, max_parts = 0, max_chunks = 0;
+  int seg_stride = 0, part_stride = 0;
+  Workspace ws{};
+  std::vector<void*> allocs;
+  std::string err;
+  bool have_sorted = false;
+  int last_N = 0, last_passes = 0;
+  hipGraphExec_t gexec = nullptr;
+  GraphKey gkey{};
+  bool gvalid = false;
+  // per-kernel timing
+  bool timing = false;
+  bool capturing = false;
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> ev_marks;
+};
+
+namespace {
+
+int fail(polyglot_ctx* ctx, int code, const std::string& msg) {
+  if (ctx) ctx->err = msg;
+  return code;
+}
+
+int hip_fail(polyglot_ctx* ctx, hipError_t e, const char* what) {
+  return fail(ctx, POLYGLOT_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int bits_for(uint32_t n) {  // smallest b >= 1 with n <= 2^b
+  int b = 1;
+  while (b < 31 && (1u << b) < n) ++b;
+  return b;
+}
+
+SortPlan make_plan(int key_range, int N) {
+  SortPlan pl{};
+  const int kb = bits_for((uint32_t)key_range);
+  pl.passes = (kb + kMaxDigitBits - 1) / kMaxDigitBits;
+  const int base = kb / pl.passes, rem = kb % pl.passes;
+  int sh = 0;
+  for (int p = 0; p < pl.passes; ++p) {
+    pl.bits[p] = base + (p < rem ? 1 : 0);
+    pl.shift[p] = sh;
+    sh += pl.bits[p];
+  }
+  pl.ntiles = ceil_div(N, kSortTile);
+  pl.val_bits = bits_for((uint32_t)std::max(N, 2));
+  pl.small = (N <= kSmallSortN && kb + pl.val_bits <= 32) ? 1 : 0;
+  return pl;
+}
+
+SortBufs sort_bufs(polyglot_ctx* ctx) {
+  SortBufs sb{};
+  sb.keys[0] = ctx->ws.keys[0];
+  sb.keys[1] = ctx->ws.keys[1];
+  sb.vals[0] = ctx->ws.vals[0];
+  sb.vals[1] = ctx->ws.vals[1];
+  sb.totals = ctx->ws.totals;
+  sb.counts = ctx->ws.counts;
+  sb.gcounts = ctx->ws.gcounts;
+  sb.max_tiles = ctx->max_tiles;
+  sb.max_groups = ctx->max_groups;
+  sb.flag = ctx->ws.flag;
+  return sb;
+}
+
+// Counters a multi-tile sort leaves nonzero (pass-0 per-tile counts are
+// overwritten by every sort and need no clearing).
+ZeroRanges sort_zero_ranges(polyglot_ctx* ctx, const SortPlan& plan) {
+  ZeroRanges z{};
+  if (plan.small) return z;
+  z.p[0] = ctx->ws.totals;
+  z.n[0] = (size_t)kMaxPasses * kMaxBins;
+  z.p[1] = ctx->ws.counts + (size_t)kMaxBins * ctx->max_tiles;
+  z.n[1] = (size_t)(plan.passes - 1) * kMaxBins * ctx->max_tiles;
+  z.p[2] = ctx->ws.gcounts;
+  z.n[2] = (size_t)plan.passes * kMaxBins * ctx->max_groups;
+  return z;
+}
+
+template <class T>
+hipError_t alloc(polyglot_ctx* ctx, T** p, size_t count) {
+  void* q = nullptr;
+  hipError_t e = hipMalloc(&q, std::max<size_t>(count, 1) * sizeof(T));
+  if (e == hipSuccess) {
+    ctx->allocs.push_back(q);
+    *p = static_cast<T*>(q);
+  }
+  return e;
+}
+
+void free_all(polyglot_ctx* ctx) {
+  for (auto& m : ctx->ev_marks) {
+    ctx->ev_pool.push_back(m.second.first);
+    ctx->ev_pool.push_back(m.second.second);
+  }
+  ctx->ev_marks.clear();
+  for (hipEvent_t ev : ctx->ev_pool) hipEventDestroy(ev);
+  ctx->ev_pool.clear();
+  if (ctx->gexec) hipGraphExecDestroy(ctx->gexec);
+  ctx->gexec = nullptr;
+  for (void* q : ctx->allocs) hipFree(q);
+  ctx->allocs.clear();
+}
+
+hipEvent_t take_event(polyglot_ctx* ctx) {
+  if (!ctx->ev_pool.empty()) {
+    hipEvent_t ev = ctx->ev_pool.back();
+    ctx->ev_pool.pop_back();
+    return ev;
+  }
+  hipEvent_t ev = nullptr;
+  if (hipEventCreate(&ev) != hipSuccess) return nullptr;
+  return ev;
+}
+
+// Brackets launches with events when timing is on (never inside capture).
+struct KernelTimer {
+  polyglot_ctx* ctx;
+  int id;
+  hipEvent_t a = nullptr, b = nullptr;
+  KernelTimer(polyglot_ctx* c, int kid) : ctx(c), id(kid) {
+    if (ctx->timing && !ctx->capturing) {
+      a = take_event(ctx);
+      b = take_event(ctx);
+      if (a && b) hipEventRecord(a, ctx->stream);
+    }
+  }
+  ~KernelTimer() {
+    if (a && b) {
+      hipEventRecord(b, ctx->stream);
+      ctx->ev_marks.push_back({id, {a, b}});
+    } else {
+      if (a) ctx->ev_pool.push_back(a);
+      if (b) ctx->ev_pool.push_back(b);
+    }
+  }
+};
+
+size_t fwdbwd_lds_bytes(int NT) {
+  return (size_t)kTileRows * (kMaxWin + 1) * 4 + (size_t)kWavesPerBlock * 3 * NT * kWave * 16;
+}
+
+// Enqueues one training step.  Arguments are already validated.
+int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
+                 const int32_t* windows, const int32_t* corrupt, int B, float lr,
+                 float* loss_dev) {
+  const polyglot_config& cf = ctx->cfg;
+  const int N = B * (cf.win + 1);
+  const bool sorted = cf.scatter_mode == POLYGLOT_SCATTER_SORTED;
+  const SortPlan plan = make_plan(cf.V, N);
+  const SortBufs sb = sort_bufs(ctx);
+
+  FwdArgs fa{};
+  fa.E = E;
+  fa.W1 = W1;
+  fa.b1 = b1;
+  fa.w2 = w2;
+  fa.b2 = b2;
+  fa.windows = windows;
+  fa.corrupt = corrupt;
+  fa.dzz = ctx->ws.dzz;
+  fa.part = ctx->ws.part;
+  fa.w1snap = ctx->ws.w1snap;
+  fa.long_count = ctx->ws.long_count;
+  fa.flag = ctx->ws.flag;
+  fa.V = cf.V;
+  fa.d = cf.d;
+  fa.win = cf.win;
+  fa.H = cf.H;
+  fa.Hp = ctx->Hp;
+  fa.K = ctx->K;
+  fa.c = ctx->c;
+  fa.B = B;
+  fa.N = N;
+  fa.ntiles = ceil_div(B, kTileRows);
+  fa.tiles_per_wg = ceil_div(fa.ntiles, ctx->max_parts);
+  const int n_fb = ceil_div(fa.ntiles, fa.tiles_per_wg);
+  fa.part_stride = ctx->part_stride;
+  fa.invB = 1.0f / (float)B;
+  fa.n_sort = sorted ? (plan.small ? 1 : plan.ntiles) : 0;
+  fa.sort_small = plan.small;
+  fa.plan = plan;
+  fa.sb = sb;
+  size_t lds = fwdbwd_lds_bytes(ctx->NT);
+  if (sorted)
+    lds = std::max(lds, (size_t)(plan.small ? kSmallSortLdsWords : kUp0LdsWords) * 4);
+  hipError_t e;
+  {
+    KernelTimer kt(ctx, POLYGLOT_K_FWDBWD);
+    e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, fa.n_sort + n_fb, lds, ctx->stream);
+  }
+  if (e != hipSuccess) return hip_fail(ctx, e, "fwd/bwd launch");
+
+  if (sorted && !plan.small) {
+    const StepKeys kf{windows, corrupt, cf.win, cf.V};
+    KernelTimer kt(ctx, POLYGLOT_K_SORT);
+    for (int p = 0; p < plan.passes && e == hipSuccess; ++p)
+      e = launch_sort_down_step(kf, N, plan, sb, p, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "sort launch");
+  }
+
+  UpdArgs ua{};
+  ua.E = E;
+  ua.W1 = W1;
+  ua.b1 = b1;
+  ua.w2 = w2;
+  ua.b2 = b2;
+  ua.loss_out = loss_dev ? loss_dev : ctx->ws.scratch_loss;
+  ua.dzz = ctx->ws.dzz;
+  ua.part = ctx->ws.part;
+  ua.w1snap = ctx->ws.w1snap;
+  ua.sk = ctx->ws.keys[plan.passes & 1];
+  ua.sv = ctx->ws.vals[plan.passes & 1];
+  ua.windows = windows;
+  ua.corrupt = corrupt;
+  ua.seg_part = ctx->ws.seg_part;
+  ua.long_list = ctx->ws.long_list;
+  ua.long_count = ctx->ws.long_count;
+  ua.flag = ctx->ws.flag;
+  if (sorted) ua.zero = sort_zero_ranges(ctx, plan);
+  ua.V = cf.V;
+  ua.d = cf.d;
+  ua.win = cf.win;
+  ua.H = cf.H;
+  ua.Hp = ctx->Hp;
+  ua.K = ctx->K;
+  ua.c = ctx->c;
+  ua.B = B;
+  ua.N = N;
+  ua.mode = sorted ? 0 : 1;
+  const int nchunks = ceil_div(N, kSegChunk);
+  ua.n_e = std::min(ceil_div(nchunks, kWavesPerBlock), 1024);
+  ua.n_d = ceil_div(ctx->Hp * ctx->K + 2 * ctx->Hp + 2, kBlock);
+  ua.n_parts = n_fb;
+  ua.part_stride = ctx->part_stride;
+  ua.seg_stride = ctx->seg_stride;
+  ua.lr = lr;
+  ua.invB = 1.0f / (float)B;
+  {
+    KernelTimer kt(ctx, POLYGLOT_K_UPDATE);
+    e = launch_step_update(ua, ua.n_e + ua.n_d, step_update_lds_bytes(ctx->Hp, ctx->K, cf.d),
+                           ctx->stream);
+    if (e == hipSuccess && sorted)
+      e = launch_step_segfix(ua, (size_t)ctx->Hp * ctx->K * 4, ctx->stream);
+  }
+  if (e != hipSuccess) return hip_fail(ctx, e, "update launch");
+
+  ctx->have_sorted = sorted;
+  ctx->last_N = N;
+  ctx->last_passes = plan.passes;
+  return POLYGLOT_OK;
+}
+
+int check_step_args(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
+                    const int32_t* windows, const int32_t* corrupt, int B, float lr) {
+  if (!E || !W1 || !b1 || !w2 || !b2 || !windows || !corrupt)
+    return fail(ctx, POLYGLOT_ENULL, "train_step: NULL tensor pointer");
+  if (B <= 0 || B > ctx->cfg.max_batch)
+    return fail(ctx, POLYGLOT_EBATCH, "train_step: B must be in [1, max_batch]");
+  if (!std::isfinite(lr)) return fail(ctx, POLYGLOT_EINVAL, "train_step: lr is not finite");
+  if (!aligned16(E) || !aligned16(W1))
+    return fail(ctx, POLYGLOT_EINVAL, "train_step: E and W1 must be 16-byte aligned");
+  return POLYGLOT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) {
+  if (!cfg || !out) return POLYGLOT_ENULL;
+  *out = nullptr;
+  const polyglot_config& c = *cfg;
+  if (c.V < 1 || c.d < 16 || c.d > kMaxD || c.d % 16 != 0 || c.win < 1 || c.win > kMaxWin ||
+      c.win % 2 == 0 || c.H < 1 || c.H > kMaxHp || c.win * c.d > kMaxK)
+    return POLYGLOT_EINVAL;
+  if (c.scatter_mode != POLYGLOT_SCATTER_SORTED && c.scatter_mode != POLYGLOT_SCATTER_ATOMIC)
+    return POLYGLOT_EINVAL;
+  if (c.max_batch < 1 || (int64_t)c.max_batch * (c.win + 1) > (1 << 26)) return POLYGLOT_EBATCH;
+  if (c.max_scatter < 0 || c.max_scatter > (1 << 26) || c.max_rows < 0 ||
+      (c.max_scatter > 0 && c.max_rows < 1))
+    return POLYGLOT_EINVAL;
+
+  polyglot_ctx* ctx = new (std::nothrow) polyglot_ctx();
+  if (!ctx) return POLYGLOT_EHIP;
+  ctx->cfg = c;
+  ctx->stream = static_cast<hipStream_t>(stream);
+  ctx->K = c.win * c.d;
+  ctx->c = c.win / 2;
+  ctx->NT = c.H <= 16 ? 1 : (c.H <= 32 ? 2 : 4);
+  ctx->Hp = 16 * ctx->NT;
+  ctx->cpw = ceil_div(ctx->K / 16, kWavesPerBlock);
+  ctx->max_entries = std::max({c.max_batch * (c.win + 1), c.max_scatter, 1});
+  ctx->max_tiles = ceil_div(ctx->max_entries, kSortTile);
+  ctx->max_groups = ceil_div(ctx->max_tiles, kCountGroup);
+  ctx->max_parts = std::min(ceil_div(c.max_batch, kTileRows), 512);
+  ctx->max_chunks = ceil_div(ctx->max_entries, kSegChunk);
+  ctx->seg_stride = std::max(c.win * ctx->Hp, c.max_scatter > 0 ? kMaxD : 0);
+  ctx->part_stride = ctx->Hp * ctx->K + 2 * ctx->Hp + 2;
+
+  hipError_t e = hipGetDevice(&ctx->device);
+  Workspace& ws = ctx->ws;
+  const size_t me = (size_t)ctx->max_entries;
+  const size_t ncount = (size_t)kMaxPasses * kMaxBins * ctx->max_tiles;
+  const size_t ngcount = (size_t)kMaxPasses * kMaxBins * ctx->max_groups;
+  if (e == hipSuccess) e = alloc(ctx, &ws.keys[0], me);
+  if (e == hipSuccess) e = alloc(ctx, &ws.keys[1], me);
+  if (e == hipSuccess) e = alloc(ctx, &ws.vals[0], me);
+  if (e == hipSuccess) e = alloc(ctx, &ws.vals[1], me);
+  if (e == hipSuccess) e = alloc(ctx, &ws.totals, (size_t)kMaxPasses * kMaxBins);
+  if (e == hipSuccess) e = alloc(ctx, &ws.counts, ncount);
+  if (e == hipSuccess) e = alloc(ctx, &ws.gcounts, ngcount);
+  if (e == hipSuccess) e = alloc(ctx, &ws.dzz, (size_t)c.max_batch * 3 * ctx->Hp);
+  if (e == hipSuccess) e = alloc(ctx, &ws.part, (size_t)ctx->max_parts * ctx->part_stride);
+  if (e == hipSuccess) e = alloc(ctx, &ws.w1snap, (size_t)ctx->Hp * ctx->K);
+  if (e == hipSuccess) e = alloc(ctx, &ws.seg_part, (size_t)ctx->max_chunks * 2 * ctx->seg_stride);
+  if (e == hipSuccess) e = alloc(ctx, &ws.long_list, (size_t)ctx->max_chunks);
+  if (e == hipSuccess) e = alloc(ctx, &ws.long_count, 1);
+  if (e == hipSuccess) e = alloc(ctx, &ws.flag, 1);
+  if (e == hipSuccess) e = alloc(ctx, &ws.scratch_loss, 1);
+  if (e == hipSuccess) e = hipMemset(ws.totals, 0, sizeof(uint32_t) * kMaxPasses * kMaxBins);
+  if (e == hipSuccess) e = hipMemset(ws.counts, 0, sizeof(uint32_t) * ncount);
+  if (e == hipSuccess) e = hipMemset(ws.gcounts, 0, sizeof(uint32_t) * ngcount);
+  if (e == hipSuccess) e = hipMemset(ws.long_count, 0, sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMemset(ws.flag, 0, sizeof(uint32_t));
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    free_all(ctx);
+    delete ctx;
+    return POLYGLOT_EHIP;
+  }
+  *out = ctx;
+  return POLYGLOT_OK;
+}
+
+int polyglot_destroy(polyglot_ctx* ctx) {
+  if (!ctx) return POLYGLOT_ENULL;
+  hipStreamSynchronize(ctx->stream);
+  free_all(ctx);
+  delete ctx;
+  return POLYGLOT_OK;
+}
+
+int polyglot_set_stream(polyglot_ctx* ctx, void* stream) {
+  if (!ctx) return POLYGLOT_ENULL;
+  ctx->stream = static_cast<hipStream_t>(stream);
+  return POLYGLOT_OK;
+}
+
+int polyglot_train_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
+                        const int32_t* windows, const int32_t* corrupt, int32_t B, float lr,
+                        float* loss_dev) {
+  if (!ctx) return POLYGLOT_ENULL;
+  const int rc = check_step_args(ctx, E, W1, b1, w2, b2, windows, corrupt, B, lr);
+  if (rc) return rc;
+  return enqueue_step(ctx, E, W1, b1, w2, b2, windows, corrupt, B, lr, loss_dev);
+}
+
+int polyglot_train_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2,
+                         float* b2, const int32_t* windows, const int32_t* corrupt, int32_t S,
+                         int32_t B, float lr, float* losses_dev) {
+  if (!ctx) return POLYGLOT_ENULL;
+  if (S <= 0) return fail(ctx, POLYGLOT_EBATCH, "train_steps: S must be >= 1");
+  const int rc = check_step_args(ctx, E, W1, b1, w2, b2, windows, corrupt, B, lr);
+  if (rc) return rc;
+  const size_t wstride = (size_t)B * ctx->cfg.win;
+  auto enqueue_all = [&]() -> int {
+    for (int s = 0; s < S; ++s) {
+      const int r = enqueue_step(ctx, E, W1, b1, w2, b2, windows + s * wstride,
+                                 corrupt + (size_t)s * B, B, lr,
+                                 losses_dev ? losses_dev + s : nullptr);
+      if (r) return r;
+    }
+    return POLYGLOT_OK;
+  };
+  if (ctx->stream == nullptr) return enqueue_all();  // the legacy stream cannot be captured
+
+  GraphKey key{{E, W1, b1, w2, b2, windows, corrupt}, losses_dev, S, B, lr, ctx->stream};
+  if (!(ctx->gvalid && ctx->gkey == key)) {
+    if (ctx->gexec) hipGraphExecDestroy(ctx->gexec);
+    ctx->gexec = nullptr;
+    ctx->gvalid = false;
+    hipError_t e = hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) return hip_fail(ctx, e, "train_steps: begin capture");
+    ctx->capturing = true;
+    const int r = enqueue_all();
+    ctx->capturing = false;
+    hipGraph_t graph = nullptr;
+    e = hipStreamEndCapture(ctx->stream, &graph);
+    if (r) {
+      if (graph) hipGraphDestroy(graph);
+      return r;
+    }
+    if (e != hipSuccess) return hip_fail(ctx, e, "train_steps: end capture");
+    e = hipGraphInstantiate(&ctx->gexec, graph, nullptr, nullptr, 0);
+    hipGraphDestroy(graph);
+    if (e != hipSuccess) return hip_fail(ctx, e, "train_steps: instantiate");
+    ctx->gkey = key;
+    ctx->gvalid = true;
+  }
+  hipError_t e = hipGraphLaunch(ctx->gexec, ctx->stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "train_steps: graph launch");
+  const int N = B * (ctx->cfg.win + 1);
+  ctx->have_sorted = ctx->cfg.scatter_mode == POLYGLOT_SCATTER_SORTED;
+  ctx->last_N = N;
+  ctx->last_passes = make_plan(ctx->cfg.V, N).passes;
+  return POLYGLOT_OK;
+}
+
+int polyglot_score(polyglot_ctx* ctx, const float* E, const float* W1, const float* b1,
+                   const float* w2, const float* b2, const int32_t* windows, int32_t B,
+                   float* scores_dev) {
+  if (!ctx) return POLYGLOT_ENULL;
+  if (!E || !W1 || !b1 || !w2 || !b2 || !windows || !scores_dev)
+    return fail(ctx, POLYGLOT_ENULL, "score: NULL pointer");
+  if (B <= 0 || B > ctx->cfg.max_batch) return fail(ctx, POLYGLOT_EBATCH, "score: bad B");
+  if (!aligned16(E) || !aligned16(W1))
+    return fail(ctx, POLYGLOT_EINVAL, "score: E and W1 must be 16-byte aligned");
+  ScoreArgs a{E, W1, b1, w2, b2, windows, scores_dev, ctx->ws.flag, ctx->cfg.V, ctx->cfg.d,
+              ctx->cfg.win, ctx->cfg.H, ctx->K, B};
+  hipError_t e;
+  {
+    KernelTimer kt(ctx, POLYGLOT_K_SCORE);
+    e = launch_score(a, ctx->NT, ctx->cpw, ctx->stream);
+  }
+  return e == hipSuccess ? POLYGLOT_OK : hip_fail(ctx, e, "score launch");
+}
+
+int polyglot_gather(polyglot_ctx* ctx, const float* E, const int32_t* windows,
+                    const int32_t* corrupt, int32_t B, float* X, float* Xc) {
+  if (!ctx) return POLYGLOT_ENULL;
+  if (!E || !windows || !corrupt || !X || !Xc) return fail(ctx, POLYGLOT_ENULL, "gather: NULL");
+  if (B <= 0 || B > ctx->cfg.max_batch) return fail(ctx, POLYGLOT_EBATCH, "gather: bad B");
+  if (!aligned16(E) || !aligned16(X) || !aligned16(Xc))
+    return fail(ctx, POLYGLOT_EINVAL, "gather: E, X, Xc must be 16-byte aligned");
+  GatherArgs a{E, windows, corrupt, X, Xc, ctx->ws.flag, ctx->cfg.V, ctx->cfg.d, ctx->cfg.win, B};
+  hipError_t e;
+  {
+    KernelTimer kt(ctx, POLYGLOT_K_GATHER);
+    e = launch_gather(a, ctx->stream);
+  }
+  return e == hipSuccess ? POLYGLOT_OK : hip_fail(ctx, e, "gather launch");
+}
+
+int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t d,
+                         const int32_t* idx, const float* Y, int32_t N, float alpha,
+                         int32_t mode) {
+  if (!ctx) return POLYGLOT_ENULL;
+  if (!table || !idx || !Y) return fail(ctx, POLYGLOT_ENULL, "scatter_add: NULL pointer");
+  if (N <= 0 || N > ctx->cfg.max_scatter)
+    return fail(ctx, POLYGLOT_EBATCH, "scatter_add: N must be in [1, max_scatter]");
+  if (rows <= 0 || rows > ctx->cfg.max_rows || d <= 0 || d > kMaxD || d % 4 != 0)
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_add: bad rows or d");
+  if (!aligned16(table))
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_add: table must be 16-byte aligned");
+  if (!std::isfinite(alpha)) return fail(ctx, POLYGLOT_EINVAL, "scatter_add: alpha not finite");
+  if (mode != POLYGLOT_SCATTER_SORTED && mode != POLYGLOT_SCATTER_ATOMIC)
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_add: bad mode");
+  ScatArgs a{};
+  a.table = table;
+  a.idx = idx;
+  a.Y = Y;
+  a.seg_part = ctx->ws.seg_part;
+  a.long_list = ctx->ws.long_list;
+  a.long_count = ctx->ws.long_count;
+  a.flag = ctx->ws.flag;
+  a.rows = rows;
+  a.d = d;
+  a.N = N;
+  a.seg_stride = ctx->seg_stride;
+  a.alpha = alpha;
+  hipError_t e;
+  KernelTimer kt(ctx, POLYGLOT_K_SCATTER);
+  if (mode == POLYGLOT_SCATTER_SORTED) {
+    const SortPlan plan = make_plan(rows, N);
+    a.sk = ctx->ws.keys[plan.passes & 1];
+    a.sv = ctx->ws.vals[plan.passes & 1];
+    a.zero = sort_zero_ranges(ctx, plan);
+    a.n_e = std::min(ceil_div(ceil_div(N, kSegChunk), kWavesPerBlock), 2048);
+    a.n_z = plan.small ? 0 : 16;
+    e = launch_scatter_sorted(a, plan, sort_bufs(ctx), ctx->stream);
+  } else {
+    e = launch_scatter_atomic(a, ctx->stream);
+  }
+  ctx->have_sorted = false;  // the sort buffers now hold this call's order
+  return e == hipSuccess ? POLYGLOT_OK : hip_fail(ctx, e, "scatter_add launch");
+}
+
+int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int32_t* count) {
+  if (!ctx || !count) return POLYGLOT_ENULL;
+  if (!ctx->have_sorted) return fail(ctx, POLYGLOT_ESTATE, "touched_rows: no sorted step yet");
+  hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "touched_rows: sync");
+  std::vector<int32_t> keys(ctx->last_N);
+  e = hipMemcpy(keys.data(), ctx->ws.keys[ctx->last_passes & 1], sizeof(int32_t) * ctx->last_N,
+                hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(ctx, e, "touched_rows: copy");
+  int32_t n = 0;
+  for (int i = 0; i < ctx->last_N; ++i) {
+    if (i > 0 && keys[i] == keys[i - 1]) continue;
+    if (ids_host && n < cap) ids_host[n] = keys[i];
+    ++n;
+  }
+  *count = n;
+  return POLYGLOT_OK;
+}
+
+int polyglot_status(polyglot_ctx* ctx) {
+  if (!ctx) return POLYGLOT_ENULL;
+  hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "status: sync");
+  uint32_t f = 0;
+  e = hipMemcpy(&f, ctx->ws.flag, sizeof(f), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(ctx, e, "status: read flag");
+  if (f) {
+    e = hipMemset(ctx->ws.flag, 0, sizeof(uint32_t));
+    if (e != hipSuccess) return hip_fail(ctx, e, "status: clear flag");
+    if (f & kFlagBadId) return fail(ctx, POLYGLOT_EID, "an id was outside its table");
+    return fail(ctx, POLYGLOT_EHIP, "internal: sort position outside the entry range");
+  }
+  return POLYGLOT_OK;
+}
+
+int polyglot_set_timing(polyglot_ctx* ctx, int enable) {
+  if (!ctx) return POLYGLOT_ENULL;
+  ctx->timing = enable != 0;
+  return POLYGLOT_OK;
+}
+
+int polyglot_kernel_times(polyglot_ctx* ctx, double* ms, int32_t* launches) {
+  if (!ctx || !ms || !launches) return POLYGLOT_ENULL;
+  hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "kernel_times: sync");
+  for (int k = 0; k < POLYGLOT_NKERNELS; ++k) {
+    ms[k] = 0.0;
+    launches[k] = 0;
+  }
+  for (auto& m : ctx->ev_marks) {
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, m.second.first, m.second.second) == hipSuccess) {
+      ms[m.first] += t;
+      launches[m.first] += 1;
+    }
+    ctx->ev_pool.push_back(m.second.first);
+    ctx->ev_pool.push_back(m.second.second);
+  }
+  ctx->ev_marks.clear();
+  return POLYGLOT_OK;
+}
+
+const char* polyglot_last_error(const polyglot_ctx* ctx) { return ctx ? ctx->err.c_str() : ""; }
+
+}  // extern "C"

@@ -1,0 +1,356 @@
+// Stable LSD radix sort of (row id, entry index) pairs.
+//
+// The embedding update of §4.2/§4.3 adds many rows into few distinct table
+// rows (Zipf-distributed word ids repeat heavily).  Sorting the entries by row
+// id turns that into a segmented sum with one writer per table row, so the
+// update is deterministic and free of atomics.  Entries with equal row ids
+// keep their entry order (stable LSD), which fixes the summation order.
+//
+// Two variants:
+//  * small: one workgroup sorts up to kSmallSortN pairs packed as
+//    (key << val_bits | entry) in LDS, all passes in one launch;
+//  * multi-tile: tiles of kSortTile keys.  up0 counts pass-0 digits per tile
+//    and the digit totals of every pass; down(p) ranks each tile stably with
+//    wave ballots, adds the counts of all earlier tiles, scatters, and counts
+//    the next pass's digits of the output tiles.  Counts are kept per tile
+//    and per group of kCountGroup tiles, so a tile's prefix needs a few dozen
+//    independent loads, not a chain over every earlier tile.
+#pragma once
+#include "common.h"
+
+namespace pg {
+
+// Key sources -------------------------------------------------------------
+
+struct StepKeys {  // entries of a training step (windows + corrupt ids)
+  const int32_t* windows;
+  const int32_t* corrupt;
+  int win, range;   // range = V
+  __device__ int32_t load(int e) const {
+    const int b = e / (win + 1);
+    const int j = e - b * (win + 1);
+    return (j < win) ? windows[(size_t)b * win + j] : corrupt[b];
+  }
+};
+
+struct IdxKeys {  // entries of the standalone scatter-add
+  const int32_t* idx;
+  int range;        // table rows
+  __device__ int32_t load(int e) const { return idx[e]; }
+};
+
+// Loads U keys per thread with all loads in flight before any check; ids
+// outside [0, range) become 0 and raise the sticky flag once.
+template <int U, class KeyFn>
+__device__ __forceinline__ void load_keys(const KeyFn& kf, int N, int e0, int stride,
+                                          uint32_t* key, uint32_t* flag) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int e = e0 + u * stride;
+    key[u] = e < N ? (uint32_t)kf.load(e) : 0u;
+  }
+  bool bad = false;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const bool b = key[u] >= (uint32_t)kf.range;
+    bad |= b;
+    key[u] = b ? 0u : key[u];
+  }
+  if (bad) atomicOr(flag, kFlagBadId);
+}
+
+// Exclusive scan over `n` (<= 2*kBlock) values in LDS `v`, in place, by one
+// workgroup of kBlock threads.
+__device__ inline void block_exclusive_scan(uint32_t* v, int n, uint32_t* wave_sums) {
+  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  const uint32_t a = (2 * t < n) ? v[2 * t] : 0u;
+  const uint32_t b = (2 * t + 1 < n) ? v[2 * t + 1] : 0u;
+  const uint32_t s = a + b;
+  uint32_t inc = s;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t y = __shfl_up(inc, o);
+    if (lane >= o) inc += y;
+  }
+  if (lane == kWave - 1) wave_sums[w] = inc;
+  __syncthreads();
+  uint32_t base = 0;
+  for (int i = 0; i < w; ++i) base += wave_sums[i];
+  const uint32_t ex = base + inc - s;
+  if (2 * t < n) v[2 * t] = ex;
+  if (2 * t + 1 < n) v[2 * t + 1] = ex + a;
+  __syncthreads();
+}
+
+// ------------------------------------------------------------------ small sort
+// LDS needed (uint32 words): 2*kSmallSortN (ping-pong) + kSmallSortN/2
+// (16-bit local ranks) + kWavesPerBlock*kMaxBins + 16.
+constexpr int kSmallSortLdsWords = 2 * kSmallSortN + kSmallSortN / 2 +
+                                   kWavesPerBlock * kMaxBins + 16;
+
+template <class KeyFn>
+__device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t* out_keys,
+                           int32_t* out_vals, uint32_t* flag, uint32_t* lds) {
+  uint32_t* bufA = lds;
+  uint32_t* bufB = bufA + kSmallSortN;
+  uint16_t* rank = reinterpret_cast<uint16_t*>(bufB + kSmallSortN);
+  uint32_t* hist = bufB + kSmallSortN + kSmallSortN / 2;  // [waves][kMaxBins]
+  uint32_t* misc = hist + kWavesPerBlock * kMaxBins;       // wave sums
+  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  const int vb = plan.val_bits;
+  const uint32_t vmask = (vb >= 32) ? 0xffffffffu : ((1u << vb) - 1u);
+
+  // keys, loaded in batches so that their global loads overlap
+  constexpr int U = 8;
+  for (int e0 = 0; e0 < N; e0 += kBlock * U) {
+    uint32_t kk[U];
+    load_keys<U>(kf, N, e0 + t, kBlock, kk, flag);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int e = e0 + u * kBlock + t;
+      if (e < N) bufA[e] = (kk[u] << vb) | (uint32_t)e;
+    }
+  }
+  __syncthreads();
+
+  const int per = ceil_div(N, kWavesPerBlock);
+  const int beg = min(N, w * per), end = min(N, beg + per);
+  uint32_t* src = bufA;
+  uint32_t* dst = bufB;
+  for (int p = 0; p < plan.passes; ++p) {
+    const int bits = plan.bits[p], shift = plan.shift[p] + vb, bins = 1 << bits;
+    for (int i = lane; i < bins; i += kWave) hist[w * kMaxBins + i] = 0;
+    __syncthreads();
+    // stable ranks within this wave's contiguous range
+    for (int base = beg; base < end; base += kWave) {
+      const int i = base + lane;
+      const bool act = i < end;
+      const uint32_t word = act ? src[i] : 0u;
+      const uint32_t dg = (word >> shift) & (uint32_t)(bins - 1);
+      const uint64_t peers = match_digit(dg, bits, __ballot(act));
+      if (act) {
+        const uint32_t below = __popcll(peers & lanemask_lt());
+        const uint32_t cnt = hist[w * kMaxBins + dg];
+        rank[i] = (uint16_t)(cnt + below);
+        if (below == 0) hist[w * kMaxBins + dg] = cnt + (uint32_t)__popcll(peers);
+      }
+    }
+    __syncthreads();
+    // per-digit totals -> digit starts; per-wave offsets
+    for (int dg = t; dg < bins; dg += kBlock) {
+      uint32_t s = 0;
+      for (int q = 0; q < kWavesPerBlock; ++q) {
+        const uint32_t c = hist[q * kMaxBins + dg];
+        hist[q * kMaxBins + dg] = s;  // exclusive over waves
+        s += c;
+      }
+      dst[dg] = s;  // dst is free until the scatter below: digit totals
+    }
+    __syncthreads();
+    block_exclusive_scan(dst, bins, misc);
+    for (int dg = t; dg < bins; dg += kBlock) {
+      const uint32_t start = dst[dg];
+      for (int q = 0; q < kWavesPerBlock; ++q) hist[q * kMaxBins + dg] += start;
+    }
+    __syncthreads();
+    for (int base = beg; base < end; base += kWave) {
+      const int i = base + lane;
+      if (i < end) {
+        const uint32_t word = src[i];
+        const uint32_t dg = (word >> shift) & (uint32_t)(bins - 1);
+        const uint32_t pos = hist[w * kMaxBins + dg] + rank[i];
+        if (pos < (uint32_t)N) dst[pos] = word;
+      }
+    }
+    __syncthreads();
+    uint32_t* tmp = src;
+    src = dst;
+    dst = tmp;
+  }
+  for (int e = t; e < N; e += kBlock) {
+    const uint32_t word = src[e];
+    out_keys[e] = (int32_t)(word >> vb);
+    out_vals[e] = (int32_t)(word & vmask);
+  }
+}
+
+// ------------------------------------------------------------ multi-tile sort
+constexpr int kCountGroup = 16;  // tiles per coarse count group
+
+struct SortBufs {
+  int32_t* keys[2];
+  int32_t* vals[2];
+  uint32_t* totals;    // [kMaxPasses][kMaxBins]
+  uint32_t* counts;    // [kMaxPasses][kMaxBins][max_tiles]
+  uint32_t* gcounts;   // [kMaxPasses][kMaxBins][max_groups]
+  int max_tiles;
+  int max_groups;
+  uint32_t* flag;      // sticky error bits
+};
+
+__device__ inline uint32_t* counts_at(const SortBufs& sb, int p, int dg) {
+  return sb.counts + ((size_t)p * kMaxBins + dg) * sb.max_tiles;
+}
+__device__ inline uint32_t* gcounts_at(const SortBufs& sb, int p, int dg) {
+  return sb.gcounts + ((size_t)p * kMaxBins + dg) * sb.max_groups;
+}
+
+constexpr int kUp0LdsWords = kMaxPasses * kMaxBins;
+
+// Pass-0 digit counts of one tile, and digit totals of every pass.
+template <class KeyFn>
+__device__ void sort_up0_tile(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
+                              int tile, uint32_t* lds) {
+  const int t = threadIdx.x;
+  for (int i = t; i < plan.passes * kMaxBins; i += kBlock) lds[i] = 0;
+  const int base = tile * kSortTile;
+  uint32_t key[kSortIPT];
+  load_keys<kSortIPT>(kf, N, base + t, kBlock, key, sb.flag);
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < kSortIPT; ++q) {
+    if (base + q * kBlock + t < N) {
+      for (int p = 0; p < plan.passes; ++p) {
+        const uint32_t dg = (key[q] >> plan.shift[p]) & ((1u << plan.bits[p]) - 1u);
+        atomicAdd(&lds[p * kMaxBins + dg], 1u);
+      }
+    }
+  }
+  __syncthreads();
+  const int bins0 = 1 << plan.bits[0];
+  for (int dg = t; dg < bins0; dg += kBlock) {
+    const uint32_t c = lds[dg];
+    counts_at(sb, 0, dg)[tile] = c;
+    if (c) atomicAdd(&gcounts_at(sb, 0, dg)[tile / kCountGroup], c);
+  }
+  for (int p = 0; p < plan.passes; ++p) {
+    const int bins = 1 << plan.bits[p];
+    for (int dg = t; dg < bins; dg += kBlock) {
+      const uint32_t c = lds[p * kMaxBins + dg];
+      if (c) atomicAdd(&sb.totals[p * kMaxBins + dg], c);
+    }
+  }
+}
+
+// LDS words for a down pass: per-wave histograms + digit scratch + scan scratch.
+constexpr int kDownLdsWords = kWavesPerBlock * kMaxBins + kMaxBins + 16;
+
+// Keys of `digit` in tiles [0, tile) of pass p: coarse groups, then the tiles
+// of the last partial group; every load is independent.
+__device__ __forceinline__ uint32_t tiles_before(const SortBufs& sb, int p, int dg, int tile) {
+  const uint32_t* gp = gcounts_at(sb, p, dg);
+  const uint32_t* cp = counts_at(sb, p, dg);
+  const int ng = tile / kCountGroup;
+  uint32_t acc[4] = {0u, 0u, 0u, 0u};
+  for (int g0 = 0; g0 < ng; g0 += 4) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (g0 + u < ng) acc[u] += gp[g0 + u];
+  }
+  const int t0 = ng * kCountGroup;
+  uint32_t v[kCountGroup];
+#pragma unroll
+  for (int u = 0; u < kCountGroup; ++u) v[u] = (t0 + u < tile) ? cp[t0 + u] : 0u;
+  uint32_t s = acc[0] + acc[1] + acc[2] + acc[3];
+#pragma unroll
+  for (int u = 0; u < kCountGroup; ++u) s += v[u];
+  return s;
+}
+
+// Pass p over one tile: stable rank, global offset, scatter, next-pass counts.
+template <class KeyFn>
+__device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
+                               int p, int tile, uint32_t* lds) {
+  uint32_t* hist = lds;                                  // [waves][kMaxBins]
+  uint32_t* dscr = hist + kWavesPerBlock * kMaxBins;     // [kMaxBins]
+  uint32_t* misc = dscr + kMaxBins;
+  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  const int bits = plan.bits[p], shift = plan.shift[p], bins = 1 << bits;
+  const int32_t* sk = sb.keys[p & 1];
+  const int32_t* sv = sb.vals[p & 1];
+  int32_t* dk = sb.keys[(p + 1) & 1];
+  int32_t* dv = sb.vals[(p + 1) & 1];
+
+  constexpr int R = kSortTile / kBlock;  // rounds per wave (blocked: a wave owns R*64 keys)
+  int32_t key[R], val[R];
+  uint32_t loc[R];
+  const int wbase = tile * kSortTile + w * (R * kWave);
+  if (p == 0) {
+    uint32_t kk[R];
+    load_keys<R>(kf, N, wbase + lane, kWave, kk, sb.flag);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      key[r] = (int32_t)kk[r];
+      val[r] = wbase + r * kWave + lane;
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int i = wbase + r * kWave + lane;
+      key[r] = i < N ? sk[i] : 0;
+      val[r] = i < N ? sv[i] : 0;
+    }
+  }
+  for (int i = lane; i < bins; i += kWave) hist[w * kMaxBins + i] = 0;
+  for (int dg = t; dg < bins; dg += kBlock) dscr[dg] = sb.totals[p * kMaxBins + dg];
+  uint32_t before[kMaxBins / kBlock];
+#pragma unroll
+  for (int q = 0; q < kMaxBins / kBlock; ++q) {
+    const int dg = t + q * kBlock;
+    before[q] = dg < bins ? tiles_before(sb, p, dg, tile) : 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = wbase + r * kWave + lane;
+    const bool act = i < N;
+    const uint32_t dg = ((uint32_t)key[r] >> shift) & (uint32_t)(bins - 1);
+    const uint64_t peers = match_digit(dg, bits, __ballot(act));
+    uint32_t l = 0;
+    if (act) {
+      const uint32_t below = __popcll(peers & lanemask_lt());
+      const uint32_t cnt = hist[w * kMaxBins + dg];
+      l = cnt + below;
+      if (below == 0) hist[w * kMaxBins + dg] = cnt + (uint32_t)__popcll(peers);
+    }
+    loc[r] = l;
+  }
+  __syncthreads();
+  block_exclusive_scan(dscr, bins, misc);  // digit starts of the pass
+#pragma unroll
+  for (int q = 0; q < kMaxBins / kBlock; ++q) {
+    const int dg = t + q * kBlock;
+    if (dg < bins) {
+      uint32_t s = dscr[dg] + before[q];
+      for (int v = 0; v < kWavesPerBlock; ++v) {
+        const uint32_t c = hist[v * kMaxBins + dg];
+        hist[v * kMaxBins + dg] = s;
+        s += c;
+      }
+    }
+  }
+  __syncthreads();
+  const bool more = p + 1 < plan.passes;
+  const int nbits = more ? plan.bits[p + 1] : 0, nshift = more ? plan.shift[p + 1] : 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = wbase + r * kWave + lane;
+    if (i < N) {
+      const uint32_t dg = ((uint32_t)key[r] >> shift) & (uint32_t)(bins - 1);
+      const uint32_t pos = hist[w * kMaxBins + dg] + loc[r];
+      if (pos >= (uint32_t)N) {  // inconsistent counters: never write out of bounds
+        atomicOr(sb.flag, kFlagInternal);
+        continue;
+      }
+      dk[pos] = key[r];
+      dv[pos] = val[r];
+      if (more) {
+        const uint32_t nd = ((uint32_t)key[r] >> nshift) & ((1u << nbits) - 1u);
+        const uint32_t ot = pos / kSortTile;
+        atomicAdd(&counts_at(sb, p + 1, nd)[ot], 1u);
+        atomicAdd(&gcounts_at(sb, p + 1, nd)[ot / kCountGroup], 1u);
+      }
+    }
+  }
+}
+
+}  // namespace pg

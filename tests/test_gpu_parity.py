@@ -1,0 +1,372 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Bars (see the design notes for their derivation):
+  * gather output, the set of touched rows: bit-exact;
+  * per-step mean loss: relative 1e-5;
+  * parameters after K steps: |gpu - ref| <= 1e-4 |ref| + 1e-4 rms(ref) per tensor;
+  * parameter deltas P_K - P_0 (the updates are ~1e-4 of the values, so the
+    bar above alone would barely see them):
+    |dgpu - dref| <= 2e-3 |dref| + 2e-3 rms(dref) per tensor;
+  * scatter-add: within the worst-case float32 summation bound
+    n * 2^-24 * (|t0| + sum |alpha Y|) per element, n = entries of the row + 1.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from workloads import PRESETS
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def pg():
+    import paper_1404_1521_amd as m
+    return m
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def params_dev(p):
+    return {k: dev(v) for k, v in p.items()}
+
+
+def rms(a):
+    a = np.asarray(a, np.float64)
+    return float(np.sqrt(np.mean(a * a))) if a.size else 0.0
+
+
+def assert_params_close(got, ref, init, stores, entries=None):
+    """stores[k]: per-element count of float32 stores over the run (steps for
+    the dense tensors, steps touching the row for E); entries: per-row count
+    of scatter entries, given for the atomic variant, which rounds once per
+    entry instead of once per row and step."""
+    for k in ("E", "W1", "b1", "w2", "b2"):
+        g = got[k].astype(np.float64)
+        r = ref[k].astype(np.float64)
+        err = np.abs(g - r)
+        bar = 1e-4 * np.abs(r) + 1e-4 * rms(r)
+        assert np.all(err <= bar), (k, float(np.max(err - bar)))
+        ulp = np.spacing(np.abs(ref[k]).astype(np.float32)).astype(np.float64)
+        n = np.broadcast_to(np.asarray(stores[k], np.float64), r.shape[:1])
+        n = n.reshape(n.shape + (1,) * (r.ndim - 1))
+        floor = 2.0 * np.sqrt(n) * ulp
+        if entries is not None and k == "E":
+            floor = floor + 0.5 * entries.reshape(-1, 1) * ulp
+        dg = g - init[k]
+        dr = r - init[k]
+        derr = np.abs(dg - dr)
+        dbar = 2e-3 * np.abs(dr) + 2e-3 * rms(dr) + floor
+        assert np.all(derr <= dbar), (k, "delta", float(np.max(derr - dbar)), rms(dr))
+
+
+def run_both(w, steps, B, mode=0, lr=None, seed=None, p0=None, batches=None, check=True):
+    """Runs `steps` SGD steps on the GPU and in the float32-storage oracle and
+    compares losses and parameters."""
+    m = pg()
+    lr = w.lr if lr is None else lr
+    p = workloads.init_params(w, seed) if p0 is None else {k: v.copy() for k, v in p0.items()}
+    init = {k: v.astype(np.float64) for k, v in p.items()}
+    pd = params_dev(p)
+    ctx = m.Context(w.V, w.d, w.win, w.H, max_batch=B, scatter_mode=mode)
+    losses = torch.zeros(steps, dtype=torch.float32, device="cuda")
+    ref_losses = []
+    row_steps = np.zeros(w.V)
+    row_entries = np.zeros(w.V)
+    for s in range(steps):
+        win, cor = batches[s] if batches is not None else workloads.batch(w, s, B)
+        ctx.train_step(pd, dev(win), dev(cor), lr, losses[s:s + 1])
+        ref_losses.append(oracle.train_step(p, win, cor, lr))
+        ids = np.concatenate([win.reshape(-1), cor])
+        row_steps[np.unique(ids)] += 1
+        row_entries += np.bincount(ids, minlength=w.V)
+    assert ctx.status() == m.OK
+    got = {k: host(v) for k, v in pd.items()}
+    gl, rl = host(losses), np.array(ref_losses)
+    if check:
+        np.testing.assert_allclose(gl, rl, rtol=1e-5, atol=1e-6)
+        stores = {"E": row_steps, "W1": steps, "b1": steps, "w2": steps, "b2": steps}
+        assert_params_close(got, p, init, stores, row_entries if mode == 1 else None)
+    return got, p, init, gl, rl, ctx
+
+
+# --------------------------------------------------------------------- gather
+
+@pytest.mark.parametrize("name,B", [("tiny", 37), ("poly256", 1000), ("poly256", 1)])
+def test_gather_bit_exact(name, B):
+    w = PRESETS[name]
+    p = workloads.init_params(w)
+    win, cor = workloads.batch(w, 5, B)
+    ctx = pg().Context(w.V, w.d, w.win, w.H, max_batch=B)
+    X, Xc = ctx.gather(dev(p["E"]), dev(win), dev(cor))
+    Xr, Xcr = oracle.gather(p["E"], win, cor)
+    assert np.array_equal(host(X), Xr)
+    assert np.array_equal(host(Xc), Xcr)
+
+
+# ---------------------------------------------------------------- scatter-add
+
+def scatter_bound(t0, idx, Y, alpha):
+    cnt = np.bincount(idx, minlength=t0.shape[0]).astype(np.float64)[:, None] + 1.0
+    mag = np.abs(t0.astype(np.float64))
+    np.add.at(mag, idx, np.abs(alpha * Y.astype(np.float64)))
+    return cnt * 2.0 ** -24 * mag + 1e-30
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("rows,d,N,s", [
+    (50, 8, 400, 1.2), (3, 4, 1, 1.0), (1000, 64, 5000, 1.2), (1000, 64, 8192, 1.2),
+    (100_000, 64, 20_000, 1.2), (100_000, 64, 4096 * 3 + 17, 1.0), (7, 256, 3000, 1.5),
+    (300_000, 16, 9000, 1.1),
+])
+def test_scatter_add_matches_oracle(mode, rows, d, N, s):
+    rng = np.random.default_rng(rows + N)
+    t0 = rng.normal(0, 0.01, (rows, d)).astype(np.float32)
+    idx = workloads.zipf_ids(rng, rows, s, N)
+    Y = rng.normal(0, 1e-3, (N, d)).astype(np.float32)
+    alpha = 0.75
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    td = dev(t0)
+    ctx.scatter_add(td, dev(idx), dev(Y), alpha, mode)
+    assert ctx.status() == pg().OK
+    got = host(td)
+    ref = t0.copy()
+    oracle.scatter_add(ref, idx, Y, alpha)
+    err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    assert np.all(err <= scatter_bound(t0, idx, Y, alpha))
+    untouched = np.setdiff1d(np.arange(rows), idx)
+    assert np.array_equal(got[untouched], t0[untouched])
+
+
+def test_scatter_add_sorted_is_deterministic():
+    table, idx, Y = workloads.scatter_inputs(N=100_000)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=idx.size, max_rows=table.shape[0])
+    outs = []
+    for _ in range(2):
+        td = dev(table)
+        ctx.scatter_add(td, dev(idx), dev(Y), 1.0, pg().SCATTER_SORTED)
+        outs.append(host(td))
+    assert np.array_equal(outs[0], outs[1])
+
+
+def test_scatter_add_bad_index_leaves_table_untouched():
+    m = pg()
+    rng = np.random.default_rng(0)
+    t0 = rng.normal(0, 1, (10, 4)).astype(np.float32)
+    idx = np.array([1, 2, 10, 3], np.int32)
+    Y = np.ones((4, 4), np.float32)
+    ctx = m.Context(1000, 16, 5, 8, max_batch=1, max_scatter=4, max_rows=10)
+    for mode in (0, 1):
+        td = dev(t0)
+        ctx.scatter_add(td, dev(idx), dev(Y), 1.0, mode)
+        assert ctx.status() == m.EID
+        assert np.array_equal(host(td), t0)
+        assert ctx.status() == m.OK
+
+
+# --------------------------------------------------------------- train steps
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_tiny_100_steps(mode):
+    w = PRESETS["tiny"]
+    run_both(w, 100, w.B, mode)
+
+
+def test_tiny_amplified_updates():
+    # larger parameters and step so that updates dominate; some hinges go inactive
+    w = dataclasses.replace(PRESETS["tiny"], init_std=0.5)
+    _, _, _, gl, _, _ = run_both(w, 30, 32, 0, lr=0.1, seed=7)
+    assert np.min(gl) < 1.0  # the run is away from the all-active start
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_poly256_1000_steps(mode):
+    w = PRESETS["poly256"]
+    run_both(w, 1000 if mode == 0 else 100, w.B, mode)
+
+
+@pytest.mark.parametrize("B,steps", [(1024, 20), (1365, 5), (1366, 3), (4096, 10), (16384, 3)])
+def test_sweep_batches(B, steps):
+    w = PRESETS["sweep_1024"].with_batch(B)
+    run_both(w, steps, B, 0)
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_full_size_batch_65536_one_step(mode):
+    w = PRESETS["sweep_65536"]
+    run_both(w, 1, w.B, mode)
+
+
+@pytest.mark.parametrize("B", [1, 17, 33])
+def test_ragged_and_single_window_batches(B):
+    w = PRESETS["tiny"]
+    run_both(w, 5, B, 0, lr=0.5)
+
+
+@pytest.mark.parametrize("name,B", [("tiny", 32), ("poly256", 256), ("poly256", 4096)])
+def test_touched_rows_bit_exact(name, B):
+    w = PRESETS[name]
+    p = params_dev(workloads.init_params(w))
+    win, cor = workloads.batch(w, 3, B)
+    ctx = pg().Context(w.V, w.d, w.win, w.H, max_batch=B)
+    ctx.train_step(p, dev(win), dev(cor), w.lr)
+    assert np.array_equal(np.array(ctx.touched_rows(), np.int32),
+                          oracle.touched_rows(w.V, win, cor))
+
+
+def test_untouched_rows_bit_identical_and_b2_constant():
+    w = PRESETS["poly256"]
+    p = workloads.init_params(w)
+    pd = params_dev(p)
+    win, cor = workloads.batch(w, 0, 4096)
+    ctx = pg().Context(w.V, w.d, w.win, w.H, max_batch=4096)
+    ctx.train_step(pd, dev(win), dev(cor), 0.5)
+    E = host(pd["E"])
+    touched = np.zeros(w.V, bool)
+    touched[win.reshape(-1)] = True
+    touched[cor] = True
+    assert np.array_equal(E[~touched], p["E"][~touched])
+    assert np.array_equal(host(pd["b2"]), p["b2"])
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_corrupt_equal_centre_changes_nothing(mode):
+    w = PRESETS["tiny"]
+    p = workloads.init_params(w, seed=3)
+    pd = params_dev(p)
+    win, _ = workloads.batch(w, 0, 40)
+    cor = win[:, w.win // 2].copy()
+    ctx = pg().Context(w.V, w.d, w.win, w.H, max_batch=40, scatter_mode=mode)
+    loss = torch.zeros(1, device="cuda")
+    ctx.train_step(pd, dev(win), dev(cor), 0.3, loss)
+    assert host(loss)[0] == 1.0
+    for k in p:
+        assert np.array_equal(host(pd[k]), p[k]), k
+
+
+def test_margin_met_and_lr_zero_change_nothing():
+    w = PRESETS["tiny"]
+    p = workloads.init_params(w, seed=4)
+    win, cor = workloads.batch(w, 0, 32)
+    ctx = pg().Context(w.V, w.d, w.win, w.H, max_batch=32)
+    pd = params_dev(p)
+    ctx.train_step(pd, dev(win), dev(cor), 0.0)
+    for k in p:
+        assert np.array_equal(host(pd[k]), p[k]), k
+    # saturate tanh so that every margin is exactly 0 (closed form): nothing moves
+    q = {k: v.copy() for k, v in p.items()}
+    q["E"][:] = 0.0
+    q["E"][:, 0] = 40.0
+    q["E"][cor, 0] = -40.0
+    q["W1"][:] = 0.0
+    q["W1"][:, (w.win // 2) * w.d] = 1.0
+    q["b1"][:] = 0.0
+    q["w2"][:] = 0.5 / w.H
+    q["b2"][:] = 0.0
+    wins = win.copy()
+    wins[:, w.win // 2] = np.setdiff1d(np.arange(w.V), cor)[: 32]
+    qd = params_dev(q)
+    loss = torch.zeros(1, device="cuda")
+    ctx.train_step(qd, dev(wins), dev(cor), 0.1, loss)
+    assert oracle.train_step({k: v.copy() for k, v in q.items()}, wins, cor, 0.1) == 0.0
+    assert host(loss)[0] == 0.0
+    for k in q:
+        assert np.array_equal(host(qd[k]), q[k]), k
+
+
+def test_sorted_mode_is_deterministic():
+    w = PRESETS["poly256"]
+    outs = []
+    for _ in range(2):
+        p = params_dev(workloads.init_params(w))
+        ctx = pg().Context(w.V, w.d, w.win, w.H, max_batch=4096)
+        for s in range(3):
+            win, cor = workloads.batch(w, s, 4096)
+            ctx.train_step(p, dev(win), dev(cor), 0.5)
+        outs.append({k: host(v) for k, v in p.items()})
+    for k in outs[0]:
+        assert np.array_equal(outs[0][k], outs[1][k]), k
+
+
+def test_train_steps_graph_equals_single_steps():
+    m = pg()
+    w = PRESETS["sweep_1024"]
+    S, B = 6, 1024
+    batches = [workloads.batch(w, s, B) for s in range(S)]
+    wall = dev(np.stack([b[0] for b in batches]))
+    call = dev(np.stack([b[1] for b in batches]))
+    p0 = workloads.init_params(w)
+    st = torch.cuda.Stream()
+    with torch.cuda.stream(st):
+        a = params_dev(p0)
+        ctx = m.Context(w.V, w.d, w.win, w.H, max_batch=B, stream=st)
+        la = torch.zeros(S, device="cuda")
+        ctx.train_steps(a, wall, call, 0.5, la)
+        ctx.train_steps(a, wall, call, 0.5, la)  # replay of the cached graph
+        b = params_dev(p0)
+        lb = torch.zeros(2 * S, device="cuda")
+        for r in range(2):
+            for s in range(S):
+                ctx.train_step(b, wall[s], call[s], 0.5, lb[r * S + s:r * S + s + 1])
+        st.synchronize()
+    assert ctx.status() == m.OK
+    for k in p0:
+        assert np.array_equal(host(a[k]), host(b[k])), k
+    assert np.array_equal(host(la), host(lb)[S:])
+
+
+def test_out_of_range_id_voids_the_step():
+    m = pg()
+    w = PRESETS["tiny"]
+    p = workloads.init_params(w)
+    for mode in (0, 1):
+        pd = params_dev(p)
+        win, cor = workloads.batch(w, 0, 32)
+        win[5, 1] = w.V
+        ctx = m.Context(w.V, w.d, w.win, w.H, max_batch=32, scatter_mode=mode)
+        loss = torch.zeros(1, device="cuda")
+        ctx.train_step(pd, dev(win), dev(cor), 0.1, loss)
+        assert ctx.status() == m.EID
+        assert np.isnan(host(loss)[0])
+        for k in p:
+            assert np.array_equal(host(pd[k]), p[k]), k
+        assert ctx.status() == m.OK
+
+
+def test_host_errors_enqueue_nothing():
+    m = pg()
+    w = PRESETS["tiny"]
+    ctx = m.Context(w.V, w.d, w.win, w.H, max_batch=8)
+    p = params_dev(workloads.init_params(w))
+    win, cor = workloads.batch(w, 0, 16)
+    with pytest.raises(m.PolyglotError) as e:
+        ctx.train_step(p, dev(win), dev(cor), 0.1)
+    assert e.value.rc == m.EBATCH
+    with pytest.raises(m.PolyglotError) as e:
+        ctx.train_step(p, dev(win[:8]), dev(cor[:8]), float("inf"))
+    assert e.value.rc == m.EINVAL
+
+
+# ---------------------------------------------------------------- score
+
+@pytest.mark.parametrize("name,B", [("tiny", 50), ("poly256", 777)])
+def test_score_matches_oracle(name, B):
+    w = PRESETS[name]
+    p = workloads.init_params(w, seed=9)
+    p["W1"] *= 30  # make the hidden layer leave the linear regime of tanh
+    win, _ = workloads.batch(w, 1, B)
+    ctx = pg().Context(w.V, w.d, w.win, w.H, max_batch=B)
+    s = host(ctx.score(params_dev(p), dev(win)))
+    r = oracle.score(p, win)
+    np.testing.assert_allclose(s, r, rtol=1e-5, atol=1e-6 * np.max(np.abs(r)))
