@@ -143,7 +143,8 @@ int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int
 #define POLYGLOT_K_GATHER 3   /* polyglot_gather */
 #define POLYGLOT_K_SCATTER 4  /* polyglot_scatter_add (all of its launches) */
 #define POLYGLOT_K_SCORE 5    /* polyglot_score */
-#define POLYGLOT_NKERNELS 6
+#define POLYGLOT_K_SEGFIX 6   /* rows whose sorted entries span several chunks */
+#define POLYGLOT_NKERNELS 7
 
 /* Per-kernel timing for measurement.  With enable != 0 every later launch of
  * this context (outside graph capture) is bracketed by two HIP events

@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "launch.h"
+#include "seg_dev.h"
 
 using namespace pg;
 
@@ -105,15 +106,13 @@ SortBufs sort_bufs(polyglot_ctx* ctx) {
   return sb;
 }
 
-// Counters a multi-tile sort leaves nonzero (pass-0 per-tile counts are
+// Counters a multi-tile sort accumulates atomically (per-tile counts are
 // overwritten by every sort and need no clearing).
 ZeroRanges sort_zero_ranges(polyglot_ctx* ctx, const SortPlan& plan) {
   ZeroRanges z{};
   if (plan.small) return z;
   z.p[0] = ctx->ws.totals;
   z.n[0] = (size_t)kMaxPasses * kMaxBins;
-  z.p[1] = ctx->ws.counts + (size_t)kMaxBins * ctx->max_tiles;
-  z.n[1] = (size_t)(plan.passes - 1) * kMaxBins * ctx->max_tiles;
   z.p[2] = ctx->ws.gcounts;
   z.n[2] = (size_t)plan.passes * kMaxBins * ctx->max_groups;
   return z;
@@ -236,8 +235,7 @@ int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, f
   if (sorted && !plan.small) {
     const StepKeys kf{windows, corrupt, cf.win, cf.V};
     KernelTimer kt(ctx, POLYGLOT_K_SORT);
-    for (int p = 0; p < plan.passes && e == hipSuccess; ++p)
-      e = launch_sort_down_step(kf, N, plan, sb, p, ctx->stream);
+    e = launch_sort_passes_step(kf, N, plan, sb, ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "sort launch");
   }
 
@@ -270,9 +268,10 @@ int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, f
   ua.B = B;
   ua.N = N;
   ua.mode = sorted ? 0 : 1;
-  const int nchunks = ceil_div(N, kSegChunk);
+  ua.ch = seg_chunk_size(N);
+  const int nchunks = ceil_div(N, sorted ? ua.ch : kAtomicChunk);
   ua.n_e = std::min(ceil_div(nchunks, kWavesPerBlock), 1024);
-  ua.n_d = ceil_div(ctx->Hp * ctx->K + 2 * ctx->Hp + 2, kBlock);
+  ua.n_d = ceil_div((ctx->Hp * ctx->K + 2 * ctx->Hp + 2) * kDenseSlices, kBlock);
   ua.n_parts = n_fb;
   ua.part_stride = ctx->part_stride;
   ua.seg_stride = ctx->seg_stride;
@@ -280,10 +279,11 @@ int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, f
   ua.invB = 1.0f / (float)B;
   {
     KernelTimer kt(ctx, POLYGLOT_K_UPDATE);
-    e = launch_step_update(ua, ua.n_e + ua.n_d, step_update_lds_bytes(ctx->Hp, ctx->K, cf.d),
-                           ctx->stream);
-    if (e == hipSuccess && sorted)
-      e = launch_step_segfix(ua, (size_t)ctx->Hp * ctx->K * 4, ctx->stream);
+    e = launch_step_update(ua, ua.n_e + ua.n_d, ctx->stream);
+  }
+  if (e == hipSuccess && sorted) {
+    KernelTimer kt(ctx, POLYGLOT_K_SEGFIX);
+    e = launch_step_segfix(ua, ctx->stream);
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "update launch");
 
@@ -336,7 +336,9 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   ctx->max_tiles = ceil_div(ctx->max_entries, kSortTile);
   ctx->max_groups = ceil_div(ctx->max_tiles, kCountGroup);
   ctx->max_parts = std::min(ceil_div(c.max_batch, kTileRows), 512);
-  ctx->max_chunks = ceil_div(ctx->max_entries, kSegChunk);
+  // most chunks any call can cut (short chunks apply up to 131072 entries)
+  ctx->max_chunks = std::max(ceil_div(std::min(ctx->max_entries, 131072), 16),
+                             ceil_div(ctx->max_entries, seg_chunk_size(ctx->max_entries)));
   ctx->seg_stride = std::max(c.win * ctx->Hp, c.max_scatter > 0 ? kMaxD : 0);
   ctx->part_stride = ctx->Hp * ctx->K + 2 * ctx->Hp + 2;
 
@@ -518,7 +520,8 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
     a.sk = ctx->ws.keys[plan.passes & 1];
     a.sv = ctx->ws.vals[plan.passes & 1];
     a.zero = sort_zero_ranges(ctx, plan);
-    a.n_e = std::min(ceil_div(ceil_div(N, kSegChunk), kWavesPerBlock), 2048);
+    a.ch = seg_chunk_size(N);
+    a.n_e = std::min(ceil_div(ceil_div(N, a.ch), kWavesPerBlock), 2048);
     a.n_z = plan.small ? 0 : 16;
     e = launch_scatter_sorted(a, plan, sort_bufs(ctx), ctx->stream);
   } else {

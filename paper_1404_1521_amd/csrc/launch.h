@@ -57,6 +57,7 @@ struct UpdArgs {
   ZeroRanges zero;
   int V, d, win, H, Hp, K, c, B, N;
   int mode;  // 0 sorted, 1 atomic
+  int ch;    // sorted entries per chunk (one wave)
   int n_e;   // embedding-role workgroups
   int n_d;   // dense-role workgroups
   int n_parts;
@@ -99,6 +100,7 @@ struct ScatArgs {
   uint32_t* flag;
   ZeroRanges zero;
   int rows, d, N;
+  int ch;  // sorted entries per chunk (one wave)
   int n_e, n_z;
   int seg_stride;
   float alpha;
@@ -106,20 +108,20 @@ struct ScatArgs {
 
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
                               hipStream_t s);
-hipError_t launch_sort_down_step(const StepKeys& kf, int N, const SortPlan& plan,
-                                 const SortBufs& sb, int p, hipStream_t s);
-hipError_t launch_step_update(const UpdArgs& a, int grid, size_t lds, hipStream_t s);
-hipError_t launch_step_segfix(const UpdArgs& a, size_t lds, hipStream_t s);
+hipError_t launch_sort_passes_step(const StepKeys& kf, int N, const SortPlan& plan,
+                                   const SortBufs& sb, hipStream_t s);
+hipError_t launch_step_update(const UpdArgs& a, int grid, hipStream_t s);
+hipError_t launch_step_segfix(const UpdArgs& a, hipStream_t s);
 hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 hipError_t launch_scatter_sorted(const ScatArgs& a, const SortPlan& plan, const SortBufs& sb,
                                  hipStream_t s);
 hipError_t launch_scatter_atomic(const ScatArgs& a, hipStream_t s);
 
-size_t step_update_lds_bytes(int Hp, int K, int d);
-
 // Launch-shape constants shared with the host.
 constexpr int kSegfixBlocks = 64;
 constexpr int kFlushGroup = 16;  // completed pieces buffered before their rows are written
+constexpr int kAtomicChunk = 8;  // entries per wave in the atomic embedding update
+constexpr int kDenseSlices = 8;  // lanes that share one element of the dense reduction
 
 }  // namespace pg

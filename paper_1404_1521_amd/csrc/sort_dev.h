@@ -10,11 +10,18 @@
 //  * small: one workgroup sorts up to kSmallSortN pairs packed as
 //    (key << val_bits | entry) in LDS, all passes in one launch;
 //  * multi-tile: tiles of kSortTile keys.  up0 counts pass-0 digits per tile
-//    and the digit totals of every pass; down(p) ranks each tile stably with
-//    wave ballots, adds the counts of all earlier tiles, scatters, and counts
-//    the next pass's digits of the output tiles.  Counts are kept per tile
-//    and per group of kCountGroup tiles, so a tile's prefix needs a few dozen
-//    independent loads, not a chain over every earlier tile.
+//    and the digit totals of every pass; down(p) ranks each tile stably,
+//    adds the counts of all earlier tiles and scatters; up(p) counts the
+//    digits of pass p per tile of the previous output.  Counts are kept per
+//    tile and per group of kCountGroup tiles, so a tile's prefix needs a few
+//    dozen independent loads, not a chain over every earlier tile.
+//
+// Ranking inside a wave: keys are held in registers, R rounds of 64; the
+// lanes of a round that share a digit are found with ballots, and the lowest
+// of them adds the group size to the wave's LDS counter with an atomic that
+// returns the old count.  The atomics of all rounds are issued back to back
+// (LDS executes one wave's operations in order, so round r sees rounds < r),
+// and the returned counts are broadcast to the group afterwards.
 #pragma once
 #include "common.h"
 
@@ -81,20 +88,51 @@ __device__ inline void block_exclusive_scan(uint32_t* v, int n, uint32_t* wave_s
   __syncthreads();
 }
 
+// Stable ranks of up to R rounds of 64 keys held by this wave (round-major
+// order); rounds r >= nr and lanes with act[r] false are skipped.  hist is
+// this wave's zeroed LDS counter array.  On return rank[r] is the number of
+// earlier keys of the wave with the same digit, and hist holds the counts.
+template <int R>
+__device__ __forceinline__ void wave_rank(const uint32_t (&dg)[R], const uint64_t (&act)[R],
+                                          int nr, int bits, uint32_t* hist, uint32_t (&rank)[R]) {
+  uint32_t old[R], below_leader[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    old[r] = 0u;
+    below_leader[r] = 0u;
+    if (r < nr) {
+      const uint64_t peers = match_digit(dg[r], bits, act[r]);
+      const uint32_t below = __popcll(peers & lanemask_lt());
+      const uint32_t leader = peers ? (uint32_t)(__ffsll((unsigned long long)peers) - 1) : 0u;
+      below_leader[r] = below | (leader << 16);
+      if (((act[r] >> lane_id()) & 1ull) && below == 0)
+        old[r] = atomicAdd(&hist[dg[r]], (uint32_t)__popcll(peers));
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const uint32_t base = __shfl(old[r], (int)(below_leader[r] >> 16));
+    rank[r] = base + (below_leader[r] & 0xffffu);
+  }
+}
+
 // ------------------------------------------------------------------ small sort
-// LDS needed (uint32 words): 2*kSmallSortN (ping-pong) + kSmallSortN/2
-// (16-bit local ranks) + kWavesPerBlock*kMaxBins + 16.
-constexpr int kSmallSortLdsWords = 2 * kSmallSortN + kSmallSortN / 2 +
-                                   kWavesPerBlock * kMaxBins + 16;
+// LDS words: 2*kSmallSortN (ping-pong) + kSmallSortN/2 (16-bit ranks) +
+// kWavesPerBlock*kMaxBins + 16.
+constexpr int kSmallSortLdsWords =
+    2 * kSmallSortN + kSmallSortN / 2 + kWavesPerBlock * kMaxBins + 16;
+constexpr int kRankBatch = 8;  // rounds ranked per batch (registers bounded)
 
 template <class KeyFn>
 __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t* out_keys,
                            int32_t* out_vals, uint32_t* flag, uint32_t* lds) {
+  constexpr int R = kRankBatch;
   uint32_t* bufA = lds;
   uint32_t* bufB = bufA + kSmallSortN;
-  uint16_t* rank = reinterpret_cast<uint16_t*>(bufB + kSmallSortN);
+  uint16_t* rank16 = reinterpret_cast<uint16_t*>(bufB + kSmallSortN);
   uint32_t* hist = bufB + kSmallSortN + kSmallSortN / 2;  // [waves][kMaxBins]
   uint32_t* misc = hist + kWavesPerBlock * kMaxBins;       // wave sums
+  uint32_t* myhist = hist + (threadIdx.x / kWave) * kMaxBins;
   const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
   const int vb = plan.val_bits;
   const uint32_t vmask = (vb >= 32) ? 0xffffffffu : ((1u << vb) - 1u);
@@ -110,55 +148,69 @@ __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t
       if (e < N) bufA[e] = (kk[u] << vb) | (uint32_t)e;
     }
   }
+  // wave w owns entries [w*per, (w+1)*per) in input order, per a multiple of 64
+  const int per = ceil_div(ceil_div(N, kWavesPerBlock), kWave) * kWave;
+  const int beg = w * per;
+  const int nr = max(0, min(per, N - beg) + kWave - 1) / kWave;
   __syncthreads();
 
-  const int per = ceil_div(N, kWavesPerBlock);
-  const int beg = min(N, w * per), end = min(N, beg + per);
   uint32_t* src = bufA;
   uint32_t* dst = bufB;
   for (int p = 0; p < plan.passes; ++p) {
     const int bits = plan.bits[p], shift = plan.shift[p] + vb, bins = 1 << bits;
-    for (int i = lane; i < bins; i += kWave) hist[w * kMaxBins + i] = 0;
-    __syncthreads();
-    // stable ranks within this wave's contiguous range
-    for (int base = beg; base < end; base += kWave) {
-      const int i = base + lane;
-      const bool act = i < end;
-      const uint32_t word = act ? src[i] : 0u;
-      const uint32_t dg = (word >> shift) & (uint32_t)(bins - 1);
-      const uint64_t peers = match_digit(dg, bits, __ballot(act));
-      if (act) {
-        const uint32_t below = __popcll(peers & lanemask_lt());
-        const uint32_t cnt = hist[w * kMaxBins + dg];
-        rank[i] = (uint16_t)(cnt + below);
-        if (below == 0) hist[w * kMaxBins + dg] = cnt + (uint32_t)__popcll(peers);
+    for (int i = lane; i < bins; i += kWave) myhist[i] = 0;
+    wave_lds_sync();
+    for (int r0 = 0; r0 < nr; r0 += R) {  // the wave's counters carry over batches
+      uint32_t dg[R], rank[R];
+      uint64_t act[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int i = beg + (r0 + r) * kWave + lane;
+        const bool ok = r0 + r < nr && i < N;
+        act[r] = __ballot(ok);
+        dg[r] = ((ok ? src[i] : 0u) >> shift) & (uint32_t)(bins - 1);
+      }
+      wave_rank<R>(dg, act, min(R, nr - r0), bits, myhist, rank);
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int i = beg + (r0 + r) * kWave + lane;
+        if ((act[r] >> lane) & 1ull) rank16[i] = (uint16_t)rank[r];
       }
     }
     __syncthreads();
     // per-digit totals -> digit starts; per-wave offsets
-    for (int dg = t; dg < bins; dg += kBlock) {
+    for (int d = t; d < bins; d += kBlock) {
       uint32_t s = 0;
       for (int q = 0; q < kWavesPerBlock; ++q) {
-        const uint32_t c = hist[q * kMaxBins + dg];
-        hist[q * kMaxBins + dg] = s;  // exclusive over waves
+        const uint32_t c = hist[q * kMaxBins + d];
+        hist[q * kMaxBins + d] = s;  // exclusive over waves
         s += c;
       }
-      dst[dg] = s;  // dst is free until the scatter below: digit totals
+      dst[d] = s;  // dst is free until the scatter below: digit totals
     }
     __syncthreads();
     block_exclusive_scan(dst, bins, misc);
-    for (int dg = t; dg < bins; dg += kBlock) {
-      const uint32_t start = dst[dg];
-      for (int q = 0; q < kWavesPerBlock; ++q) hist[q * kMaxBins + dg] += start;
+    for (int d = t; d < bins; d += kBlock) {
+      const uint32_t start = dst[d];
+      for (int q = 0; q < kWavesPerBlock; ++q) hist[q * kMaxBins + d] += start;
     }
     __syncthreads();
-    for (int base = beg; base < end; base += kWave) {
-      const int i = base + lane;
-      if (i < end) {
-        const uint32_t word = src[i];
-        const uint32_t dg = (word >> shift) & (uint32_t)(bins - 1);
-        const uint32_t pos = hist[w * kMaxBins + dg] + rank[i];
-        if (pos < (uint32_t)N) dst[pos] = word;
+    for (int r0 = 0; r0 < nr; r0 += R) {
+      uint32_t word[R], rk[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int i = beg + (r0 + r) * kWave + lane;
+        const bool ok = r0 + r < nr && i < N;
+        word[r] = ok ? src[i] : 0u;
+        rk[r] = ok ? (uint32_t)rank16[i] : 0u;
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int i = beg + (r0 + r) * kWave + lane;
+        if (r0 + r < nr && i < N) {
+          const uint32_t pos = myhist[(word[r] >> shift) & (uint32_t)(bins - 1)] + rk[r];
+          if (pos < (uint32_t)N) dst[pos] = word[r];
+        }
       }
     }
     __syncthreads();
@@ -256,7 +308,7 @@ __device__ __forceinline__ uint32_t tiles_before(const SortBufs& sb, int p, int 
   return s;
 }
 
-// Pass p over one tile: stable rank, global offset, scatter, next-pass counts.
+// Pass p over one tile: stable rank, global offset, scatter.
 template <class KeyFn>
 __device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
                                int p, int tile, uint32_t* lds) {
@@ -264,6 +316,7 @@ __device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, con
   uint32_t* dscr = hist + kWavesPerBlock * kMaxBins;     // [kMaxBins]
   uint32_t* misc = dscr + kMaxBins;
   const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  uint32_t* myhist = hist + w * kMaxBins;
   const int bits = plan.bits[p], shift = plan.shift[p], bins = 1 << bits;
   const int32_t* sk = sb.keys[p & 1];
   const int32_t* sv = sb.vals[p & 1];
@@ -271,85 +324,91 @@ __device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, con
   int32_t* dv = sb.vals[(p + 1) & 1];
 
   constexpr int R = kSortTile / kBlock;  // rounds per wave (blocked: a wave owns R*64 keys)
-  int32_t key[R], val[R];
-  uint32_t loc[R];
+  uint32_t key[R], dg[R], loc[R];
+  int32_t val[R];
+  uint64_t act[R];
   const int wbase = tile * kSortTile + w * (R * kWave);
   if (p == 0) {
-    uint32_t kk[R];
-    load_keys<R>(kf, N, wbase + lane, kWave, kk, sb.flag);
+    load_keys<R>(kf, N, wbase + lane, kWave, key, sb.flag);
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      key[r] = (int32_t)kk[r];
-      val[r] = wbase + r * kWave + lane;
-    }
+    for (int r = 0; r < R; ++r) val[r] = wbase + r * kWave + lane;
   } else {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int i = wbase + r * kWave + lane;
-      key[r] = i < N ? sk[i] : 0;
+      key[r] = i < N ? (uint32_t)sk[i] : 0u;
       val[r] = i < N ? sv[i] : 0;
     }
   }
-  for (int i = lane; i < bins; i += kWave) hist[w * kMaxBins + i] = 0;
-  for (int dg = t; dg < bins; dg += kBlock) dscr[dg] = sb.totals[p * kMaxBins + dg];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    act[r] = __ballot(wbase + r * kWave + lane < N);
+    dg[r] = (key[r] >> shift) & (uint32_t)(bins - 1);
+  }
+  for (int i = lane; i < bins; i += kWave) myhist[i] = 0;
+  for (int d = t; d < bins; d += kBlock) dscr[d] = sb.totals[p * kMaxBins + d];
   uint32_t before[kMaxBins / kBlock];
 #pragma unroll
   for (int q = 0; q < kMaxBins / kBlock; ++q) {
-    const int dg = t + q * kBlock;
-    before[q] = dg < bins ? tiles_before(sb, p, dg, tile) : 0u;
+    const int d = t + q * kBlock;
+    before[q] = d < bins ? tiles_before(sb, p, d, tile) : 0u;
   }
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int i = wbase + r * kWave + lane;
-    const bool act = i < N;
-    const uint32_t dg = ((uint32_t)key[r] >> shift) & (uint32_t)(bins - 1);
-    const uint64_t peers = match_digit(dg, bits, __ballot(act));
-    uint32_t l = 0;
-    if (act) {
-      const uint32_t below = __popcll(peers & lanemask_lt());
-      const uint32_t cnt = hist[w * kMaxBins + dg];
-      l = cnt + below;
-      if (below == 0) hist[w * kMaxBins + dg] = cnt + (uint32_t)__popcll(peers);
-    }
-    loc[r] = l;
-  }
+  wave_lds_sync();
+  wave_rank<R>(dg, act, R, bits, myhist, loc);
   __syncthreads();
   block_exclusive_scan(dscr, bins, misc);  // digit starts of the pass
 #pragma unroll
   for (int q = 0; q < kMaxBins / kBlock; ++q) {
-    const int dg = t + q * kBlock;
-    if (dg < bins) {
-      uint32_t s = dscr[dg] + before[q];
+    const int d = t + q * kBlock;
+    if (d < bins) {
+      uint32_t s = dscr[d] + before[q];
       for (int v = 0; v < kWavesPerBlock; ++v) {
-        const uint32_t c = hist[v * kMaxBins + dg];
-        hist[v * kMaxBins + dg] = s;
+        const uint32_t c = hist[v * kMaxBins + d];
+        hist[v * kMaxBins + d] = s;
         s += c;
       }
     }
   }
   __syncthreads();
-  const bool more = p + 1 < plan.passes;
-  const int nbits = more ? plan.bits[p + 1] : 0, nshift = more ? plan.shift[p + 1] : 0;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int i = wbase + r * kWave + lane;
-    if (i < N) {
-      const uint32_t dg = ((uint32_t)key[r] >> shift) & (uint32_t)(bins - 1);
-      const uint32_t pos = hist[w * kMaxBins + dg] + loc[r];
+    if ((act[r] >> lane) & 1ull) {
+      const uint32_t pos = myhist[dg[r]] + loc[r];
       if (pos >= (uint32_t)N) {  // inconsistent counters: never write out of bounds
         atomicOr(sb.flag, kFlagInternal);
         continue;
       }
-      dk[pos] = key[r];
+      dk[pos] = (int32_t)key[r];
       dv[pos] = val[r];
-      if (more) {
-        const uint32_t nd = ((uint32_t)key[r] >> nshift) & ((1u << nbits) - 1u);
-        const uint32_t ot = pos / kSortTile;
-        atomicAdd(&counts_at(sb, p + 1, nd)[ot], 1u);
-        atomicAdd(&gcounts_at(sb, p + 1, nd)[ot / kCountGroup], 1u);
-      }
     }
+  }
+}
+
+// Digit counts of pass p (p >= 1) for one tile of the previous pass's output:
+// counts in LDS, one store per (digit, tile) and one atomic per (digit, tile)
+// into the 16-tile group, so heavy Zipf digits never pile up on one counter.
+__device__ void sort_up_tile(int N, const SortPlan& plan, const SortBufs& sb, int p, int tile,
+                             uint32_t* lds) {
+  const int t = threadIdx.x;
+  const int bits = plan.bits[p], shift = plan.shift[p], bins = 1 << bits;
+  for (int i = t; i < bins; i += kBlock) lds[i] = 0;
+  const int32_t* sk = sb.keys[p & 1];
+  const int base = tile * kSortTile;
+  uint32_t key[kSortIPT];
+#pragma unroll
+  for (int q = 0; q < kSortIPT; ++q) {
+    const int e = base + q * kBlock + t;
+    key[q] = e < N ? (uint32_t)sk[e] : 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < kSortIPT; ++q)
+    if (base + q * kBlock + t < N) atomicAdd(&lds[(key[q] >> shift) & (uint32_t)(bins - 1)], 1u);
+  __syncthreads();
+  for (int dg = t; dg < bins; dg += kBlock) {
+    const uint32_t c = lds[dg];
+    counts_at(sb, p, dg)[tile] = c;
+    if (c) atomicAdd(&gcounts_at(sb, p, dg)[tile / kCountGroup], c);
   }
 }
 
