@@ -6,15 +6,17 @@ and scores for the true and the corrupted windows, hinge loss, backward, the
 sorted-segment embedding scatter-add and the dense SGD update.  Inputs are
 seeded synthetic Zipf word windows, staged in device memory before timing.
 
-Prints ONE JSON line (rank 0) with windows/s, the roofline of the dominant
-kernel (per-kernel HIP events on the library's stream) and the CPU oracle
-timed on the host as a baseline.
+Prints ONE JSON line with windows/s, the roofline of the dominant kernel of
+the step (per-kernel HIP events on the library's stream), the standalone
+gather and scatter-add kernels at their full sizes against the HBM roofline,
+and the CPU oracle timed on the host as a baseline.
 """
 from __future__ import annotations
 
 import argparse
 import json
 import os
+import platform
 import sys
 import time
 
@@ -22,8 +24,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
-MFMA_F32_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix, published
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+F32_MATRIX_PEAK_TFLOPS = 157.3  # MI355X dense fp32 MFMA, published
+F32_VECTOR_PEAK_TFLOPS = 157.3  # 256 CU x 4 SIMD x 64 lanes x 2 flop (FMA) x 2.4 GHz
 
 
 def parse():
@@ -33,59 +36,191 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="sweep_1024")
     ap.add_argument("--mode", choices=("sorted", "atomic"), default="sorted")
-    ap.add_argument("--graph", action="store_true",
-                    help="replay the timed steps as one captured HIP graph")
+    ap.add_argument("--eager", action="store_true",
+                    help="one library call per step instead of one captured graph of all steps")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernels", action="store_true",
+                    help="skip the standalone gather / scatter-add measurements")
     return ap.parse_args()
 
 
-def kernel_model(w, B, U, n_parts):
-    """Algorithmic bytes and flops of one launch of each kernel of a step."""
+# ---------------------------------------------------------------------------
+# Algorithmic bytes and flops of each kernel, from the batch itself.
+
+def _hp(H):
+    return -(-H // 16) * 16
+
+
+def seg_chunk(N):
+    """Sorted entries per wave in the segmented update (mirrors the library's choice)."""
+    return 16 if N <= 131072 else 64
+
+
+def batch_structure(wins, cors, ch):
+    """Distinct rows U, rows whose sorted entries span several chunks, and the
+    chunk partials those rows leave (entry order = window-major, corrupt last)."""
+    import numpy as np
+    B, win = wins.shape
+    keys = np.concatenate([wins, cors[:, None]], axis=1).ravel()
+    order = np.argsort(keys, kind="stable")
+    sk = keys[order]
+    heads = np.flatnonzero(np.r_[True, sk[1:] != sk[:-1]])
+    ends = np.r_[heads[1:], sk.size]
+    cs, ce = heads // ch, (ends - 1) // ch
+    long_rows = cs != ce
+    return {"U": int(heads.size), "long_rows": int(long_rows.sum()),
+            "partials": int((ce - cs + 1)[long_rows].sum())}
+
+
+def step_model(w, B, st, passes, n_parts):
+    """{kernel: (bytes, flops, engine)} of one step.
+
+    fwdbwd: ids + every window row read (the gather), the three dz-space
+      vectors written per window, W1 read + its snapshot written, dense
+      partials written; flops = forward 2HK+2Hd and dW1 2HK+2Hd per window.
+    sort: 16 B per entry per radix pass (keys and values, read and written).
+    update: sorted keys+values, each window's dz-space vectors read once,
+      every distinct row read and written, dense partials read, W1/b1/w2/b2
+      read and written; flops = the row gradients (win+1)*2Hd per window.
+    segfix: the chunk partials of long rows (win*H floats each) read and their
+      rows read and written.
+    """
     d, win, H, K = w.d, w.win, w.H, w.K
     N = B * (win + 1)
-    fwd_bytes = B * ((win + 1) * 4 + (win + 1) * d * 4 + 3 * H * 4) + H * K * 4
-    fwd_flops = B * 4 * H * (K + d)
-    upd_bytes = N * (8 + 4 * H) + U * 2 * d * 4 + 2 * H * K * 4
-    upd_flops = 0
-    sort_bytes = N * 16
-    return {
-        "fwdbwd": (fwd_bytes, fwd_flops),
-        "update": (upd_bytes, upd_flops),
-        "sort": (sort_bytes, 0),
+    Hp = _hp(H)
+    part_stride = Hp * K + 2 * Hp + 2
+    dense = (H * K + 2 * H + 1) * 4
+    m = {
+        "fwdbwd": (B * ((win + 1) * 4 + (win + 1) * d * 4 + 3 * H * 4) + 2 * H * K * 4
+                   + n_parts * part_stride * 4,
+                   B * (4 * H * K + 4 * H * d), "mfma"),
+        "sort": (N * 16 * passes, 0, "hbm"),
+        "update": (N * 8 + B * 3 * H * 4 + 2 * st["U"] * d * 4 + n_parts * part_stride * 4
+                   + 2 * dense, N * 2 * H * d, "alu"),
+        "segfix": (st["partials"] * win * H * 4 + 2 * st["long_rows"] * d * 4,
+                   st["long_rows"] * win * 2 * H * d, "alu"),
     }
+    return m
+
+
+def roofline(nbytes, nflops, engine, ms):
+    """Bound by intensity against the ridge of the kernel's own engine."""
+    sec = ms * 1e-3
+    peak_f = F32_MATRIX_PEAK_TFLOPS if engine == "mfma" else F32_VECTOR_PEAK_TFLOPS
+    ridge = peak_f * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if nflops and nbytes and nflops / nbytes > ridge:
+        ach = nflops / sec / 1e12
+        return {"bound": engine, "achieved": round(ach, 4), "peak": peak_f, "unit": "TFLOP/s",
+                "frac": round(ach / peak_f, 5)}
+    ach = nbytes / sec / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(ach / HBM_PEAK_GBS, 5)}
+
+
+# ---------------------------------------------------------------------------
+
+def cpu_model_name():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
 
 
 def cpu_baseline(w, seconds):
-    import numpy as np
+    """The float64-arithmetic C++ oracle, one thread, on the first steps of the workload."""
     import oracle
     import workloads
     p = workloads.init_params(w)
-    steps = 0
-    t0 = time.perf_counter()
-    busy = 0.0
+    steps, busy = 0, 0.0
     while busy < seconds:
         win, cor = workloads.batch(w, steps, w.B)
         a = time.perf_counter()
         oracle.train_step(p, win, cor, w.lr)
         busy += time.perf_counter() - a
         steps += 1
-    del t0
     return {
         "value": round(w.B * steps / busy, 1),
         "unit": "windows/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": f"first {steps} steps of {w.name} (B={w.B}), float32-storage float64-arithmetic "
-                  f"C++ oracle, single thread, {busy:.1f} s of step time",
+        "sample": f"first {steps} steps of {w.name} (B={w.B}): float32 storage, float64 "
+                  f"arithmetic C++ oracle, 1 thread of {os.cpu_count()} on {cpu_model_name()}, "
+                  f"{busy:.1f} s of step time",
     }
+
+
+def time_events(torch, stream, fn, reps):
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    fn()
+    stream.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    stream.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
+    """Standalone gather (B=65536 windows) and scatter-add (327,680 Zipf(1.2)
+    rows into a 100k x 64 table) with their HBM rooflines.  Durations are the
+    library's own per-kernel HIP events on its stream."""
+    w = workloads.PRESETS["sweep_65536"]
+    sw = workloads.SCATTER_ISO
+    out = {}
+    ctx = pg.Context(w.V, w.d, w.win, w.H, max_batch=w.B, max_scatter=sw.N, max_rows=sw.rows,
+                     stream=stream)
+    try:
+        p = workloads.init_params(w)
+        E = torch.from_numpy(p["E"]).cuda()
+        wins, cors = workloads.batch(w, 0, w.B)
+        dw, dc = torch.from_numpy(wins).cuda(), torch.from_numpy(cors).cuda()
+        X = torch.empty(w.B, w.K, device="cuda")
+        Xc = torch.empty(w.B, w.d, device="cuda")
+        ctx.gather(E, dw, dc, X, Xc)
+        stream.synchronize()
+        ctx.set_timing(True)
+        for _ in range(reps):
+            ctx.gather(E, dw, dc, X, Xc)
+        ms, n = ctx.kernel_times()["gather"]
+        nbytes = w.B * ((w.win + 1) * 4 + 2 * (w.win + 1) * w.d * 4)
+        out["gather"] = dict(roofline(nbytes, 0, "hbm", ms / n), avg_launch_us=round(ms / n * 1e3, 3),
+                             bytes_per_launch=nbytes, workload=f"B={w.B} V={w.V} d={w.d} win={w.win}")
+
+        table0, idx, Y = workloads.scatter_inputs(sw)
+        T = torch.from_numpy(table0).cuda()
+        I = torch.from_numpy(idx).cuda()
+        Yd = torch.from_numpy(Y).cuda()
+        U = int(np.unique(idx).size)
+        nbytes = sw.N * (4 + 4 * sw.d) + 2 * U * sw.d * 4
+        for name, mode in (("scatter_sorted", pg.SCATTER_SORTED), ("scatter_atomic", pg.SCATTER_ATOMIC)):
+            ctx.scatter_add(T, I, Yd, 1.0, mode)
+            ctx.kernel_times()
+            for _ in range(reps):
+                ctx.scatter_add(T, I, Yd, 1.0, mode)
+            ms, n = ctx.kernel_times()["scatter"]
+            out[name] = dict(roofline(nbytes, 0, "hbm", ms / n), avg_call_us=round(ms / n * 1e3, 3),
+                             bytes_per_call=nbytes,
+                             workload=f"{sw.N} rows Zipf({sw.zipf_s}) into {sw.rows}x{sw.d}, U={U}")
+        ctx.set_timing(False)
+        if ctx.status() != pg.OK:
+            raise RuntimeError("device error flag raised in the kernel measurements")
+    finally:
+        ctx.close()
+    return out
 
 
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
-              "multi-GPU path", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the step has no "
+              "multi-GPU path; see the sharding notes in the design document", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
@@ -95,6 +230,7 @@ def main():
 
     w = workloads.PRESETS[args.workload]
     B, K, Wm = w.B, args.steps, args.warmup
+    N = B * (w.win + 1)
     mode = pg.SCATTER_SORTED if args.mode == "sorted" else pg.SCATTER_ATOMIC
     torch.cuda.set_device(0)
     stream = torch.cuda.Stream()
@@ -106,25 +242,22 @@ def main():
         cors = np.empty((nb, B), np.int32)
         for s in range(nb):
             wins[s], cors[s] = workloads.batch(w, s, B)
-        U = int(np.mean([np.unique(np.concatenate([wins[s].ravel(), cors[s]])).size
-                         for s in range(min(nb, 8))]))
         dwin = torch.from_numpy(wins).cuda()
         dcor = torch.from_numpy(cors).cuda()
         losses = torch.zeros(nb, device="cuda")
         ctx = pg.Context(w.V, w.d, w.win, w.H, max_batch=B, scatter_mode=mode, stream=stream)
 
         def run(lo, hi):
-            if args.graph:
-                ctx.train_steps(pd, dwin[lo:hi], dcor[lo:hi], w.lr, losses[lo:hi])
-            else:
+            if args.eager:
                 for s in range(lo, hi):
                     ctx.train_step(pd, dwin[s], dcor[s], w.lr, losses[s:s + 1])
+            else:
+                ctx.train_steps(pd, dwin[lo:hi], dcor[lo:hi], w.lr, losses[lo:hi])
 
-        # warmup (with --graph this also captures the graph of the timed steps)
         for s in range(Wm):
             ctx.train_step(pd, dwin[s], dcor[s], w.lr, losses[s:s + 1])
-        if args.graph:
-            run(Wm, Wm + K)
+        if not args.eager:
+            run(Wm, Wm + K)  # captures the graph of K steps; the timed call replays it
         stream.synchronize()
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
@@ -140,7 +273,8 @@ def main():
         if ctx.status() != pg.OK:
             raise RuntimeError("device error flag raised during the benchmark")
 
-        # per-kernel durations: the next K steps with event brackets on the library stream
+        # per-kernel durations: K more steps, one call each, HIP events around
+        # every launch on the library stream
         ctx.set_timing(True)
         for s in range(Wm + K, Wm + 2 * K):
             ctx.train_step(pd, dwin[s], dcor[s], w.lr, losses[s:s + 1])
@@ -149,25 +283,29 @@ def main():
         lh = losses.cpu().numpy()
         if not np.all(np.isfinite(lh)):
             raise RuntimeError("non-finite loss")
+        kern = None if args.no_kernels else kernel_rooflines(torch, np, pg, workloads, stream)
+        ctx.close()
 
+    # structure of the timed batches (sampled) for the byte model
+    ch = seg_chunk(N)
+    samp = [batch_structure(wins[s], cors[s], ch) for s in range(Wm + K, Wm + K + min(K, 8))]
+    st = {k: float(np.mean([x[k] for x in samp])) for k in samp[0]}
+    small = N <= 8192
+    key_bits = max(1, int(w.V - 1).bit_length())
+    passes = 0 if small else -(-key_bits // 9)
     n_parts = min(-(-B // 16), 512)
-    model = kernel_model(w, B, U, n_parts)
-    per = {k: (v[0] / v[1] if v[1] else 0.0, v[1]) for k, v in kt.items() if v[1]}
+    model = step_model(w, B, st, passes, n_parts)
+    per = {k: (v[0] / v[1], v[1] / K) for k, v in kt.items() if v[1]}
     dom = max(per, key=lambda k: per[k][0] * per[k][1])
-    dms, dlaunch = per[dom]
-    nbytes, nflops = model.get(dom, (0, 0))
-    intensity = nflops / nbytes if nbytes else 0.0
-    if nflops and intensity > MFMA_F32_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
-        ach = nflops / (dms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(ach, 3), "peak": MFMA_F32_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(ach / MFMA_F32_PEAK_TFLOPS, 5), "traffic": None}
-    else:
-        ach = nbytes / (dms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(ach, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 5), "traffic": None}
+    dms = per[dom][0]
+    nbytes, nflops, engine = model[dom]
+    roof = roofline(nbytes, nflops, engine, dms)
+    roof["traffic"] = None
     roof["kernel"] = dom
     roof["avg_launch_us"] = round(dms * 1e3, 3)
-    roof["kernels_us"] = {k: round(v[0] * 1e3, 3) for k, v in per.items()}
+    roof["bytes_per_launch"] = int(nbytes)
+    roof["flops_per_launch"] = int(nflops)
+    roof["kernels_us_per_step"] = {k: round(v[0] * v[1] * 1e3, 3) for k, v in per.items()}
 
     value = B * K / (ms * 1e-3)
     out = {
@@ -185,11 +323,14 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{w.name}: V={w.V} d={w.d} win={w.win} H={w.H} B={B} "
                                f"ids Zipf({w.zipf_s}) corrupt uniform lr={w.lr} "
-                               f"scatter={args.mode}{' graph' if args.graph else ''}",
-                   "global_batch": B, "parallelism": "single-gpu"},
+                               f"scatter={args.mode} {'eager' if args.eager else 'graph'}",
+                   "global_batch": B, "parallelism": "single-gpu",
+                   "distinct_rows_per_step": round(st["U"], 1)},
         "roofline": roof,
         "wall_s": round(wall, 4),
     }
+    if kern is not None:
+        out["kernels"] = kern
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)
