@@ -11,7 +11,7 @@
  * -----------------------------------------
  * The paper (Kulkarni, Al-Rfou, Perozzi, Skiena: "Exploring the power of
  * GPU's for training Polyglot language models", arXiv:1404.1521) trains the
- * Polyglot language model, which it calls "very similar" to the SENNA
+ * Polyglot language model, which it describes as close to the SENNA
  * ranking language model (§1 Introduction), with minibatch SGD in Theano
  * (§2 Experimental Setup; minibatch size, §4.6).  The paper does not write
  * the model out.  The reading adopted here is the SENNA-style window ranker:
