@@ -36,6 +36,10 @@ struct GraphKey {
 struct polyglot_ctx {
   polyglot_config cfg{};
   hipStream_t stream = nullptr;
+  // the step's sort depends only on the ids: it runs on a second stream,
+  // forked from and joined back into `stream` around the fused kernel
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   int device = 0;
   int Hp = 0, NT = 0, K = 0, c = 0, cpw = 0;
   int max_entries = 0, max_tiles = 0, max_groups = 0, max_parts = 0, max_chunks = 0;
@@ -139,6 +143,11 @@ void free_all(polyglot_ctx* ctx) {
   ctx->ev_pool.clear();
   if (ctx->gexec) hipGraphExecDestroy(ctx->gexec);
   ctx->gexec = nullptr;
+  if (ctx->ev_fork) hipEventDestroy(ctx->ev_fork);
+  if (ctx->ev_join) hipEventDestroy(ctx->ev_join);
+  if (ctx->side) hipStreamDestroy(ctx->side);
+  ctx->ev_fork = ctx->ev_join = nullptr;
+  ctx->side = nullptr;
   for (void* q : ctx->allocs) hipFree(q);
   ctx->allocs.clear();
 }
@@ -158,17 +167,19 @@ hipEvent_t take_event(polyglot_ctx* ctx) {
 struct KernelTimer {
   polyglot_ctx* ctx;
   int id;
+  hipStream_t st;
   hipEvent_t a = nullptr, b = nullptr;
-  KernelTimer(polyglot_ctx* c, int kid) : ctx(c), id(kid) {
+  KernelTimer(polyglot_ctx* c, int kid, hipStream_t s) : ctx(c), id(kid), st(s) {
     if (ctx->timing && !ctx->capturing) {
       a = take_event(ctx);
       b = take_event(ctx);
-      if (a && b) hipEventRecord(a, ctx->stream);
+      if (a && b) hipEventRecord(a, st);
     }
   }
+  KernelTimer(polyglot_ctx* c, int kid) : KernelTimer(c, kid, c->stream) {}
   ~KernelTimer() {
     if (a && b) {
-      hipEventRecord(b, ctx->stream);
+      hipEventRecord(b, st);
       ctx->ev_marks.push_back({id, {a, b}});
     } else {
       if (a) ctx->ev_pool.push_back(a);
@@ -177,8 +188,35 @@ struct KernelTimer {
   }
 };
 
-size_t fwdbwd_lds_bytes(int NT) {
-  return (size_t)kTileRows * (kMaxWin + 1) * 4 + (size_t)kWavesPerBlock * 3 * NT * kWave * 16;
+SegArgs seg_args(polyglot_ctx* ctx, float* table, const float* Y, const SortPlan& plan, int N,
+                 int d, float alpha) {
+  SegArgs a{};
+  a.table = table;
+  a.Y = Y;
+  a.sk = ctx->ws.keys[plan.passes & 1];
+  a.sv = ctx->ws.vals[plan.passes & 1];
+  a.seg_part = ctx->ws.seg_part;
+  a.long_list = ctx->ws.long_list;
+  a.long_count = ctx->ws.long_count;
+  a.seg_end = ctx->ws.seg_end;
+  a.flag = ctx->ws.flag;
+  a.N = N;
+  a.d = d;
+  a.ch = seg_chunk_size(N);
+  a.seg_stride = ctx->seg_stride;
+  a.alpha = alpha;
+  return a;
+}
+
+// Workgroups of the table role of k_apply.
+int table_workgroups(const SegArgs& s, int mode) {
+  const int units = mode == 0 ? ceil_div(ceil_div(s.N, s.ch), kWavesPerBlock)
+                              : (int)std::min<int64_t>((int64_t)s.N * s.d / kBlock + 1, 1 << 20);
+  return std::max(1, std::min(units, mode == 0 ? 2048 : 8192));
+}
+
+int segfix_workgroups(const SegArgs& s) {
+  return std::max(1, std::min(ceil_div(s.N, s.ch), 2048));
 }
 
 // Enqueues one training step.  Arguments are already validated.
@@ -189,7 +227,19 @@ int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, f
   const int N = B * (cf.win + 1);
   const bool sorted = cf.scatter_mode == POLYGLOT_SCATTER_SORTED;
   const SortPlan plan = make_plan(cf.V, N);
-  const SortBufs sb = sort_bufs(ctx);
+  const StepKeys kf{windows, corrupt, cf.win, cf.V};
+  hipError_t e = hipSuccess;
+
+  if (sorted) {  // sort on the side stream, concurrent with the fused kernel
+    e = hipEventRecord(ctx->ev_fork, ctx->stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(ctx->side, ctx->ev_fork, 0);
+    if (e == hipSuccess) {
+      KernelTimer kt(ctx, POLYGLOT_K_SORT, ctx->side);
+      e = launch_sort_step(kf, N, plan, sort_bufs(ctx), ctx->ws.long_count, ctx->side);
+    }
+    if (e == hipSuccess) e = hipEventRecord(ctx->ev_join, ctx->side);
+    if (e != hipSuccess) return hip_fail(ctx, e, "sort launch");
+  }
 
   FwdArgs fa{};
   fa.E = E;
@@ -199,10 +249,8 @@ int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, f
   fa.b2 = b2;
   fa.windows = windows;
   fa.corrupt = corrupt;
-  fa.dzz = ctx->ws.dzz;
+  fa.G = ctx->ws.G;
   fa.part = ctx->ws.part;
-  fa.w1snap = ctx->ws.w1snap;
-  fa.long_count = ctx->ws.long_count;
   fa.flag = ctx->ws.flag;
   fa.V = cf.V;
   fa.d = cf.d;
@@ -212,78 +260,48 @@ int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, f
   fa.K = ctx->K;
   fa.c = ctx->c;
   fa.B = B;
-  fa.N = N;
   fa.ntiles = ceil_div(B, kTileRows);
   fa.tiles_per_wg = ceil_div(fa.ntiles, ctx->max_parts);
   const int n_fb = ceil_div(fa.ntiles, fa.tiles_per_wg);
   fa.part_stride = ctx->part_stride;
   fa.invB = 1.0f / (float)B;
-  fa.n_sort = sorted ? (plan.small ? 1 : plan.ntiles) : 0;
-  fa.sort_small = plan.small;
-  fa.plan = plan;
-  fa.sb = sb;
-  size_t lds = fwdbwd_lds_bytes(ctx->NT);
-  if (sorted)
-    lds = std::max(lds, (size_t)(plan.small ? kSmallSortLdsWords : kUp0LdsWords) * 4);
-  hipError_t e;
   {
     KernelTimer kt(ctx, POLYGLOT_K_FWDBWD);
-    e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, fa.n_sort + n_fb, lds, ctx->stream);
+    e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, n_fb, fwdbwd_lds_floats(ctx->Hp, ctx->K) * 4,
+                           ctx->stream);
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "fwd/bwd launch");
-
-  if (sorted && !plan.small) {
-    const StepKeys kf{windows, corrupt, cf.win, cf.V};
-    KernelTimer kt(ctx, POLYGLOT_K_SORT);
-    e = launch_sort_passes_step(kf, N, plan, sb, ctx->stream);
-    if (e != hipSuccess) return hip_fail(ctx, e, "sort launch");
+  if (sorted) {
+    e = hipStreamWaitEvent(ctx->stream, ctx->ev_join, 0);
+    if (e != hipSuccess) return hip_fail(ctx, e, "sort join");
   }
 
-  UpdArgs ua{};
-  ua.E = E;
-  ua.W1 = W1;
-  ua.b1 = b1;
-  ua.w2 = w2;
-  ua.b2 = b2;
-  ua.loss_out = loss_dev ? loss_dev : ctx->ws.scratch_loss;
-  ua.dzz = ctx->ws.dzz;
-  ua.part = ctx->ws.part;
-  ua.w1snap = ctx->ws.w1snap;
-  ua.sk = ctx->ws.keys[plan.passes & 1];
-  ua.sv = ctx->ws.vals[plan.passes & 1];
-  ua.windows = windows;
-  ua.corrupt = corrupt;
-  ua.seg_part = ctx->ws.seg_part;
-  ua.long_list = ctx->ws.long_list;
-  ua.long_count = ctx->ws.long_count;
-  ua.flag = ctx->ws.flag;
-  if (sorted) ua.zero = sort_zero_ranges(ctx, plan);
-  ua.V = cf.V;
-  ua.d = cf.d;
-  ua.win = cf.win;
-  ua.H = cf.H;
-  ua.Hp = ctx->Hp;
-  ua.K = ctx->K;
-  ua.c = ctx->c;
-  ua.B = B;
-  ua.N = N;
-  ua.mode = sorted ? 0 : 1;
-  ua.ch = seg_chunk_size(N);
-  const int nchunks = ceil_div(N, sorted ? ua.ch : kAtomicChunk);
-  ua.n_e = std::min(ceil_div(nchunks, kWavesPerBlock), 1024);
-  ua.n_d = ceil_div((ctx->Hp * ctx->K + 2 * ctx->Hp + 2) * kDenseSlices, kBlock);
-  ua.n_parts = n_fb;
-  ua.part_stride = ctx->part_stride;
-  ua.seg_stride = ctx->seg_stride;
-  ua.lr = lr;
-  ua.invB = 1.0f / (float)B;
+  ApplyArgs aa{};
+  aa.s = seg_args(ctx, E, ctx->ws.G, plan, N, cf.d, -lr);
+  aa.mode = sorted ? 0 : 1;
+  aa.n_e = table_workgroups(aa.s, aa.mode);
+  aa.n_d = ceil_div(ctx->part_stride * kDenseSlices, kBlock);
+  aa.dn.W1 = W1;
+  aa.dn.b1 = b1;
+  aa.dn.w2 = w2;
+  aa.dn.b2 = b2;
+  aa.dn.loss_out = loss_dev ? loss_dev : ctx->ws.scratch_loss;
+  aa.dn.part = ctx->ws.part;
+  aa.dn.n_parts = n_fb;
+  aa.dn.part_stride = ctx->part_stride;
+  aa.dn.H = cf.H;
+  aa.dn.Hp = ctx->Hp;
+  aa.dn.K = ctx->K;
+  aa.dn.lr = lr;
+  aa.dn.invB = 1.0f / (float)B;
+  if (sorted) aa.zero = sort_zero_ranges(ctx, plan);
   {
     KernelTimer kt(ctx, POLYGLOT_K_UPDATE);
-    e = launch_step_update(ua, ua.n_e + ua.n_d, ctx->stream);
+    e = launch_apply_step(aa, kf, aa.n_e + aa.n_d, ctx->stream);
   }
   if (e == hipSuccess && sorted) {
     KernelTimer kt(ctx, POLYGLOT_K_SEGFIX);
-    e = launch_step_segfix(ua, ctx->stream);
+    e = launch_segfix(aa.s, segfix_workgroups(aa.s), ctx->stream);
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "update launch");
 
@@ -322,6 +340,10 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   if (c.max_scatter < 0 || c.max_scatter > (1 << 26) || c.max_rows < 0 ||
       (c.max_scatter > 0 && c.max_rows < 1))
     return POLYGLOT_EINVAL;
+  {  // the fused kernel keeps W1 and its tile buffers in one workgroup's LDS
+    const int hp = c.H <= 16 ? 16 : (c.H <= 32 ? 32 : 64);
+    if (fwdbwd_lds_floats(hp, c.win * c.d) * 4 > (size_t)kMaxLdsBytes) return POLYGLOT_EINVAL;
+  }
 
   polyglot_ctx* ctx = new (std::nothrow) polyglot_ctx();
   if (!ctx) return POLYGLOT_EHIP;
@@ -339,7 +361,7 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   // most chunks any call can cut (short chunks apply up to 131072 entries)
   ctx->max_chunks = std::max(ceil_div(std::min(ctx->max_entries, 131072), 16),
                              ceil_div(ctx->max_entries, seg_chunk_size(ctx->max_entries)));
-  ctx->seg_stride = std::max(c.win * ctx->Hp, c.max_scatter > 0 ? kMaxD : 0);
+  ctx->seg_stride = std::max(c.d, c.max_scatter > 0 ? kMaxD : 0);
   ctx->part_stride = ctx->Hp * ctx->K + 2 * ctx->Hp + 2;
 
   hipError_t e = hipGetDevice(&ctx->device);
@@ -354,9 +376,9 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   if (e == hipSuccess) e = alloc(ctx, &ws.totals, (size_t)kMaxPasses * kMaxBins);
   if (e == hipSuccess) e = alloc(ctx, &ws.counts, ncount);
   if (e == hipSuccess) e = alloc(ctx, &ws.gcounts, ngcount);
-  if (e == hipSuccess) e = alloc(ctx, &ws.dzz, (size_t)c.max_batch * 3 * ctx->Hp);
+  if (e == hipSuccess) e = alloc(ctx, &ws.G, (size_t)c.max_batch * (c.win + 1) * c.d);
   if (e == hipSuccess) e = alloc(ctx, &ws.part, (size_t)ctx->max_parts * ctx->part_stride);
-  if (e == hipSuccess) e = alloc(ctx, &ws.w1snap, (size_t)ctx->Hp * ctx->K);
+  if (e == hipSuccess) e = alloc(ctx, &ws.seg_end, (size_t)std::max(c.V, c.max_rows));
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_part, (size_t)ctx->max_chunks * 2 * ctx->seg_stride);
   if (e == hipSuccess) e = alloc(ctx, &ws.long_list, (size_t)ctx->max_chunks);
   if (e == hipSuccess) e = alloc(ctx, &ws.long_count, 1);
@@ -367,6 +389,9 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   if (e == hipSuccess) e = hipMemset(ws.gcounts, 0, sizeof(uint32_t) * ngcount);
   if (e == hipSuccess) e = hipMemset(ws.long_count, 0, sizeof(uint32_t));
   if (e == hipSuccess) e = hipMemset(ws.flag, 0, sizeof(uint32_t));
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&ctx->ev_fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&ctx->ev_join, hipEventDisableTiming);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     free_all(ctx);
@@ -380,6 +405,7 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
 int polyglot_destroy(polyglot_ctx* ctx) {
   if (!ctx) return POLYGLOT_ENULL;
   hipStreamSynchronize(ctx->stream);
+  if (ctx->side) hipStreamSynchronize(ctx->side);
   free_all(ctx);
   delete ctx;
   return POLYGLOT_OK;
@@ -495,37 +521,30 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
     return fail(ctx, POLYGLOT_EBATCH, "scatter_add: N must be in [1, max_scatter]");
   if (rows <= 0 || rows > ctx->cfg.max_rows || d <= 0 || d > kMaxD || d % 4 != 0)
     return fail(ctx, POLYGLOT_EINVAL, "scatter_add: bad rows or d");
-  if (!aligned16(table))
-    return fail(ctx, POLYGLOT_EINVAL, "scatter_add: table must be 16-byte aligned");
+  if (!aligned16(table) || !aligned16(Y))
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_add: table and Y must be 16-byte aligned");
   if (!std::isfinite(alpha)) return fail(ctx, POLYGLOT_EINVAL, "scatter_add: alpha not finite");
   if (mode != POLYGLOT_SCATTER_SORTED && mode != POLYGLOT_SCATTER_ATOMIC)
     return fail(ctx, POLYGLOT_EINVAL, "scatter_add: bad mode");
-  ScatArgs a{};
-  a.table = table;
-  a.idx = idx;
-  a.Y = Y;
-  a.seg_part = ctx->ws.seg_part;
-  a.long_list = ctx->ws.long_list;
-  a.long_count = ctx->ws.long_count;
-  a.flag = ctx->ws.flag;
-  a.rows = rows;
-  a.d = d;
-  a.N = N;
-  a.seg_stride = ctx->seg_stride;
-  a.alpha = alpha;
+  const SortPlan plan = make_plan(rows, N);
+  const IdxKeys kf{idx, rows};
+  ApplyArgs aa{};
+  aa.s = seg_args(ctx, table, Y, plan, N, d, alpha);
+  aa.mode = mode == POLYGLOT_SCATTER_SORTED ? 0 : 1;
+  aa.n_e = table_workgroups(aa.s, aa.mode);
+  aa.n_d = 0;
   hipError_t e;
   KernelTimer kt(ctx, POLYGLOT_K_SCATTER);
-  if (mode == POLYGLOT_SCATTER_SORTED) {
-    const SortPlan plan = make_plan(rows, N);
-    a.sk = ctx->ws.keys[plan.passes & 1];
-    a.sv = ctx->ws.vals[plan.passes & 1];
-    a.zero = sort_zero_ranges(ctx, plan);
-    a.ch = seg_chunk_size(N);
-    a.n_e = std::min(ceil_div(ceil_div(N, a.ch), kWavesPerBlock), 2048);
-    a.n_z = plan.small ? 0 : 16;
-    e = launch_scatter_sorted(a, plan, sort_bufs(ctx), ctx->stream);
+  if (aa.mode == 0) {
+    // the sort validates the indices (sticky flag) and clears the task list
+    aa.zero = sort_zero_ranges(ctx, plan);
+    const int n_z = plan.small ? 0 : 16;
+    e = launch_sort_idx(kf, N, plan, sort_bufs(ctx), ctx->ws.long_count, ctx->stream);
+    if (e == hipSuccess) e = launch_apply_idx(aa, kf, aa.n_e + n_z, ctx->stream);
+    if (e == hipSuccess) e = launch_segfix(aa.s, segfix_workgroups(aa.s), ctx->stream);
   } else {
-    e = launch_scatter_atomic(a, ctx->stream);
+    e = launch_check_idx(idx, N, rows, ctx->ws.flag, ctx->stream);
+    if (e == hipSuccess) e = launch_apply_idx(aa, kf, aa.n_e, ctx->stream);
   }
   ctx->have_sorted = false;  // the sort buffers now hold this call's order
   return e == hipSuccess ? POLYGLOT_OK : hip_fail(ctx, e, "scatter_add launch");
@@ -575,6 +594,7 @@ int polyglot_set_timing(polyglot_ctx* ctx, int enable) {
 int polyglot_kernel_times(polyglot_ctx* ctx, double* ms, int32_t* launches) {
   if (!ctx || !ms || !launches) return POLYGLOT_ENULL;
   hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->side);
   if (e != hipSuccess) return hip_fail(ctx, e, "kernel_times: sync");
   for (int k = 0; k < POLYGLOT_NKERNELS; ++k) {
     ms[k] = 0.0;

@@ -1,9 +1,8 @@
-// Score, gather and standalone scatter-add kernels.
+// Score, gather and index-check kernels.
 #pragma once
 #include "common.h"
+#include "fwdbwd_dev.h"
 #include "launch.h"
-#include "seg_dev.h"
-#include "sort_dev.h"
 
 namespace pg {
 
@@ -112,136 +111,7 @@ __global__ __launch_bounds__(kBlock) void k_gather(GatherArgs a) {
   }
 }
 
-// =============================================================== scatter-add
-
-// LDS floats of the scatter segment role (per wave: gradient rows + keys).
-__host__ __device__ inline size_t scatter_lds_floats(int d) {
-  return (size_t)kWavesPerBlock * (kFlushGroup * d + 16);
-}
-
-__device__ void scatter_chunk(const ScatArgs& a, int chunk, float* gbuf, int32_t* pk) {
-  const int lane = lane_id();
-  const ChunkInfo ci = chunk_info(a.sk, a.sv, a.N, chunk, a.ch);
-  constexpr int U = kMaxD / kWave;
-  int nslot = 0;
-  for (int p0 = 0; p0 < ci.nact;) {
-    const int p1 = piece_end(ci, p0);
-    const int32_t pkey = __builtin_amdgcn_readlane(ci.key, p0);
-    float acc[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) acc[u] = 0.f;
-    for (int q = p0; q < p1; q += 8) {  // 8 rows of Y in flight, added in entry order
-      float v[8][U];
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const int k = __builtin_amdgcn_readlane(ci.ent, min(q + r, kWave - 1));
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int col = lane + u * kWave;
-          v[r][u] = (q + r < p1 && col < a.d) ? a.Y[(size_t)k * a.d + col] : 0.f;
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < 8; ++r)
-#pragma unroll
-        for (int u = 0; u < U; ++u) acc[u] += a.alpha * v[r][u];
-    }
-    const bool is_cont = p0 == 0 && ci.cont_first;
-    const bool is_open = p1 == ci.nact && ci.open_last;
-    if (!is_cont && !is_open) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int col = lane + u * kWave;
-        if (col < a.d) gbuf[nslot * a.d + col] = acc[u];
-      }
-      if (lane == 0) pk[nslot] = pkey;
-      if (++nslot == kFlushGroup) {
-        flush_rows(a.table, a.d, 1.f, gbuf, pk, nslot);
-        nslot = 0;
-      }
-    } else {
-      float* dst = a.seg_part + ((size_t)chunk * 2 + (is_cont ? 0 : 1)) * a.seg_stride;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int col = lane + u * kWave;
-        if (col < a.d) dst[col] = acc[u];
-      }
-      if (is_open && !is_cont && lane == 0) a.long_list[atomicAdd(a.long_count, 1u)] = chunk;
-    }
-    p0 = p1;
-  }
-  if (nslot) flush_rows(a.table, a.d, 1.f, gbuf, pk, nslot);
-}
-
-__global__ __launch_bounds__(kBlock) void k_scatter_segments(ScatArgs a) {
-  extern __shared__ uint32_t lds[];
-  const int t = threadIdx.x, w = t / kWave;
-  const bool bad = (*reinterpret_cast<volatile uint32_t*>(a.flag)) != 0u;
-  if ((int)blockIdx.x < a.n_e) {
-    if (bad) return;
-    float* gbuf = reinterpret_cast<float*>(lds) + (size_t)w * (kFlushGroup * a.d + 16);
-    int32_t* pk = reinterpret_cast<int32_t*>(gbuf + kFlushGroup * a.d);
-    const int nchunks = ceil_div(a.N, a.ch);
-    for (int c = blockIdx.x * kWavesPerBlock + w; c < nchunks; c += a.n_e * kWavesPerBlock)
-      scatter_chunk(a, c, gbuf, pk);
-    return;
-  }
-  const size_t gid = (size_t)(blockIdx.x - a.n_e) * kBlock + t;
-  zero_ranges(a.zero, gid, (size_t)a.n_z * kBlock);
-}
-
-__global__ __launch_bounds__(kBlock) void k_scatter_segfix(ScatArgs a) {
-  // one workgroup per row; wave w adds chunks cs+1+w, cs+5+w, ... (wave 0
-  // also the open piece of the start chunk); wave sums are added in order
-  __shared__ float red[kWavesPerBlock][kMaxD];
-  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
-  const uint32_t cnt = *a.long_count;
-  if (blockIdx.x >= cnt || *reinterpret_cast<volatile uint32_t*>(a.flag)) return;
-  constexpr int U = kMaxD / kWave;
-  constexpr int R = 8;
-  for (uint32_t li = blockIdx.x; li < cnt; li += gridDim.x) {
-    const int cs = a.long_list[li];
-    const int32_t key = a.sk[(size_t)cs * a.ch + a.ch - 1];
-    const int ce = cs + seg_count_fwd(a.sk, a.N, cs, key, a.ch);
-    float acc[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int col = lane + u * kWave;
-      acc[u] = (w == 0 && col < a.d) ? a.seg_part[((size_t)cs * 2 + 1) * a.seg_stride + col] : 0.f;
-    }
-    for (int y0 = cs + 1 + w; y0 <= ce; y0 += R * kWavesPerBlock) {
-      float v[R][U];
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        const int y = y0 + r * kWavesPerBlock;
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int col = lane + u * kWave;
-          v[r][u] = (y <= ce && col < a.d) ? a.seg_part[((size_t)y * 2) * a.seg_stride + col] : 0.f;
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < R; ++r)
-#pragma unroll
-        for (int u = 0; u < U; ++u) acc[u] += v[r][u];
-    }
-    __syncthreads();  // previous row's reduction buffer is no longer read
-#pragma unroll
-    for (int u = 0; u < U; ++u) red[w][lane + u * kWave] = acc[u];
-    __syncthreads();
-    if (w == 0) {
-      float* tr = a.table + (size_t)key * a.d;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int col = lane + u * kWave;
-        float s = red[0][col];
-#pragma unroll
-        for (int v = 1; v < kWavesPerBlock; ++v) s += red[v][col];
-        if (col < a.d) tr[col] = tr[col] + s;
-      }
-    }
-  }
-}
+// =============================================================== index check
 
 __global__ __launch_bounds__(kBlock) void k_check_idx(const int32_t* idx, int N, int rows,
                                                       uint32_t* flag) {
@@ -249,17 +119,6 @@ __global__ __launch_bounds__(kBlock) void k_check_idx(const int32_t* idx, int N,
   for (int i = blockIdx.x * kBlock + threadIdx.x; i < N; i += gridDim.x * kBlock)
     bad |= (uint32_t)idx[i] >= (uint32_t)rows;
   if (bad) atomicOr(flag, kFlagBadId);
-}
-
-__global__ __launch_bounds__(kBlock) void k_scatter_atomic(ScatArgs a) {
-  if (*reinterpret_cast<volatile uint32_t*>(a.flag)) return;
-  const size_t total = (size_t)a.N * a.d;
-  for (size_t i = (size_t)blockIdx.x * kBlock + threadIdx.x; i < total;
-       i += (size_t)gridDim.x * kBlock) {
-    const size_t k = i / a.d;
-    const int col = (int)(i - k * a.d);
-    unsafeAtomicAdd(a.table + (size_t)a.idx[k] * a.d + col, a.alpha * a.Y[i]);
-  }
 }
 
 

@@ -13,11 +13,11 @@ constexpr int kBlock = 256;             // threads per workgroup of every kernel
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kTileRows = 16;           // windows per MFMA tile (16x16x4 f32)
 constexpr int kMaxK = 512;              // win*d handled by the fused step kernel
-constexpr int kMaxChunksPerWave = kMaxK / 16 / kWavesPerBlock;  // 8
 constexpr int kMaxHp = 64;              // hidden units, padded to a multiple of 16
 constexpr int kMaxNT = kMaxHp / 16;
 constexpr int kMaxWin = 31;
 constexpr int kMaxD = 256;
+constexpr int kMaxLdsBytes = 160 * 1024;  // LDS per workgroup on gfx950
 
 // Radix sort of (row id, entry) pairs.
 constexpr int kSortIPT = 16;                       // keys per thread in a tile
@@ -26,7 +26,6 @@ constexpr int kMaxDigitBits = 9;
 constexpr int kMaxBins = 1 << kMaxDigitBits;
 constexpr int kMaxPasses = 4;                      // 31-bit keys at most
 constexpr int kSmallSortN = 8192;                  // single-workgroup LDS sort up to this N
-constexpr int kSegChunk = 64;                      // sorted entries per wave in segment kernels
 
 // Sticky device error bits.
 constexpr uint32_t kFlagBadId = 1u;
@@ -50,12 +49,13 @@ struct Workspace {
   uint32_t* counts;         // [kMaxPasses][kMaxBins][max_tiles] per-tile digit counts
   uint32_t* gcounts;        // [kMaxPasses][kMaxBins][max_groups] per-16-tile digit counts
   // step
-  float* dzz;               // [max_batch][3][Hp]: dz+dz~, dz, dz~ per window
+  float* G;                 // [max_batch*(win+1)][d] per-entry embedding gradients
   float* part;              // [max_parts][part_stride] dense-gradient partials
-  float* w1snap;            // [Hp][K] copy of W1 taken before the update
+  // segmented update
   float* seg_part;          // [max_chunks][2][seg_stride] partial sums of long segments
   int32_t* long_list;       // [max_chunks] start chunks of segments spanning chunks
   uint32_t* long_count;     // number of entries in long_list
+  int32_t* seg_end;         // [max(V, max_rows)] end chunk of a long segment, by row id
   uint32_t* flag;           // sticky error bits
   float* scratch_loss;      // loss slot used when the caller passes no loss pointer
 };

@@ -1,6 +1,7 @@
 // Argument blocks and launchers shared by kernels.hip and the host API.
 #pragma once
 #include "common.h"
+#include "seg_dev.h"
 #include "sort_dev.h"
 
 namespace pg {
@@ -13,21 +14,14 @@ struct FwdArgs {
   const float* b2;
   const int32_t* windows;
   const int32_t* corrupt;
-  float* dzz;
-  float* part;
-  float* w1snap;
-  uint32_t* long_count;  // cleared here for the update launch of the same step
+  float* G;          // [B*(win+1)][d] per-entry embedding gradients
+  float* part;       // [workgroups][part_stride] dense partials
   uint32_t* flag;
-  int V, d, win, H, Hp, K, c, B, N;
+  int V, d, win, H, Hp, K, c, B;
   int ntiles;        // ceil(B / 16)
-  int tiles_per_wg;  // consecutive tiles per fwd/bwd workgroup
+  int tiles_per_wg;  // consecutive tiles per workgroup
   int part_stride;   // floats per dense partial slot: Hp*K + 2*Hp + 2
   float invB;
-  // sort role (workgroups [0, n_sort))
-  int n_sort;
-  int sort_small;
-  SortPlan plan;
-  SortBufs sb;
 };
 
 // Zero ranges of the sort counters, cleared after their last use in a call.
@@ -36,34 +30,28 @@ struct ZeroRanges {
   size_t n[3];
 };
 
-struct UpdArgs {
-  float* E;
+// Dense SGD of a step: reduce the fused kernel's partials in slot order.
+struct DenseArgs {
   float* W1;
   float* b1;
   float* w2;
   float* b2;
   float* loss_out;
-  const float* dzz;
   const float* part;
-  const float* w1snap;
-  const int32_t* sk;  // sorted keys (sorted mode)
-  const int32_t* sv;  // sorted entry ids
-  const int32_t* windows;
-  const int32_t* corrupt;
-  float* seg_part;
-  int32_t* long_list;
-  uint32_t* long_count;
-  uint32_t* flag;
-  ZeroRanges zero;
-  int V, d, win, H, Hp, K, c, B, N;
-  int mode;  // 0 sorted, 1 atomic
-  int ch;    // sorted entries per chunk (one wave)
-  int n_e;   // embedding-role workgroups
-  int n_d;   // dense-role workgroups
-  int n_parts;
-  int part_stride;
-  int seg_stride;
+  int n_parts, part_stride, H, Hp, K;
   float lr, invB;
+};
+
+// One launch with roles: workgroups [0, n_e) update the table (sorted
+// segments or atomics); the rest run the dense SGD (if n_d > 0) and clear
+// the sort counters.
+struct ApplyArgs {
+  SegArgs s;
+  int mode;  // 0 sorted segments, 1 atomic
+  int n_e;
+  int n_d;
+  DenseArgs dn;
+  ZeroRanges zero;
 };
 
 struct ScoreArgs {
@@ -88,40 +76,29 @@ struct GatherArgs {
   int V, d, win, B;
 };
 
-struct ScatArgs {
-  float* table;
-  const int32_t* idx;
-  const float* Y;
-  const int32_t* sk;
-  const int32_t* sv;
-  float* seg_part;
-  int32_t* long_list;
-  uint32_t* long_count;
-  uint32_t* flag;
-  ZeroRanges zero;
-  int rows, d, N;
-  int ch;  // sorted entries per chunk (one wave)
-  int n_e, n_z;
-  int seg_stride;
-  float alpha;
-};
-
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
                               hipStream_t s);
-hipError_t launch_sort_passes_step(const StepKeys& kf, int N, const SortPlan& plan,
-                                   const SortBufs& sb, hipStream_t s);
-hipError_t launch_step_update(const UpdArgs& a, int grid, hipStream_t s);
-hipError_t launch_step_segfix(const UpdArgs& a, hipStream_t s);
+// First sort launch (whole small sort, or pass-0 tile counts) and, for
+// multi-tile plans, every later pass; clears *long_count.
+hipError_t launch_sort_step(const StepKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
+                            uint32_t* long_count, hipStream_t s);
+hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
+                           uint32_t* long_count, hipStream_t s);
+hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, hipStream_t s);
+hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, hipStream_t s);
+hipError_t launch_segfix(const SegArgs& a, int grid, hipStream_t s);
+hipError_t launch_check_idx(const int32_t* idx, int N, int rows, uint32_t* flag, hipStream_t s);
 hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
-hipError_t launch_scatter_sorted(const ScatArgs& a, const SortPlan& plan, const SortBufs& sb,
-                                 hipStream_t s);
-hipError_t launch_scatter_atomic(const ScatArgs& a, hipStream_t s);
+
+// LDS of the fused kernel, in floats: W1 [Hp][K+4], split-K partials
+// [4 waves][3][NT][64] f4, transposed V [3][16][Hp+1], tile ids [16][32].
+__host__ __device__ inline size_t fwdbwd_lds_floats(int Hp, int K) {
+  return (size_t)Hp * (K + 4) + (size_t)kWavesPerBlock * 3 * (Hp / 16) * kWave * 4 +
+         (size_t)3 * kTileRows * (Hp + 1) + (size_t)kTileRows * (kMaxWin + 1);
+}
 
 // Launch-shape constants shared with the host.
-constexpr int kSegfixBlocks = 64;
-constexpr int kFlushGroup = 16;  // completed pieces buffered before their rows are written
-constexpr int kAtomicChunk = 8;  // entries per wave in the atomic embedding update
 constexpr int kDenseSlices = 8;  // lanes that share one element of the dense reduction
 
 }  // namespace pg

@@ -1,42 +1,46 @@
-// Segmented sums over entries sorted by table row (the deterministic form of
-// the advanced-indexing increment of §4.2/§4.3).
+// Segmented row sums over entries sorted by table row: the deterministic
+// form of the advanced-indexing increment of §4.2/§4.3,
+//   table[key(e)] += alpha * sum of Y[e] over the entries e of that key.
+// The training step uses it with Y = the per-entry embedding gradients and
+// alpha = -lr; polyglot_scatter_add with the caller's Y and alpha.
 //
-// The sorted entry list is cut into chunks of `ch` entries (16 or 64), one
-// per wave.  Inside a chunk every maximal run of equal keys ("piece") is
-// summed in entry order.  A piece whose segment lies wholly inside the chunk
-// is applied to its table row by that wave, the row's only writer.  A
-// segment that crosses chunk boundaries (a heavy Zipf row) leaves one partial
-// sum per spanned chunk (slot 1: the open last piece of the chunk where the
-// segment starts; slot 0: the first piece of every later spanned chunk) and
-// its start chunk is appended to a task list; a second launch adds the
-// partials in a fixed order and applies the row.  Sums never depend on
-// scheduling and no row is written twice, without any inter-workgroup wait.
+// The sorted entry list is cut into chunks of CH entries (16 or 64), one per
+// wave.  A wave loads every Y row of its chunk at once (lane = column), and
+// runs one pass of running sums that closes at each piece end (a "piece" is
+// a maximal run of equal keys inside the chunk).  Pieces whose segment lies
+// wholly inside the chunk are added to their table rows by that wave, the
+// rows' only writer; the table rows were loaded together with the Y rows.
+// A segment that crosses chunk boundaries (a heavy Zipf row) leaves one
+// partial per spanned chunk (slot 1: the open last piece of the chunk where
+// it starts; slot 0: the first piece of every later spanned chunk).  Its
+// start chunk goes to a task list and its end chunk is recorded by key; the
+// fix-up launch adds the partials in a fixed order and applies the row.
+// Sums never depend on scheduling, no row is written twice and no wave
+// waits on another workgroup.
 #pragma once
 #include "common.h"
 
 namespace pg {
 
-// Number of consecutive chunks after `chunk` whose first entry has `key`.
-__device__ __forceinline__ int seg_count_fwd(const int32_t* sk, int N, int chunk, int32_t key,
-                                             int ch) {
-  const int lane = lane_id();
-  int m = 0;
-  for (int base = chunk + 1;; base += kWave) {
-    const int y = base + lane;
-    const bool eq = ((size_t)y * ch < (size_t)N) && sk[(size_t)y * ch] == key;
-    const uint64_t b = __ballot(eq);
-    const int run = (~b) ? (__ffsll((unsigned long long)~b) - 1) : kWave;
-    m += run;
-    if (run < kWave) break;
-  }
-  return m;
-}
+struct SegArgs {
+  float* table;             // [rows][d]
+  const float* Y;           // [N][d], row e = entry e
+  const int32_t* sk;        // sorted keys [N]
+  const int32_t* sv;        // entry ids in sorted order [N]
+  float* seg_part;          // [chunks][2][seg_stride]
+  int32_t* long_list;       // start chunks of segments that cross chunks
+  uint32_t* long_count;     // cleared by the sort launch of the same call
+  int32_t* seg_end;         // [rows]: end chunk of a crossing segment, by key
+  const uint32_t* flag;     // sticky error bits: nonzero voids the update
+  int N, d, ch, seg_stride;
+  float alpha;
+};
 
 // Piece structure of one chunk, computed by the whole wave (lanes < ch).
 struct ChunkInfo {
   int i0, nact;
   int32_t key;      // this lane's sorted key (-1 beyond the chunk)
-  int32_t ent;      // this lane's entry id
+  int32_t ent;      // this lane's entry id (0 beyond the chunk)
   uint64_t heads;   // lanes that start a piece
   bool cont_first;  // the first piece continues a segment from the previous chunk
   bool open_last;   // the last piece continues into the next chunk
@@ -63,15 +67,118 @@ __device__ __forceinline__ ChunkInfo chunk_info(const int32_t* __restrict__ sk,
   return ci;
 }
 
-// End (exclusive) of the piece starting at p0.
-__device__ __forceinline__ int piece_end(const ChunkInfo& ci, int p0) {
-  const uint64_t rest = ci.heads & ~((2ull << p0) - 1ull);
-  const int p1 = rest ? (__ffsll((unsigned long long)rest) - 1) : ci.nact;
-  return p1 > ci.nact ? ci.nact : p1;
-}
-
 // Chunk size of a sorted list of N entries: short chunks spread small
 // batches over more waves; long chunks keep partials few for large ones.
 __host__ __device__ inline int seg_chunk_size(int N) { return N <= 131072 ? 16 : 64; }
+
+// One wave applies chunk `chunk` of the sorted list (see the file comment).
+template <int CH>
+__device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
+  const int lane = lane_id();
+  const ChunkInfo ci = chunk_info(a.sk, a.sv, a.N, chunk, CH);
+  const int nact = ci.nact;
+  const uint64_t act = nact >= 64 ? ~0ull : ((1ull << nact) - 1ull);
+  // piece ends: the lane before every later head, and the last active lane
+  const uint64_t tails = ((ci.heads >> 1) | (1ull << (nact - 1))) & act;
+  const int first_tail = __ffsll((unsigned long long)tails) - 1;
+  const bool single = first_tail == nact - 1;  // the chunk is one piece
+  uint64_t complete = tails;
+  if (ci.cont_first) complete &= ~(1ull << first_tail);
+  if (ci.open_last) complete &= ~(1ull << (nact - 1));
+  const bool starts_long = ci.open_last && !(ci.cont_first && single);
+  const bool ends_long = ci.cont_first && !(ci.open_last && single);
+  if (lane == 0) {
+    if (starts_long) a.long_list[atomicAdd(a.long_count, 1u)] = chunk;
+    if (ends_long) a.seg_end[ci.key] = chunk;  // lane 0 holds the first piece's key
+  }
+
+  for (int c0 = 0; c0 < a.d; c0 += kWave) {
+    const int col = c0 + lane;
+    const bool cok = col < a.d;
+    // every Y row and every completed piece's table row, all in flight
+    float v[CH], t[CH];
+#pragma unroll
+    for (int r = 0; r < CH; ++r) {
+      const int ent = __builtin_amdgcn_readlane(ci.ent, r);
+      v[r] = (r < nact && cok) ? a.Y[(size_t)ent * a.d + col] : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < CH; ++r) {
+      const int32_t key = __builtin_amdgcn_readlane(ci.key, r);
+      t[r] = (((complete >> r) & 1ull) && cok) ? a.table[(size_t)key * a.d + col] : 0.f;
+    }
+    // running sum in entry order, closed at every piece end
+    float acc = 0.f, first_sum = 0.f, last_sum = 0.f;
+#pragma unroll
+    for (int r = 0; r < CH; ++r) {
+      acc += v[r];
+      const bool tail = (tails >> r) & 1ull;
+      if (r == first_tail) first_sum = acc;
+      if (r == nact - 1) last_sum = acc;
+      v[r] = tail ? acc : v[r];
+      acc = tail ? 0.f : acc;
+    }
+#pragma unroll
+    for (int r = 0; r < CH; ++r) {
+      const int32_t key = __builtin_amdgcn_readlane(ci.key, r);
+      if (((complete >> r) & 1ull) && cok) a.table[(size_t)key * a.d + col] = t[r] + a.alpha * v[r];
+    }
+    if (cok) {
+      if (ci.cont_first) a.seg_part[((size_t)chunk * 2 + 0) * a.seg_stride + col] = first_sum;
+      if (starts_long) a.seg_part[((size_t)chunk * 2 + 1) * a.seg_stride + col] = last_sum;
+    }
+  }
+}
+
+// Threads of the fix-up workgroup: one workgroup per crossing segment.
+constexpr int kSegfixThreads = 512;
+constexpr int kSegfixWaves = kSegfixThreads / kWave;
+constexpr int kSegfixUnroll = 16;
+
+// Adds the partials of crossing segment li and applies its row.  Lane group
+// gq = lane/16 of wave w takes partials i = G*u + 4*w + gq, G = 4 * waves (i = 0 is
+// the open piece of the start chunk, i >= 1 the first piece of chunk cs+i),
+// each lane four consecutive columns; group sums are combined by a fixed
+// butterfly and the wave sums in wave order, so the result is independent
+// of scheduling.
+__device__ void seg_fix_row(const SegArgs& a, int li, float* red /* [waves][kMaxD] */) {
+  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  const int q = lane & 15, gq = lane >> 4;
+  const int cs = a.long_list[li];
+  const int32_t key = a.sk[(size_t)cs * a.ch + a.ch - 1];
+  const int m = a.seg_end[key] - cs + 1;  // partials of this segment
+  constexpr int G = kSegfixWaves * 4;     // lane groups per workgroup
+  for (int c0 = 0; c0 < a.d; c0 += 64) {
+    const int col = c0 + 4 * q;
+    const bool cok = col < a.d;
+    f4 acc = kZero4;
+    for (int base = 0; base < m; base += G * kSegfixUnroll) {
+      f4 x[kSegfixUnroll];
+#pragma unroll
+      for (int u = 0; u < kSegfixUnroll; ++u) {
+        const int i = base + u * G + w * 4 + gq;
+        const size_t slot = i == 0 ? (size_t)cs * 2 + 1 : (size_t)(cs + i) * 2;
+        x[u] = (i < m && cok) ? ld4(a.seg_part + slot * a.seg_stride + col) : kZero4;
+      }
+#pragma unroll
+      for (int u = 0; u < kSegfixUnroll; ++u) acc += x[u];
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      acc[k] += __shfl_xor(acc[k], 16);
+      acc[k] += __shfl_xor(acc[k], 32);
+    }
+    __syncthreads();  // red of the previous column block is no longer read
+    if (gq == 0) st4(red + w * kMaxD + 4 * q, acc);
+    __syncthreads();
+    if (w == 0 && gq == 0 && cok) {
+      f4 s = ld4(red + 4 * q);
+#pragma unroll
+      for (int v = 1; v < kSegfixWaves; ++v) s += ld4(red + v * kMaxD + 4 * q);
+      float* tr = a.table + (size_t)key * a.d + col;
+      st4(tr, ld4(tr) + a.alpha * s);
+    }
+  }
+}
 
 }  // namespace pg

@@ -66,8 +66,9 @@ __device__ __forceinline__ void load_keys(const KeyFn& kf, int N, int e0, int st
   if (bad) atomicOr(flag, kFlagBadId);
 }
 
-// Exclusive scan over `n` (<= 2*kBlock) values in LDS `v`, in place, by one
-// workgroup of kBlock threads.
+// Exclusive scan over `n` (<= 2*NTH) values in LDS `v`, in place, by one
+// workgroup of NTH threads.
+template <int NTH = kBlock>
 __device__ inline void block_exclusive_scan(uint32_t* v, int n, uint32_t* wave_sums) {
   const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
   const uint32_t a = (2 * t < n) ? v[2 * t] : 0u;
@@ -117,21 +118,25 @@ __device__ __forceinline__ void wave_rank(const uint32_t (&dg)[R], const uint64_
 }
 
 // ------------------------------------------------------------------ small sort
+// One workgroup of kSmallSortThreads sorts the whole list in LDS.
 // LDS words: 2*kSmallSortN (ping-pong) + kSmallSortN/2 (16-bit ranks) +
-// kWavesPerBlock*kMaxBins + 16.
+// waves*kMaxBins + 16.
+constexpr int kSmallSortThreads = 1024;
+constexpr int kSmallSortWaves = kSmallSortThreads / kWave;
 constexpr int kSmallSortLdsWords =
-    2 * kSmallSortN + kSmallSortN / 2 + kWavesPerBlock * kMaxBins + 16;
+    2 * kSmallSortN + kSmallSortN / 2 + kSmallSortWaves * kMaxBins + 16;
 constexpr int kRankBatch = 8;  // rounds ranked per batch (registers bounded)
 
 template <class KeyFn>
 __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t* out_keys,
                            int32_t* out_vals, uint32_t* flag, uint32_t* lds) {
   constexpr int R = kRankBatch;
+  constexpr int NTH = kSmallSortThreads, NW = kSmallSortWaves;
   uint32_t* bufA = lds;
   uint32_t* bufB = bufA + kSmallSortN;
   uint16_t* rank16 = reinterpret_cast<uint16_t*>(bufB + kSmallSortN);
   uint32_t* hist = bufB + kSmallSortN + kSmallSortN / 2;  // [waves][kMaxBins]
-  uint32_t* misc = hist + kWavesPerBlock * kMaxBins;       // wave sums
+  uint32_t* misc = hist + NW * kMaxBins;                  // wave sums
   uint32_t* myhist = hist + (threadIdx.x / kWave) * kMaxBins;
   const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
   const int vb = plan.val_bits;
@@ -139,17 +144,17 @@ __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t
 
   // keys, loaded in batches so that their global loads overlap
   constexpr int U = 8;
-  for (int e0 = 0; e0 < N; e0 += kBlock * U) {
+  for (int e0 = 0; e0 < N; e0 += NTH * U) {
     uint32_t kk[U];
-    load_keys<U>(kf, N, e0 + t, kBlock, kk, flag);
+    load_keys<U>(kf, N, e0 + t, NTH, kk, flag);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int e = e0 + u * kBlock + t;
+      const int e = e0 + u * NTH + t;
       if (e < N) bufA[e] = (kk[u] << vb) | (uint32_t)e;
     }
   }
   // wave w owns entries [w*per, (w+1)*per) in input order, per a multiple of 64
-  const int per = ceil_div(ceil_div(N, kWavesPerBlock), kWave) * kWave;
+  const int per = ceil_div(ceil_div(N, NW), kWave) * kWave;
   const int beg = w * per;
   const int nr = max(0, min(per, N - beg) + kWave - 1) / kWave;
   __syncthreads();
@@ -179,9 +184,9 @@ __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t
     }
     __syncthreads();
     // per-digit totals -> digit starts; per-wave offsets
-    for (int d = t; d < bins; d += kBlock) {
+    for (int d = t; d < bins; d += NTH) {
       uint32_t s = 0;
-      for (int q = 0; q < kWavesPerBlock; ++q) {
+      for (int q = 0; q < NW; ++q) {
         const uint32_t c = hist[q * kMaxBins + d];
         hist[q * kMaxBins + d] = s;  // exclusive over waves
         s += c;
@@ -189,10 +194,10 @@ __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t
       dst[d] = s;  // dst is free until the scatter below: digit totals
     }
     __syncthreads();
-    block_exclusive_scan(dst, bins, misc);
-    for (int d = t; d < bins; d += kBlock) {
+    block_exclusive_scan<NTH>(dst, bins, misc);
+    for (int d = t; d < bins; d += NTH) {
       const uint32_t start = dst[d];
-      for (int q = 0; q < kWavesPerBlock; ++q) hist[q * kMaxBins + d] += start;
+      for (int q = 0; q < NW; ++q) hist[q * kMaxBins + d] += start;
     }
     __syncthreads();
     for (int r0 = 0; r0 < nr; r0 += R) {
@@ -218,7 +223,7 @@ __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t
     src = dst;
     dst = tmp;
   }
-  for (int e = t; e < N; e += kBlock) {
+  for (int e = t; e < N; e += NTH) {
     const uint32_t word = src[e];
     out_keys[e] = (int32_t)(word >> vb);
     out_vals[e] = (int32_t)(word & vmask);

@@ -214,6 +214,29 @@ def test_ragged_and_single_window_batches(B):
     run_both(w, 5, B, 0, lr=0.5)
 
 
+# Shapes that reach the other kernel variants: hidden widths padded to 16,
+# 32 and 64, K-chunks per wave up to 8, window 1 (the centre is the whole
+# window) and the widest window.
+OTHER_SHAPES = [
+    workloads.Workload("w7_d32_h20", V=5000, d=32, win=7, H=20, B=300, lr=0.05, steps=4,
+                       zipf_s=1.0, seed=11),
+    workloads.Workload("w5_d64_h64", V=3000, d=64, win=5, H=64, B=200, lr=0.05, steps=3,
+                       zipf_s=1.1, seed=12),
+    workloads.Workload("w3_d128_h48", V=2000, d=128, win=3, H=48, B=150, lr=0.05, steps=3,
+                       zipf_s=1.0, seed=13),
+    workloads.Workload("w1_d16_h1", V=500, d=16, win=1, H=1, B=50, lr=0.5, steps=5,
+                       zipf_s=1.0, seed=14),
+    workloads.Workload("w31_d16_h8", V=800, d=16, win=31, H=8, B=70, lr=0.1, steps=3,
+                       zipf_s=1.0, seed=15),
+]
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("w", OTHER_SHAPES, ids=[w.name for w in OTHER_SHAPES])
+def test_other_shapes(w, mode):
+    run_both(w, w.steps, w.B, mode)
+
+
 @pytest.mark.parametrize("name,B", [("tiny", 32), ("poly256", 256), ("poly256", 4096)])
 def test_touched_rows_bit_exact(name, B):
     w = PRESETS[name]
