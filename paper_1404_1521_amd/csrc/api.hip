@@ -36,10 +36,13 @@ struct GraphKey {
 struct polyglot_ctx {
   polyglot_config cfg{};
   hipStream_t stream = nullptr;
-  // the step's sort depends only on the ids: it runs on a second stream,
-  // forked from and joined back into `stream` around the fused kernel
+  // a step's sort depends only on its ids: it runs on a second stream,
+  // forked from `stream` and joined back before the table update.  In a
+  // multi-step call the sort of step s+1 (sort set (s+1)&1) runs while step s
+  // computes.
   hipStream_t side = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_sorted[2] = {nullptr, nullptr},
+             ev_done[2] = {nullptr, nullptr};
   int device = 0;
   int Hp = 0, NT = 0, K = 0, c = 0, cpw = 0;
   int max_entries = 0, max_tiles = 0, max_groups = 0, max_parts = 0, max_chunks = 0;
@@ -48,7 +51,7 @@ struct polyglot_ctx {
   std::vector<void*> allocs;
   std::string err;
   bool have_sorted = false;
-  int last_N = 0, last_passes = 0;
+  int last_N = 0, last_passes = 0, last_set = 0;
   hipGraphExec_t gexec = nullptr;
   GraphKey gkey{};
   bool gvalid = false;
@@ -95,15 +98,15 @@ SortPlan make_plan(int key_range, int N) {
   return pl;
 }
 
-SortBufs sort_bufs(polyglot_ctx* ctx) {
+SortBufs sort_bufs(polyglot_ctx* ctx, int set) {
   SortBufs sb{};
-  sb.keys[0] = ctx->ws.keys[0];
-  sb.keys[1] = ctx->ws.keys[1];
-  sb.vals[0] = ctx->ws.vals[0];
-  sb.vals[1] = ctx->ws.vals[1];
-  sb.totals = ctx->ws.totals;
+  sb.keys[0] = ctx->ws.keys[2 * set];
+  sb.keys[1] = ctx->ws.keys[2 * set + 1];
+  sb.vals[0] = ctx->ws.vals[2 * set];
+  sb.vals[1] = ctx->ws.vals[2 * set + 1];
+  sb.totals = ctx->ws.totals[set];
   sb.counts = ctx->ws.counts;
-  sb.gcounts = ctx->ws.gcounts;
+  sb.gcounts = ctx->ws.gcounts[set];
   sb.max_tiles = ctx->max_tiles;
   sb.max_groups = ctx->max_groups;
   sb.flag = ctx->ws.flag;
@@ -112,12 +115,12 @@ SortBufs sort_bufs(polyglot_ctx* ctx) {
 
 // Counters a multi-tile sort accumulates atomically (per-tile counts are
 // overwritten by every sort and need no clearing).
-ZeroRanges sort_zero_ranges(polyglot_ctx* ctx, const SortPlan& plan) {
+ZeroRanges sort_zero_ranges(polyglot_ctx* ctx, const SortPlan& plan, int set) {
   ZeroRanges z{};
   if (plan.small) return z;
-  z.p[0] = ctx->ws.totals;
+  z.p[0] = ctx->ws.totals[set];
   z.n[0] = (size_t)kMaxPasses * kMaxBins;
-  z.p[2] = ctx->ws.gcounts;
+  z.p[2] = ctx->ws.gcounts[set];
   z.n[2] = (size_t)plan.passes * kMaxBins * ctx->max_groups;
   return z;
 }
@@ -143,10 +146,12 @@ void free_all(polyglot_ctx* ctx) {
   ctx->ev_pool.clear();
   if (ctx->gexec) hipGraphExecDestroy(ctx->gexec);
   ctx->gexec = nullptr;
-  if (ctx->ev_fork) hipEventDestroy(ctx->ev_fork);
-  if (ctx->ev_join) hipEventDestroy(ctx->ev_join);
+  for (hipEvent_t* ev : {&ctx->ev_fork, &ctx->ev_sorted[0], &ctx->ev_sorted[1], &ctx->ev_done[0],
+                         &ctx->ev_done[1]}) {
+    if (*ev) hipEventDestroy(*ev);
+    *ev = nullptr;
+  }
   if (ctx->side) hipStreamDestroy(ctx->side);
-  ctx->ev_fork = ctx->ev_join = nullptr;
   ctx->side = nullptr;
   for (void* q : ctx->allocs) hipFree(q);
   ctx->allocs.clear();
@@ -188,13 +193,13 @@ struct KernelTimer {
   }
 };
 
-SegArgs seg_args(polyglot_ctx* ctx, float* table, const float* Y, const SortPlan& plan, int N,
-                 int d, float alpha) {
+SegArgs seg_args(polyglot_ctx* ctx, float* table, const float* Y, const SortPlan& plan, int set,
+                 int N, int d, float alpha) {
   SegArgs a{};
   a.table = table;
   a.Y = Y;
-  a.sk = ctx->ws.keys[plan.passes & 1];
-  a.sv = ctx->ws.vals[plan.passes & 1];
+  a.sk = ctx->ws.keys[2 * set + (plan.passes & 1)];
+  a.sv = ctx->ws.vals[2 * set + (plan.passes & 1)];
   a.seg_part = ctx->ws.seg_part;
   a.long_list = ctx->ws.long_list;
   a.long_count = ctx->ws.long_count;
@@ -219,27 +224,28 @@ int segfix_workgroups(const SegArgs& s) {
   return std::max(1, std::min(ceil_div(s.N, s.ch), 2048));
 }
 
-// Enqueues one training step.  Arguments are already validated.
-int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
-                 const int32_t* windows, const int32_t* corrupt, int B, float lr,
-                 float* loss_dev) {
+// The sort of one step's entries into sort set `set`, on the side stream.
+hipError_t enqueue_sort(polyglot_ctx* ctx, const int32_t* windows, const int32_t* corrupt, int B,
+                        int set) {
+  const polyglot_config& cf = ctx->cfg;
+  const int N = B * (cf.win + 1);
+  const StepKeys kf{windows, corrupt, cf.win, cf.V};
+  KernelTimer kt(ctx, POLYGLOT_K_SORT, ctx->side);
+  return launch_sort_step(kf, N, make_plan(cf.V, N), sort_bufs(ctx, set), nullptr, ctx->side);
+}
+
+// The fused kernel, then (after `sorted_ev`, if any) the table update and
+// the long-segment fix-up of one step, on the main stream; sorted mode reads
+// sort set `set`.
+int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
+                    const int32_t* windows, const int32_t* corrupt, int B, float lr,
+                    float* loss_dev, int set, hipEvent_t sorted_ev) {
   const polyglot_config& cf = ctx->cfg;
   const int N = B * (cf.win + 1);
   const bool sorted = cf.scatter_mode == POLYGLOT_SCATTER_SORTED;
   const SortPlan plan = make_plan(cf.V, N);
   const StepKeys kf{windows, corrupt, cf.win, cf.V};
   hipError_t e = hipSuccess;
-
-  if (sorted) {  // sort on the side stream, concurrent with the fused kernel
-    e = hipEventRecord(ctx->ev_fork, ctx->stream);
-    if (e == hipSuccess) e = hipStreamWaitEvent(ctx->side, ctx->ev_fork, 0);
-    if (e == hipSuccess) {
-      KernelTimer kt(ctx, POLYGLOT_K_SORT, ctx->side);
-      e = launch_sort_step(kf, N, plan, sort_bufs(ctx), ctx->ws.long_count, ctx->side);
-    }
-    if (e == hipSuccess) e = hipEventRecord(ctx->ev_join, ctx->side);
-    if (e != hipSuccess) return hip_fail(ctx, e, "sort launch");
-  }
 
   FwdArgs fa{};
   fa.E = E;
@@ -251,6 +257,7 @@ int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, f
   fa.corrupt = corrupt;
   fa.G = ctx->ws.G;
   fa.part = ctx->ws.part;
+  fa.long_count = ctx->ws.long_count;
   fa.flag = ctx->ws.flag;
   fa.V = cf.V;
   fa.d = cf.d;
@@ -271,13 +278,13 @@ int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, f
                            ctx->stream);
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "fwd/bwd launch");
-  if (sorted) {
-    e = hipStreamWaitEvent(ctx->stream, ctx->ev_join, 0);
+  if (sorted_ev) {
+    e = hipStreamWaitEvent(ctx->stream, sorted_ev, 0);
     if (e != hipSuccess) return hip_fail(ctx, e, "sort join");
   }
 
   ApplyArgs aa{};
-  aa.s = seg_args(ctx, E, ctx->ws.G, plan, N, cf.d, -lr);
+  aa.s = seg_args(ctx, E, ctx->ws.G, plan, set, N, cf.d, -lr);
   aa.mode = sorted ? 0 : 1;
   aa.n_e = table_workgroups(aa.s, aa.mode);
   aa.n_d = ceil_div(ctx->part_stride * kDenseSlices, kBlock);
@@ -294,7 +301,7 @@ int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, f
   aa.dn.K = ctx->K;
   aa.dn.lr = lr;
   aa.dn.invB = 1.0f / (float)B;
-  if (sorted) aa.zero = sort_zero_ranges(ctx, plan);
+  if (sorted) aa.zero = sort_zero_ranges(ctx, plan, set);  // counters of this set, now read
   {
     KernelTimer kt(ctx, POLYGLOT_K_UPDATE);
     e = launch_apply_step(aa, kf, aa.n_e + aa.n_d, ctx->stream);
@@ -308,6 +315,47 @@ int enqueue_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, f
   ctx->have_sorted = sorted;
   ctx->last_N = N;
   ctx->last_passes = plan.passes;
+  ctx->last_set = set;
+  return POLYGLOT_OK;
+}
+
+// Enqueues S consecutive steps (arguments already validated), step s using
+// windows + s*B*win and corrupt + s*B.  Sorted mode: the sort of step s+1
+// runs on the side stream while step s computes; it waits for step s-1,
+// the last reader of the same sort set.
+int enqueue_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
+                  const int32_t* windows, const int32_t* corrupt, int S, int B, float lr,
+                  float* losses_dev) {
+  const bool sorted = ctx->cfg.scatter_mode == POLYGLOT_SCATTER_SORTED;
+  const size_t wstride = (size_t)B * ctx->cfg.win;
+  hipError_t e = hipSuccess;
+  if (sorted) {
+    e = hipEventRecord(ctx->ev_fork, ctx->stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(ctx->side, ctx->ev_fork, 0);
+    if (e == hipSuccess) e = enqueue_sort(ctx, windows, corrupt, B, 0);
+    if (e == hipSuccess) e = hipEventRecord(ctx->ev_sorted[0], ctx->side);
+    if (e != hipSuccess) return hip_fail(ctx, e, "sort launch");
+  }
+  for (int s = 0; s < S; ++s) {
+    const int q = s & 1;
+    if (sorted && s + 1 < S) {
+      if (s >= 1) e = hipStreamWaitEvent(ctx->side, ctx->ev_done[1 - q], 0);
+      if (e == hipSuccess)
+        e = enqueue_sort(ctx, windows + (s + 1) * wstride, corrupt + (size_t)(s + 1) * B, B,
+                         1 - q);
+      if (e == hipSuccess) e = hipEventRecord(ctx->ev_sorted[1 - q], ctx->side);
+      if (e != hipSuccess) return hip_fail(ctx, e, "sort launch");
+    }
+    const int r = enqueue_compute(ctx, E, W1, b1, w2, b2, windows + s * wstride,
+                                  corrupt + (size_t)s * B, B, lr,
+                                  losses_dev ? losses_dev + s : nullptr, q,
+                                  sorted ? ctx->ev_sorted[q] : nullptr);
+    if (r) return r;
+    if (sorted) {
+      e = hipEventRecord(ctx->ev_done[q], ctx->stream);
+      if (e != hipSuccess) return hip_fail(ctx, e, "step event");
+    }
+  }
   return POLYGLOT_OK;
 }
 
@@ -369,13 +417,15 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   const size_t me = (size_t)ctx->max_entries;
   const size_t ncount = (size_t)kMaxPasses * kMaxBins * ctx->max_tiles;
   const size_t ngcount = (size_t)kMaxPasses * kMaxBins * ctx->max_groups;
-  if (e == hipSuccess) e = alloc(ctx, &ws.keys[0], me);
-  if (e == hipSuccess) e = alloc(ctx, &ws.keys[1], me);
-  if (e == hipSuccess) e = alloc(ctx, &ws.vals[0], me);
-  if (e == hipSuccess) e = alloc(ctx, &ws.vals[1], me);
-  if (e == hipSuccess) e = alloc(ctx, &ws.totals, (size_t)kMaxPasses * kMaxBins);
+  for (int k = 0; k < 4; ++k) {
+    if (e == hipSuccess) e = alloc(ctx, &ws.keys[k], me);
+    if (e == hipSuccess) e = alloc(ctx, &ws.vals[k], me);
+  }
+  for (int k = 0; k < 2; ++k) {
+    if (e == hipSuccess) e = alloc(ctx, &ws.totals[k], (size_t)kMaxPasses * kMaxBins);
+    if (e == hipSuccess) e = alloc(ctx, &ws.gcounts[k], ngcount);
+  }
   if (e == hipSuccess) e = alloc(ctx, &ws.counts, ncount);
-  if (e == hipSuccess) e = alloc(ctx, &ws.gcounts, ngcount);
   if (e == hipSuccess) e = alloc(ctx, &ws.G, (size_t)c.max_batch * (c.win + 1) * c.d);
   if (e == hipSuccess) e = alloc(ctx, &ws.part, (size_t)ctx->max_parts * ctx->part_stride);
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_end, (size_t)std::max(c.V, c.max_rows));
@@ -384,14 +434,18 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   if (e == hipSuccess) e = alloc(ctx, &ws.long_count, 1);
   if (e == hipSuccess) e = alloc(ctx, &ws.flag, 1);
   if (e == hipSuccess) e = alloc(ctx, &ws.scratch_loss, 1);
-  if (e == hipSuccess) e = hipMemset(ws.totals, 0, sizeof(uint32_t) * kMaxPasses * kMaxBins);
+  for (int k = 0; k < 2; ++k) {
+    if (e == hipSuccess)
+      e = hipMemset(ws.totals[k], 0, sizeof(uint32_t) * kMaxPasses * kMaxBins);
+    if (e == hipSuccess) e = hipMemset(ws.gcounts[k], 0, sizeof(uint32_t) * ngcount);
+  }
   if (e == hipSuccess) e = hipMemset(ws.counts, 0, sizeof(uint32_t) * ncount);
-  if (e == hipSuccess) e = hipMemset(ws.gcounts, 0, sizeof(uint32_t) * ngcount);
   if (e == hipSuccess) e = hipMemset(ws.long_count, 0, sizeof(uint32_t));
   if (e == hipSuccess) e = hipMemset(ws.flag, 0, sizeof(uint32_t));
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&ctx->ev_fork, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&ctx->ev_join, hipEventDisableTiming);
+  for (hipEvent_t* ev : {&ctx->ev_fork, &ctx->ev_sorted[0], &ctx->ev_sorted[1], &ctx->ev_done[0],
+                         &ctx->ev_done[1]})
+    if (e == hipSuccess) e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     free_all(ctx);
@@ -423,7 +477,7 @@ int polyglot_train_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float
   if (!ctx) return POLYGLOT_ENULL;
   const int rc = check_step_args(ctx, E, W1, b1, w2, b2, windows, corrupt, B, lr);
   if (rc) return rc;
-  return enqueue_step(ctx, E, W1, b1, w2, b2, windows, corrupt, B, lr, loss_dev);
+  return enqueue_steps(ctx, E, W1, b1, w2, b2, windows, corrupt, 1, B, lr, loss_dev);
 }
 
 int polyglot_train_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2,
@@ -433,15 +487,8 @@ int polyglot_train_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, floa
   if (S <= 0) return fail(ctx, POLYGLOT_EBATCH, "train_steps: S must be >= 1");
   const int rc = check_step_args(ctx, E, W1, b1, w2, b2, windows, corrupt, B, lr);
   if (rc) return rc;
-  const size_t wstride = (size_t)B * ctx->cfg.win;
   auto enqueue_all = [&]() -> int {
-    for (int s = 0; s < S; ++s) {
-      const int r = enqueue_step(ctx, E, W1, b1, w2, b2, windows + s * wstride,
-                                 corrupt + (size_t)s * B, B, lr,
-                                 losses_dev ? losses_dev + s : nullptr);
-      if (r) return r;
-    }
-    return POLYGLOT_OK;
+    return enqueue_steps(ctx, E, W1, b1, w2, b2, windows, corrupt, S, B, lr, losses_dev);
   };
   if (ctx->stream == nullptr) return enqueue_all();  // the legacy stream cannot be captured
 
@@ -474,6 +521,7 @@ int polyglot_train_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, floa
   ctx->have_sorted = ctx->cfg.scatter_mode == POLYGLOT_SCATTER_SORTED;
   ctx->last_N = N;
   ctx->last_passes = make_plan(ctx->cfg.V, N).passes;
+  ctx->last_set = (S - 1) & 1;
   return POLYGLOT_OK;
 }
 
@@ -529,7 +577,7 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
   const SortPlan plan = make_plan(rows, N);
   const IdxKeys kf{idx, rows};
   ApplyArgs aa{};
-  aa.s = seg_args(ctx, table, Y, plan, N, d, alpha);
+  aa.s = seg_args(ctx, table, Y, plan, 0, N, d, alpha);
   aa.mode = mode == POLYGLOT_SCATTER_SORTED ? 0 : 1;
   aa.n_e = table_workgroups(aa.s, aa.mode);
   aa.n_d = 0;
@@ -537,9 +585,9 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
   KernelTimer kt(ctx, POLYGLOT_K_SCATTER);
   if (aa.mode == 0) {
     // the sort validates the indices (sticky flag) and clears the task list
-    aa.zero = sort_zero_ranges(ctx, plan);
+    aa.zero = sort_zero_ranges(ctx, plan, 0);
     const int n_z = plan.small ? 0 : 16;
-    e = launch_sort_idx(kf, N, plan, sort_bufs(ctx), ctx->ws.long_count, ctx->stream);
+    e = launch_sort_idx(kf, N, plan, sort_bufs(ctx, 0), ctx->ws.long_count, ctx->stream);
     if (e == hipSuccess) e = launch_apply_idx(aa, kf, aa.n_e + n_z, ctx->stream);
     if (e == hipSuccess) e = launch_segfix(aa.s, segfix_workgroups(aa.s), ctx->stream);
   } else {
@@ -556,7 +604,8 @@ int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int
   hipError_t e = hipStreamSynchronize(ctx->stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "touched_rows: sync");
   std::vector<int32_t> keys(ctx->last_N);
-  e = hipMemcpy(keys.data(), ctx->ws.keys[ctx->last_passes & 1], sizeof(int32_t) * ctx->last_N,
+  e = hipMemcpy(keys.data(), ctx->ws.keys[2 * ctx->last_set + (ctx->last_passes & 1)],
+                sizeof(int32_t) * ctx->last_N,
                 hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(ctx, e, "touched_rows: copy");
   int32_t n = 0;

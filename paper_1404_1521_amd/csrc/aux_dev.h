@@ -11,7 +11,8 @@ namespace pg {
 template <int NT, int CPW>
 __global__ __launch_bounds__(kBlock) void k_score(ScoreArgs a) {
   extern __shared__ uint32_t lds[];
-  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const int n16 = lane & 15, g = lane >> 4;
   const int dq = a.d / 16, nchunk = a.K / 16;
   int32_t* ids = reinterpret_cast<int32_t*>(lds);                  // [16][win]
@@ -69,7 +70,7 @@ __global__ __launch_bounds__(kBlock) void k_score(ScoreArgs a) {
     const int n = nt * 16 + n16;
     const float b1v = n < a.H ? a.b1[n] : 0.f, w2v = n < a.H ? a.w2[n] : 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ps[i] += w2v * tanhf(b1v + Z[i]);
+    for (int i = 0; i < 4; ++i) ps[i] += w2v * tanh_fast(b1v + Z[i]);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)

@@ -43,11 +43,14 @@ struct SortPlan {
 // Device workspace owned by a context (all sizes fixed at init).
 struct Workspace {
   // sort
-  int32_t* keys[2];         // ping-pong sorted keys [max_entries]
-  int32_t* vals[2];         // ping-pong entry ids   [max_entries]
-  uint32_t* totals;         // [kMaxPasses][kMaxBins] global digit counts
+  // Two sort sets, so that the sort of the next step can run while the
+  // current step reads its own: set q uses keys/vals[2q] and [2q+1] as
+  // ping-pong buffers and its own accumulated digit counters.
+  int32_t* keys[4];         // sorted keys [max_entries]
+  int32_t* vals[4];         // entry ids   [max_entries]
+  uint32_t* totals[2];      // [kMaxPasses][kMaxBins] global digit counts
   uint32_t* counts;         // [kMaxPasses][kMaxBins][max_tiles] per-tile digit counts
-  uint32_t* gcounts;        // [kMaxPasses][kMaxBins][max_groups] per-16-tile digit counts
+  uint32_t* gcounts[2];     // [kMaxPasses][kMaxBins][max_groups] per-16-tile digit counts
   // step
   float* G;                 // [max_batch*(win+1)][d] per-entry embedding gradients
   float* part;              // [max_parts][part_stride] dense-gradient partials
@@ -84,6 +87,30 @@ __device__ inline uint64_t match_digit(uint32_t digit, int bits, uint64_t active
 
 __device__ inline float readlane_f(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// tanh of the hidden layer, from two identities of the function:
+//  |x| < 0.4   the Maclaurin series of tanh, odd terms through x^13 (the
+//              coefficients are 2^2n (2^2n - 1) B_2n / (2n)!, B the Bernoulli
+//              numbers); the first omitted term is below 2^-27 of tanh(x);
+//  |x| >= 0.4  tanh|x| = 1 - 2 / (1 + e^(2|x|)) with the hardware base-2
+//              exponential and reciprocal (a few ulp; e^(2|x|) overflowing
+//              to infinity gives exactly 1), sign restored.
+// Pre-activations of this model are mostly far below 0.4, where the series
+// has no cancellation.
+__device__ __forceinline__ float tanh_fast(float x) {
+  const float ax = __builtin_fabsf(x);
+  const float x2 = x * x;
+  float p = 21844.f / 6081075.f;
+  p = p * x2 - 1382.f / 155925.f;
+  p = p * x2 + 62.f / 2835.f;
+  p = p * x2 - 17.f / 315.f;
+  p = p * x2 + 2.f / 15.f;
+  p = p * x2 - 1.f / 3.f;
+  const float small = x + x * x2 * p;
+  const float e = __builtin_amdgcn_exp2f(2.8853900817779268f * ax);  // e^(2|x|) = 2^(2|x| log2 e)
+  const float big = 1.f - 2.f * __builtin_amdgcn_rcpf(1.f + e);
+  return ax < 0.4f ? small : __builtin_copysignf(big, x);
 }
 
 __device__ __forceinline__ f4 ld4(const float* p) { return *reinterpret_cast<const f4*>(p); }

@@ -49,22 +49,24 @@ __global__ __launch_bounds__(kBlock, (NT == 1 || (NT == 2 && CPW <= 5)) ? 2 : 1)
 
 // =============================================================== sort
 
-// Whole sort of a small list by one workgroup (clears the segment task list).
+// Whole sort of a small list by one workgroup (clears the segment task list
+// when given one).
 template <class KeyFn>
 __global__ __launch_bounds__(kSmallSortThreads) void k_sort_small(KeyFn kf, int N, SortPlan plan,
                                                                   SortBufs sb,
                                                                   uint32_t* long_count) {
   extern __shared__ uint32_t lds[];
-  if (threadIdx.x == 0) *long_count = 0u;
+  if (long_count && threadIdx.x == 0) *long_count = 0u;
   small_sort(kf, N, plan, sb.keys[plan.passes & 1], sb.vals[plan.passes & 1], sb.flag, lds);
 }
 
-// Pass-0 digit counts of every tile of a large list (clears the task list).
+// Pass-0 digit counts of every tile of a large list (clears the task list
+// when given one).
 template <class KeyFn>
 __global__ __launch_bounds__(kBlock) void k_sort_first(KeyFn kf, int N, SortPlan plan, SortBufs sb,
                                                        uint32_t* long_count) {
   extern __shared__ uint32_t lds[];
-  if (blockIdx.x == 0 && threadIdx.x == 0) *long_count = 0u;
+  if (long_count && blockIdx.x == 0 && threadIdx.x == 0) *long_count = 0u;
   sort_up0_tile(kf, N, plan, sb, blockIdx.x, lds);
 }
 

@@ -16,6 +16,7 @@ struct FwdArgs {
   const int32_t* corrupt;
   float* G;          // [B*(win+1)][d] per-entry embedding gradients
   float* part;       // [workgroups][part_stride] dense partials
+  uint32_t* long_count;  // segment task list of this step, cleared here
   uint32_t* flag;
   int V, d, win, H, Hp, K, c, B;
   int ntiles;        // ceil(B / 16)
@@ -79,7 +80,7 @@ struct GatherArgs {
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
                               hipStream_t s);
 // First sort launch (whole small sort, or pass-0 tile counts) and, for
-// multi-tile plans, every later pass; clears *long_count.
+// multi-tile plans, every later pass; clears *long_count if not NULL.
 hipError_t launch_sort_step(const StepKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
                             uint32_t* long_count, hipStream_t s);
 hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
@@ -92,10 +93,12 @@ hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, hipStream_t s);
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 
 // LDS of the fused kernel, in floats: W1 [Hp][K+4], split-K partials
-// [4 waves][3][NT][64] f4, transposed V [3][16][Hp+1], tile ids [16][32].
+// [4 waves][3][NT][64] f4, V [3][16][Hp+1], per-wave dense sums [4][2Hp+2],
+// two tile id tables [2][16][32].
 __host__ __device__ inline size_t fwdbwd_lds_floats(int Hp, int K) {
   return (size_t)Hp * (K + 4) + (size_t)kWavesPerBlock * 3 * (Hp / 16) * kWave * 4 +
-         (size_t)3 * kTileRows * (Hp + 1) + (size_t)kTileRows * (kMaxWin + 1);
+         (size_t)3 * kTileRows * (Hp + 1) + (size_t)kWavesPerBlock * (2 * Hp + 2) +
+         (size_t)2 * kTileRows * (kMaxWin + 1);
 }
 
 // Launch-shape constants shared with the host.

@@ -142,7 +142,8 @@ constexpr int kSegfixUnroll = 16;
 // butterfly and the wave sums in wave order, so the result is independent
 // of scheduling.
 __device__ void seg_fix_row(const SegArgs& a, int li, float* red /* [waves][kMaxD] */) {
-  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const int q = lane & 15, gq = lane >> 4;
   const int cs = a.long_list[li];
   const int32_t key = a.sk[(size_t)cs * a.ch + a.ch - 1];

@@ -70,7 +70,8 @@ __device__ __forceinline__ void load_keys(const KeyFn& kf, int N, int e0, int st
 // workgroup of NTH threads.
 template <int NTH = kBlock>
 __device__ inline void block_exclusive_scan(uint32_t* v, int n, uint32_t* wave_sums) {
-  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const uint32_t a = (2 * t < n) ? v[2 * t] : 0u;
   const uint32_t b = (2 * t + 1 < n) ? v[2 * t + 1] : 0u;
   const uint32_t s = a + b;
@@ -137,8 +138,9 @@ __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t
   uint16_t* rank16 = reinterpret_cast<uint16_t*>(bufB + kSmallSortN);
   uint32_t* hist = bufB + kSmallSortN + kSmallSortN / 2;  // [waves][kMaxBins]
   uint32_t* misc = hist + NW * kMaxBins;                  // wave sums
-  uint32_t* myhist = hist + (threadIdx.x / kWave) * kMaxBins;
-  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  uint32_t* myhist = hist + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * kMaxBins;
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const int vb = plan.val_bits;
   const uint32_t vmask = (vb >= 32) ? 0xffffffffu : ((1u << vb) - 1u);
 
@@ -320,7 +322,8 @@ __device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, con
   uint32_t* hist = lds;                                  // [waves][kMaxBins]
   uint32_t* dscr = hist + kWavesPerBlock * kMaxBins;     // [kMaxBins]
   uint32_t* misc = dscr + kMaxBins;
-  const int t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   uint32_t* myhist = hist + w * kMaxBins;
   const int bits = plan.bits[p], shift = plan.shift[p], bins = 1 << bits;
   const int32_t* sk = sb.keys[p & 1];

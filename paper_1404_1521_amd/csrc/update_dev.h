@@ -74,7 +74,8 @@ __device__ void dense_sgd(const DenseArgs& a, int gid, int nthreads, bool bad) {
 
 template <int CH, class KeyFn>
 __global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a, KeyFn kf) {
-  const int t = threadIdx.x, w = t / kWave;
+  const int t = threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const bool bad = (*reinterpret_cast<const volatile uint32_t*>(a.s.flag)) != 0u;
   if ((int)blockIdx.x < a.n_e) {
     if (bad) return;  // all-or-nothing: an out-of-range id voids the update

@@ -60,6 +60,8 @@ def _cfg(**kw):
     dict(d=24), dict(d=0), dict(d=272), dict(win=4), dict(win=0), dict(win=33), dict(H=0),
     dict(H=65), dict(V=0), dict(win=9, d=64), dict(scatter_mode=2), dict(max_scatter=-1),
     dict(max_scatter=10, max_rows=0),
+    # W1 (64 x 388 floats) and the tile buffers exceed one workgroup's 160 KiB of LDS
+    dict(H=48, d=128, win=3),
 ])
 def test_init_rejects_bad_config_before_any_device_call(lib, kw):
     import paper_1404_1521_amd as pg

@@ -222,7 +222,7 @@ OTHER_SHAPES = [
                        zipf_s=1.0, seed=11),
     workloads.Workload("w5_d64_h64", V=3000, d=64, win=5, H=64, B=200, lr=0.05, steps=3,
                        zipf_s=1.1, seed=12),
-    workloads.Workload("w3_d128_h48", V=2000, d=128, win=3, H=48, B=150, lr=0.05, steps=3,
+    workloads.Workload("w3_d112_h48", V=2000, d=112, win=3, H=48, B=150, lr=0.05, steps=3,
                        zipf_s=1.0, seed=13),
     workloads.Workload("w1_d16_h1", V=500, d=16, win=1, H=1, B=50, lr=0.5, steps=5,
                        zipf_s=1.0, seed=14),
