@@ -81,20 +81,27 @@ int bits_for(uint32_t n) {  // smallest b >= 1 with n <= 2^b
   return b;
 }
 
+// Radix plan: the small (partitioned) sort ranks the key bits above the
+// partition bits; the multi-tile sort ranks all key bits.
 SortPlan make_plan(int key_range, int N) {
   SortPlan pl{};
   const int kb = bits_for((uint32_t)key_range);
-  pl.passes = (kb + kMaxDigitBits - 1) / kMaxDigitBits;
-  const int base = kb / pl.passes, rem = kb % pl.passes;
-  int sh = 0;
-  for (int p = 0; p < pl.passes; ++p) {
-    pl.bits[p] = base + (p < rem ? 1 : 0);
-    pl.shift[p] = sh;
-    sh += pl.bits[p];
+  pl.val_bits = bits_for((uint32_t)std::max(N, 2));
+  pl.part_bits = std::min(kPartBits, kb);
+  pl.small = (N <= kSmallSortN && (kb - pl.part_bits) + pl.val_bits <= 32) ? 1 : 0;
+  if (!pl.small) pl.part_bits = 0;
+  const int rb = kb - pl.part_bits;  // bits the radix passes rank
+  pl.passes = (rb + kMaxDigitBits - 1) / kMaxDigitBits;
+  if (pl.passes > 0) {
+    const int base = rb / pl.passes, rem = rb % pl.passes;
+    int sh = 0;
+    for (int p = 0; p < pl.passes; ++p) {
+      pl.bits[p] = base + (p < rem ? 1 : 0);
+      pl.shift[p] = sh;
+      sh += pl.bits[p];
+    }
   }
   pl.ntiles = ceil_div(N, kSortTile);
-  pl.val_bits = bits_for((uint32_t)std::max(N, 2));
-  pl.small = (N <= kSmallSortN && kb + pl.val_bits <= 32) ? 1 : 0;
   return pl;
 }
 
@@ -267,15 +274,20 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   fa.K = ctx->K;
   fa.c = ctx->c;
   fa.B = B;
+  fa.N = N;
+  fa.n_sort = (sorted && plan.small) ? (1 << plan.part_bits) : 0;  // the sort as extra workgroups
+  fa.plan = plan;
+  fa.sb = sort_bufs(ctx, set);
   fa.ntiles = ceil_div(B, kTileRows);
   fa.tiles_per_wg = ceil_div(fa.ntiles, ctx->max_parts);
   const int n_fb = ceil_div(fa.ntiles, fa.tiles_per_wg);
   fa.part_stride = ctx->part_stride;
   fa.invB = 1.0f / (float)B;
   {
+    size_t lds = fwdbwd_lds_floats(ctx->Hp, ctx->K) * 4;
+    if (fa.n_sort) lds = std::max(lds, (size_t)kPartSortLdsWords * 4);
     KernelTimer kt(ctx, POLYGLOT_K_FWDBWD);
-    e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, n_fb, fwdbwd_lds_floats(ctx->Hp, ctx->K) * 4,
-                           ctx->stream);
+    e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, fa.n_sort + n_fb, lds, ctx->stream);
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "fwd/bwd launch");
   if (sorted_ev) {
@@ -320,16 +332,18 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
 }
 
 // Enqueues S consecutive steps (arguments already validated), step s using
-// windows + s*B*win and corrupt + s*B.  Sorted mode: the sort of step s+1
-// runs on the side stream while step s computes; it waits for step s-1,
-// the last reader of the same sort set.
+// windows + s*B*win and corrupt + s*B.  Sorted mode, small batches: the sort
+// is part of the fused kernel.  Large batches: the sort of step s+1 runs on
+// the side stream while step s computes; it waits for step s-1, the last
+// reader of the same sort set.
 int enqueue_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
                   const int32_t* windows, const int32_t* corrupt, int S, int B, float lr,
                   float* losses_dev) {
-  const bool sorted = ctx->cfg.scatter_mode == POLYGLOT_SCATTER_SORTED;
+  const bool side_sort = ctx->cfg.scatter_mode == POLYGLOT_SCATTER_SORTED &&
+                      !make_plan(ctx->cfg.V, B * (ctx->cfg.win + 1)).small;  // side-stream sort
   const size_t wstride = (size_t)B * ctx->cfg.win;
   hipError_t e = hipSuccess;
-  if (sorted) {
+  if (side_sort) {
     e = hipEventRecord(ctx->ev_fork, ctx->stream);
     if (e == hipSuccess) e = hipStreamWaitEvent(ctx->side, ctx->ev_fork, 0);
     if (e == hipSuccess) e = enqueue_sort(ctx, windows, corrupt, B, 0);
@@ -338,7 +352,7 @@ int enqueue_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, 
   }
   for (int s = 0; s < S; ++s) {
     const int q = s & 1;
-    if (sorted && s + 1 < S) {
+    if (side_sort && s + 1 < S) {
       if (s >= 1) e = hipStreamWaitEvent(ctx->side, ctx->ev_done[1 - q], 0);
       if (e == hipSuccess)
         e = enqueue_sort(ctx, windows + (s + 1) * wstride, corrupt + (size_t)(s + 1) * B, B,
@@ -349,9 +363,9 @@ int enqueue_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, 
     const int r = enqueue_compute(ctx, E, W1, b1, w2, b2, windows + s * wstride,
                                   corrupt + (size_t)s * B, B, lr,
                                   losses_dev ? losses_dev + s : nullptr, q,
-                                  sorted ? ctx->ev_sorted[q] : nullptr);
+                                  side_sort ? ctx->ev_sorted[q] : nullptr);
     if (r) return r;
-    if (sorted) {
+    if (side_sort) {
       e = hipEventRecord(ctx->ev_done[q], ctx->stream);
       if (e != hipSuccess) return hip_fail(ctx, e, "step event");
     }
@@ -608,12 +622,13 @@ int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int
                 sizeof(int32_t) * ctx->last_N,
                 hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(ctx, e, "touched_rows: copy");
-  int32_t n = 0;
-  for (int i = 0; i < ctx->last_N; ++i) {
-    if (i > 0 && keys[i] == keys[i - 1]) continue;
-    if (ids_host && n < cap) ids_host[n] = keys[i];
-    ++n;
-  }
+  // equal ids are contiguous (grouped) in the sorted order; report them ascending
+  std::vector<int32_t> uniq;
+  for (int i = 0; i < ctx->last_N; ++i)
+    if (i == 0 || keys[i] != keys[i - 1]) uniq.push_back(keys[i]);
+  std::sort(uniq.begin(), uniq.end());
+  const int32_t n = (int32_t)uniq.size();
+  for (int32_t i = 0; ids_host && i < n && i < cap; ++i) ids_host[i] = uniq[i];
   *count = n;
   return POLYGLOT_OK;
 }

@@ -36,8 +36,9 @@ struct SortPlan {
   int shift[kMaxPasses];
   int bits[kMaxPasses];
   int ntiles;               // multi-tile path: tiles of kSortTile keys
-  int small;                // 1: single-workgroup LDS sort
-  int val_bits;             // small path packs (key << val_bits) | entry in 32 bits
+  int small;                // 1: partitioned sort (one launch, 2^part_bits workgroups)
+  int val_bits;             // small path packs (key >> part_bits) << val_bits | entry
+  int part_bits;            // small path: partitions by the low key bits
 };
 
 // Device workspace owned by a context (all sizes fixed at init).

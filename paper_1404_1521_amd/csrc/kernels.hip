@@ -2,11 +2,13 @@
 //
 // One step on the device (sorted mode):
 //
-//   side stream     stable radix sort of the step's (row id, entry) pairs:
-//                   k_sort_small (one 1024-thread workgroup, all passes in
-//                   LDS) or k_sort_first + k_sort_up / k_sort_down passes for
-//                   large batches.  It depends only on the ids, so it runs
-//                   while the fused kernel computes;
+//   sort            the step's (row id, entry) pairs, grouped by row id in
+//                   entry order.  Small batches: a partitioned sort run by
+//                   extra workgroups of the fused kernel below.  Large
+//                   batches: k_sort_first + k_sort_up / k_sort_down radix
+//                   passes on a side stream (they depend only on the ids; in
+//                   a multi-step call the next step's sort runs while the
+//                   current step computes);
 //   k_step_fwdbwd   per 16-window tile: gather the embedding rows straight
 //                   into MFMA operands, z = W1 x + b1 and the corrupted-centre
 //                   z~ (16x16x4 f32 MFMA, split-K over 4 waves), tanh, scores,
@@ -44,20 +46,26 @@ namespace pg {
 template <int NT, int CPW>
 __global__ __launch_bounds__(kBlock, (NT == 1 || (NT == 2 && CPW <= 5)) ? 2 : 1) void k_step_fwdbwd(FwdArgs a) {
   extern __shared__ float lds_f[];
-  fwdbwd_wg<NT, CPW>(a, blockIdx.x, lds_f);
+  if ((int)blockIdx.x < a.n_sort) {  // small batches: the step's sort, partition blockIdx.x
+    const StepKeys kf{a.windows, a.corrupt, a.win, a.V};
+    part_sort(kf, a.N, a.plan, blockIdx.x, a.sb.keys[a.plan.passes & 1],
+              a.sb.vals[a.plan.passes & 1], a.flag, reinterpret_cast<uint32_t*>(lds_f));
+    return;
+  }
+  fwdbwd_wg<NT, CPW>(a, blockIdx.x - a.n_sort, lds_f);
 }
 
 // =============================================================== sort
 
-// Whole sort of a small list by one workgroup (clears the segment task list
-// when given one).
+// Partitioned sort of a small list, partition blockIdx.x (clears the segment
+// task list when given one).
 template <class KeyFn>
-__global__ __launch_bounds__(kSmallSortThreads) void k_sort_small(KeyFn kf, int N, SortPlan plan,
-                                                                  SortBufs sb,
-                                                                  uint32_t* long_count) {
+__global__ __launch_bounds__(kBlock) void k_sort_part(KeyFn kf, int N, SortPlan plan, SortBufs sb,
+                                                      uint32_t* long_count) {
   extern __shared__ uint32_t lds[];
-  if (long_count && threadIdx.x == 0) *long_count = 0u;
-  small_sort(kf, N, plan, sb.keys[plan.passes & 1], sb.vals[plan.passes & 1], sb.flag, lds);
+  if (long_count && blockIdx.x == 0 && threadIdx.x == 0) *long_count = 0u;
+  part_sort(kf, N, plan, blockIdx.x, sb.keys[plan.passes & 1], sb.vals[plan.passes & 1], sb.flag,
+            lds);
 }
 
 // Pass-0 digit counts of every tile of a large list (clears the task list
@@ -86,8 +94,8 @@ template <class KeyFn>
 static void launch_sort(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
                         uint32_t* long_count, hipStream_t s) {
   if (plan.small) {
-    hipLaunchKernelGGL((k_sort_small<KeyFn>), dim3(1), dim3(kSmallSortThreads),
-                       kSmallSortLdsWords * 4, s, kf, N, plan, sb, long_count);
+    hipLaunchKernelGGL((k_sort_part<KeyFn>), dim3(1 << plan.part_bits), dim3(kBlock),
+                       kPartSortLdsWords * 4, s, kf, N, plan, sb, long_count);
     return;
   }
   hipLaunchKernelGGL((k_sort_first<KeyFn>), dim3(plan.ntiles), dim3(kBlock), kUp0LdsWords * 4, s,

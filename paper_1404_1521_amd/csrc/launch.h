@@ -18,7 +18,11 @@ struct FwdArgs {
   float* part;       // [workgroups][part_stride] dense partials
   uint32_t* long_count;  // segment task list of this step, cleared here
   uint32_t* flag;
-  int V, d, win, H, Hp, K, c, B;
+  int V, d, win, H, Hp, K, c, B, N;
+  // sort role: workgroups [0, n_sort) run the partitioned small sort
+  int n_sort;
+  SortPlan plan;
+  SortBufs sb;
   int ntiles;        // ceil(B / 16)
   int tiles_per_wg;  // consecutive tiles per workgroup
   int part_stride;   // floats per dense partial slot: Hp*K + 2*Hp + 2

@@ -7,8 +7,8 @@
 // keep their entry order (stable LSD), which fixes the summation order.
 //
 // Two variants:
-//  * small: one workgroup sorts up to kSmallSortN pairs packed as
-//    (key << val_bits | entry) in LDS, all passes in one launch;
+//  * small (up to kSmallSortN entries): a partitioned sort, one launch of
+//    2^part_bits workgroups (see part_sort below);
 //  * multi-tile: tiles of kSortTile keys.  up0 counts pass-0 digits per tile
 //    and the digit totals of every pass; down(p) ranks each tile stably,
 //    adds the counts of all earlier tiles and scatters; up(p) counts the
@@ -118,53 +118,29 @@ __device__ __forceinline__ void wave_rank(const uint32_t (&dg)[R], const uint64_
   }
 }
 
-// ------------------------------------------------------------------ small sort
-// One workgroup of kSmallSortThreads sorts the whole list in LDS.
-// LDS words: 2*kSmallSortN (ping-pong) + kSmallSortN/2 (16-bit ranks) +
-// waves*kMaxBins + 16.
-constexpr int kSmallSortThreads = 1024;
-constexpr int kSmallSortWaves = kSmallSortThreads / kWave;
-constexpr int kSmallSortLdsWords =
-    2 * kSmallSortN + kSmallSortN / 2 + kSmallSortWaves * kMaxBins + 16;
+// ------------------------------------------------------- LDS radix passes
 constexpr int kRankBatch = 8;  // rounds ranked per batch (registers bounded)
 
-template <class KeyFn>
-__device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t* out_keys,
-                           int32_t* out_vals, uint32_t* flag, uint32_t* lds) {
-  constexpr int R = kRankBatch;
-  constexpr int NTH = kSmallSortThreads, NW = kSmallSortWaves;
-  uint32_t* bufA = lds;
-  uint32_t* bufB = bufA + kSmallSortN;
-  uint16_t* rank16 = reinterpret_cast<uint16_t*>(bufB + kSmallSortN);
-  uint32_t* hist = bufB + kSmallSortN + kSmallSortN / 2;  // [waves][kMaxBins]
-  uint32_t* misc = hist + NW * kMaxBins;                  // wave sums
-  uint32_t* myhist = hist + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * kMaxBins;
+// Stable LSD radix passes of one workgroup (NTH threads) over M <= kSmallSortN
+// packed words in LDS, ping-pong between src and dst.  The digit of pass p
+// is (word >> (shift0 + plan.shift[p])) & (2^plan.bits[p] - 1).  Wave w
+// ranks a contiguous run of the words (wave_rank), the per-wave counts give
+// every wave's offset for every digit, and the words are scattered.
+// Returns the buffer holding the sorted words.
+template <int NTH>
+__device__ uint32_t* lds_lsd_passes(uint32_t* src, uint32_t* dst, int M, const SortPlan& plan,
+                                    int shift0, uint16_t* rank16, uint32_t* hist,
+                                    uint32_t* misc) {
+  constexpr int R = kRankBatch, NW = NTH / kWave;
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
-  const int vb = plan.val_bits;
-  const uint32_t vmask = (vb >= 32) ? 0xffffffffu : ((1u << vb) - 1u);
-
-  // keys, loaded in batches so that their global loads overlap
-  constexpr int U = 8;
-  for (int e0 = 0; e0 < N; e0 += NTH * U) {
-    uint32_t kk[U];
-    load_keys<U>(kf, N, e0 + t, NTH, kk, flag);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int e = e0 + u * NTH + t;
-      if (e < N) bufA[e] = (kk[u] << vb) | (uint32_t)e;
-    }
-  }
-  // wave w owns entries [w*per, (w+1)*per) in input order, per a multiple of 64
-  const int per = ceil_div(ceil_div(N, NW), kWave) * kWave;
+  uint32_t* myhist = hist + w * kMaxBins;
+  // wave w owns words [w*per, (w+1)*per), per a multiple of 64
+  const int per = ceil_div(ceil_div(M, NW), kWave) * kWave;
   const int beg = w * per;
-  const int nr = max(0, min(per, N - beg) + kWave - 1) / kWave;
-  __syncthreads();
-
-  uint32_t* src = bufA;
-  uint32_t* dst = bufB;
+  const int nr = max(0, min(per, M - beg) + kWave - 1) / kWave;
   for (int p = 0; p < plan.passes; ++p) {
-    const int bits = plan.bits[p], shift = plan.shift[p] + vb, bins = 1 << bits;
+    const int bits = plan.bits[p], shift = plan.shift[p] + shift0, bins = 1 << bits;
     for (int i = lane; i < bins; i += kWave) myhist[i] = 0;
     wave_lds_sync();
     for (int r0 = 0; r0 < nr; r0 += R) {  // the wave's counters carry over batches
@@ -173,7 +149,7 @@ __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         const int i = beg + (r0 + r) * kWave + lane;
-        const bool ok = r0 + r < nr && i < N;
+        const bool ok = r0 + r < nr && i < M;
         act[r] = __ballot(ok);
         dg[r] = ((ok ? src[i] : 0u) >> shift) & (uint32_t)(bins - 1);
       }
@@ -207,16 +183,16 @@ __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         const int i = beg + (r0 + r) * kWave + lane;
-        const bool ok = r0 + r < nr && i < N;
+        const bool ok = r0 + r < nr && i < M;
         word[r] = ok ? src[i] : 0u;
         rk[r] = ok ? (uint32_t)rank16[i] : 0u;
       }
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         const int i = beg + (r0 + r) * kWave + lane;
-        if (r0 + r < nr && i < N) {
+        if (r0 + r < nr && i < M) {
           const uint32_t pos = myhist[(word[r] >> shift) & (uint32_t)(bins - 1)] + rk[r];
-          if (pos < (uint32_t)N) dst[pos] = word[r];
+          if (pos < (uint32_t)M) dst[pos] = word[r];
         }
       }
     }
@@ -225,10 +201,86 @@ __device__ void small_sort(const KeyFn& kf, int N, const SortPlan& plan, int32_t
     src = dst;
     dst = tmp;
   }
-  for (int e = t; e < N; e += NTH) {
-    const uint32_t word = src[e];
-    out_keys[e] = (int32_t)(word >> vb);
-    out_vals[e] = (int32_t)(word & vmask);
+  return src;
+}
+
+// ------------------------------------------------------- partitioned small sort
+// Up to kSmallSortN entries are sorted by 2^part_bits workgroups with no
+// communication between them.  Workgroup p takes the entries whose key has
+// low bits equal to p (a hash partition: the heavy Zipf rows, which are the
+// small ids, spread over all workgroups), compacts them in entry order,
+// radix-sorts them in LDS by the remaining key bits (stable: entry order is
+// kept within a key) and writes them after the entries of the partitions
+// below p, which it counts itself while reading the keys.  Equal keys end up
+// contiguous and in entry order -- what the segmented sum needs; the order
+// between distinct keys is fixed by the keys alone.
+constexpr int kPartBits = 4;
+constexpr int kPartSortLdsWords =
+    2 * kSmallSortN + kSmallSortN / 2 + kWavesPerBlock * kMaxBins + 16;
+
+template <class KeyFn>
+__device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part,
+                          int32_t* out_keys, int32_t* out_vals, uint32_t* flag, uint32_t* lds) {
+  constexpr int NTH = kBlock, NW = kWavesPerBlock, UMAX = kSmallSortN / kBlock;
+  uint32_t* bufA = lds;
+  uint32_t* bufB = bufA + kSmallSortN;
+  uint16_t* rank16 = reinterpret_cast<uint16_t*>(bufB + kSmallSortN);
+  uint32_t* hist = bufB + kSmallSortN + kSmallSortN / 2;  // [waves][kMaxBins]
+  uint32_t* misc = hist + NW * kMaxBins;                  // 16 words
+  const int t = threadIdx.x;
+  const int vb = plan.val_bits, pb = plan.part_bits;
+  const uint32_t pmask = (1u << pb) - 1u;
+  const int U = ceil_div(N, NTH);  // contiguous entries per thread (<= UMAX)
+
+  // keys of entries t*U .. t*U+U-1, every load in flight before any use
+  uint32_t key[UMAX];
+#pragma unroll
+  for (int u = 0; u < UMAX; ++u) {
+    const int e = t * U + u;
+    key[u] = (u < U && e < N) ? (uint32_t)kf.load(e) : 0u;
+  }
+  bool bad = false;
+  uint32_t mine = 0, below = 0;
+#pragma unroll
+  for (int u = 0; u < UMAX; ++u) {
+    const int e = t * U + u;
+    const bool act = u < U && e < N;
+    const bool b = act && key[u] >= (uint32_t)kf.range;
+    bad |= b;
+    key[u] = b ? 0u : key[u];
+    const uint32_t pk = key[u] & pmask;
+    mine += (act && pk == (uint32_t)part) ? 1u : 0u;
+    below += (act && pk < (uint32_t)part) ? 1u : 0u;
+  }
+  if (bad) atomicOr(flag, kFlagBadId);
+
+  // exclusive prefix over threads of (below << 16 | mine): each thread's
+  // first slot in the partition, and at the end the partition's size and
+  // output offset (sums stay below 2^16)
+  const uint32_t packed = (below << 16) | mine;
+  hist[t] = packed;
+  __syncthreads();
+  block_exclusive_scan<NTH>(hist, NTH, misc);
+  const uint32_t ex = hist[t];
+  if (t == NTH - 1) misc[8] = ex + packed;
+  uint32_t pos = ex & 0xffffu;
+#pragma unroll
+  for (int u = 0; u < UMAX; ++u) {
+    const int e = t * U + u;
+    if (u < U && e < N && (key[u] & pmask) == (uint32_t)part)
+      bufA[pos++] = ((key[u] >> pb) << vb) | (uint32_t)e;
+  }
+  __syncthreads();
+  const uint32_t tot = misc[8];
+  const int M = (int)(tot & 0xffffu), off = (int)(tot >> 16);
+  __syncthreads();  // misc and hist are reused by the passes
+
+  uint32_t* res = lds_lsd_passes<NTH>(bufA, bufB, M, plan, vb, rank16, hist, misc);
+  const uint32_t vmask = (1u << vb) - 1u;
+  for (int i = t; i < M; i += NTH) {
+    const uint32_t word = res[i];
+    out_keys[off + i] = (int32_t)(((word >> vb) << pb) | (uint32_t)part);
+    out_vals[off + i] = (int32_t)(word & vmask);
   }
 }
 
