@@ -5,11 +5,14 @@
 // alpha = -lr; polyglot_scatter_add with the caller's Y and alpha.
 //
 // The sorted entry list is cut into chunks of CH entries (16 or 64), one per
-// wave.  A wave loads every Y row of its chunk at once (lane = column), and
-// runs one pass of running sums that closes at each piece end (a "piece" is
-// a maximal run of equal keys inside the chunk).  Pieces whose segment lies
-// wholly inside the chunk are added to their table rows by that wave, the
-// rows' only writer; the table rows were loaded together with the Y rows.
+// wave.  A wave walks its chunk in groups of 16 rows (lane = column), the
+// next group's Y rows in flight while the current group is summed, with a
+// running sum that closes at each piece end (a "piece" is a maximal run of
+// equal keys inside the chunk).  Pieces whose segment lies wholly inside the
+// chunk are added to their table rows by that wave, the rows' only writer,
+// with one float add per element performed at the L2 (no read round trip;
+// one add per element, so the result does not depend on scheduling).  Few
+// registers per wave keep every wave of a large launch resident at once.
 // A segment that crosses chunk boundaries (a heavy Zipf row) leaves one
 // partial per spanned chunk (slot 1: the open last piece of the chunk where
 // it starts; slot 0: the first piece of every later spanned chunk).  Its
@@ -92,36 +95,40 @@ __device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
     if (ends_long) a.seg_end[ci.key] = chunk;  // lane 0 holds the first piece's key
   }
 
+  constexpr int GR = CH < 16 ? CH : 16;  // rows per group
   for (int c0 = 0; c0 < a.d; c0 += kWave) {
     const int col = c0 + lane;
     const bool cok = col < a.d;
-    // every Y row and every completed piece's table row, all in flight
-    float v[CH], t[CH];
+    auto load_group = [&](int g0, float (&v)[GR]) {
 #pragma unroll
-    for (int r = 0; r < CH; ++r) {
-      const int ent = __builtin_amdgcn_readlane(ci.ent, r);
-      v[r] = (r < nact && cok) ? a.Y[(size_t)ent * a.d + col] : 0.f;
-    }
-#pragma unroll
-    for (int r = 0; r < CH; ++r) {
-      const int32_t key = __builtin_amdgcn_readlane(ci.key, r);
-      t[r] = (((complete >> r) & 1ull) && cok) ? a.table[(size_t)key * a.d + col] : 0.f;
-    }
-    // running sum in entry order, closed at every piece end
+      for (int r = 0; r < GR; ++r) {
+        const int row = g0 + r;
+        const int ent = __builtin_amdgcn_readlane(ci.ent, row);
+        v[r] = (row < nact && cok) ? a.Y[(size_t)ent * a.d + col] : 0.f;
+      }
+    };
+    float va[GR], vb[GR];
+    load_group(0, va);
     float acc = 0.f, first_sum = 0.f, last_sum = 0.f;
+#pragma unroll 1
+    for (int g0 = 0; g0 < CH; g0 += GR) {
+      if (g0 + GR < CH) load_group(g0 + GR, vb);  // next group in flight
+      // running sum in entry order, closed at every piece end; completed
+      // pieces go straight to their rows
 #pragma unroll
-    for (int r = 0; r < CH; ++r) {
-      acc += v[r];
-      const bool tail = (tails >> r) & 1ull;
-      if (r == first_tail) first_sum = acc;
-      if (r == nact - 1) last_sum = acc;
-      v[r] = tail ? acc : v[r];
-      acc = tail ? 0.f : acc;
-    }
+      for (int r = 0; r < GR; ++r) {
+        const int row = g0 + r;
+        acc += va[r];
+        if (row == first_tail) first_sum = acc;
+        if (row == nact - 1) last_sum = acc;
+        if (((complete >> row) & 1ull) && cok) {
+          const int32_t key = __builtin_amdgcn_readlane(ci.key, row);
+          unsafeAtomicAdd(a.table + (size_t)key * a.d + col, a.alpha * acc);
+        }
+        if ((tails >> row) & 1ull) acc = 0.f;
+      }
 #pragma unroll
-    for (int r = 0; r < CH; ++r) {
-      const int32_t key = __builtin_amdgcn_readlane(ci.key, r);
-      if (((complete >> r) & 1ull) && cok) a.table[(size_t)key * a.d + col] = t[r] + a.alpha * v[r];
+      for (int r = 0; r < GR; ++r) va[r] = vb[r];
     }
     if (cok) {
       if (ci.cont_first) a.seg_part[((size_t)chunk * 2 + 0) * a.seg_stride + col] = first_sum;
