@@ -76,15 +76,16 @@ def batch_structure(wins, cors, ch):
 def step_model(w, B, st, passes, n_parts):
     """{kernel: (bytes, flops, engine)} of one step.
 
-    fwdbwd: ids + every window row read (the gather), the three dz-space
-      vectors written per window, W1 read + its snapshot written, dense
-      partials written; flops = forward 2HK+2Hd and dW1 2HK+2Hd per window.
+    fwdbwd: ids + every window row and corrupt row read once (the gather),
+      the per-entry gradient rows G written ((win+1) rows of d floats per
+      window), W1 read once, dense partials written; flops = forward 2HK +
+      2Hd (corrupted centre block), dW1 2HK + 2Hd, G (win+1) 2Hd per window.
     sort: 16 B per entry per radix pass (keys and values, read and written).
-    update: sorted keys+values, each window's dz-space vectors read once,
-      every distinct row read and written, dense partials read, W1/b1/w2/b2
-      read and written; flops = the row gradients (win+1)*2Hd per window.
-    segfix: the chunk partials of long rows (win*H floats each) read and their
-      rows read and written.
+    update: sorted keys+values and every G row read once, every distinct row
+      of E read and written, dense partials read, W1/b1/w2/b2 read and
+      written; flops = one add per G element.
+    segfix: the chunk partials of long rows (d floats each) read, their rows
+      read and written.
     """
     d, win, H, K = w.d, w.win, w.H, w.K
     N = B * (win + 1)
@@ -92,14 +93,14 @@ def step_model(w, B, st, passes, n_parts):
     part_stride = Hp * K + 2 * Hp + 2
     dense = (H * K + 2 * H + 1) * 4
     m = {
-        "fwdbwd": (B * ((win + 1) * 4 + (win + 1) * d * 4 + 3 * H * 4) + 2 * H * K * 4
+        "fwdbwd": (B * ((win + 1) * 4 + 2 * (win + 1) * d * 4) + H * K * 4
                    + n_parts * part_stride * 4,
-                   B * (4 * H * K + 4 * H * d), "mfma"),
+                   B * (4 * H * K + 4 * H * d + (win + 1) * 2 * H * d), "mfma"),
         "sort": (N * 16 * passes, 0, "hbm"),
-        "update": (N * 8 + B * 3 * H * 4 + 2 * st["U"] * d * 4 + n_parts * part_stride * 4
-                   + 2 * dense, N * 2 * H * d, "alu"),
-        "segfix": (st["partials"] * win * H * 4 + 2 * st["long_rows"] * d * 4,
-                   st["long_rows"] * win * 2 * H * d, "alu"),
+        "update": (N * (8 + d * 4) + 2 * st["U"] * d * 4 + n_parts * part_stride * 4
+                   + 2 * dense, N * d, "alu"),
+        "segfix": (st["partials"] * d * 4 + 2 * st["long_rows"] * d * 4,
+                   st["partials"] * d, "alu"),
     }
     return m
 
