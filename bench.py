@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernels", action="store_true",
                     help="skip the standalone gather / scatter-add measurements")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run 5 plain device copies of MIB MiB (calibrates the HBM byte "
+                         "counters: each copy reads and writes exactly MIB MiB) and exit")
     return ap.parse_args()
 
 
@@ -170,8 +173,10 @@ def time_events(torch, stream, fn, reps):
 
 def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
     """Standalone gather (B=65536 windows) and scatter-add (327,680 Zipf(1.2)
-    rows into a 100k x 64 table) with their HBM rooflines.  Durations are the
-    library's own per-kernel HIP events on its stream."""
+    rows into a 100k x 64 table) with their HBM rooflines.  The gather's
+    duration is the library's per-kernel events (bound to the dispatch); a
+    scatter-add call is timed end to end on the stream, and its kernels'
+    summed durations are reported beside it."""
     w = workloads.PRESETS["sweep_65536"]
     sw = workloads.SCATTER_ISO
     out = {}
@@ -200,14 +205,19 @@ def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
         Yd = torch.from_numpy(Y).cuda()
         U = int(np.unique(idx).size)
         nbytes = sw.N * (4 + 4 * sw.d) + 2 * U * sw.d * 4
+        ctx.set_timing(False)
         for name, mode in (("scatter_sorted", pg.SCATTER_SORTED), ("scatter_atomic", pg.SCATTER_ATOMIC)):
-            ctx.scatter_add(T, I, Yd, 1.0, mode)
-            ctx.kernel_times()
+            # whole calls back to back (every launch of the call and the gaps
+            # between them), then the same calls with per-kernel events
+            call_ms = time_events(torch, stream, lambda: ctx.scatter_add(T, I, Yd, 1.0, mode), reps)
+            ctx.set_timing(True)
             for _ in range(reps):
                 ctx.scatter_add(T, I, Yd, 1.0, mode)
             ms, n = ctx.kernel_times()["scatter"]
-            out[name] = dict(roofline(nbytes, 0, "hbm", ms / n), avg_call_us=round(ms / n * 1e3, 3),
-                             bytes_per_call=nbytes,
+            ctx.set_timing(False)
+            out[name] = dict(roofline(nbytes, 0, "hbm", call_ms), avg_call_us=round(call_ms * 1e3, 3),
+                             kernel_us_per_call=round(ms / reps * 1e3, 3),
+                             launches_per_call=n // reps, bytes_per_call=nbytes,
                              workload=f"{sw.N} rows Zipf({sw.zipf_s}) into {sw.rows}x{sw.d}, U={U}")
         ctx.set_timing(False)
         if ctx.status() != pg.OK:
@@ -225,6 +235,17 @@ def main():
         sys.exit(2)
     import numpy as np
     import torch
+
+    if args.copy_probe:
+        n = args.copy_probe * (1 << 20) // 4
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4,
+                          "copies": 5}), flush=True)
+        return
 
     import paper_1404_1521_amd as pg
     import workloads
@@ -288,10 +309,9 @@ def main():
         ctx.close()
 
     # structure of the timed batches (sampled) for the byte model
-    ch = seg_chunk(N)
-    samp = [batch_structure(wins[s], cors[s], ch) for s in range(Wm + K, Wm + K + min(K, 8))]
-    st = {k: float(np.mean([x[k] for x in samp])) for k in samp[0]}
     small = N <= 8192
+    samp = [batch_structure(wins[s], cors[s], seg_chunk(N)) for s in range(Wm + K, Wm + K + min(K, 8))]
+    st = {k: float(np.mean([x[k] for x in samp])) for k in samp[0]}
     key_bits = max(1, int(w.V - 1).bit_length())
     passes = 0 if small else -(-key_bits // 9)
     n_parts = min(-(-B // 16), 512)

@@ -146,13 +146,15 @@ int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int
 #define POLYGLOT_K_SEGFIX 6   /* rows whose sorted entries span several chunks */
 #define POLYGLOT_NKERNELS 7
 
-/* Per-kernel timing for measurement.  With enable != 0 every later launch of
- * this context (outside graph capture) is bracketed by two HIP events
- * recorded on the context stream; polyglot_kernel_times() synchronises the
- * stream, writes the summed elapsed milliseconds and the launch count of
- * each kernel id into ms[POLYGLOT_NKERNELS] and launches[POLYGLOT_NKERNELS]
- * (host arrays), and resets the sums.  Timing costs two event records per
- * launch on the host. */
+/* Per-kernel timing for measurement.  With enable != 0 every later kernel
+ * launch of this context (outside graph capture) gets a start/stop event
+ * pair that the HIP runtime binds to the kernel's own dispatch
+ * (hipExtLaunchKernel), so the elapsed time is the kernel's execution, not
+ * the host enqueue.  polyglot_kernel_times() synchronises the streams,
+ * writes the summed elapsed milliseconds and the launch count of each kernel
+ * id into ms[POLYGLOT_NKERNELS] and launches[POLYGLOT_NKERNELS] (host
+ * arrays), and resets the sums.  POLYGLOT_K_SCATTER and POLYGLOT_K_SORT sum
+ * every launch of their call. */
 int polyglot_set_timing(polyglot_ctx* ctx, int enable);
 int polyglot_kernel_times(polyglot_ctx* ctx, double* ms, int32_t* launches);
 

@@ -3,6 +3,7 @@
 // event timing.
 #include "polyglot.h"
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -101,7 +102,8 @@ SortPlan make_plan(int key_range, int N) {
       sh += pl.bits[p];
     }
   }
-  pl.ntiles = ceil_div(N, kSortTile);
+  pl.ipt = N <= kSortShortTilesMaxN ? kSortIptShort : kSortIptLong;
+  pl.ntiles = ceil_div(N, kBlock * pl.ipt);
   return pl;
 }
 
@@ -175,28 +177,35 @@ hipEvent_t take_event(polyglot_ctx* ctx) {
   return ev;
 }
 
-// Brackets launches with events when timing is on (never inside capture).
-struct KernelTimer {
+// Launch parameters for kernel id `kid` on stream `st`.  When timing is on
+// (and no graph is being captured) every launch made with it gets its own
+// start/stop event pair, bound to the kernel's dispatch.
+struct Timed {
   polyglot_ctx* ctx;
-  int id;
-  hipStream_t st;
-  hipEvent_t a = nullptr, b = nullptr;
-  KernelTimer(polyglot_ctx* c, int kid, hipStream_t s) : ctx(c), id(kid), st(s) {
+  int kid;
+  Launch L;
+  Timed(polyglot_ctx* c, int k, hipStream_t st) : ctx(c), kid(k) {
+    L.s = st;
     if (ctx->timing && !ctx->capturing) {
-      a = take_event(ctx);
-      b = take_event(ctx);
-      if (a && b) hipEventRecord(a, st);
+      L.owner = this;
+      L.take = &Timed::take;
     }
   }
-  KernelTimer(polyglot_ctx* c, int kid) : KernelTimer(c, kid, c->stream) {}
-  ~KernelTimer() {
-    if (a && b) {
-      hipEventRecord(b, st);
-      ctx->ev_marks.push_back({id, {a, b}});
-    } else {
-      if (a) ctx->ev_pool.push_back(a);
-      if (b) ctx->ev_pool.push_back(b);
+  Timed(polyglot_ctx* c, int k) : Timed(c, k, c->stream) {}
+  Timed(const Timed&) = delete;
+  Timed& operator=(const Timed&) = delete;
+  static bool take(void* owner, hipEvent_t* start, hipEvent_t* stop) {
+    Timed* t = static_cast<Timed*>(owner);
+    hipEvent_t a = take_event(t->ctx), b = take_event(t->ctx);
+    if (!a || !b) {
+      if (a) t->ctx->ev_pool.push_back(a);
+      if (b) t->ctx->ev_pool.push_back(b);
+      return false;
     }
+    t->ctx->ev_marks.push_back({t->kid, {a, b}});
+    *start = a;
+    *stop = b;
+    return true;
   }
 };
 
@@ -236,9 +245,9 @@ hipError_t enqueue_sort(polyglot_ctx* ctx, const int32_t* windows, const int32_t
                         int set) {
   const polyglot_config& cf = ctx->cfg;
   const int N = B * (cf.win + 1);
-  const StepKeys kf{windows, corrupt, cf.win, cf.V};
-  KernelTimer kt(ctx, POLYGLOT_K_SORT, ctx->side);
-  return launch_sort_step(kf, N, make_plan(cf.V, N), sort_bufs(ctx, set), nullptr, ctx->side);
+  const StepKeys kf = step_keys(windows, corrupt, cf.win, cf.V);
+  Timed tm(ctx, POLYGLOT_K_SORT, ctx->side);
+  return launch_sort_step(kf, N, make_plan(cf.V, N), sort_bufs(ctx, set), nullptr, tm.L);
 }
 
 // The fused kernel, then (after `sorted_ev`, if any) the table update and
@@ -251,7 +260,7 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   const int N = B * (cf.win + 1);
   const bool sorted = cf.scatter_mode == POLYGLOT_SCATTER_SORTED;
   const SortPlan plan = make_plan(cf.V, N);
-  const StepKeys kf{windows, corrupt, cf.win, cf.V};
+  const StepKeys kf = step_keys(windows, corrupt, cf.win, cf.V);
   hipError_t e = hipSuccess;
 
   FwdArgs fa{};
@@ -285,9 +294,9 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   fa.invB = 1.0f / (float)B;
   {
     size_t lds = fwdbwd_lds_floats(ctx->Hp, ctx->K) * 4;
-    if (fa.n_sort) lds = std::max(lds, (size_t)kPartSortLdsWords * 4);
-    KernelTimer kt(ctx, POLYGLOT_K_FWDBWD);
-    e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, fa.n_sort + n_fb, lds, ctx->stream);
+    if (fa.n_sort) lds = std::max(lds, part_sort_lds_words(kBlock) * 4);
+    Timed tm(ctx, POLYGLOT_K_FWDBWD);
+    e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, fa.n_sort + n_fb, lds, tm.L);
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "fwd/bwd launch");
   if (sorted_ev) {
@@ -315,12 +324,12 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   aa.dn.invB = 1.0f / (float)B;
   if (sorted) aa.zero = sort_zero_ranges(ctx, plan, set);  // counters of this set, now read
   {
-    KernelTimer kt(ctx, POLYGLOT_K_UPDATE);
-    e = launch_apply_step(aa, kf, aa.n_e + aa.n_d, ctx->stream);
+    Timed tm(ctx, POLYGLOT_K_UPDATE);
+    e = launch_apply_step(aa, kf, aa.n_e + aa.n_d, tm.L);
   }
   if (e == hipSuccess && sorted) {
-    KernelTimer kt(ctx, POLYGLOT_K_SEGFIX);
-    e = launch_segfix(aa.s, segfix_workgroups(aa.s), ctx->stream);
+    Timed tm(ctx, POLYGLOT_K_SEGFIX);
+    e = launch_segfix(aa.s, segfix_workgroups(aa.s), tm.L);
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "update launch");
 
@@ -333,14 +342,14 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
 
 // Enqueues S consecutive steps (arguments already validated), step s using
 // windows + s*B*win and corrupt + s*B.  Sorted mode, small batches: the sort
-// is part of the fused kernel.  Large batches: the sort of step s+1 runs on
-// the side stream while step s computes; it waits for step s-1, the last
-// reader of the same sort set.
+// is a role of the fused kernel (extra workgroups, no cross-stream join).
+// Large batches: the sort of step s+1 runs on the side stream while step s
+// computes; it waits for step s-1, the last reader of the same sort set.
 int enqueue_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
                   const int32_t* windows, const int32_t* corrupt, int S, int B, float lr,
                   float* losses_dev) {
   const bool side_sort = ctx->cfg.scatter_mode == POLYGLOT_SCATTER_SORTED &&
-                      !make_plan(ctx->cfg.V, B * (ctx->cfg.win + 1)).small;  // side-stream sort
+                         !make_plan(ctx->cfg.V, B * (ctx->cfg.win + 1)).small;
   const size_t wstride = (size_t)B * ctx->cfg.win;
   hipError_t e = hipSuccess;
   if (side_sort) {
@@ -417,7 +426,10 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   ctx->Hp = 16 * ctx->NT;
   ctx->cpw = ceil_div(ctx->K / 16, kWavesPerBlock);
   ctx->max_entries = std::max({c.max_batch * (c.win + 1), c.max_scatter, 1});
-  ctx->max_tiles = ceil_div(ctx->max_entries, kSortTile);
+  // most tiles any list up to max_entries keys is cut into
+  ctx->max_tiles = std::max(ceil_div(std::min(ctx->max_entries, kSortShortTilesMaxN),
+                                     kBlock * kSortIptShort),
+                            ceil_div(ctx->max_entries, kBlock * kSortIptLong));
   ctx->max_groups = ceil_div(ctx->max_tiles, kCountGroup);
   ctx->max_parts = std::min(ceil_div(c.max_batch, kTileRows), 512);
   // most chunks any call can cut (short chunks apply up to 131072 entries)
@@ -552,8 +564,8 @@ int polyglot_score(polyglot_ctx* ctx, const float* E, const float* W1, const flo
               ctx->cfg.win, ctx->cfg.H, ctx->K, B};
   hipError_t e;
   {
-    KernelTimer kt(ctx, POLYGLOT_K_SCORE);
-    e = launch_score(a, ctx->NT, ctx->cpw, ctx->stream);
+    Timed tm(ctx, POLYGLOT_K_SCORE);
+    e = launch_score(a, ctx->NT, ctx->cpw, tm.L);
   }
   return e == hipSuccess ? POLYGLOT_OK : hip_fail(ctx, e, "score launch");
 }
@@ -568,8 +580,8 @@ int polyglot_gather(polyglot_ctx* ctx, const float* E, const int32_t* windows,
   GatherArgs a{E, windows, corrupt, X, Xc, ctx->ws.flag, ctx->cfg.V, ctx->cfg.d, ctx->cfg.win, B};
   hipError_t e;
   {
-    KernelTimer kt(ctx, POLYGLOT_K_GATHER);
-    e = launch_gather(a, ctx->stream);
+    Timed tm(ctx, POLYGLOT_K_GATHER);
+    e = launch_gather(a, tm.L);
   }
   return e == hipSuccess ? POLYGLOT_OK : hip_fail(ctx, e, "gather launch");
 }
@@ -596,17 +608,17 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
   aa.n_e = table_workgroups(aa.s, aa.mode);
   aa.n_d = 0;
   hipError_t e;
-  KernelTimer kt(ctx, POLYGLOT_K_SCATTER);
+  Timed tm(ctx, POLYGLOT_K_SCATTER);
   if (aa.mode == 0) {
     // the sort validates the indices (sticky flag) and clears the task list
     aa.zero = sort_zero_ranges(ctx, plan, 0);
     const int n_z = plan.small ? 0 : 16;
-    e = launch_sort_idx(kf, N, plan, sort_bufs(ctx, 0), ctx->ws.long_count, ctx->stream);
-    if (e == hipSuccess) e = launch_apply_idx(aa, kf, aa.n_e + n_z, ctx->stream);
-    if (e == hipSuccess) e = launch_segfix(aa.s, segfix_workgroups(aa.s), ctx->stream);
+    e = launch_sort_idx(kf, N, plan, sort_bufs(ctx, 0), ctx->ws.long_count, tm.L);
+    if (e == hipSuccess) e = launch_apply_idx(aa, kf, aa.n_e + n_z, tm.L);
+    if (e == hipSuccess) e = launch_segfix(aa.s, segfix_workgroups(aa.s), tm.L);
   } else {
-    e = launch_check_idx(idx, N, rows, ctx->ws.flag, ctx->stream);
-    if (e == hipSuccess) e = launch_apply_idx(aa, kf, aa.n_e, ctx->stream);
+    e = launch_check_idx(idx, N, rows, ctx->ws.flag, tm.L);
+    if (e == hipSuccess) e = launch_apply_idx(aa, kf, aa.n_e, tm.L);
   }
   ctx->have_sorted = false;  // the sort buffers now hold this call's order
   return e == hipSuccess ? POLYGLOT_OK : hip_fail(ctx, e, "scatter_add launch");

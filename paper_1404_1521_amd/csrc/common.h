@@ -20,8 +20,12 @@ constexpr int kMaxD = 256;
 constexpr int kMaxLdsBytes = 160 * 1024;  // LDS per workgroup on gfx950
 
 // Radix sort of (row id, entry) pairs.
-constexpr int kSortIPT = 16;                       // keys per thread in a tile
-constexpr int kSortTile = kBlock * kSortIPT;       // 4096 keys per tile
+// Multi-tile sort: keys per thread of a tile.  Short tiles (1024 keys) up to
+// kSortShortTilesMaxN keys spread a mid-sized list over many workgroups;
+// longer lists use 4096-key tiles, which keep the per-tile counters small.
+constexpr int kSortIptShort = 4;
+constexpr int kSortIptLong = 16;
+constexpr int kSortShortTilesMaxN = 1 << 20;
 constexpr int kMaxDigitBits = 9;
 constexpr int kMaxBins = 1 << kMaxDigitBits;
 constexpr int kMaxPasses = 4;                      // 31-bit keys at most
@@ -35,7 +39,8 @@ struct SortPlan {
   int passes;               // 0 when N <= 1 (nothing to order)
   int shift[kMaxPasses];
   int bits[kMaxPasses];
-  int ntiles;               // multi-tile path: tiles of kSortTile keys
+  int ntiles;               // multi-tile path: tiles of kBlock * ipt keys
+  int ipt;                  // multi-tile path: keys per thread of a tile
   int small;                // 1: partitioned sort (one launch, 2^part_bits workgroups)
   int val_bits;             // small path packs (key >> part_bits) << val_bits | entry
   int part_bits;            // small path: partitions by the low key bits

@@ -35,16 +35,22 @@ __device__ __forceinline__ f4 mfma16(float a, float b, f4 c) {
 // = 24 tiles of window 5, d 64 in one pass of the four waves.
 constexpr int kGTiles = 6;
 
-template <int NT, int CPW>
+// D_ and WIN_ fix the embedding width and the window at compile time for
+// the common shapes (0: taken from the arguments).
+template <int NT, int CPW, int D_, int WIN_>
 __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
   constexpr int HP = NT * 16;
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);  // wave-uniform: scalar branches
   const int n16 = lane & 15, g = lane >> 4;
-  const int W1p = a.win + 1;
-  const int dq = a.d / 16;
-  const int nchunk = a.K / 16;
-  const int S = a.K + 4;
+  const int d = D_ ? D_ : a.d;
+  const int win = WIN_ ? WIN_ : a.win;
+  const int K = d * win;
+  const int cc = win / 2;
+  const int W1p = win + 1;
+  const int dq = d / 16;
+  const int nchunk = K / 16;
+  const int S = K + 4;
   float* w1s = lds;                                        // [HP][K+4]
   float* zp = w1s + (size_t)HP * S;                        // [4][3][NT][4][64]
   float* vt = zp + kWavesPerBlock * 3 * NT * kWave * 4;    // [3][16][HP+1]
@@ -62,7 +68,7 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
       const int b = tile * kTileRows + r;
       v[k] = 0;
       if (i < kTileRows * W1p && b < a.B)
-        v[k] = (j < a.win) ? a.windows[(size_t)b * a.win + j] : a.corrupt[b];
+        v[k] = (j < win) ? a.windows[(size_t)b * win + j] : a.corrupt[b];
     }
     bool bad = false;
 #pragma unroll
@@ -86,7 +92,7 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
   auto load_fwd = [&](int buf, f4 (&xa)[CPW], f4 (&xt)[CPW]) {
     const int32_t* rid = idt + (buf * kTileRows + n16) * (kMaxWin + 1);
     int32_t idr[CPW];
-    const int32_t idc = rid[a.win];
+    const int32_t idc = rid[win];
 #pragma unroll
     for (int ci = 0; ci < CPW; ++ci) {
       const int kc = w + kWavesPerBlock * ci;
@@ -97,10 +103,10 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
       const int kc = w + kWavesPerBlock * ci;
       const bool ok = kc < nchunk;
       const int j = ok ? kc / dq : 0;
-      const bool ctr = ok && j == a.c;
+      const bool ctr = ok && j == cc;
       const int q16 = (kc - j * dq) * 16;
-      xa[ci] = ok ? ld4(a.E + (size_t)idr[ci] * a.d + q16 + 4 * g) : kZero4;
-      xt[ci] = ctr ? ld4(a.E + (size_t)idc * a.d + q16 + 4 * g) : kZero4;
+      xa[ci] = ok ? ld4(a.E + (size_t)idr[ci] * d + q16 + 4 * g) : kZero4;
+      xt[ci] = ctr ? ld4(a.E + (size_t)idc * d + q16 + 4 * g) : kZero4;
     }
   };
 
@@ -108,14 +114,14 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
   load_ids(wg * a.tiles_per_wg, idv);  // in flight with the W1 loads
   {  // W1 into LDS, rows >= H zero; loads batched before the stores
     constexpr int U = 16;  // one batch up to Hp*K = 16384 floats
-    const int k4 = a.K / 4, n4 = HP * k4;
+    const int k4 = K / 4, n4 = HP * k4;
     for (int i0 = 0; i0 < n4; i0 += kBlock * U) {
       f4 v[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int i = i0 + u * kBlock + t;
         const int n = i / k4;
-        v[u] = (i < n4 && n < a.H) ? ld4(a.W1 + (size_t)n * a.K + 4 * (i - n * k4)) : kZero4;
+        v[u] = (i < n4 && n < a.H) ? ld4(a.W1 + (size_t)n * K + 4 * (i - n * k4)) : kZero4;
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -174,7 +180,7 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
           wb[nt] = ld4(w1s + (size_t)(nt * 16 + n16) * S + kc * 16 + 4 * g);
-        if (kc / dq != a.c) {
+        if (kc / dq != cc) {
 #pragma unroll
           for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -209,7 +215,7 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int32_t* ri = idt + (buf * kTileRows + 4 * g + i) * (kMaxWin + 1);
-        idq[i] = ri[a.win];
+        idq[i] = ri[win];
 #pragma unroll
         for (int ci = 0; ci < CPW; ++ci) {
           const int kc = w + kWavesPerBlock * ci;
@@ -221,12 +227,12 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
         const int kc = w + kWavesPerBlock * ci;
         const bool ok = kc < nchunk;
         const int j = ok ? kc / dq : 0;
-        const bool ctr = ok && j == a.c;
+        const bool ctr = ok && j == cc;
         const int q16 = (kc - j * dq) * 16;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          xb[ci][i] = ok ? a.E[(size_t)idb[ci][i] * a.d + q16 + n16] : 0.f;
-          xr[ci][i] = ctr ? a.E[(size_t)idq[i] * a.d + q16 + n16] : 0.f;
+          xb[ci][i] = ok ? a.E[(size_t)idb[ci][i] * d + q16 + n16] : 0.f;
+          xr[ci][i] = ctr ? a.E[(size_t)idq[i] * d + q16 + n16] : 0.f;
         }
       }
     }
@@ -305,7 +311,7 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
       for (int ci = 0; ci < CPW; ++ci) {
         const int kc = w + kWavesPerBlock * ci;
         if (kc < nchunk) {
-          if (kc / dq != a.c) {
+          if (kc / dq != cc) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -340,8 +346,8 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
       for (int u = 0; u < kGTiles; ++u) {
         const int ot = min(t0 + u * kWavesPerBlock, ngt - 1);
         const int j = ot / dq, cb = ot - j * dq;
-        typ[u] = (j == a.win) ? 2 : (j == a.c ? 1 : 0);
-        off[u] = ((j == a.win) ? a.c : j) * a.d + cb * 16 + n16;
+        typ[u] = (j == win) ? 2 : (j == cc ? 1 : 0);
+        off[u] = ((j == win) ? cc : j) * d + cb * 16 + n16;
         acc[u] = kZero4;
       }
       const int nu = min(kGTiles, (ngt - t0 + kWavesPerBlock - 1) / kWavesPerBlock);
@@ -378,7 +384,7 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int row = row0 + 4 * g + i;
-            if (row < a.B) a.G[((size_t)row * W1p + j) * a.d + cb * 16 + n16] = acc[u][i];
+            if (row < a.B) a.G[((size_t)row * W1p + j) * d + cb * 16 + n16] = acc[u][i];
           }
         }
       }
@@ -395,7 +401,7 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          P[(size_t)(nt * 16 + 4 * g + i) * a.K + kc * 16 + n16] = accW[ci][nt][i];
+          P[(size_t)(nt * 16 + 4 * g + i) * K + kc * 16 + n16] = accW[ci][nt][i];
     }
   }
   // db1, dw2, loss, db2: per-wave sums (fixed butterflies), then the four
@@ -428,7 +434,7 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
 #pragma unroll
       for (int v = 1; v < kWavesPerBlock; ++v) s += red[v * (2 * HP + 2) + e];
       // slot layout: dW1 [Hp][K], db1 [Hp], dw2 [Hp], loss, db2
-      P[(size_t)a.Hp * a.K + e] = s;
+      P[(size_t)a.Hp * K + e] = s;
     }
   }
 }

@@ -43,16 +43,18 @@
 namespace pg {
 
 // Two workgroups per CU when the shape's registers allow it without spills.
-template <int NT, int CPW>
+// D and WIN (0: runtime) fix the embedding width and window of the common
+// shapes at compile time.
+template <int NT, int CPW, int D, int WIN>
 __global__ __launch_bounds__(kBlock, (NT == 1 || (NT == 2 && CPW <= 5)) ? 2 : 1) void k_step_fwdbwd(FwdArgs a) {
   extern __shared__ float lds_f[];
   if ((int)blockIdx.x < a.n_sort) {  // small batches: the step's sort, partition blockIdx.x
-    const StepKeys kf{a.windows, a.corrupt, a.win, a.V};
-    part_sort(kf, a.N, a.plan, blockIdx.x, a.sb.keys[a.plan.passes & 1],
-              a.sb.vals[a.plan.passes & 1], a.flag, reinterpret_cast<uint32_t*>(lds_f));
+    const StepKeys kf = step_keys(a.windows, a.corrupt, a.win, a.V);
+    part_sort<kBlock>(kf, a.N, a.plan, blockIdx.x, a.sb.keys[a.plan.passes & 1],
+                      a.sb.vals[a.plan.passes & 1], a.flag, reinterpret_cast<uint32_t*>(lds_f));
     return;
   }
-  fwdbwd_wg<NT, CPW>(a, blockIdx.x - a.n_sort, lds_f);
+  fwdbwd_wg<NT, CPW, D, WIN>(a, blockIdx.x - a.n_sort, lds_f);
 }
 
 // =============================================================== sort
@@ -60,148 +62,141 @@ __global__ __launch_bounds__(kBlock, (NT == 1 || (NT == 2 && CPW <= 5)) ? 2 : 1)
 // Partitioned sort of a small list, partition blockIdx.x (clears the segment
 // task list when given one).
 template <class KeyFn>
-__global__ __launch_bounds__(kBlock) void k_sort_part(KeyFn kf, int N, SortPlan plan, SortBufs sb,
-                                                      uint32_t* long_count) {
+__global__ __launch_bounds__(kPartSortThreads) void k_sort_part(KeyFn kf, int N, SortPlan plan,
+                                                                SortBufs sb, uint32_t* long_count) {
   extern __shared__ uint32_t lds[];
   if (long_count && blockIdx.x == 0 && threadIdx.x == 0) *long_count = 0u;
-  part_sort(kf, N, plan, blockIdx.x, sb.keys[plan.passes & 1], sb.vals[plan.passes & 1], sb.flag,
-            lds);
+  part_sort<kPartSortThreads>(kf, N, plan, blockIdx.x, sb.keys[plan.passes & 1],
+                              sb.vals[plan.passes & 1], sb.flag, lds);
 }
 
 // Pass-0 digit counts of every tile of a large list (clears the task list
 // when given one).
-template <class KeyFn>
+template <int IPT, class KeyFn>
 __global__ __launch_bounds__(kBlock) void k_sort_first(KeyFn kf, int N, SortPlan plan, SortBufs sb,
                                                        uint32_t* long_count) {
   extern __shared__ uint32_t lds[];
   if (long_count && blockIdx.x == 0 && threadIdx.x == 0) *long_count = 0u;
-  sort_up0_tile(kf, N, plan, sb, blockIdx.x, lds);
+  sort_up0_tile<IPT>(kf, N, plan, sb, blockIdx.x, lds);
 }
 
-template <class KeyFn>
+template <int IPT, class KeyFn>
 __global__ __launch_bounds__(kBlock) void k_sort_down(KeyFn kf, int N, SortPlan plan, SortBufs sb,
                                                       int p) {
   extern __shared__ uint32_t lds[];
-  sort_down_tile(kf, N, plan, sb, p, blockIdx.x, lds);
+  sort_down_tile<IPT>(kf, N, plan, sb, p, blockIdx.x, lds);
 }
 
+template <int IPT>
 __global__ __launch_bounds__(kBlock) void k_sort_up(int N, SortPlan plan, SortBufs sb, int p) {
   extern __shared__ uint32_t lds[];
-  sort_up_tile(N, plan, sb, p, blockIdx.x, lds);
+  sort_up_tile<IPT>(N, plan, sb, p, blockIdx.x, lds);
+}
+
+template <int IPT, class KeyFn>
+static hipError_t launch_tiled_sort(const KeyFn& kf, int N, const SortPlan& plan,
+                                    const SortBufs& sb, uint32_t* long_count, const Launch& L) {
+  hipError_t e = pg_launch(k_sort_first<IPT, KeyFn>, dim3(plan.ntiles), dim3(kBlock),
+                           kUp0LdsWords * 4, L, kf, N, plan, sb, long_count);
+  for (int p = 0; p < plan.passes && e == hipSuccess; ++p) {
+    if (p > 0)
+      e = pg_launch(k_sort_up<IPT>, dim3(plan.ntiles), dim3(kBlock), kMaxBins * 4, L, N, plan,
+                    sb, p);
+    if (e == hipSuccess)
+      e = pg_launch(k_sort_down<IPT, KeyFn>, dim3(plan.ntiles), dim3(kBlock), kDownLdsWords * 4,
+                    L, kf, N, plan, sb, p);
+  }
+  return e;
 }
 
 template <class KeyFn>
-static void launch_sort(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                        uint32_t* long_count, hipStream_t s) {
-  if (plan.small) {
-    hipLaunchKernelGGL((k_sort_part<KeyFn>), dim3(1 << plan.part_bits), dim3(kBlock),
-                       kPartSortLdsWords * 4, s, kf, N, plan, sb, long_count);
-    return;
-  }
-  hipLaunchKernelGGL((k_sort_first<KeyFn>), dim3(plan.ntiles), dim3(kBlock), kUp0LdsWords * 4, s,
-                     kf, N, plan, sb, long_count);
-  for (int p = 0; p < plan.passes; ++p) {
-    if (p > 0)
-      hipLaunchKernelGGL(k_sort_up, dim3(plan.ntiles), dim3(kBlock), kMaxBins * 4, s, N, plan, sb,
-                         p);
-    hipLaunchKernelGGL((k_sort_down<KeyFn>), dim3(plan.ntiles), dim3(kBlock), kDownLdsWords * 4,
-                       s, kf, N, plan, sb, p);
-  }
+static hipError_t launch_sort(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
+                              uint32_t* long_count, const Launch& L) {
+  if (plan.small)
+    return pg_launch(k_sort_part<KeyFn>, dim3(1 << plan.part_bits), dim3(kPartSortThreads),
+                     part_sort_lds_words(kPartSortThreads) * 4, L, kf, N, plan, sb, long_count);
+  if (plan.ipt == kSortIptShort)
+    return launch_tiled_sort<kSortIptShort>(kf, N, plan, sb, long_count, L);
+  return launch_tiled_sort<kSortIptLong>(kf, N, plan, sb, long_count, L);
 }
 
 // =============================================================== launchers
 
-static hipError_t launch_err() { return hipGetLastError(); }
-
-template <int NT, int CPW>
-static void launch_fwdbwd_t(const FwdArgs& a, int grid, size_t lds, hipStream_t s) {
-  hipLaunchKernelGGL((k_step_fwdbwd<NT, CPW>), dim3(grid), dim3(kBlock), lds, s, a);
-}
-
 template <int NT>
-static void launch_fwdbwd_nt(const FwdArgs& a, int cpw, int grid, size_t lds, hipStream_t s) {
-  if (cpw <= 2)
-    launch_fwdbwd_t<NT, 2>(a, grid, lds, s);
-  else if (cpw <= 5)
-    launch_fwdbwd_t<NT, 5>(a, grid, lds, s);
-  else
-    launch_fwdbwd_t<NT, 8>(a, grid, lds, s);
+static hipError_t launch_fwdbwd_nt(const FwdArgs& a, int cpw, int grid, size_t lds,
+                                   const Launch& L) {
+  if (cpw <= 2) return pg_launch(k_step_fwdbwd<NT, 2, 0, 0>, dim3(grid), dim3(kBlock), lds, L, a);
+  if (cpw <= 5) return pg_launch(k_step_fwdbwd<NT, 5, 0, 0>, dim3(grid), dim3(kBlock), lds, L, a);
+  return pg_launch(k_step_fwdbwd<NT, 8, 0, 0>, dim3(grid), dim3(kBlock), lds, L, a);
 }
 
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
-                              hipStream_t s) {
-  if (NT == 1)
-    launch_fwdbwd_nt<1>(a, cpw, grid, lds, s);
-  else if (NT == 2)
-    launch_fwdbwd_nt<2>(a, cpw, grid, lds, s);
-  else
-    launch_fwdbwd_nt<4>(a, cpw, grid, lds, s);
-  return launch_err();
+                              const Launch& L) {
+  // compile-time shapes: the Polyglot-scale model (d 64, window 5, H <= 32)
+  // and the small test model (d 16, window 5, H <= 16)
+  if (a.d == 64 && a.win == 5 && NT == 2)
+    return pg_launch(k_step_fwdbwd<2, 5, 64, 5>, dim3(grid), dim3(kBlock), lds, L, a);
+  if (a.d == 16 && a.win == 5 && NT == 1)
+    return pg_launch(k_step_fwdbwd<1, 2, 16, 5>, dim3(grid), dim3(kBlock), lds, L, a);
+  if (NT == 1) return launch_fwdbwd_nt<1>(a, cpw, grid, lds, L);
+  if (NT == 2) return launch_fwdbwd_nt<2>(a, cpw, grid, lds, L);
+  return launch_fwdbwd_nt<4>(a, cpw, grid, lds, L);
 }
 
 hipError_t launch_sort_step(const StepKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                            uint32_t* long_count, hipStream_t s) {
-  launch_sort(kf, N, plan, sb, long_count, s);
-  return launch_err();
+                            uint32_t* long_count, const Launch& L) {
+  return launch_sort(kf, N, plan, sb, long_count, L);
 }
 
 hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                           uint32_t* long_count, hipStream_t s) {
-  launch_sort(kf, N, plan, sb, long_count, s);
-  return launch_err();
+                           uint32_t* long_count, const Launch& L) {
+  return launch_sort(kf, N, plan, sb, long_count, L);
 }
 
 template <class KeyFn>
-static void launch_apply(const ApplyArgs& a, const KeyFn& kf, int grid, hipStream_t s) {
-  if (a.s.ch == 16)
-    hipLaunchKernelGGL((k_apply<16, KeyFn>), dim3(grid), dim3(kBlock), 0, s, a, kf);
-  else
-    hipLaunchKernelGGL((k_apply<64, KeyFn>), dim3(grid), dim3(kBlock), 0, s, a, kf);
+static hipError_t launch_apply(const ApplyArgs& a, const KeyFn& kf, int grid, const Launch& L) {
+  if (a.s.ch == 16) return pg_launch(k_apply<16, KeyFn>, dim3(grid), dim3(kBlock), 0, L, a, kf);
+  return pg_launch(k_apply<64, KeyFn>, dim3(grid), dim3(kBlock), 0, L, a, kf);
 }
 
-hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, hipStream_t s) {
-  launch_apply(a, kf, grid, s);
-  return launch_err();
+hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, const Launch& L) {
+  return launch_apply(a, kf, grid, L);
 }
 
-hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, hipStream_t s) {
-  launch_apply(a, kf, grid, s);
-  return launch_err();
+hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, const Launch& L) {
+  return launch_apply(a, kf, grid, L);
 }
 
-hipError_t launch_segfix(const SegArgs& a, int grid, hipStream_t s) {
-  hipLaunchKernelGGL(k_segfix, dim3(grid), dim3(kSegfixThreads), 0, s, a);
-  return launch_err();
+hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L) {
+  return pg_launch(k_segfix, dim3(grid), dim3(kSegfixThreads), 0, L, a);
 }
 
-hipError_t launch_check_idx(const int32_t* idx, int N, int rows, uint32_t* flag, hipStream_t s) {
+hipError_t launch_check_idx(const int32_t* idx, int N, int rows, uint32_t* flag, const Launch& L) {
   const int g = std::min(std::max(ceil_div(N, kBlock), 1), 1024);
-  hipLaunchKernelGGL(k_check_idx, dim3(g), dim3(kBlock), 0, s, idx, N, rows, flag);
-  return launch_err();
+  return pg_launch(k_check_idx, dim3(g), dim3(kBlock), 0, L, idx, N, rows, flag);
 }
 
-hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, hipStream_t s) {
+template <int NT>
+static hipError_t launch_score_nt(const ScoreArgs& a, int cpw, int grid, size_t lds,
+                                  const Launch& L) {
+  if (cpw <= 2) return pg_launch(k_score<NT, 2>, dim3(grid), dim3(kBlock), lds, L, a);
+  if (cpw <= 5) return pg_launch(k_score<NT, 5>, dim3(grid), dim3(kBlock), lds, L, a);
+  return pg_launch(k_score<NT, 8>, dim3(grid), dim3(kBlock), lds, L, a);
+}
+
+hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, const Launch& L) {
   const int grid = ceil_div(a.B, kTileRows);
   const size_t lds = (kTileRows * (kMaxWin + 1)) * 4 + kWavesPerBlock * kMaxNT * kWave * 16;
-#define PG_SCORE(NTV, CPWV) \
-  hipLaunchKernelGGL((k_score<NTV, CPWV>), dim3(grid), dim3(kBlock), lds, s, a)
-  if (NT == 1) {
-    if (cpw <= 2) PG_SCORE(1, 2); else if (cpw <= 5) PG_SCORE(1, 5); else PG_SCORE(1, 8);
-  } else if (NT == 2) {
-    if (cpw <= 2) PG_SCORE(2, 2); else if (cpw <= 5) PG_SCORE(2, 5); else PG_SCORE(2, 8);
-  } else {
-    if (cpw <= 2) PG_SCORE(4, 2); else if (cpw <= 5) PG_SCORE(4, 5); else PG_SCORE(4, 8);
-  }
-#undef PG_SCORE
-  return launch_err();
+  if (NT == 1) return launch_score_nt<1>(a, cpw, grid, lds, L);
+  if (NT == 2) return launch_score_nt<2>(a, cpw, grid, lds, L);
+  return launch_score_nt<4>(a, cpw, grid, lds, L);
 }
 
-hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
+hipError_t launch_gather(const GatherArgs& a, const Launch& L) {
   const size_t total = (size_t)a.B * (a.win + 1) * (a.d / 4);
   const size_t want = (total + kBlock - 1) / kBlock;
   const int grid = (int)(want < 8192 ? (want > 0 ? want : 1) : 8192);
-  hipLaunchKernelGGL(k_gather, dim3(grid), dim3(kBlock), 0, s, a);
-  return launch_err();
+  return pg_launch(k_gather, dim3(grid), dim3(kBlock), 0, L, a);
 }
 
 }  // namespace pg

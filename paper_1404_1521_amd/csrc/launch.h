@@ -1,10 +1,40 @@
 // Argument blocks and launchers shared by kernels.hip and the host API.
 #pragma once
+#include <tuple>
+#include <utility>
+
 #include "common.h"
 #include "seg_dev.h"
 #include "sort_dev.h"
 
 namespace pg {
+
+// Where a kernel is launched: the stream and, when launches are being
+// measured, a source of start/stop events that the runtime binds to the
+// kernel's own dispatch (so they time the kernel, not the host enqueue).
+struct Launch {
+  hipStream_t s = nullptr;
+  void* owner = nullptr;
+  bool (*take)(void* owner, hipEvent_t* start, hipEvent_t* stop) = nullptr;
+};
+
+// Launches kernel k with the given arguments (converted to its parameter
+// types); timed through hipExtLaunchKernel when L supplies events.
+template <typename... KArgs, typename... Args>
+inline hipError_t pg_launch(void (*k)(KArgs...), dim3 grid, dim3 block, uint32_t lds,
+                            const Launch& L, Args&&... args) {
+  std::tuple<KArgs...> tup{std::forward<Args>(args)...};
+  void* argv[sizeof...(KArgs) > 0 ? sizeof...(KArgs) : 1];
+  std::apply([&](auto&... x) {
+    int i = 0;
+    ((argv[i++] = static_cast<void*>(&x)), ...);
+  }, tup);
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (L.take && L.take(L.owner, &e0, &e1))
+    return hipExtLaunchKernel(reinterpret_cast<const void*>(k), grid, block, argv, lds, L.s, e0,
+                              e1, 0);
+  return hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, argv, lds, L.s);
+}
 
 struct FwdArgs {
   const float* E;
@@ -82,19 +112,19 @@ struct GatherArgs {
 };
 
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
-                              hipStream_t s);
+                              const Launch& L);
 // First sort launch (whole small sort, or pass-0 tile counts) and, for
 // multi-tile plans, every later pass; clears *long_count if not NULL.
 hipError_t launch_sort_step(const StepKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                            uint32_t* long_count, hipStream_t s);
+                            uint32_t* long_count, const Launch& L);
 hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                           uint32_t* long_count, hipStream_t s);
-hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, hipStream_t s);
-hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, hipStream_t s);
-hipError_t launch_segfix(const SegArgs& a, int grid, hipStream_t s);
-hipError_t launch_check_idx(const int32_t* idx, int N, int rows, uint32_t* flag, hipStream_t s);
-hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, hipStream_t s);
-hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
+                           uint32_t* long_count, const Launch& L);
+hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, const Launch& L);
+hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, const Launch& L);
+hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L);
+hipError_t launch_check_idx(const int32_t* idx, int N, int rows, uint32_t* flag, const Launch& L);
+hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, const Launch& L);
+hipError_t launch_gather(const GatherArgs& a, const Launch& L);
 
 // LDS of the fused kernel, in floats: W1 [Hp][K+4], split-K partials
 // [4 waves][3][NT][64] f4, V [3][16][Hp+1], per-wave dense sums [4][2Hp+2],

@@ -5,9 +5,8 @@
 // alpha = -lr; polyglot_scatter_add with the caller's Y and alpha.
 //
 // The sorted entry list is cut into chunks of CH entries (16 or 64), one per
-// wave.  A wave walks its chunk in groups of 16 rows (lane = column), the
-// next group's Y rows in flight while the current group is summed, with a
-// running sum that closes at each piece end (a "piece" is a maximal run of
+// wave.  A wave loads the Y rows of its whole chunk at once (lane = column)
+// and walks them with a running sum that closes at each piece end (a "piece" is a maximal run of
 // equal keys inside the chunk).  Pieces whose segment lies wholly inside the
 // chunk are added to their table rows by that wave, the rows' only writer,
 // with one float add per element performed at the L2 (no read round trip;
@@ -95,40 +94,29 @@ __device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
     if (ends_long) a.seg_end[ci.key] = chunk;  // lane 0 holds the first piece's key
   }
 
-  constexpr int GR = CH < 16 ? CH : 16;  // rows per group
   for (int c0 = 0; c0 < a.d; c0 += kWave) {
     const int col = c0 + lane;
     const bool cok = col < a.d;
-    auto load_group = [&](int g0, float (&v)[GR]) {
+    // every row of the chunk in flight at once (lane = column)
+    float v[CH];
 #pragma unroll
-      for (int r = 0; r < GR; ++r) {
-        const int row = g0 + r;
-        const int ent = __builtin_amdgcn_readlane(ci.ent, row);
-        v[r] = (row < nact && cok) ? a.Y[(size_t)ent * a.d + col] : 0.f;
-      }
-    };
-    float va[GR], vb[GR];
-    load_group(0, va);
+    for (int r = 0; r < CH; ++r) {
+      const int ent = __builtin_amdgcn_readlane(ci.ent, r);
+      v[r] = (r < nact && cok) ? a.Y[(size_t)ent * a.d + col] : 0.f;
+    }
+    // running sum in entry order, closed at every piece end; completed
+    // pieces go straight to their rows
     float acc = 0.f, first_sum = 0.f, last_sum = 0.f;
-#pragma unroll 1
-    for (int g0 = 0; g0 < CH; g0 += GR) {
-      if (g0 + GR < CH) load_group(g0 + GR, vb);  // next group in flight
-      // running sum in entry order, closed at every piece end; completed
-      // pieces go straight to their rows
 #pragma unroll
-      for (int r = 0; r < GR; ++r) {
-        const int row = g0 + r;
-        acc += va[r];
-        if (row == first_tail) first_sum = acc;
-        if (row == nact - 1) last_sum = acc;
-        if (((complete >> row) & 1ull) && cok) {
-          const int32_t key = __builtin_amdgcn_readlane(ci.key, row);
-          unsafeAtomicAdd(a.table + (size_t)key * a.d + col, a.alpha * acc);
-        }
-        if ((tails >> row) & 1ull) acc = 0.f;
+    for (int r = 0; r < CH; ++r) {
+      acc += v[r];
+      if (r == first_tail) first_sum = acc;
+      if (r == nact - 1) last_sum = acc;
+      if (((complete >> r) & 1ull) && cok) {
+        const int32_t key = __builtin_amdgcn_readlane(ci.key, r);
+        unsafeAtomicAdd(a.table + (size_t)key * a.d + col, a.alpha * acc);
       }
-#pragma unroll
-      for (int r = 0; r < GR; ++r) va[r] = vb[r];
+      if ((tails >> r) & 1ull) acc = 0.f;
     }
     if (cok) {
       if (ci.cont_first) a.seg_part[((size_t)chunk * 2 + 0) * a.seg_stride + col] = first_sum;

@@ -9,7 +9,7 @@
 // Two variants:
 //  * small (up to kSmallSortN entries): a partitioned sort, one launch of
 //    2^part_bits workgroups (see part_sort below);
-//  * multi-tile: tiles of kSortTile keys.  up0 counts pass-0 digits per tile
+//  * multi-tile: tiles of 256 * IPT keys.  up0 counts pass-0 digits per tile
 //    and the digit totals of every pass; down(p) ranks each tile stably,
 //    adds the counts of all earlier tiles and scatters; up(p) counts the
 //    digits of pass p per tile of the previous output.  Counts are kept per
@@ -29,16 +29,27 @@ namespace pg {
 
 // Key sources -------------------------------------------------------------
 
-struct StepKeys {  // entries of a training step (windows + corrupt ids)
+// Entries of a training step: entry e = b*(win+1) + j is windows[b][j] for
+// j < win and corrupt[b] for j = win.  b = e / (win+1) is taken as the high
+// word of e * inv with inv = ceil(2^32 / (win+1)), which is exact for
+// e < 2^26 and win + 1 <= 32 (the error term e * (inv*(win+1) - 2^32) / 2^32
+// stays below 1/(win+1)).
+struct StepKeys {
   const int32_t* windows;
   const int32_t* corrupt;
   int win, range;   // range = V
+  uint32_t inv;
   __device__ int32_t load(int e) const {
-    const int b = e / (win + 1);
+    const int b = (int)__umulhi((uint32_t)e, inv);
     const int j = e - b * (win + 1);
     return (j < win) ? windows[(size_t)b * win + j] : corrupt[b];
   }
 };
+
+__host__ __device__ inline StepKeys step_keys(const int32_t* windows, const int32_t* corrupt,
+                                              int win, int V) {
+  return StepKeys{windows, corrupt, win, V, (uint32_t)(0xffffffffu / (uint32_t)(win + 1)) + 1u};
+}
 
 struct IdxKeys {  // entries of the standalone scatter-add
   const int32_t* idx;
@@ -215,18 +226,22 @@ __device__ uint32_t* lds_lsd_passes(uint32_t* src, uint32_t* dst, int M, const S
 // contiguous and in entry order -- what the segmented sum needs; the order
 // between distinct keys is fixed by the keys alone.
 constexpr int kPartBits = 4;
-constexpr int kPartSortLdsWords =
-    2 * kSmallSortN + kSmallSortN / 2 + kWavesPerBlock * kMaxBins + 16;
+constexpr int kPartSortThreads = 1024;  // one workgroup of 16 waves per partition
+constexpr int kPartSortMisc = 32;       // scan scratch: wave sums, then the partition total
+__host__ __device__ constexpr size_t part_sort_lds_words(int nth) {
+  return 2 * kSmallSortN + kSmallSortN / 2 + (size_t)(nth / kWave) * kMaxBins + kPartSortMisc;
+}
 
-template <class KeyFn>
+template <int NTH, class KeyFn>
 __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part,
                           int32_t* out_keys, int32_t* out_vals, uint32_t* flag, uint32_t* lds) {
-  constexpr int NTH = kBlock, NW = kWavesPerBlock, UMAX = kSmallSortN / kBlock;
+  constexpr int NW = NTH / kWave, UMAX = kSmallSortN / NTH;
+  static_assert(NW + 1 <= kPartSortMisc, "scan scratch too small");
   uint32_t* bufA = lds;
   uint32_t* bufB = bufA + kSmallSortN;
   uint16_t* rank16 = reinterpret_cast<uint16_t*>(bufB + kSmallSortN);
   uint32_t* hist = bufB + kSmallSortN + kSmallSortN / 2;  // [waves][kMaxBins]
-  uint32_t* misc = hist + NW * kMaxBins;                  // 16 words
+  uint32_t* misc = hist + NW * kMaxBins;                  // kPartSortMisc words
   const int t = threadIdx.x;
   const int vb = plan.val_bits, pb = plan.part_bits;
   const uint32_t pmask = (1u << pb) - 1u;
@@ -262,7 +277,7 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
   __syncthreads();
   block_exclusive_scan<NTH>(hist, NTH, misc);
   const uint32_t ex = hist[t];
-  if (t == NTH - 1) misc[8] = ex + packed;
+  if (t == NTH - 1) misc[NW] = ex + packed;  // after the NW wave sums
   uint32_t pos = ex & 0xffffu;
 #pragma unroll
   for (int u = 0; u < UMAX; ++u) {
@@ -271,7 +286,7 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
       bufA[pos++] = ((key[u] >> pb) << vb) | (uint32_t)e;
   }
   __syncthreads();
-  const uint32_t tot = misc[8];
+  const uint32_t tot = misc[NW];
   const int M = (int)(tot & 0xffffu), off = (int)(tot >> 16);
   __syncthreads();  // misc and hist are reused by the passes
 
@@ -308,17 +323,17 @@ __device__ inline uint32_t* gcounts_at(const SortBufs& sb, int p, int dg) {
 constexpr int kUp0LdsWords = kMaxPasses * kMaxBins;
 
 // Pass-0 digit counts of one tile, and digit totals of every pass.
-template <class KeyFn>
+template <int IPT, class KeyFn>
 __device__ void sort_up0_tile(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
                               int tile, uint32_t* lds) {
   const int t = threadIdx.x;
   for (int i = t; i < plan.passes * kMaxBins; i += kBlock) lds[i] = 0;
-  const int base = tile * kSortTile;
-  uint32_t key[kSortIPT];
-  load_keys<kSortIPT>(kf, N, base + t, kBlock, key, sb.flag);
+  const int base = tile * kBlock * IPT;
+  uint32_t key[IPT];
+  load_keys<IPT>(kf, N, base + t, kBlock, key, sb.flag);
   __syncthreads();
 #pragma unroll
-  for (int q = 0; q < kSortIPT; ++q) {
+  for (int q = 0; q < IPT; ++q) {
     if (base + q * kBlock + t < N) {
       for (int p = 0; p < plan.passes; ++p) {
         const uint32_t dg = (key[q] >> plan.shift[p]) & ((1u << plan.bits[p]) - 1u);
@@ -368,7 +383,7 @@ __device__ __forceinline__ uint32_t tiles_before(const SortBufs& sb, int p, int 
 }
 
 // Pass p over one tile: stable rank, global offset, scatter.
-template <class KeyFn>
+template <int IPT, class KeyFn>
 __device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
                                int p, int tile, uint32_t* lds) {
   uint32_t* hist = lds;                                  // [waves][kMaxBins]
@@ -383,11 +398,11 @@ __device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, con
   int32_t* dk = sb.keys[(p + 1) & 1];
   int32_t* dv = sb.vals[(p + 1) & 1];
 
-  constexpr int R = kSortTile / kBlock;  // rounds per wave (blocked: a wave owns R*64 keys)
+  constexpr int R = IPT;  // rounds per wave (blocked: a wave owns R*64 keys)
   uint32_t key[R], dg[R], loc[R];
   int32_t val[R];
   uint64_t act[R];
-  const int wbase = tile * kSortTile + w * (R * kWave);
+  const int wbase = tile * kBlock * IPT + w * (R * kWave);
   if (p == 0) {
     load_keys<R>(kf, N, wbase + lane, kWave, key, sb.flag);
 #pragma unroll
@@ -447,22 +462,23 @@ __device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, con
 // Digit counts of pass p (p >= 1) for one tile of the previous pass's output:
 // counts in LDS, one store per (digit, tile) and one atomic per (digit, tile)
 // into the 16-tile group, so heavy Zipf digits never pile up on one counter.
+template <int IPT>
 __device__ void sort_up_tile(int N, const SortPlan& plan, const SortBufs& sb, int p, int tile,
                              uint32_t* lds) {
   const int t = threadIdx.x;
   const int bits = plan.bits[p], shift = plan.shift[p], bins = 1 << bits;
   for (int i = t; i < bins; i += kBlock) lds[i] = 0;
   const int32_t* sk = sb.keys[p & 1];
-  const int base = tile * kSortTile;
-  uint32_t key[kSortIPT];
+  const int base = tile * kBlock * IPT;
+  uint32_t key[IPT];
 #pragma unroll
-  for (int q = 0; q < kSortIPT; ++q) {
+  for (int q = 0; q < IPT; ++q) {
     const int e = base + q * kBlock + t;
     key[q] = e < N ? (uint32_t)sk[e] : 0u;
   }
   __syncthreads();
 #pragma unroll
-  for (int q = 0; q < kSortIPT; ++q)
+  for (int q = 0; q < IPT; ++q)
     if (base + q * kBlock + t < N) atomicAdd(&lds[(key[q] >> shift) & (uint32_t)(bins - 1)], 1u);
   __syncthreads();
   for (int dg = t; dg < bins; dg += kBlock) {
