@@ -314,7 +314,10 @@ def main():
     st = {k: float(np.mean([x[k] for x in samp])) for k in samp[0]}
     key_bits = max(1, int(w.V - 1).bit_length())
     passes = 0 if small else -(-key_bits // 9)
-    n_parts = min(-(-B // 16), 512)
+    # dense-partial slots: one per workgroup of the fused kernel (256 at most
+    # for the compile-time shapes d 64 / d 16 with window 5, 512 otherwise)
+    nt = -(-w.H // 16)
+    n_parts = min(-(-B // 16), 256 if (w.d, w.win, nt) in ((64, 5, 2), (16, 5, 1)) else 512)
     model = step_model(w, B, st, passes, n_parts)
     per = {k: (v[0] / v[1], v[1] / K) for k, v in kt.items() if v[1]}
     dom = max(per, key=lambda k: per[k][0] * per[k][1])

@@ -92,7 +92,8 @@ SortPlan make_plan(int key_range, int N) {
   pl.small = (N <= kSmallSortN && (kb - pl.part_bits) + pl.val_bits <= 32) ? 1 : 0;
   if (!pl.small) pl.part_bits = 0;
   const int rb = kb - pl.part_bits;  // bits the radix passes rank
-  pl.passes = (rb + kMaxDigitBits - 1) / kMaxDigitBits;
+  const int digit = pl.small ? kSmallDigitBits : kMaxDigitBits;
+  pl.passes = (rb + digit - 1) / digit;
   if (pl.passes > 0) {
     const int base = rb / pl.passes, rem = rb % pl.passes;
     int sh = 0;
@@ -288,15 +289,23 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   fa.plan = plan;
   fa.sb = sort_bufs(ctx, set);
   fa.ntiles = ceil_div(B, kTileRows);
-  fa.tiles_per_wg = ceil_div(fa.ntiles, ctx->max_parts);
+  const int shape8 = fwdbwd8_shape(cf.d, cf.win, ctx->NT);
+  fa.tiles_per_wg = ceil_div(fa.ntiles, shape8 ? std::min(ctx->max_parts, kF8MaxWorkgroups)
+                                               : ctx->max_parts);
   const int n_fb = ceil_div(fa.ntiles, fa.tiles_per_wg);
   fa.part_stride = ctx->part_stride;
   fa.invB = 1.0f / (float)B;
   {
-    size_t lds = fwdbwd_lds_floats(ctx->Hp, ctx->K) * 4;
-    if (fa.n_sort) lds = std::max(lds, part_sort_lds_words(kBlock) * 4);
     Timed tm(ctx, POLYGLOT_K_FWDBWD);
-    e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, fa.n_sort + n_fb, lds, tm.L);
+    if (shape8) {
+      size_t lds = fwdbwd8_lds_bytes(shape8);
+      if (fa.n_sort) lds = std::max(lds, part_sort_lds_words(kF8Threads) * 4);
+      e = launch_step_fwdbwd8(fa, shape8, fa.n_sort + n_fb, lds, tm.L);
+    } else {
+      size_t lds = fwdbwd_lds_floats(ctx->Hp, ctx->K) * 4;
+      if (fa.n_sort) lds = std::max(lds, part_sort_lds_words(kBlock) * 4);
+      e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, fa.n_sort + n_fb, lds, tm.L);
+    }
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "fwd/bwd launch");
   if (sorted_ev) {

@@ -29,7 +29,9 @@ constexpr int kSortShortTilesMaxN = 1 << 20;
 constexpr int kMaxDigitBits = 9;
 constexpr int kMaxBins = 1 << kMaxDigitBits;
 constexpr int kMaxPasses = 4;                      // 31-bit keys at most
-constexpr int kSmallSortN = 8192;                  // single-workgroup LDS sort up to this N
+constexpr int kSmallSortN = 8192;                  // partitioned LDS sort up to this N
+constexpr int kSmallDigitBits = 10;                // digit width of the partitioned sort's passes
+constexpr int kSmallBins = 1 << kSmallDigitBits;
 
 // Sticky device error bits.
 constexpr uint32_t kFlagBadId = 1u;
@@ -89,6 +91,20 @@ __device__ inline uint64_t match_digit(uint32_t digit, int bits, uint64_t active
     m &= set ? bal : ~bal;
   }
   return m;
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave with DPP moves: shifts by
+// 1, 2, 4, 8 inside each row of 16 lanes, then the last lane of row 0 (2) is
+// broadcast into row 1 (3), and lane 31 into rows 2 and 3.  Out-of-row
+// sources and masked rows contribute 0.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
 }
 
 __device__ inline float readlane_f(float v, int lane) {

@@ -1,0 +1,338 @@
+// Fused gather + forward + hinge + backward for compile-time shapes, one
+// workgroup of 8 waves per group of consecutive 16-window tiles (16x16x4 f32
+// MFMA), ending in the per-entry embedding gradient rows G.
+//
+// Per tile of 16 windows (rows r), with V = dz + dz~, dz or dz~ (per window,
+// H values each):
+//   X         the tile's embedding rows -- positions 0..win-1 and the
+//             corrupt row as position win -- staged in LDS once, laid out
+//             [position][column quad][window] so that both MFMA operand
+//             layouts read it without bank conflicts; the rows of tile k+1
+//             are loaded into registers while tile k computes, and the ids
+//             of tile k+2 are loaded at the same time;
+//   forward   Z = X W1^T: wave w takes hidden block nt = w % NT and the
+//             K-chunks kc = w / NT + (8 / NT) i; the corrupted copy only
+//             differs in block c, so z~ = z - zctr + zcor (§1 model, x~);
+//   epilogue  tanh, both scores, hinge mask, dz, dz~ and their sum; a lane
+//             takes one hidden unit of one row;
+//   dW1       dW1 += V^T X for the wave's (nt, chunks), held in registers
+//             across the workgroup's tiles and written once as its partial;
+//   G         G[e][:] = W1_j^T V for entry e = b(win+1) + j: context
+//             positions take dz + dz~, the true centre dz, the corrupt entry
+//             (j = win) dz~ through block c; 16x16 output tiles (position,
+//             16 columns) round-robin over the waves.
+// W1 is staged once per workgroup in LDS (row stride K + 4 floats, rows
+// >= H zero) and read from there as the B operand of the forward and of G.
+// A tile takes three workgroup barriers: X staged, forward partials, V.
+#pragma once
+#include "common.h"
+#include "launch.h"
+
+namespace pg {
+
+__device__ __forceinline__ f4 mfma16x4(float a, float b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+template <int D, int WIN, int NT>
+struct F8Shape {
+  static constexpr int HP = NT * 16;         // hidden units, padded
+  static constexpr int K = D * WIN;          // window vector length
+  static constexpr int C = WIN / 2;          // centre position
+  static constexpr int W1P = WIN + 1;        // positions incl. the corrupt row
+  static constexpr int DQ = D / 16;          // 16-column chunks per row
+  static constexpr int QD = D / 4;           // column quads per row
+  static constexpr int NCH = K / 16;         // K-chunks
+  static constexpr int KW = kF8Waves / NT;   // waves per hidden block
+  static constexpr int CPW = (NCH + KW - 1) / KW;  // chunks per wave
+  static constexpr int NGT = W1P * DQ;       // G output tiles per 16-window tile
+  static constexpr int GPW = (NGT + kF8Waves - 1) / kF8Waves;  // G tiles per wave
+  static constexpr int XF4 = W1P * QD * kTileRows;  // float4 pieces of X per tile
+  static constexpr int XPT = (XF4 + kF8Threads - 1) / kF8Threads;  // pieces per thread
+  static constexpr int S = K + 4;            // W1 row stride in LDS
+  // LDS, in floats
+  static constexpr int kW1 = HP * S;
+  static constexpr int kX = XF4 * 4;                       // one X buffer
+  static constexpr int kZp = kF8Waves * 3 * 4 * kWave;     // forward split-K partials
+  static constexpr int kVt = 3 * kTileRows * (HP + 1);
+  static constexpr int kRed = kF8Waves * (2 * HP + 2);
+  static constexpr int kLds = kW1 + 2 * kX + kZp + kVt + kRed;
+  static_assert(D % 16 == 0 && WIN % 2 == 1 && kF8Waves % NT == 0, "shape");
+  static_assert(HP <= 32, "one hidden unit per lane of each 32-lane row half");
+};
+
+template <int D, int WIN, int NT>
+__device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
+  using Sh = F8Shape<D, WIN, NT>;
+  constexpr int HP = Sh::HP, K = Sh::K, C = Sh::C, W1P = Sh::W1P, DQ = Sh::DQ, QD = Sh::QD;
+  constexpr int NCH = Sh::NCH, KW = Sh::KW, CPW = Sh::CPW, NGT = Sh::NGT, GPW = Sh::GPW;
+  constexpr int XF4 = Sh::XF4, XPT = Sh::XPT, S = Sh::S;
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);  // wave-uniform
+  const int n16 = lane & 15, g = lane >> 4;
+  const int nt_w = w % NT, kq = w / NT;  // this wave's hidden block and chunk set
+
+  float* w1s = lds;                       // [HP][K+4]
+  float* xl = w1s + Sh::kW1;              // [2][W1P][QD][16] float4
+  float* zp = xl + 2 * Sh::kX;            // [kq][3][nt][4][64]
+  float* vt = zp + Sh::kZp;               // [3][16][HP+1]
+  float* red = vt + Sh::kVt;              // [waves][2*HP+2]
+
+  const int tile0 = wg * a.tiles_per_wg;
+  const int ntl = min(a.tiles_per_wg, a.ntiles - tile0);  // tiles of this workgroup (>= 1)
+
+  // ids of the X pieces of this thread in tile `tile`: piece pi = t + 512 p
+  // covers window r = pi % 16, column quad (pi / 16) % QD, position
+  // pi / (16 QD) (position win: the corrupt id).  Rows >= B read row 0; an
+  // id outside [0, V) raises the flag and reads row 0.
+  auto load_ids = [&](int tile, int32_t (&id)[XPT]) {
+#pragma unroll
+    for (int p = 0; p < XPT; ++p) {
+      const int pi = t + kF8Threads * p;
+      const int r = pi % kTileRows, j = pi / (kTileRows * QD);
+      const int b = tile * kTileRows + r;
+      id[p] = 0;
+      if (pi < XF4 && b < a.B) id[p] = (j < WIN) ? a.windows[(size_t)b * WIN + j] : a.corrupt[b];
+    }
+    bool bad = false;
+#pragma unroll
+    for (int p = 0; p < XPT; ++p) {
+      const bool bk = (uint32_t)id[p] >= (uint32_t)a.V;
+      bad |= bk;
+      id[p] = bk ? 0 : id[p];
+    }
+    if (bad) atomicOr(a.flag, kFlagBadId);
+  };
+  auto load_x = [&](const int32_t (&id)[XPT], f4 (&xr)[XPT]) {
+#pragma unroll
+    for (int p = 0; p < XPT; ++p) {
+      const int pi = t + kF8Threads * p;
+      const int qq = (pi / kTileRows) % QD;
+      xr[p] = pi < XF4 ? ld4(a.E + (size_t)id[p] * D + 4 * qq) : kZero4;
+    }
+  };
+  auto store_x = [&](int buf, const f4 (&xr)[XPT]) {
+#pragma unroll
+    for (int p = 0; p < XPT; ++p) {
+      const int pi = t + kF8Threads * p;
+      if (pi < XF4) st4(xl + buf * Sh::kX + 4 * pi, xr[p]);
+    }
+  };
+
+  // ---- prologue: ids of the first two tiles, W1, the first tile's rows
+  int32_t ids[2][XPT];
+  load_ids(tile0, ids[0]);
+  {  // W1 into LDS (rows >= H zero); loads batched before the stores
+    constexpr int N4 = HP * (K / 4);
+    constexpr int U = (N4 + kF8Threads - 1) / kF8Threads;
+    f4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = u * kF8Threads + t;
+      const int n = i / (K / 4), k4 = i - n * (K / 4);
+      v[u] = (i < N4 && n < a.H) ? ld4(a.W1 + (size_t)n * K + 4 * k4) : kZero4;
+    }
+    if (ntl > 1) load_ids(tile0 + 1, ids[1]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = u * kF8Threads + t;
+      const int n = i / (K / 4), k4 = i - n * (K / 4);
+      if (i < N4) st4(w1s + n * S + 4 * k4, v[u]);
+    }
+  }
+  f4 xr[XPT];
+  load_x(ids[0], xr);
+  // epilogue lane map: hidden unit hn = lane % 32 of row 2w + lane / 32
+  const int hn = lane & 31, rsel = lane >> 5;
+  const float b1v = hn < a.H ? a.b1[hn] : 0.f;
+  const float w2v = hn < a.H ? a.w2[hn] : 0.f;
+  const float b2v = a.b2[0];
+  if (wg == 0 && t == 0) *a.long_count = 0u;  // read only by this step's later launches
+
+  f4 accW[CPW];
+#pragma unroll
+  for (int ci = 0; ci < CPW; ++ci) accW[ci] = kZero4;
+  float db1a = 0.f, dw2a = 0.f, lossa = 0.f;
+
+  for (int tt = 0; tt < ntl; ++tt) {
+    const int tile = tile0 + tt;
+    const int row0 = tile * kTileRows;
+    const int buf = tt & 1;
+    const float* X = xl + buf * Sh::kX;
+    store_x(buf, xr);
+    __syncthreads();  // X of this tile (and W1) staged
+    if (tt + 1 < ntl) {
+      load_x(ids[(tt + 1) & 1], xr);                           // rows of the next tile
+      if (tt + 2 < ntl) load_ids(tile + 2, ids[tt & 1]);       // ids two tiles ahead
+    }
+
+    // ---- forward: wave (nt_w, kq) over chunks kc = kq + KW ci; common
+    // blocks, true centre and corrupt centre accumulate separately
+    f4 zc = kZero4, zctr = kZero4, zcor = kZero4;
+#pragma unroll
+    for (int ci = 0; ci < CPW; ++ci) {
+      const int kc = kq + KW * ci;
+      if (kc < NCH) {
+        const int j = kc / DQ, qq = 4 * (kc % DQ) + g;
+        const f4 xa = ld4(X + 4 * ((j * QD + qq) * kTileRows + n16));
+        const f4 wb = ld4(w1s + (nt_w * 16 + n16) * S + kc * 16 + 4 * g);
+        if (j != C) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) zc = mfma16x4(xa[q], wb[q], zc);
+        } else {
+          const f4 xt = ld4(X + 4 * ((WIN * QD + qq) * kTileRows + n16));
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            zctr = mfma16x4(xa[q], wb[q], zctr);
+            zcor = mfma16x4(xt[q], wb[q], zcor);
+          }
+        }
+      }
+    }
+    // partials [kq][type][nt][component][lane] (component-major: a reader of
+    // one component of every lane touches consecutive words)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      zp[(((kq * 3 + 0) * NT + nt_w) * 4 + i) * kWave + lane] = zc[i];
+      zp[(((kq * 3 + 1) * NT + nt_w) * 4 + i) * kWave + lane] = zctr[i];
+      zp[(((kq * 3 + 2) * NT + nt_w) * 4 + i) * kWave + lane] = zcor[i];
+    }
+    __syncthreads();  // forward partials written
+
+    // ---- epilogue: lane (hn, rsel) takes hidden unit hn of row 2w + rsel
+    {
+      const int r = 2 * w + rsel;
+      const int row = row0 + r;
+      const int nt = hn >> 4, src = (hn & 15) + 16 * (r >> 2), comp = r & 3;
+      float Zc = 0.f, Zctr = 0.f, Zcor = 0.f;
+      if (hn < HP) {
+#pragma unroll
+        for (int v = 0; v < KW; ++v) {
+          Zc += zp[(((v * 3 + 0) * NT + nt) * 4 + comp) * kWave + src];
+          Zctr += zp[(((v * 3 + 1) * NT + nt) * 4 + comp) * kWave + src];
+          Zcor += zp[(((v * 3 + 2) * NT + nt) * 4 + comp) * kWave + src];
+        }
+      }
+      const float z = b1v + (Zc + Zctr);
+      const float zt = b1v + (Zc + Zcor);
+      const float h = tanh_fast(z), ht = tanh_fast(zt);
+      // h - h~ = tanh(z - z~) (1 - h h~), z - z~ = zctr - zcor without
+      // cancellation against the common part
+      const float hmh = tanh_fast(Zctr - Zcor) * (1.f - h * ht);
+      float ps = w2v * h, pst = w2v * ht;
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) {
+        ps += __shfl_xor(ps, o);
+        pst += __shfl_xor(pst, o);
+      }
+      const float mg = 1.f - (b2v + ps) + (b2v + pst);
+      const bool on = row < a.B && mg > 0.f;  // hinge active (derivative 0 at margin 0)
+      const float gst = on ? a.invB : 0.f;    // d loss/d s~ = m/B, d loss/d s = -m/B
+      const float gw = gst * w2v;
+      const float dz = -gw * (1.f - h * h);
+      const float dzt = gw * (1.f - ht * ht);
+      const float dsum = gw * hmh * (h + ht);  // dz + dz~ = g w2 (h - h~)(h + h~)
+      if (hn < HP) {
+        vt[(0 * kTileRows + r) * (HP + 1) + hn] = dsum;
+        vt[(1 * kTileRows + r) * (HP + 1) + hn] = dz;
+        vt[(2 * kTileRows + r) * (HP + 1) + hn] = dzt;
+      }
+      db1a += dsum;
+      dw2a -= gst * hmh;  // -(m/B) h + (m/B) h~
+      if (hn == 0) lossa += on ? mg : 0.f;
+    }
+    __syncthreads();  // V written
+
+    // ---- dW1 += V^T X for this wave's (nt, chunks).  A operand: lane (n16,
+    // g) holds V[4ii+g][nt*16 + n16]; B operand: X[4ii+g][16kc + n16].
+    {
+      float vc[3][4];
+#pragma unroll
+      for (int ty = 0; ty < 3; ++ty)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii)
+          vc[ty][ii] = vt[(ty * kTileRows + 4 * ii + g) * (HP + 1) + nt_w * 16 + n16];
+#pragma unroll
+      for (int ci = 0; ci < CPW; ++ci) {
+        const int kc = kq + KW * ci;
+        if (kc < NCH) {
+          const int j = kc / DQ, qq = 4 * (kc % DQ) + (n16 >> 2);
+#pragma unroll
+          for (int ii = 0; ii < 4; ++ii) {
+            const float xb = X[4 * ((j * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
+            if (j != C) {
+              accW[ci] = mfma16x4(vc[0][ii], xb, accW[ci]);
+            } else {
+              const float xc = X[4 * ((WIN * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
+              accW[ci] = mfma16x4(vc[1][ii], xb, accW[ci]);
+              accW[ci] = mfma16x4(vc[2][ii], xc, accW[ci]);
+            }
+          }
+        }
+      }
+    }
+
+    // ---- G: output tiles ot = w + 8u (position j = ot / DQ, columns cb*16).
+    // A operand: lane (r = n16, g) holds V_ty[r][4q + g]; B operand: lane
+    // (col = n16, g) holds W1[4q + g][jj*D + cb*16 + col].
+#pragma unroll
+    for (int u = 0; u < GPW; ++u) {
+      const int ot = w + kF8Waves * u;
+      if (ot < NGT) {
+        const int j = ot / DQ, cb = ot - (ot / DQ) * DQ;
+        const int ty = (j == WIN) ? 2 : (j == C ? 1 : 0);
+        const int jj = (j == WIN) ? C : j;
+        f4 acc = kZero4;
+#pragma unroll
+        for (int q = 0; q < HP / 4; ++q) {
+          const float av = vt[(ty * kTileRows + n16) * (HP + 1) + 4 * q + g];
+          const float bv = w1s[(4 * q + g) * S + jj * D + cb * 16 + n16];
+          acc = mfma16x4(av, bv, acc);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = row0 + 4 * g + i;
+          if (row < a.B) a.G[((size_t)row * W1P + j) * D + cb * 16 + n16] = acc[i];
+        }
+      }
+    }
+  }
+
+  // ---- this workgroup's partial of the dense gradients.  Slot layout:
+  // dW1 [Hp][K], db1 [Hp], dw2 [Hp], loss, db2.
+  float* P = a.part + (size_t)wg * a.part_stride;
+#pragma unroll
+  for (int ci = 0; ci < CPW; ++ci) {
+    const int kc = kq + KW * ci;
+    if (kc < NCH) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) P[(nt_w * 16 + 4 * g + i) * K + kc * 16 + n16] = accW[ci][i];
+    }
+  }
+  // db1, dw2 (per hidden unit: the two row halves of the wave, then the
+  // waves in order), loss (one value per wave); db2 is identically 0 (both
+  // scores share b2)
+  db1a += __shfl_xor(db1a, 32);
+  dw2a += __shfl_xor(dw2a, 32);
+  for (int o = 1; o < kWave; o <<= 1) lossa += __shfl_xor(lossa, o);
+  float* rw = red + w * (2 * HP + 2);
+  if (rsel == 0 && hn < HP) {
+    rw[hn] = db1a;
+    rw[HP + hn] = dw2a;
+  }
+  if (lane == 0) {
+    rw[2 * HP] = lossa;
+    rw[2 * HP + 1] = 0.f;
+  }
+  __syncthreads();
+  if (w == 0) {
+    for (int e = lane; e < 2 * HP + 2; e += kWave) {
+      float s = red[e];
+#pragma unroll
+      for (int v = 1; v < kF8Waves; ++v) s += red[v * (2 * HP + 2) + e];
+      P[HP * K + e] = s;
+    }
+  }
+}
+
+}  // namespace pg

@@ -37,6 +37,7 @@
 #include "seg_dev.h"
 #include "sort_dev.h"
 #include "fwdbwd_dev.h"
+#include "fwdbwd8_dev.h"
 #include "update_dev.h"
 #include "aux_dev.h"
 
@@ -55,6 +56,21 @@ __global__ __launch_bounds__(kBlock, (NT == 1 || (NT == 2 && CPW <= 5)) ? 2 : 1)
     return;
   }
   fwdbwd_wg<NT, CPW, D, WIN>(a, blockIdx.x - a.n_sort, lds_f);
+}
+
+// The same step for the compile-time shapes, 8 waves per workgroup; the
+// sort role (small batches) runs in 512-thread workgroups.
+template <int D, int WIN, int NT>
+__global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {
+  extern __shared__ float lds_f[];
+  if ((int)blockIdx.x < a.n_sort) {
+    const StepKeys kf = step_keys(a.windows, a.corrupt, a.win, a.V);
+    part_sort<kF8Threads>(kf, a.N, a.plan, blockIdx.x, a.sb.keys[a.plan.passes & 1],
+                          a.sb.vals[a.plan.passes & 1], a.flag,
+                          reinterpret_cast<uint32_t*>(lds_f));
+    return;
+  }
+  fwdbwd8_wg<D, WIN, NT>(a, blockIdx.x - a.n_sort, lds_f);
 }
 
 // =============================================================== sort
@@ -130,14 +146,25 @@ static hipError_t launch_fwdbwd_nt(const FwdArgs& a, int cpw, int grid, size_t l
   return pg_launch(k_step_fwdbwd<NT, 8, 0, 0>, dim3(grid), dim3(kBlock), lds, L, a);
 }
 
+int fwdbwd8_shape(int d, int win, int NT) {
+  if (d == 64 && win == 5 && NT == 2) return 1;  // the Polyglot-scale model, H <= 32
+  if (d == 16 && win == 5 && NT == 1) return 2;  // the small model, H <= 16
+  return 0;
+}
+
+size_t fwdbwd8_lds_bytes(int shape) {
+  return (shape == 1 ? F8Shape<64, 5, 2>::kLds : F8Shape<16, 5, 1>::kLds) * sizeof(float);
+}
+
+hipError_t launch_step_fwdbwd8(const FwdArgs& a, int shape, int grid, size_t lds,
+                               const Launch& L) {
+  if (shape == 1)
+    return pg_launch(k_step_fwdbwd8<64, 5, 2>, dim3(grid), dim3(kF8Threads), lds, L, a);
+  return pg_launch(k_step_fwdbwd8<16, 5, 1>, dim3(grid), dim3(kF8Threads), lds, L, a);
+}
+
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
                               const Launch& L) {
-  // compile-time shapes: the Polyglot-scale model (d 64, window 5, H <= 32)
-  // and the small test model (d 16, window 5, H <= 16)
-  if (a.d == 64 && a.win == 5 && NT == 2)
-    return pg_launch(k_step_fwdbwd<2, 5, 64, 5>, dim3(grid), dim3(kBlock), lds, L, a);
-  if (a.d == 16 && a.win == 5 && NT == 1)
-    return pg_launch(k_step_fwdbwd<1, 2, 16, 5>, dim3(grid), dim3(kBlock), lds, L, a);
   if (NT == 1) return launch_fwdbwd_nt<1>(a, cpw, grid, lds, L);
   if (NT == 2) return launch_fwdbwd_nt<2>(a, cpw, grid, lds, L);
   return launch_fwdbwd_nt<4>(a, cpw, grid, lds, L);

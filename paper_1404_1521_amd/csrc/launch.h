@@ -113,6 +113,15 @@ struct GatherArgs {
 
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
                               const Launch& L);
+// 8-wave fused kernel for the compile-time shapes: fwdbwd8_shape() gives the
+// shape id (0: not covered), fwdbwd8_lds_bytes() its LDS.
+int fwdbwd8_shape(int d, int win, int NT);
+size_t fwdbwd8_lds_bytes(int shape);
+constexpr int kF8Waves = 8;
+constexpr int kF8Threads = kF8Waves * kWave;  // 512
+constexpr int kF8MaxWorkgroups = 256;         // one workgroup per CU
+hipError_t launch_step_fwdbwd8(const FwdArgs& a, int shape, int grid, size_t lds,
+                               const Launch& L);
 // First sort launch (whole small sort, or pass-0 tile counts) and, for
 // multi-tile plans, every later pass; clears *long_count if not NULL.
 hipError_t launch_sort_step(const StepKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,

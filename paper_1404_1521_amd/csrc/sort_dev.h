@@ -86,28 +86,53 @@ __device__ inline void block_exclusive_scan(uint32_t* v, int n, uint32_t* wave_s
   const uint32_t a = (2 * t < n) ? v[2 * t] : 0u;
   const uint32_t b = (2 * t + 1 < n) ? v[2 * t + 1] : 0u;
   const uint32_t s = a + b;
-  uint32_t inc = s;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t y = __shfl_up(inc, o);
-    if (lane >= o) inc += y;
-  }
+  const uint32_t inc = wave_incl_scan(s);
   if (lane == kWave - 1) wave_sums[w] = inc;
   __syncthreads();
   uint32_t base = 0;
-  for (int i = 0; i < w; ++i) base += wave_sums[i];
+#pragma unroll
+  for (int i = 0; i < NTH / kWave; ++i) base += i < w ? wave_sums[i] : 0u;  // loads in parallel
   const uint32_t ex = base + inc - s;
   if (2 * t < n) v[2 * t] = ex;
   if (2 * t + 1 < n) v[2 * t + 1] = ex + a;
   __syncthreads();
 }
 
+// Exclusive scan over `n` (<= 16*NTH) values in LDS `v`, in place, by one
+// workgroup of NTH threads: thread t takes a run of ceil(n/NTH) values.
+template <int NTH>
+__device__ inline void block_exclusive_scan_runs(uint32_t* v, int n, uint32_t* wave_sums) {
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
+  const int E = ceil_div(n, NTH), b0 = t * E;
+  uint32_t s = 0;
+  for (int i = 0; i < E; ++i)
+    if (b0 + i < n) s += v[b0 + i];
+  const uint32_t inc = wave_incl_scan(s);
+  if (lane == kWave - 1) wave_sums[w] = inc;
+  __syncthreads();
+  uint32_t run = inc - s;
+#pragma unroll
+  for (int i = 0; i < NTH / kWave; ++i) run += i < w ? wave_sums[i] : 0u;  // loads in parallel
+  for (int i = 0; i < E; ++i) {
+    if (b0 + i < n) {
+      const uint32_t c = v[b0 + i];
+      v[b0 + i] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+}
+
 // Stable ranks of up to R rounds of 64 keys held by this wave (round-major
-// order); rounds r >= nr and lanes with act[r] false are skipped.  hist is
-// this wave's zeroed LDS counter array.  On return rank[r] is the number of
-// earlier keys of the wave with the same digit, and hist holds the counts.
+// order); rounds r >= nr and lanes with act[r] false are skipped.  The
+// wave's zeroed LDS counter of digit d is hist[d * stride].  On return
+// rank[r] is the number of earlier keys of the wave with the same digit, and
+// the counters hold the wave's digit counts.
 template <int R>
 __device__ __forceinline__ void wave_rank(const uint32_t (&dg)[R], const uint64_t (&act)[R],
-                                          int nr, int bits, uint32_t* hist, uint32_t (&rank)[R]) {
+                                          int nr, int bits, uint32_t* hist, uint32_t (&rank)[R],
+                                          int stride = 1) {
   uint32_t old[R], below_leader[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -119,7 +144,7 @@ __device__ __forceinline__ void wave_rank(const uint32_t (&dg)[R], const uint64_
       const uint32_t leader = peers ? (uint32_t)(__ffsll((unsigned long long)peers) - 1) : 0u;
       below_leader[r] = below | (leader << 16);
       if (((act[r] >> lane_id()) & 1ull) && below == 0)
-        old[r] = atomicAdd(&hist[dg[r]], (uint32_t)__popcll(peers));
+        old[r] = atomicAdd(&hist[dg[r] * stride], (uint32_t)__popcll(peers));
     }
   }
 #pragma unroll
@@ -135,24 +160,31 @@ constexpr int kRankBatch = 8;  // rounds ranked per batch (registers bounded)
 // Stable LSD radix passes of one workgroup (NTH threads) over M <= kSmallSortN
 // packed words in LDS, ping-pong between src and dst.  The digit of pass p
 // is (word >> (shift0 + plan.shift[p])) & (2^plan.bits[p] - 1).  Wave w
-// ranks a contiguous run of the words (wave_rank), the per-wave counts give
-// every wave's offset for every digit, and the words are scattered.
-// Returns the buffer holding the sorted words.
+// ranks a contiguous run of the words (wave_rank) into its column of the
+// counter table hist[digit][wave]; one exclusive scan of that table in
+// (digit, wave) order gives every wave the output offset of every digit, and
+// the words are scattered.  Returns the buffer holding the sorted words.
 template <int NTH>
 __device__ uint32_t* lds_lsd_passes(uint32_t* src, uint32_t* dst, int M, const SortPlan& plan,
                                     int shift0, uint16_t* rank16, uint32_t* hist,
                                     uint32_t* misc) {
   constexpr int R = kRankBatch, NW = NTH / kWave;
-  const int t = threadIdx.x, lane = t & (kWave - 1);
-  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
-  uint32_t* myhist = hist + w * kMaxBins;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  // counter of digit d for wave w at hist[d * (NW + 1) + w]; the extra
+  // column (always 0) spreads the digits of one wave over the LDS banks
+  constexpr int CS = NW + 1;
+  uint32_t* mycol = hist + w;
   // wave w owns words [w*per, (w+1)*per), per a multiple of 64
   const int per = ceil_div(ceil_div(M, NW), kWave) * kWave;
   const int beg = w * per;
   const int nr = max(0, min(per, M - beg) + kWave - 1) / kWave;
   for (int p = 0; p < plan.passes; ++p) {
     const int bits = plan.bits[p], shift = plan.shift[p] + shift0, bins = 1 << bits;
-    for (int i = lane; i < bins; i += kWave) myhist[i] = 0;
+    for (int d = lane; d < bins; d += kWave) {
+      mycol[d * CS] = 0;
+      if (w == 0) hist[d * CS + NW] = 0;  // the padding column
+    }
     wave_lds_sync();
     for (int r0 = 0; r0 < nr; r0 += R) {  // the wave's counters carry over batches
       uint32_t dg[R], rank[R];
@@ -164,7 +196,7 @@ __device__ uint32_t* lds_lsd_passes(uint32_t* src, uint32_t* dst, int M, const S
         act[r] = __ballot(ok);
         dg[r] = ((ok ? src[i] : 0u) >> shift) & (uint32_t)(bins - 1);
       }
-      wave_rank<R>(dg, act, min(R, nr - r0), bits, myhist, rank);
+      wave_rank<R>(dg, act, min(R, nr - r0), bits, mycol, rank, CS);
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         const int i = beg + (r0 + r) * kWave + lane;
@@ -172,23 +204,7 @@ __device__ uint32_t* lds_lsd_passes(uint32_t* src, uint32_t* dst, int M, const S
       }
     }
     __syncthreads();
-    // per-digit totals -> digit starts; per-wave offsets
-    for (int d = t; d < bins; d += NTH) {
-      uint32_t s = 0;
-      for (int q = 0; q < NW; ++q) {
-        const uint32_t c = hist[q * kMaxBins + d];
-        hist[q * kMaxBins + d] = s;  // exclusive over waves
-        s += c;
-      }
-      dst[d] = s;  // dst is free until the scatter below: digit totals
-    }
-    __syncthreads();
-    block_exclusive_scan<NTH>(dst, bins, misc);
-    for (int d = t; d < bins; d += NTH) {
-      const uint32_t start = dst[d];
-      for (int q = 0; q < NW; ++q) hist[q * kMaxBins + d] += start;
-    }
-    __syncthreads();
+    block_exclusive_scan_runs<NTH>(hist, bins * CS, misc);  // offsets by (digit, wave)
     for (int r0 = 0; r0 < nr; r0 += R) {
       uint32_t word[R], rk[R];
 #pragma unroll
@@ -202,7 +218,7 @@ __device__ uint32_t* lds_lsd_passes(uint32_t* src, uint32_t* dst, int M, const S
       for (int r = 0; r < R; ++r) {
         const int i = beg + (r0 + r) * kWave + lane;
         if (r0 + r < nr && i < M) {
-          const uint32_t pos = myhist[(word[r] >> shift) & (uint32_t)(bins - 1)] + rk[r];
+          const uint32_t pos = mycol[((word[r] >> shift) & (uint32_t)(bins - 1)) * CS] + rk[r];
           if (pos < (uint32_t)M) dst[pos] = word[r];
         }
       }
@@ -225,11 +241,11 @@ __device__ uint32_t* lds_lsd_passes(uint32_t* src, uint32_t* dst, int M, const S
 // below p, which it counts itself while reading the keys.  Equal keys end up
 // contiguous and in entry order -- what the segmented sum needs; the order
 // between distinct keys is fixed by the keys alone.
-constexpr int kPartBits = 4;
+constexpr int kPartBits = 7;
 constexpr int kPartSortThreads = 1024;  // one workgroup of 16 waves per partition
 constexpr int kPartSortMisc = 32;       // scan scratch: wave sums, then the partition total
 __host__ __device__ constexpr size_t part_sort_lds_words(int nth) {
-  return 2 * kSmallSortN + kSmallSortN / 2 + (size_t)(nth / kWave) * kMaxBins + kPartSortMisc;
+  return 2 * kSmallSortN + kSmallSortN / 2 + (size_t)(nth / kWave + 1) * kSmallBins + kPartSortMisc;
 }
 
 template <int NTH, class KeyFn>
@@ -240,8 +256,8 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
   uint32_t* bufA = lds;
   uint32_t* bufB = bufA + kSmallSortN;
   uint16_t* rank16 = reinterpret_cast<uint16_t*>(bufB + kSmallSortN);
-  uint32_t* hist = bufB + kSmallSortN + kSmallSortN / 2;  // [waves][kMaxBins]
-  uint32_t* misc = hist + NW * kMaxBins;                  // kPartSortMisc words
+  uint32_t* hist = bufB + kSmallSortN + kSmallSortN / 2;  // [kSmallBins][waves + 1]
+  uint32_t* misc = hist + (NW + 1) * kSmallBins;          // kPartSortMisc words
   const int t = threadIdx.x;
   const int vb = plan.val_bits, pb = plan.part_bits;
   const uint32_t pmask = (1u << pb) - 1u;
