@@ -46,7 +46,7 @@ struct polyglot_ctx {
              ev_done[2] = {nullptr, nullptr};
   int device = 0;
   int Hp = 0, NT = 0, K = 0, c = 0, cpw = 0;
-  int max_entries = 0, max_tiles = 0, max_groups = 0, max_parts = 0, max_chunks = 0;
+  int max_entries = 0, max_tiles = 0, max_parts = 0, max_chunks = 0;
   int seg_stride = 0, part_stride = 0;
   Workspace ws{};
   std::vector<void*> allocs;
@@ -103,8 +103,7 @@ SortPlan make_plan(int key_range, int N) {
       sh += pl.bits[p];
     }
   }
-  pl.ipt = N <= kSortShortTilesMaxN ? kSortIptShort : kSortIptLong;
-  pl.ntiles = ceil_div(N, kBlock * pl.ipt);
+  pl.ntiles = ceil_div(N, kSortTileKeys);
   return pl;
 }
 
@@ -115,23 +114,21 @@ SortBufs sort_bufs(polyglot_ctx* ctx, int set) {
   sb.vals[0] = ctx->ws.vals[2 * set];
   sb.vals[1] = ctx->ws.vals[2 * set + 1];
   sb.totals = ctx->ws.totals[set];
-  sb.counts = ctx->ws.counts;
-  sb.gcounts = ctx->ws.gcounts[set];
+  sb.status = ctx->ws.status[set];
+  sb.tile_ctr = ctx->ws.tile_ctr[set];
+  sb.epoch = ctx->ws.epoch[set];
   sb.max_tiles = ctx->max_tiles;
-  sb.max_groups = ctx->max_groups;
   sb.flag = ctx->ws.flag;
   return sb;
 }
 
-// Counters a multi-tile sort accumulates atomically (per-tile counts are
-// overwritten by every sort and need no clearing).
+// Counters a multi-tile sort accumulates atomically (the look-back words are
+// told apart by the sort epoch and need no clearing).
 ZeroRanges sort_zero_ranges(polyglot_ctx* ctx, const SortPlan& plan, int set) {
   ZeroRanges z{};
   if (plan.small) return z;
   z.p[0] = ctx->ws.totals[set];
   z.n[0] = (size_t)kMaxPasses * kMaxBins;
-  z.p[2] = ctx->ws.gcounts[set];
-  z.n[2] = (size_t)plan.passes * kMaxBins * ctx->max_groups;
   return z;
 }
 
@@ -435,11 +432,7 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   ctx->Hp = 16 * ctx->NT;
   ctx->cpw = ceil_div(ctx->K / 16, kWavesPerBlock);
   ctx->max_entries = std::max({c.max_batch * (c.win + 1), c.max_scatter, 1});
-  // most tiles any list up to max_entries keys is cut into
-  ctx->max_tiles = std::max(ceil_div(std::min(ctx->max_entries, kSortShortTilesMaxN),
-                                     kBlock * kSortIptShort),
-                            ceil_div(ctx->max_entries, kBlock * kSortIptLong));
-  ctx->max_groups = ceil_div(ctx->max_tiles, kCountGroup);
+  ctx->max_tiles = ceil_div(ctx->max_entries, kSortTileKeys);
   ctx->max_parts = std::min(ceil_div(c.max_batch, kTileRows), 512);
   // most chunks any call can cut (short chunks apply up to 131072 entries)
   ctx->max_chunks = std::max(ceil_div(std::min(ctx->max_entries, 131072), 16),
@@ -450,17 +443,20 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   hipError_t e = hipGetDevice(&ctx->device);
   Workspace& ws = ctx->ws;
   const size_t me = (size_t)ctx->max_entries;
-  const size_t ncount = (size_t)kMaxPasses * kMaxBins * ctx->max_tiles;
-  const size_t ngcount = (size_t)kMaxPasses * kMaxBins * ctx->max_groups;
+  // passes of the largest key range this context sorts
+  const int key_bits = bits_for((uint32_t)std::max({c.V, c.max_rows, 2}));
+  const int max_passes = (key_bits + kMaxDigitBits - 1) / kMaxDigitBits;
+  const size_t nstatus = (size_t)max_passes * kMaxBins * ctx->max_tiles;
   for (int k = 0; k < 4; ++k) {
     if (e == hipSuccess) e = alloc(ctx, &ws.keys[k], me);
     if (e == hipSuccess) e = alloc(ctx, &ws.vals[k], me);
   }
   for (int k = 0; k < 2; ++k) {
     if (e == hipSuccess) e = alloc(ctx, &ws.totals[k], (size_t)kMaxPasses * kMaxBins);
-    if (e == hipSuccess) e = alloc(ctx, &ws.gcounts[k], ngcount);
+    if (e == hipSuccess) e = alloc(ctx, &ws.status[k], nstatus);
+    if (e == hipSuccess) e = alloc(ctx, &ws.tile_ctr[k], (size_t)kMaxPasses);
+    if (e == hipSuccess) e = alloc(ctx, &ws.epoch[k], 1);
   }
-  if (e == hipSuccess) e = alloc(ctx, &ws.counts, ncount);
   if (e == hipSuccess) e = alloc(ctx, &ws.G, (size_t)c.max_batch * (c.win + 1) * c.d);
   if (e == hipSuccess) e = alloc(ctx, &ws.part, (size_t)ctx->max_parts * ctx->part_stride);
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_end, (size_t)std::max(c.V, c.max_rows));
@@ -472,9 +468,10 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   for (int k = 0; k < 2; ++k) {
     if (e == hipSuccess)
       e = hipMemset(ws.totals[k], 0, sizeof(uint32_t) * kMaxPasses * kMaxBins);
-    if (e == hipSuccess) e = hipMemset(ws.gcounts[k], 0, sizeof(uint32_t) * ngcount);
+    if (e == hipSuccess) e = hipMemset(ws.status[k], 0, sizeof(unsigned long long) * nstatus);
+    if (e == hipSuccess) e = hipMemset(ws.tile_ctr[k], 0, sizeof(uint32_t) * kMaxPasses);
+    if (e == hipSuccess) e = hipMemset(ws.epoch[k], 0, sizeof(uint32_t));
   }
-  if (e == hipSuccess) e = hipMemset(ws.counts, 0, sizeof(uint32_t) * ncount);
   if (e == hipSuccess) e = hipMemset(ws.long_count, 0, sizeof(uint32_t));
   if (e == hipSuccess) e = hipMemset(ws.flag, 0, sizeof(uint32_t));
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);

@@ -20,12 +20,7 @@ constexpr int kMaxD = 256;
 constexpr int kMaxLdsBytes = 160 * 1024;  // LDS per workgroup on gfx950
 
 // Radix sort of (row id, entry) pairs.
-// Multi-tile sort: keys per thread of a tile.  Short tiles (1024 keys) up to
-// kSortShortTilesMaxN keys spread a mid-sized list over many workgroups;
-// longer lists use 4096-key tiles, which keep the per-tile counters small.
-constexpr int kSortIptShort = 4;
-constexpr int kSortIptLong = 16;
-constexpr int kSortShortTilesMaxN = 1 << 20;
+constexpr int kSortTileKeys = 4096;                // multi-tile sort: keys per tile
 constexpr int kMaxDigitBits = 9;
 constexpr int kMaxBins = 1 << kMaxDigitBits;
 constexpr int kMaxPasses = 4;                      // 31-bit keys at most
@@ -41,8 +36,7 @@ struct SortPlan {
   int passes;               // 0 when N <= 1 (nothing to order)
   int shift[kMaxPasses];
   int bits[kMaxPasses];
-  int ntiles;               // multi-tile path: tiles of kBlock * ipt keys
-  int ipt;                  // multi-tile path: keys per thread of a tile
+  int ntiles;               // multi-tile path: tiles of kSortTileKeys keys
   int small;                // 1: partitioned sort (one launch, 2^part_bits workgroups)
   int val_bits;             // small path packs (key >> part_bits) << val_bits | entry
   int part_bits;            // small path: partitions by the low key bits
@@ -57,8 +51,9 @@ struct Workspace {
   int32_t* keys[4];         // sorted keys [max_entries]
   int32_t* vals[4];         // entry ids   [max_entries]
   uint32_t* totals[2];      // [kMaxPasses][kMaxBins] global digit counts
-  uint32_t* counts;         // [kMaxPasses][kMaxBins][max_tiles] per-tile digit counts
-  uint32_t* gcounts[2];     // [kMaxPasses][kMaxBins][max_groups] per-16-tile digit counts
+  unsigned long long* status[2];  // [kMaxPasses][max_tiles][kMaxBins] look-back words
+  uint32_t* tile_ctr[2];    // [kMaxPasses] tile id counters
+  uint32_t* epoch[2];       // sort epoch of each set
   // step
   float* G;                 // [max_batch*(win+1)][d] per-entry embedding gradients
   float* part;              // [max_parts][part_stride] dense-gradient partials

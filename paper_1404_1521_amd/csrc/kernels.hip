@@ -86,42 +86,31 @@ __global__ __launch_bounds__(kPartSortThreads) void k_sort_part(KeyFn kf, int N,
                               sb.vals[plan.passes & 1], sb.flag, lds);
 }
 
-// Pass-0 digit counts of every tile of a large list (clears the task list
-// when given one).
-template <int IPT, class KeyFn>
-__global__ __launch_bounds__(kBlock) void k_sort_first(KeyFn kf, int N, SortPlan plan, SortBufs sb,
-                                                       uint32_t* long_count) {
+// Digit totals of a large list (clears the segment task list when given one).
+template <class KeyFn>
+__global__ __launch_bounds__(kBlock) void k_os_hist(KeyFn kf, int N, SortPlan plan, SortBufs sb,
+                                                    uint32_t* long_count) {
   extern __shared__ uint32_t lds[];
   if (long_count && blockIdx.x == 0 && threadIdx.x == 0) *long_count = 0u;
-  sort_up0_tile<IPT>(kf, N, plan, sb, blockIdx.x, lds);
+  os_hist(kf, N, plan, sb, blockIdx.x, lds);
 }
 
-template <int IPT, class KeyFn>
-__global__ __launch_bounds__(kBlock) void k_sort_down(KeyFn kf, int N, SortPlan plan, SortBufs sb,
-                                                      int p) {
+// One radix pass over the tiles of a large list.
+template <class KeyFn>
+__global__ __launch_bounds__(kOsThreads) void k_os_pass(KeyFn kf, int N, SortPlan plan,
+                                                        SortBufs sb, int p) {
   extern __shared__ uint32_t lds[];
-  sort_down_tile<IPT>(kf, N, plan, sb, p, blockIdx.x, lds);
+  os_pass(kf, N, plan, sb, p, lds);
 }
 
-template <int IPT>
-__global__ __launch_bounds__(kBlock) void k_sort_up(int N, SortPlan plan, SortBufs sb, int p) {
-  extern __shared__ uint32_t lds[];
-  sort_up_tile<IPT>(N, plan, sb, p, blockIdx.x, lds);
-}
-
-template <int IPT, class KeyFn>
+template <class KeyFn>
 static hipError_t launch_tiled_sort(const KeyFn& kf, int N, const SortPlan& plan,
                                     const SortBufs& sb, uint32_t* long_count, const Launch& L) {
-  hipError_t e = pg_launch(k_sort_first<IPT, KeyFn>, dim3(plan.ntiles), dim3(kBlock),
-                           kUp0LdsWords * 4, L, kf, N, plan, sb, long_count);
-  for (int p = 0; p < plan.passes && e == hipSuccess; ++p) {
-    if (p > 0)
-      e = pg_launch(k_sort_up<IPT>, dim3(plan.ntiles), dim3(kBlock), kMaxBins * 4, L, N, plan,
-                    sb, p);
-    if (e == hipSuccess)
-      e = pg_launch(k_sort_down<IPT, KeyFn>, dim3(plan.ntiles), dim3(kBlock), kDownLdsWords * 4,
-                    L, kf, N, plan, sb, p);
-  }
+  hipError_t e = pg_launch(k_os_hist<KeyFn>, dim3(ceil_div(N, kBlock * kOsHistIpt)), dim3(kBlock),
+                           kOsHistLdsWords * 4, L, kf, N, plan, sb, long_count);
+  for (int p = 0; p < plan.passes && e == hipSuccess; ++p)
+    e = pg_launch(k_os_pass<KeyFn>, dim3(plan.ntiles), dim3(kOsThreads), kOsPassLdsWords * 4, L,
+                  kf, N, plan, sb, p);
   return e;
 }
 
@@ -131,9 +120,7 @@ static hipError_t launch_sort(const KeyFn& kf, int N, const SortPlan& plan, cons
   if (plan.small)
     return pg_launch(k_sort_part<KeyFn>, dim3(1 << plan.part_bits), dim3(kPartSortThreads),
                      part_sort_lds_words(kPartSortThreads) * 4, L, kf, N, plan, sb, long_count);
-  if (plan.ipt == kSortIptShort)
-    return launch_tiled_sort<kSortIptShort>(kf, N, plan, sb, long_count, L);
-  return launch_tiled_sort<kSortIptLong>(kf, N, plan, sb, long_count, L);
+  return launch_tiled_sort(kf, N, plan, sb, long_count, L);
 }
 
 // =============================================================== launchers

@@ -9,12 +9,9 @@
 // Two variants:
 //  * small (up to kSmallSortN entries): a partitioned sort, one launch of
 //    2^part_bits workgroups (see part_sort below);
-//  * multi-tile: tiles of 256 * IPT keys.  up0 counts pass-0 digits per tile
-//    and the digit totals of every pass; down(p) ranks each tile stably,
-//    adds the counts of all earlier tiles and scatters; up(p) counts the
-//    digits of pass p per tile of the previous output.  Counts are kept per
-//    tile and per group of kCountGroup tiles, so a tile's prefix needs a few
-//    dozen independent loads, not a chain over every earlier tile.
+//  * multi-tile: a histogram launch, then one launch per radix pass over
+//    4096-key tiles with a decoupled look-back over earlier tiles' digit
+//    counts (see the multi-tile section below).
 //
 // Ranking inside a wave: keys are held in registers, R rounds of 64; the
 // lanes of a round that share a digit are found with ballots, and the lowest
@@ -316,40 +313,62 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
 }
 
 // ------------------------------------------------------------ multi-tile sort
-constexpr int kCountGroup = 16;  // tiles per coarse count group
+// Lists above kSmallSortN keys: LSD passes of at most 9 bits over tiles of
+// 256 * IPT keys, one launch per pass plus one histogram launch.
+//   histogram   every workgroup counts the digits of all passes for a share
+//               of the keys (LDS) and adds them into the digit totals; it
+//               also resets the per-pass tile counters and advances the
+//               sort set's epoch;
+//   pass p      a workgroup takes the next tile id from an atomic counter
+//               (so every tile it waits for below is already running),
+//               ranks its keys stably in LDS, publishes the tile's digit
+//               counts, and finds the keys of each digit in all earlier
+//               tiles by looking back over their published counts: a tile
+//               publishes its count first and, once its own prefix is
+//               known, its inclusive prefix, so a look-back stops at the
+//               first prefix it meets.  Keys and entry ids are then
+//               scattered to digit start + earlier tiles + rank.
+// Status words carry the epoch of the sort that wrote them, so no clearing
+// is needed between calls (graph replays included).  A look-back that
+// waits implausibly long raises kFlagInternal and stops (the update is then
+// voided), so a library bug cannot hang the device.
+constexpr uint32_t kOsAgg = 1u;     // status: the tile's own digit count
+constexpr uint32_t kOsPrefix = 2u;  // status: inclusive count over tiles 0..tile
+constexpr int kOsHistIpt = 16;      // keys per thread of a histogram workgroup
+constexpr uint32_t kOsSpinLimit = 1u << 22;
+constexpr int kOsWindow = 32;       // earlier tiles read per look-back step
 
 struct SortBufs {
   int32_t* keys[2];
   int32_t* vals[2];
-  uint32_t* totals;    // [kMaxPasses][kMaxBins]
-  uint32_t* counts;    // [kMaxPasses][kMaxBins][max_tiles]
-  uint32_t* gcounts;   // [kMaxPasses][kMaxBins][max_groups]
+  uint32_t* totals;                 // [kMaxPasses][kMaxBins] digit totals
+  unsigned long long* status;       // [kMaxPasses][max_tiles][kMaxBins] look-back words
+  uint32_t* tile_ctr;               // [kMaxPasses] next tile id of each pass
+  uint32_t* epoch;                  // [1] advanced by every histogram launch
   int max_tiles;
-  int max_groups;
-  uint32_t* flag;      // sticky error bits
+  uint32_t* flag;                   // sticky error bits
 };
 
-__device__ inline uint32_t* counts_at(const SortBufs& sb, int p, int dg) {
-  return sb.counts + ((size_t)p * kMaxBins + dg) * sb.max_tiles;
-}
-__device__ inline uint32_t* gcounts_at(const SortBufs& sb, int p, int dg) {
-  return sb.gcounts + ((size_t)p * kMaxBins + dg) * sb.max_groups;
+__device__ __forceinline__ unsigned long long os_word(uint32_t epoch, uint32_t fl, uint32_t v) {
+  return ((unsigned long long)epoch << 32) | ((unsigned long long)fl << 30) | v;
 }
 
-constexpr int kUp0LdsWords = kMaxPasses * kMaxBins;
+constexpr int kOsHistLdsWords = kMaxPasses * kMaxBins;
 
-// Pass-0 digit counts of one tile, and digit totals of every pass.
-template <int IPT, class KeyFn>
-__device__ void sort_up0_tile(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                              int tile, uint32_t* lds) {
+// Digit totals of every pass over keys [blk*256*kOsHistIpt, ...).
+template <class KeyFn>
+__device__ void os_hist(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb, int blk,
+                        uint32_t* lds) {
   const int t = threadIdx.x;
+  if (blk == 0 && t < kMaxPasses) sb.tile_ctr[t] = 0u;
+  if (blk == 0 && t == 0) sb.epoch[0] = sb.epoch[0] + 1u;
   for (int i = t; i < plan.passes * kMaxBins; i += kBlock) lds[i] = 0;
-  const int base = tile * kBlock * IPT;
-  uint32_t key[IPT];
-  load_keys<IPT>(kf, N, base + t, kBlock, key, sb.flag);
+  const int base = blk * kBlock * kOsHistIpt;
+  uint32_t key[kOsHistIpt];
+  load_keys<kOsHistIpt>(kf, N, base + t, kBlock, key, sb.flag);
   __syncthreads();
 #pragma unroll
-  for (int q = 0; q < IPT; ++q) {
+  for (int q = 0; q < kOsHistIpt; ++q) {
     if (base + q * kBlock + t < N) {
       for (int p = 0; p < plan.passes; ++p) {
         const uint32_t dg = (key[q] >> plan.shift[p]) & ((1u << plan.bits[p]) - 1u);
@@ -358,12 +377,6 @@ __device__ void sort_up0_tile(const KeyFn& kf, int N, const SortPlan& plan, cons
     }
   }
   __syncthreads();
-  const int bins0 = 1 << plan.bits[0];
-  for (int dg = t; dg < bins0; dg += kBlock) {
-    const uint32_t c = lds[dg];
-    counts_at(sb, 0, dg)[tile] = c;
-    if (c) atomicAdd(&gcounts_at(sb, 0, dg)[tile / kCountGroup], c);
-  }
   for (int p = 0; p < plan.passes; ++p) {
     const int bins = 1 << plan.bits[p];
     for (int dg = t; dg < bins; dg += kBlock) {
@@ -373,52 +386,45 @@ __device__ void sort_up0_tile(const KeyFn& kf, int N, const SortPlan& plan, cons
   }
 }
 
-// LDS words for a down pass: per-wave histograms + digit scratch + scan scratch.
-constexpr int kDownLdsWords = kWavesPerBlock * kMaxBins + kMaxBins + 16;
+// One radix pass: a workgroup of kOsThreads threads per 4096-key tile.
+constexpr int kOsThreads = 1024;
+constexpr int kOsWaves = kOsThreads / kWave;
+// LDS of a pass: counters [kMaxBins][waves + 1], digit bases, scan scratch,
+// the tile id.
+constexpr int kOsPassLdsWords = kMaxBins * (kOsWaves + 1) + kMaxBins + 2 * kOsWaves + 1;
 
-// Keys of `digit` in tiles [0, tile) of pass p: coarse groups, then the tiles
-// of the last partial group; every load is independent.
-__device__ __forceinline__ uint32_t tiles_before(const SortBufs& sb, int p, int dg, int tile) {
-  const uint32_t* gp = gcounts_at(sb, p, dg);
-  const uint32_t* cp = counts_at(sb, p, dg);
-  const int ng = tile / kCountGroup;
-  uint32_t acc[4] = {0u, 0u, 0u, 0u};
-  for (int g0 = 0; g0 < ng; g0 += 4) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (g0 + u < ng) acc[u] += gp[g0 + u];
-  }
-  const int t0 = ng * kCountGroup;
-  uint32_t v[kCountGroup];
-#pragma unroll
-  for (int u = 0; u < kCountGroup; ++u) v[u] = (t0 + u < tile) ? cp[t0 + u] : 0u;
-  uint32_t s = acc[0] + acc[1] + acc[2] + acc[3];
-#pragma unroll
-  for (int u = 0; u < kCountGroup; ++u) s += v[u];
-  return s;
-}
-
-// Pass p over one tile: stable rank, global offset, scatter.
-template <int IPT, class KeyFn>
-__device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                               int p, int tile, uint32_t* lds) {
-  uint32_t* hist = lds;                                  // [waves][kMaxBins]
-  uint32_t* dscr = hist + kWavesPerBlock * kMaxBins;     // [kMaxBins]
-  uint32_t* misc = dscr + kMaxBins;
+template <class KeyFn>
+__device__ void os_pass(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb, int p,
+                        uint32_t* lds) {
+  constexpr int NW = kOsWaves, CS = NW + 1, R = kSortTileKeys / kOsThreads;
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
-  uint32_t* myhist = hist + w * kMaxBins;
+  uint32_t* hist = lds;                      // [kMaxBins][CS]: counts, then wave offsets
+  uint32_t* base = hist + kMaxBins * CS;     // [kMaxBins] start of the digit's keys of this tile
+  uint32_t* misc = base + kMaxBins;          // scan scratch
+  uint32_t* tid_s = misc + 2 * NW;
   const int bits = plan.bits[p], shift = plan.shift[p], bins = 1 << bits;
+  if (t == 0) tid_s[0] = atomicAdd(&sb.tile_ctr[p], 1u);
+  // digit total of digit t (complete: written by the histogram launch)
+  const uint32_t tot = t < bins ? sb.totals[p * kMaxBins + t] : 0u;
+  const uint32_t epoch = sb.epoch[0];
+  uint32_t* mycol = hist + w;
+  for (int d = lane; d < bins; d += kWave) {
+    mycol[d * CS] = 0;
+    if (w == 0) hist[d * CS + NW] = 0;
+  }
+  __syncthreads();
+  const int tile = (int)tid_s[0];
   const int32_t* sk = sb.keys[p & 1];
   const int32_t* sv = sb.vals[p & 1];
   int32_t* dk = sb.keys[(p + 1) & 1];
   int32_t* dv = sb.vals[(p + 1) & 1];
 
-  constexpr int R = IPT;  // rounds per wave (blocked: a wave owns R*64 keys)
+  // keys of the tile: wave w owns R rounds of 64 consecutive keys
   uint32_t key[R], dg[R], loc[R];
   int32_t val[R];
   uint64_t act[R];
-  const int wbase = tile * kBlock * IPT + w * (R * kWave);
+  const int wbase = tile * kSortTileKeys + w * (R * kWave);
   if (p == 0) {
     load_keys<R>(kf, N, wbase + lane, kWave, key, sb.flag);
 #pragma unroll
@@ -436,35 +442,79 @@ __device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, con
     act[r] = __ballot(wbase + r * kWave + lane < N);
     dg[r] = (key[r] >> shift) & (uint32_t)(bins - 1);
   }
-  for (int i = lane; i < bins; i += kWave) myhist[i] = 0;
-  for (int d = t; d < bins; d += kBlock) dscr[d] = sb.totals[p * kMaxBins + d];
-  uint32_t before[kMaxBins / kBlock];
-#pragma unroll
-  for (int q = 0; q < kMaxBins / kBlock; ++q) {
-    const int d = t + q * kBlock;
-    before[q] = d < bins ? tiles_before(sb, p, d, tile) : 0u;
-  }
-  wave_lds_sync();
-  wave_rank<R>(dg, act, R, bits, myhist, loc);
+  wave_rank<R>(dg, act, R, bits, mycol, loc, CS);
   __syncthreads();
-  block_exclusive_scan(dscr, bins, misc);  // digit starts of the pass
+  // thread t < bins: digit t's count in every wave -> the tile's count of the
+  // digit, and each wave's offset inside the digit (written back in place)
+  const bool mine = t < bins;
+  uint32_t cnt = 0u;
+  if (mine) {
+    uint32_t c[NW];
 #pragma unroll
-  for (int q = 0; q < kMaxBins / kBlock; ++q) {
-    const int d = t + q * kBlock;
-    if (d < bins) {
-      uint32_t s = dscr[d] + before[q];
-      for (int v = 0; v < kWavesPerBlock; ++v) {
-        const uint32_t c = hist[v * kMaxBins + d];
-        hist[v * kMaxBins + d] = s;
-        s += c;
-      }
+    for (int v = 0; v < NW; ++v) c[v] = hist[t * CS + v];
+#pragma unroll
+    for (int v = 0; v < NW; ++v) {
+      hist[t * CS + v] = cnt;
+      cnt += c[v];
     }
+  }
+
+  // publish this tile's digit counts, look back over earlier tiles, publish
+  // the inclusive prefix; thread t < bins takes digit t.  A look-back step
+  // reads a window of kOsWindow earlier tiles at once and adds them from the
+  // nearest down to the first inclusive prefix; a tile that has not
+  // published yet ends the step (it is read again in the next one).
+  unsigned long long* st = sb.status + (size_t)p * sb.max_tiles * kMaxBins;
+  uint32_t excl = 0u;
+  int cur = mine ? tile - 1 : -1;  // next earlier tile to read; -1: done
+  if (mine)
+    __hip_atomic_store(&st[(size_t)tile * kMaxBins + t],
+                       os_word(epoch, tile == 0 ? kOsPrefix : kOsAgg, cnt), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  for (uint32_t spins = 0; cur >= 0; ++spins) {
+    if (spins > kOsSpinLimit) {  // never expected: give up, void the update
+      atomicOr(sb.flag, kFlagInternal);
+      break;
+    }
+    unsigned long long sw[kOsWindow];
+#pragma unroll
+    for (int i = 0; i < kOsWindow; ++i)
+      sw[i] = cur - i >= 0 ? __hip_atomic_load(&st[(size_t)(cur - i) * kMaxBins + t],
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                           : 0ull;
+    bool stop = false;
+#pragma unroll
+    for (int i = 0; i < kOsWindow; ++i) {
+      if (stop || cur < 0) continue;
+      const uint32_t ep = (uint32_t)(sw[i] >> 32), fl = (uint32_t)(sw[i] >> 30) & 3u;
+      if (ep != epoch || fl == 0u) {  // not published yet: read it again next step
+        stop = true;
+        continue;
+      }
+      excl += (uint32_t)sw[i] & 0x3fffffffu;
+      cur = (fl == kOsPrefix || cur == 0) ? -1 : cur - 1;
+    }
+  }
+  if (mine) {
+    if (tile > 0)
+      __hip_atomic_store(&st[(size_t)tile * kMaxBins + t], os_word(epoch, kOsPrefix, excl + cnt),
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  // digit starts of the pass: exclusive scan of the totals over digits
+  {
+    const uint32_t inc = wave_incl_scan(tot);
+    if (lane == kWave - 1) misc[w] = inc;
+    __syncthreads();
+    uint32_t b = 0;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) b += v < w ? misc[v] : 0u;
+    if (mine) base[t] = b + inc - tot + excl;
   }
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     if ((act[r] >> lane) & 1ull) {
-      const uint32_t pos = myhist[dg[r]] + loc[r];
+      const uint32_t pos = base[dg[r]] + mycol[dg[r] * CS] + loc[r];
       if (pos >= (uint32_t)N) {  // inconsistent counters: never write out of bounds
         atomicOr(sb.flag, kFlagInternal);
         continue;
@@ -472,35 +522,6 @@ __device__ void sort_down_tile(const KeyFn& kf, int N, const SortPlan& plan, con
       dk[pos] = (int32_t)key[r];
       dv[pos] = val[r];
     }
-  }
-}
-
-// Digit counts of pass p (p >= 1) for one tile of the previous pass's output:
-// counts in LDS, one store per (digit, tile) and one atomic per (digit, tile)
-// into the 16-tile group, so heavy Zipf digits never pile up on one counter.
-template <int IPT>
-__device__ void sort_up_tile(int N, const SortPlan& plan, const SortBufs& sb, int p, int tile,
-                             uint32_t* lds) {
-  const int t = threadIdx.x;
-  const int bits = plan.bits[p], shift = plan.shift[p], bins = 1 << bits;
-  for (int i = t; i < bins; i += kBlock) lds[i] = 0;
-  const int32_t* sk = sb.keys[p & 1];
-  const int base = tile * kBlock * IPT;
-  uint32_t key[IPT];
-#pragma unroll
-  for (int q = 0; q < IPT; ++q) {
-    const int e = base + q * kBlock + t;
-    key[q] = e < N ? (uint32_t)sk[e] : 0u;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int q = 0; q < IPT; ++q)
-    if (base + q * kBlock + t < N) atomicAdd(&lds[(key[q] >> shift) & (uint32_t)(bins - 1)], 1u);
-  __syncthreads();
-  for (int dg = t; dg < bins; dg += kBlock) {
-    const uint32_t c = lds[dg];
-    counts_at(sb, p, dg)[tile] = c;
-    if (c) atomicAdd(&gcounts_at(sb, p, dg)[tile / kCountGroup], c);
   }
 }
 
