@@ -68,9 +68,12 @@ typedef struct polyglot_ctx polyglot_ctx;
 
 typedef struct {
   int32_t V;            /* vocabulary rows of E, >= 1 */
-  int32_t d;            /* embedding width, multiple of 16, 16..256 */
+  int32_t d;            /* embedding width, multiple of 16, 16..256; for H <= 64,
+                           W1 (H x win*d floats) must also fit one workgroup's LDS */
   int32_t win;          /* window length, odd, 1..31 */
-  int32_t H;            /* hidden units, 1..64 */
+  int32_t H;            /* hidden units: 1..64, or a multiple of 64 up to 256 with d a
+                           multiple of 64 (wide layers run as three separate
+                           contractions: forward, dW1, per-entry gradient rows) */
   int32_t max_batch;    /* largest B accepted by train_step / score / gather */
   int32_t scatter_mode; /* POLYGLOT_SCATTER_SORTED or POLYGLOT_SCATTER_ATOMIC */
   int32_t max_scatter;  /* largest N accepted by polyglot_scatter_add (0: no workspace) */

@@ -46,6 +46,7 @@ struct polyglot_ctx {
              ev_done[2] = {nullptr, nullptr};
   int device = 0;
   int Hp = 0, NT = 0, K = 0, c = 0, cpw = 0;
+  bool large = false;  // hidden layer above 64 units: the three-contraction path
   int max_entries = 0, max_tiles = 0, max_parts = 0, max_chunks = 0;
   int seg_stride = 0, part_stride = 0;
   Workspace ws{};
@@ -261,47 +262,79 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   const StepKeys kf = step_keys(windows, corrupt, cf.win, cf.V);
   hipError_t e = hipSuccess;
 
-  FwdArgs fa{};
-  fa.E = E;
-  fa.W1 = W1;
-  fa.b1 = b1;
-  fa.w2 = w2;
-  fa.b2 = b2;
-  fa.windows = windows;
-  fa.corrupt = corrupt;
-  fa.G = ctx->ws.G;
-  fa.part = ctx->ws.part;
-  fa.long_count = ctx->ws.long_count;
-  fa.flag = ctx->ws.flag;
-  fa.V = cf.V;
-  fa.d = cf.d;
-  fa.win = cf.win;
-  fa.H = cf.H;
-  fa.Hp = ctx->Hp;
-  fa.K = ctx->K;
-  fa.c = ctx->c;
-  fa.B = B;
-  fa.N = N;
-  fa.n_sort = (sorted && plan.small) ? (1 << plan.part_bits) : 0;  // the sort as extra workgroups
-  fa.plan = plan;
-  fa.sb = sort_bufs(ctx, set);
-  fa.ntiles = ceil_div(B, kTileRows);
-  const int shape8 = fwdbwd8_shape(cf.d, cf.win, ctx->NT);
-  fa.tiles_per_wg = ceil_div(fa.ntiles, shape8 ? std::min(ctx->max_parts, kF8MaxWorkgroups)
-                                               : ctx->max_parts);
-  const int n_fb = ceil_div(fa.ntiles, fa.tiles_per_wg);
-  fa.part_stride = ctx->part_stride;
-  fa.invB = 1.0f / (float)B;
-  {
-    Timed tm(ctx, POLYGLOT_K_FWDBWD);
-    if (shape8) {
-      size_t lds = fwdbwd8_lds_bytes(shape8);
-      if (fa.n_sort) lds = std::max(lds, part_sort_lds_words(kF8Threads) * 4);
-      e = launch_step_fwdbwd8(fa, shape8, fa.n_sort + n_fb, lds, tm.L);
-    } else {
-      size_t lds = fwdbwd_lds_floats(ctx->Hp, ctx->K) * 4;
-      if (fa.n_sort) lds = std::max(lds, part_sort_lds_words(kBlock) * 4);
-      e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, fa.n_sort + n_fb, lds, tm.L);
+  LargeArgs la{};
+  int n_fb = 0;
+  if (ctx->large) {
+    la.E = E;
+    la.W1 = W1;
+    la.b1 = b1;
+    la.w2 = w2;
+    la.b2 = b2;
+    la.windows = windows;
+    la.corrupt = corrupt;
+    la.V = ctx->ws.vbuf;
+    la.vpart = ctx->ws.vpart;
+    la.part = ctx->ws.part;
+    la.G = ctx->ws.G;
+    la.flag = ctx->ws.flag;
+    la.long_count = ctx->ws.long_count;
+    la.V_rows = cf.V;
+    la.d = cf.d;
+    la.win = cf.win;
+    la.H = cf.H;
+    la.K = ctx->K;
+    la.c = ctx->c;
+    la.B = B;
+    la.invB = 1.0f / (float)B;
+    {
+      Timed tm(ctx, POLYGLOT_K_FWDBWD);
+      e = launch_large_fwd(la, 0, tm.L);
+      if (e == hipSuccess) e = launch_large_dw1(la, tm.L);
+      if (e == hipSuccess) e = launch_large_g(la, tm.L);
+    }
+  } else {
+    FwdArgs fa{};
+    fa.E = E;
+    fa.W1 = W1;
+    fa.b1 = b1;
+    fa.w2 = w2;
+    fa.b2 = b2;
+    fa.windows = windows;
+    fa.corrupt = corrupt;
+    fa.G = ctx->ws.G;
+    fa.part = ctx->ws.part;
+    fa.long_count = ctx->ws.long_count;
+    fa.flag = ctx->ws.flag;
+    fa.V = cf.V;
+    fa.d = cf.d;
+    fa.win = cf.win;
+    fa.H = cf.H;
+    fa.Hp = ctx->Hp;
+    fa.K = ctx->K;
+    fa.c = ctx->c;
+    fa.B = B;
+    fa.N = N;
+    fa.n_sort = (sorted && plan.small) ? (1 << plan.part_bits) : 0;  // the sort as extra workgroups
+    fa.plan = plan;
+    fa.sb = sort_bufs(ctx, set);
+    fa.ntiles = ceil_div(B, kTileRows);
+    const int shape8 = fwdbwd8_shape(cf.d, cf.win, ctx->NT);
+    fa.tiles_per_wg = ceil_div(fa.ntiles, shape8 ? std::min(ctx->max_parts, kF8MaxWorkgroups)
+                                                 : ctx->max_parts);
+    n_fb = ceil_div(fa.ntiles, fa.tiles_per_wg);
+    fa.part_stride = ctx->part_stride;
+    fa.invB = 1.0f / (float)B;
+    {
+      Timed tm(ctx, POLYGLOT_K_FWDBWD);
+      if (shape8) {
+        size_t lds = fwdbwd8_lds_bytes(shape8);
+        if (fa.n_sort) lds = std::max(lds, part_sort_lds_words(kF8Threads) * 4);
+        e = launch_step_fwdbwd8(fa, shape8, fa.n_sort + n_fb, lds, tm.L);
+      } else {
+        size_t lds = fwdbwd_lds_floats(ctx->Hp, ctx->K) * 4;
+        if (fa.n_sort) lds = std::max(lds, part_sort_lds_words(kBlock) * 4);
+        e = launch_step_fwdbwd(fa, ctx->NT, ctx->cpw, fa.n_sort + n_fb, lds, tm.L);
+      }
     }
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "fwd/bwd launch");
@@ -321,8 +354,19 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   aa.dn.b2 = b2;
   aa.dn.loss_out = loss_dev ? loss_dev : ctx->ws.scratch_loss;
   aa.dn.part = ctx->ws.part;
-  aa.dn.n_parts = n_fb;
-  aa.dn.part_stride = ctx->part_stride;
+  if (ctx->large) {  // dW1 slices; db1 / dw2 / loss partials of the forward workgroups
+    aa.dn.n_parts = ceil_div(B, kLgSlice);
+    aa.dn.part_stride = cf.H * ctx->K;
+    aa.dn.vpart = ctx->ws.vpart;
+    aa.dn.n_vparts = ceil_div(B, kLgRows);
+    aa.dn.vstride = 2 * cf.H + 2;
+  } else {
+    aa.dn.n_parts = n_fb;
+    aa.dn.part_stride = ctx->part_stride;
+    aa.dn.vpart = ctx->ws.part + (size_t)ctx->Hp * ctx->K;
+    aa.dn.n_vparts = n_fb;
+    aa.dn.vstride = ctx->part_stride;
+  }
   aa.dn.H = cf.H;
   aa.dn.Hp = ctx->Hp;
   aa.dn.K = ctx->K;
@@ -355,7 +399,7 @@ int enqueue_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, 
                   const int32_t* windows, const int32_t* corrupt, int S, int B, float lr,
                   float* losses_dev) {
   const bool side_sort = ctx->cfg.scatter_mode == POLYGLOT_SCATTER_SORTED &&
-                         !make_plan(ctx->cfg.V, B * (ctx->cfg.win + 1)).small;
+                         (ctx->large || !make_plan(ctx->cfg.V, B * (ctx->cfg.win + 1)).small);
   const size_t wstride = (size_t)B * ctx->cfg.win;
   hipError_t e = hipSuccess;
   if (side_sort) {
@@ -409,15 +453,18 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   *out = nullptr;
   const polyglot_config& c = *cfg;
   if (c.V < 1 || c.d < 16 || c.d > kMaxD || c.d % 16 != 0 || c.win < 1 || c.win > kMaxWin ||
-      c.win % 2 == 0 || c.H < 1 || c.H > kMaxHp || c.win * c.d > kMaxK)
+      c.win % 2 == 0 || c.H < 1 || c.H > kMaxLargeH)
     return POLYGLOT_EINVAL;
+  const bool large = c.H > kMaxHp;
+  if (large && (c.H % 64 != 0 || c.d % 64 != 0)) return POLYGLOT_EINVAL;
+  if (!large && c.win * c.d > kMaxK) return POLYGLOT_EINVAL;
   if (c.scatter_mode != POLYGLOT_SCATTER_SORTED && c.scatter_mode != POLYGLOT_SCATTER_ATOMIC)
     return POLYGLOT_EINVAL;
   if (c.max_batch < 1 || (int64_t)c.max_batch * (c.win + 1) > (1 << 26)) return POLYGLOT_EBATCH;
   if (c.max_scatter < 0 || c.max_scatter > (1 << 26) || c.max_rows < 0 ||
       (c.max_scatter > 0 && c.max_rows < 1))
     return POLYGLOT_EINVAL;
-  {  // the fused kernel keeps W1 and its tile buffers in one workgroup's LDS
+  if (!large) {  // the fused kernel keeps W1 and its tile buffers in one workgroup's LDS
     const int hp = c.H <= 16 ? 16 : (c.H <= 32 ? 32 : 64);
     if (fwdbwd_lds_floats(hp, c.win * c.d) * 4 > (size_t)kMaxLdsBytes) return POLYGLOT_EINVAL;
   }
@@ -428,7 +475,8 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   ctx->stream = static_cast<hipStream_t>(stream);
   ctx->K = c.win * c.d;
   ctx->c = c.win / 2;
-  ctx->NT = c.H <= 16 ? 1 : (c.H <= 32 ? 2 : 4);
+  ctx->large = large;
+  ctx->NT = large ? c.H / 16 : (c.H <= 16 ? 1 : (c.H <= 32 ? 2 : 4));
   ctx->Hp = 16 * ctx->NT;
   ctx->cpw = ceil_div(ctx->K / 16, kWavesPerBlock);
   ctx->max_entries = std::max({c.max_batch * (c.win + 1), c.max_scatter, 1});
@@ -458,7 +506,15 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
     if (e == hipSuccess) e = alloc(ctx, &ws.epoch[k], 1);
   }
   if (e == hipSuccess) e = alloc(ctx, &ws.G, (size_t)c.max_batch * (c.win + 1) * c.d);
-  if (e == hipSuccess) e = alloc(ctx, &ws.part, (size_t)ctx->max_parts * ctx->part_stride);
+  if (large) {
+    const int slices = ceil_div(c.max_batch, kLgSlice);
+    if (e == hipSuccess) e = alloc(ctx, &ws.part, (size_t)slices * c.H * ctx->K);
+    if (e == hipSuccess)
+      e = alloc(ctx, &ws.vpart, (size_t)ceil_div(c.max_batch, kLgRows) * (2 * c.H + 2));
+    if (e == hipSuccess) e = alloc(ctx, &ws.vbuf, (size_t)c.max_batch * 3 * c.H);
+  } else if (e == hipSuccess) {
+    e = alloc(ctx, &ws.part, (size_t)ctx->max_parts * ctx->part_stride);
+  }
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_end, (size_t)std::max(c.V, c.max_rows));
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_part, (size_t)ctx->max_chunks * 2 * ctx->seg_stride);
   if (e == hipSuccess) e = alloc(ctx, &ws.long_list, (size_t)ctx->max_chunks);
@@ -566,10 +622,29 @@ int polyglot_score(polyglot_ctx* ctx, const float* E, const float* W1, const flo
   if (B <= 0 || B > ctx->cfg.max_batch) return fail(ctx, POLYGLOT_EBATCH, "score: bad B");
   if (!aligned16(E) || !aligned16(W1))
     return fail(ctx, POLYGLOT_EINVAL, "score: E and W1 must be 16-byte aligned");
-  ScoreArgs a{E, W1, b1, w2, b2, windows, scores_dev, ctx->ws.flag, ctx->cfg.V, ctx->cfg.d,
-              ctx->cfg.win, ctx->cfg.H, ctx->K, B};
   hipError_t e;
-  {
+  if (ctx->large) {
+    LargeArgs la{};
+    la.E = E;
+    la.W1 = W1;
+    la.b1 = b1;
+    la.w2 = w2;
+    la.b2 = b2;
+    la.windows = windows;
+    la.scores = scores_dev;
+    la.flag = ctx->ws.flag;
+    la.V_rows = ctx->cfg.V;
+    la.d = ctx->cfg.d;
+    la.win = ctx->cfg.win;
+    la.H = ctx->cfg.H;
+    la.K = ctx->K;
+    la.c = ctx->c;
+    la.B = B;
+    Timed tm(ctx, POLYGLOT_K_SCORE);
+    e = launch_large_fwd(la, 1, tm.L);
+  } else {
+    ScoreArgs a{E, W1, b1, w2, b2, windows, scores_dev, ctx->ws.flag, ctx->cfg.V, ctx->cfg.d,
+                ctx->cfg.win, ctx->cfg.H, ctx->K, B};
     Timed tm(ctx, POLYGLOT_K_SCORE);
     e = launch_score(a, ctx->NT, ctx->cpw, tm.L);
   }

@@ -13,7 +13,8 @@ constexpr int kBlock = 256;             // threads per workgroup of every kernel
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kTileRows = 16;           // windows per MFMA tile (16x16x4 f32)
 constexpr int kMaxK = 512;              // win*d handled by the fused step kernel
-constexpr int kMaxHp = 64;              // hidden units, padded to a multiple of 16
+constexpr int kMaxHp = 64;              // hidden units of the fused step kernel, padded to 16
+constexpr int kMaxLargeH = 256;         // hidden units of the three-contraction path (multiple of 64)
 constexpr int kMaxNT = kMaxHp / 16;
 constexpr int kMaxWin = 31;
 constexpr int kMaxD = 256;
@@ -56,7 +57,10 @@ struct Workspace {
   uint32_t* epoch[2];       // sort epoch of each set
   // step
   float* G;                 // [max_batch*(win+1)][d] per-entry embedding gradients
-  float* part;              // [max_parts][part_stride] dense-gradient partials
+  float* part;              // dense-gradient partials: [max_parts][part_stride], or
+                            // [slices][H][K] dW1 partials of the three-contraction path
+  float* vpart;             // three-contraction path: [forward workgroups][2H + 2]
+  float* vbuf;              // three-contraction path: [max_batch][3][H] dz + dz~, dz, dz~
   // segmented update
   float* seg_part;          // [max_chunks][2][seg_stride] partial sums of long segments
   int32_t* long_list;       // [max_chunks] start chunks of segments spanning chunks

@@ -38,6 +38,7 @@
 #include "sort_dev.h"
 #include "fwdbwd_dev.h"
 #include "fwdbwd8_dev.h"
+#include "large_dev.h"
 #include "update_dev.h"
 #include "aux_dev.h"
 
@@ -204,6 +205,30 @@ hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, const Launch& L) {
   if (NT == 1) return launch_score_nt<1>(a, cpw, grid, lds, L);
   if (NT == 2) return launch_score_nt<2>(a, cpw, grid, lds, L);
   return launch_score_nt<4>(a, cpw, grid, lds, L);
+}
+
+hipError_t launch_large_fwd(const LargeArgs& a, int score_only, const Launch& L) {
+  const dim3 grid(ceil_div(a.B, kLgRows));
+  switch (a.H / 64) {
+    case 2: return pg_launch(k_large_fwd<2>, grid, dim3(2 * kWave), 0, L, a, score_only);
+    case 3: return pg_launch(k_large_fwd<3>, grid, dim3(3 * kWave), 0, L, a, score_only);
+    default: return pg_launch(k_large_fwd<4>, grid, dim3(4 * kWave), 0, L, a, score_only);
+  }
+}
+
+hipError_t launch_large_dw1(const LargeArgs& a, const Launch& L) {
+  return pg_launch(k_large_dw1, dim3(a.H / 64, a.K / 64, ceil_div(a.B, kLgSlice)), dim3(kBlock), 0,
+                   L, a);
+}
+
+hipError_t launch_large_g(const LargeArgs& a, const Launch& L) {
+  const dim3 grid(ceil_div(a.B, kLgGRows), a.win + 1);
+  switch (a.d / 16) {
+    case 4: return pg_launch(k_large_g<4>, grid, dim3(kBlock), 0, L, a);
+    case 8: return pg_launch(k_large_g<8>, grid, dim3(kBlock), 0, L, a);
+    case 12: return pg_launch(k_large_g<12>, grid, dim3(kBlock), 0, L, a);
+    default: return pg_launch(k_large_g<16>, grid, dim3(kBlock), 0, L, a);
+  }
 }
 
 hipError_t launch_gather(const GatherArgs& a, const Launch& L) {

@@ -1,0 +1,325 @@
+// The SGD step for models whose W1 does not fit in a workgroup's LDS (hidden
+// layer wider than 64 units, e.g. d 128, window 11, H 256): three MFMA
+// contractions (16x16x4 f32) with the embedding rows gathered on the fly.
+//
+//   k_large_fwd   Z = X W1^T and, for the corrupted copy, the centre-block
+//                 difference D = (e~ - e_c) W1_c^T (so z~ = z + D; §1 model,
+//                 x~); then tanh, both scores, hinge and the per-window
+//                 vectors V = (dz + dz~, dz, dz~), written to global memory,
+//                 and this workgroup's db1 / dw2 / loss partial.  32 windows
+//                 per workgroup, one wave per 64 hidden units.  In score-only
+//                 mode it writes s(x) instead.
+//   k_large_dw1   dW1 partials: dW1[h][k] = sum_b V_b[h] x_b[k] (centre block:
+//                 dz e_c + dz~ e~) over 1024-window slices; a workgroup owns a
+//                 64 x 64 block of dW1 and one slice.
+//   k_large_g     G[e][:] = W1_j^T V for entry e = b(win+1) + j (context
+//                 positions dz + dz~, the true centre dz, the corrupt entry dz~
+//                 through block c); a workgroup owns 64 windows of one entry
+//                 position.
+// Rows b >= B read row 0 and are masked out of every result.
+#pragma once
+#include "common.h"
+#include "launch.h"
+
+namespace pg {
+
+__device__ __forceinline__ f4 lg_mfma(float a, float b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// HW waves, wave w owns hidden units [64w, 64w + 64) (4 column blocks of 16);
+// both 16-row blocks of the workgroup's 32 windows.
+template <int HW>
+__global__ __launch_bounds__(HW * kWave) void k_large_fwd(LargeArgs a, int score_only) {
+  __shared__ int32_t ids[kLgRows][kMaxWin + 1];
+  __shared__ float sred[2][HW][kLgRows];
+  __shared__ float gsh[kLgRows];
+  __shared__ int badrow[kLgRows];
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
+  const int i = lane & 15, g = lane >> 4;
+  const int r0 = blockIdx.x * kLgRows;
+  const int W1p = a.win + 1, d = a.d, K = a.K;
+  if (blockIdx.x == 0 && t == 0 && a.long_count) *a.long_count = 0u;
+  if (t < kLgRows) badrow[t] = 0;
+  __syncthreads();
+  for (int k = t; k < kLgRows * W1p; k += HW * kWave) {
+    const int r = k / W1p, j = k - r * W1p;
+    const int b = r0 + r;
+    int32_t id = 0;  // score-only mode has no corrupt ids
+    if (b < a.B && (j < a.win || !score_only))
+      id = j < a.win ? a.windows[(size_t)b * a.win + j] : a.corrupt[b];
+    const bool bad = (uint32_t)id >= (uint32_t)a.V_rows;
+    if (bad) {
+      atomicOr(a.flag, kFlagBadId);
+      badrow[r] = 1;
+    }
+    ids[r][j] = ((uint32_t)id < (uint32_t)a.V_rows) ? id : 0;
+  }
+  __syncthreads();
+
+  f4 Z[2][4], D[2][4];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) Z[rb][cb] = D[rb][cb] = kZero4;
+  const int cpb = d / 16;  // 16-column chunks per embedding row
+  const int nch = K / 16;
+  const float* wrow[4];
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb) wrow[cb] = a.W1 + (size_t)(64 * w + 16 * cb + i) * K + 4 * g;
+  // operands of chunk kc: A = X rows (lane: row 16rb + i, k = 16kc + 4g..+3),
+  // B = W1 rows (lane: hidden 64w + 16cb + i)
+  auto load = [&](int kc, f4 (&A)[2], f4 (&Bv)[4], f4 (&At)[2]) {
+    const int j = kc / cpb, off = (kc - j * cpb) * 16 + 4 * g;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) A[rb] = ld4(a.E + (size_t)ids[16 * rb + i][j] * d + off);
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) Bv[cb] = ld4(wrow[cb] + 16 * kc);
+    if (j == a.c && !score_only) {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) At[rb] = ld4(a.E + (size_t)ids[16 * rb + i][a.win] * d + off);
+    }
+  };
+  f4 A[2], Bv[4], At[2];
+  load(0, A, Bv, At);
+  for (int kc = 0; kc < nch; ++kc) {
+    f4 An[2], Bn[4], Atn[2];
+    if (kc + 1 < nch) load(kc + 1, An, Bn, Atn);  // next chunk in flight
+    const bool ctr = kc / cpb == a.c && !score_only;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) Z[rb][cb] = lg_mfma(A[rb][q], Bv[cb][q], Z[rb][cb]);
+    if (ctr) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+          const float dx = At[rb][q] - A[rb][q];
+#pragma unroll
+          for (int cb = 0; cb < 4; ++cb) D[rb][cb] = lg_mfma(dx, Bv[cb][q], D[rb][cb]);
+        }
+    }
+    if (kc + 1 < nch) {
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        A[rb] = An[rb];
+        At[rb] = Atn[rb];
+      }
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) Bv[cb] = Bn[cb];
+    }
+  }
+
+  // ---- epilogue.  Lane (i, g), component q of Z[rb][cb]: row 16rb + 4g + q,
+  // hidden 64w + 16cb + i.
+  float b1v[4], w2v[4];
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb) {
+    const int h = 64 * w + 16 * cb + i;
+    b1v[cb] = h < a.H ? a.b1[h] : 0.f;
+    w2v[cb] = h < a.H ? a.w2[h] : 0.f;
+  }
+  float ps[2][4], pst[2][4];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float s = 0.f, st = 0.f;
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        const float z = Z[rb][cb][q] + b1v[cb];
+        s += w2v[cb] * tanh_fast(z);
+        if (!score_only) st += w2v[cb] * tanh_fast(z + D[rb][cb][q]);
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        s += __shfl_xor(s, o);
+        st += __shfl_xor(st, o);
+      }
+      ps[rb][q] = s;
+      pst[rb][q] = st;
+    }
+  if (i == 0) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        sred[0][w][16 * rb + 4 * g + q] = ps[rb][q];
+        sred[1][w][16 * rb + 4 * g + q] = pst[rb][q];
+      }
+  }
+  __syncthreads();
+  float lossr = 0.f;
+  if (t < kLgRows) {
+    float s = 0.f, st = 0.f;
+#pragma unroll
+    for (int v = 0; v < HW; ++v) {
+      s += sred[0][v][t];
+      st += sred[1][v][t];
+    }
+    const int b = r0 + t;
+    const float b2v = a.b2[0];
+    if (score_only) {
+      if (b < a.B) a.scores[b] = badrow[t] ? __builtin_nanf("") : b2v + s;
+    } else {
+      const float mg = 1.f - (b2v + s) + (b2v + st);
+      const bool on = b < a.B && mg > 0.f;  // hinge active (derivative 0 at margin 0)
+      gsh[t] = on ? a.invB : 0.f;           // d loss/d s~ = m/B, d loss/d s = -m/B
+      lossr = on ? mg : 0.f;
+    }
+  }
+  if (score_only) return;
+  __syncthreads();
+
+  // V and the db1 / dw2 sums of this lane's hidden units over its 8 rows
+  float db1[4] = {0.f, 0.f, 0.f, 0.f}, dw2[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = 16 * rb + 4 * g + q, b = r0 + r;
+      const float gst = gsh[r];
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        const int h = 64 * w + 16 * cb + i;
+        const float z = Z[rb][cb][q] + b1v[cb];
+        const float hh = tanh_fast(z), ht = tanh_fast(z + D[rb][cb][q]);
+        // h - h~ = tanh(z - z~) (1 - h h~) with z - z~ = -D
+        const float hmh = tanh_fast(-D[rb][cb][q]) * (1.f - hh * ht);
+        const float gw = gst * w2v[cb];
+        const float dz = -gw * (1.f - hh * hh);
+        const float dzt = gw * (1.f - ht * ht);
+        const float dsum = gw * hmh * (hh + ht);
+        if (b < a.B && h < a.H) {
+          float* vr = a.V + (size_t)b * 3 * a.H + h;
+          vr[0] = dsum;
+          vr[a.H] = dz;
+          vr[2 * a.H] = dzt;
+        }
+        db1[cb] += dsum;
+        dw2[cb] -= gst * hmh;  // -(m/B) h + (m/B) h~
+      }
+    }
+  float* vp = a.vpart + (size_t)blockIdx.x * (2 * a.H + 2);
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb) {
+    float x = db1[cb], y = dw2[cb];
+    x += __shfl_xor(x, 16);
+    x += __shfl_xor(x, 32);
+    y += __shfl_xor(y, 16);
+    y += __shfl_xor(y, 32);
+    const int h = 64 * w + 16 * cb + i;
+    if (g == 0 && h < a.H) {
+      vp[h] = x;
+      vp[a.H + h] = y;
+    }
+  }
+  if (w == 0) {  // the workgroup's hinge sum (rows in order), db2 = 0
+    for (int o = 1; o < kWave; o <<= 1) lossr += __shfl_xor(lossr, o);
+    if (lane == 0) {
+      vp[2 * a.H] = lossr;
+      vp[2 * a.H + 1] = 0.f;
+    }
+  }
+}
+
+// dW1 partial of a 64 x 64 block (hidden h0.., columns k0..) over one slice
+// of windows; wave w owns hidden rows h0 + 16w .. +15.
+__global__ __launch_bounds__(kBlock) void k_large_dw1(LargeArgs a) {
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
+  const int i = lane & 15, g = lane >> 4;
+  const int h0 = blockIdx.x * 64, k0 = blockIdx.y * 64, sl = blockIdx.z;
+  const int d = a.d, j = k0 / d, off0 = k0 - j * d;  // 64 columns inside one position
+  const bool ctr = j == a.c;
+  const int b_lo = sl * kLgSlice, b_hi = min(a.B, b_lo + kLgSlice);
+  const int hA = h0 + 16 * w + i;  // A operand hidden unit of this lane
+  f4 acc[4];
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb) acc[cb] = kZero4;
+  for (int b0 = b_lo; b0 < b_hi; b0 += 16) {
+    // windows of this chunk for k-index g: b0 + 4g + q
+    float av[4], ac[4], x[4][4], xc[4][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int b = b0 + 4 * g + q;
+      const bool ok = b < b_hi;
+      int32_t id = ok ? a.windows[(size_t)b * a.win + j] : 0;
+      id = (uint32_t)id < (uint32_t)a.V_rows ? id : 0;
+      const float* vr = a.V + (size_t)b * 3 * a.H + hA;
+      av[q] = ok ? vr[ctr ? a.H : 0] : 0.f;
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) x[cb][q] = a.E[(size_t)id * d + off0 + 16 * cb + i];
+      if (ctr) {
+        int32_t ic = ok ? a.corrupt[b] : 0;
+        ic = (uint32_t)ic < (uint32_t)a.V_rows ? ic : 0;
+        ac[q] = ok ? vr[2 * a.H] : 0.f;
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) xc[cb][q] = a.E[(size_t)ic * d + off0 + 16 * cb + i];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) acc[cb] = lg_mfma(av[q], x[cb][q], acc[cb]);
+    if (ctr) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) acc[cb] = lg_mfma(ac[q], xc[cb][q], acc[cb]);
+    }
+  }
+  // lane (i, g), component q: hidden h0 + 16w + 4g + q, column k0 + 16cb + i
+  float* P = a.part + (size_t)sl * a.H * a.K;
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      P[(size_t)(h0 + 16 * w + 4 * g + q) * a.K + k0 + 16 * cb + i] = acc[cb][q];
+}
+
+// G rows of 64 windows at entry position j = blockIdx.y; wave w owns
+// windows b0 + 16w .. +15 and all DQ column blocks of the row.
+template <int DQ>
+__global__ __launch_bounds__(kBlock) void k_large_g(LargeArgs a) {
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
+  const int i = lane & 15, g = lane >> 4;
+  const int j = blockIdx.y, b0 = blockIdx.x * kLgGRows + 16 * w;
+  const int ty = (j == a.win) ? 2 : (j == a.c ? 1 : 0);
+  const int jj = (j == a.win) ? a.c : j;
+  const int bA = b0 + i;  // A operand window of this lane
+  const float* vr = a.V + (size_t)bA * 3 * a.H + (size_t)ty * a.H + 4 * g;
+  const float* wc = a.W1 + (size_t)jj * a.d + i;
+  f4 acc[DQ];
+#pragma unroll
+  for (int cb = 0; cb < DQ; ++cb) acc[cb] = kZero4;
+  for (int hc = 0; hc < a.H; hc += 16) {
+    const f4 av = bA < a.B ? ld4(vr + hc) : kZero4;
+    float bv[DQ][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int cb = 0; cb < DQ; ++cb) bv[cb][q] = wc[(size_t)(hc + 4 * g + q) * a.K + 16 * cb];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int cb = 0; cb < DQ; ++cb) acc[cb] = lg_mfma(av[q], bv[cb][q], acc[cb]);
+  }
+  // lane (i, g), component q: window b0 + 4g + q, column 16cb + i
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int b = b0 + 4 * g + q;
+    if (b < a.B) {
+      float* gr = a.G + ((size_t)b * (a.win + 1) + j) * a.d + i;
+#pragma unroll
+      for (int cb = 0; cb < DQ; ++cb) gr[16 * cb] = acc[cb][q];
+    }
+  }
+}
+
+}  // namespace pg

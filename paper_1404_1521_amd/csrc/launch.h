@@ -59,6 +59,30 @@ struct FwdArgs {
   float invB;
 };
 
+// Three-contraction path (hidden layer above 64 units).
+constexpr int kLgRows = 32;        // windows per forward workgroup
+constexpr int kLgSlice = 1024;     // windows per dW1 slice
+constexpr int kLgGRows = 64;       // windows per G workgroup
+
+struct LargeArgs {
+  const float* E;
+  const float* W1;
+  const float* b1;
+  const float* w2;
+  const float* b2;
+  const int32_t* windows;
+  const int32_t* corrupt;
+  float* V;          // [B][3][H]
+  float* vpart;      // [forward workgroups][2H + 2]: db1, dw2, loss, db2
+  float* part;       // [slices][H][K] dW1 partials
+  float* G;          // [B*(win+1)][d]
+  float* scores;     // score-only mode: s(x) [B]
+  uint32_t* flag;
+  uint32_t* long_count;
+  int V_rows, d, win, H, K, c, B;
+  float invB;
+};
+
 // Zero ranges of the sort counters, cleared after their last use in a call.
 struct ZeroRanges {
   uint32_t* p[3];
@@ -72,8 +96,9 @@ struct DenseArgs {
   float* w2;
   float* b2;
   float* loss_out;
-  const float* part;
-  int n_parts, part_stride, H, Hp, K;
+  const float* part;   // dW1 partials: slot p at part + p * part_stride
+  const float* vpart;  // db1, dw2, loss, db2 partials: slot p at vpart + p * vstride
+  int n_parts, part_stride, n_vparts, vstride, H, Hp, K;
   float lr, invB;
 };
 
@@ -134,6 +159,10 @@ hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L);
 hipError_t launch_check_idx(const int32_t* idx, int N, int rows, uint32_t* flag, const Launch& L);
 hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, const Launch& L);
 hipError_t launch_gather(const GatherArgs& a, const Launch& L);
+// three-contraction path: forward (or score only), dW1 partials, G rows
+hipError_t launch_large_fwd(const LargeArgs& a, int score_only, const Launch& L);
+hipError_t launch_large_dw1(const LargeArgs& a, const Launch& L);
+hipError_t launch_large_g(const LargeArgs& a, const Launch& L);
 
 // LDS of the fused kernel, in floats: W1 [Hp][K+4], split-K partials
 // [4 waves][3][NT][64] f4, V [3][16][Hp+1], per-wave dense sums [4][2Hp+2],

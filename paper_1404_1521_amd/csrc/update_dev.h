@@ -33,21 +33,25 @@ __device__ __forceinline__ void zero_ranges(const ZeroRanges& z, size_t gid, siz
 
 // Dense SGD: kDenseSlices adjacent lanes share an element; lane s sums the
 // partial slots s, s+8, ... in order, then a fixed butterfly adds the eight
-// sums, so the reduction is deterministic.  Layout of a slot: dW1 [Hp][K],
-// db1 [Hp], dw2 [Hp], loss, db2.
+// sums, so the reduction is deterministic.  Elements: dW1 [Hp][K] from the
+// dW1 partials, then db1 [Hp], dw2 [Hp], loss, db2 from the vector partials.
 __device__ void dense_sgd(const DenseArgs& a, int gid, int nthreads, bool bad) {
   const int HK = a.Hp * a.K;
   const int nel = HK + 2 * a.Hp + 2;
   constexpr int SL = kDenseSlices;
   const int sl = gid % SL;
   for (int e0 = gid / SL; e0 < nel; e0 += nthreads / SL) {
+    const bool mat = e0 < HK;
+    const float* src = mat ? a.part + e0 : a.vpart + (e0 - HK);
+    const int np = mat ? a.n_parts : a.n_vparts;
+    const size_t stride = mat ? (size_t)a.part_stride : (size_t)a.vstride;
     float s = 0.f;
-    for (int p0 = sl; p0 < a.n_parts; p0 += 8 * SL) {
+    for (int p0 = sl; p0 < np; p0 += 8 * SL) {
       float v[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int p = p0 + u * SL;
-        v[u] = p < a.n_parts ? a.part[(size_t)p * a.part_stride + e0] : 0.f;
+        v[u] = p < np ? src[(size_t)p * stride] : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) s += v[u];

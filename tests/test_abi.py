@@ -62,6 +62,8 @@ def _cfg(**kw):
     dict(max_scatter=10, max_rows=0),
     # W1 (64 x 388 floats) and the tile buffers exceed one workgroup's 160 KiB of LDS
     dict(H=48, d=128, win=3),
+    # hidden layers above 64 units: multiples of 64 up to 256, d a multiple of 64
+    dict(H=96, d=64), dict(H=128, d=80), dict(H=320, d=64),
 ])
 def test_init_rejects_bad_config_before_any_device_call(lib, kw):
     import paper_1404_1521_amd as pg

@@ -237,6 +237,65 @@ def test_other_shapes(w, mode):
     run_both(w, w.steps, w.B, mode)
 
 
+# Hidden layers wider than 64 units take the three-contraction path
+# (forward, dW1 slices, per-entry rows); B = 1030 crosses a 1024-window slice.
+LARGE_SHAPES = [
+    workloads.Workload("w11_d128_h256", V=3000, d=128, win=11, H=256, B=100, lr=0.05, steps=3,
+                       zipf_s=1.0, seed=21),
+    workloads.Workload("w3_d64_h128", V=2000, d=64, win=3, H=128, B=1030, lr=0.05, steps=2,
+                       zipf_s=1.0, seed=22),
+    workloads.Workload("w5_d192_h192", V=1500, d=192, win=5, H=192, B=70, lr=0.05, steps=2,
+                       zipf_s=1.1, seed=23),
+]
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("w", LARGE_SHAPES, ids=[w.name for w in LARGE_SHAPES])
+def test_large_hidden_layer_shapes(w, mode):
+    run_both(w, w.steps, w.B, mode)
+
+
+@pytest.mark.parametrize("w", LARGE_SHAPES[:2], ids=[w.name for w in LARGE_SHAPES[:2]])
+def test_large_hidden_layer_scores(w):
+    p = workloads.init_params(w)
+    win, _ = workloads.batch(w, 1, w.B)
+    ctx = pg().Context(w.V, w.d, w.win, w.H, max_batch=w.B)
+    got = host(ctx.score(params_dev(p), dev(win)))
+    np.testing.assert_allclose(got, oracle.score(p, win), rtol=1e-5, atol=1e-6)
+
+
+def test_stress_full_size_sampled():
+    """The stress workload at its full size (V 1M, d 128, window 11, H 256,
+    B 16384): scores of sampled true and corrupted windows against the oracle,
+    then one sorted step: status clean, loss finite and in the hinge range,
+    rows outside the batch and b2 bit-identical."""
+    w = PRESETS["stress"]
+    p = workloads.init_params(w)
+    pd = params_dev(p)
+    win, cor = workloads.batch(w, 0, w.B)
+    ctx = pg().Context(w.V, w.d, w.win, w.H, max_batch=w.B)
+    rng = np.random.default_rng(0)
+    pick = np.sort(rng.choice(w.B, 48, replace=False))
+    sample = np.ascontiguousarray(win[pick])
+    corrupted = sample.copy()
+    corrupted[:, w.win // 2] = cor[pick]
+    both = np.concatenate([sample, corrupted])
+    got = host(ctx.score(pd, dev(both)))
+    np.testing.assert_allclose(got, oracle.score(p, both), rtol=1e-5, atol=1e-6)
+    loss = torch.zeros(1, device="cuda")
+    ctx.train_step(pd, dev(win), dev(cor), w.lr, loss)
+    assert ctx.status() == pg().OK
+    lv = float(host(loss)[0])
+    assert np.isfinite(lv) and 0.0 < lv < 2.0
+    touched = np.zeros(w.V, bool)
+    touched[win.reshape(-1)] = True
+    touched[cor] = True
+    E = host(pd["E"])
+    assert np.array_equal(E[~touched], p["E"][~touched])
+    assert not np.array_equal(E[touched], p["E"][touched])
+    assert np.array_equal(host(pd["b2"]), p["b2"])
+
+
 @pytest.mark.parametrize("name,B", [("tiny", 32), ("poly256", 256), ("poly256", 4096)])
 def test_touched_rows_bit_exact(name, B):
     w = PRESETS[name]
