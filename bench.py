@@ -24,6 +24,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters_{}.md")
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 F32_MATRIX_PEAK_TFLOPS = 157.3  # MI355X dense fp32 MFMA, published
 F32_VECTOR_PEAK_TFLOPS = 157.3  # 256 CU x 4 SIMD x 64 lanes x 2 flop (FMA) x 2.4 GHz
@@ -42,6 +43,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernels", action="store_true",
                     help="skip the standalone gather / scatter-add measurements")
+    ap.add_argument("--only-kernels", action="store_true",
+                    help="run only the standalone gather / scatter-add measurements (no step, "
+                         "no JSON line): isolates their dispatches under a counter profiler")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device copies of MIB MiB (calibrates the HBM byte "
                          "counters: each copy reads and writes exactly MIB MiB) and exit")
@@ -79,10 +83,18 @@ def batch_structure(wins, cors, ch):
 def step_model(w, B, st, passes, n_parts):
     """{kernel: (bytes, flops, engine)} of one step.
 
+    Hidden layers of at most 64 units (one fused kernel):
     fwdbwd: ids + every window row and corrupt row read once (the gather),
       the per-entry gradient rows G written ((win+1) rows of d floats per
       window), W1 read once, dense partials written; flops = forward 2HK +
       2Hd (corrupted centre block), dW1 2HK + 2Hd, G (win+1) 2Hd per window.
+    Wider layers (three contractions):
+    fwdbwd: ids and rows read, W1 read, the per-window vectors (3H floats)
+      and the db1/dw2/loss partials written; flops 2HK + 2Hd per window.
+    wide_dw1: ids and rows read, the per-window vectors read, one dW1
+      partial per 1024-window slice written; flops 2HK + 2Hd per window.
+    wide_g: the per-window vectors and W1 read, G written; flops
+      (win+1) 2Hd per window.
     sort: 16 B per entry per radix pass (keys and values, read and written).
     update: sorted keys+values and every G row read once, every distinct row
       of E read and written, dense partials read, W1/b1/w2/b2 read and
@@ -92,19 +104,31 @@ def step_model(w, B, st, passes, n_parts):
     """
     d, win, H, K = w.d, w.win, w.H, w.K
     N = B * (win + 1)
-    Hp = _hp(H)
-    part_stride = Hp * K + 2 * Hp + 2
     dense = (H * K + 2 * H + 1) * 4
-    m = {
-        "fwdbwd": (B * ((win + 1) * 4 + 2 * (win + 1) * d * 4) + H * K * 4
-                   + n_parts * part_stride * 4,
-                   B * (4 * H * K + 4 * H * d + (win + 1) * 2 * H * d), "mfma"),
-        "sort": (N * 16 * passes, 0, "hbm"),
-        "update": (N * (8 + d * 4) + 2 * st["U"] * d * 4 + n_parts * part_stride * 4
-                   + 2 * dense, N * d, "alu"),
-        "segfix": (st["partials"] * d * 4 + 2 * st["long_rows"] * d * 4,
-                   st["partials"] * d, "alu"),
-    }
+    rows_in = B * ((win + 1) * 4 + (win + 1) * d * 4)
+    g_out = B * (win + 1) * d * 4
+    if H > 64:
+        slices = -(-B // 1024)
+        vparts = -(-B // 32)
+        vec = B * 3 * H * 4
+        part_bytes = slices * H * K * 4 + vparts * (2 * H + 2) * 4
+        m = {
+            "fwdbwd": (rows_in + H * K * 4 + vec + vparts * (2 * H + 2) * 4,
+                       B * (2 * H * K + 2 * H * d), "mfma"),
+            "wide_dw1": (rows_in + vec + slices * H * K * 4, B * (2 * H * K + 2 * H * d), "mfma"),
+            "wide_g": (vec + H * K * 4 + g_out, B * (win + 1) * 2 * H * d, "mfma"),
+        }
+    else:
+        Hp = _hp(H)
+        part_stride = Hp * K + 2 * Hp + 2
+        part_bytes = n_parts * part_stride * 4
+        m = {
+            "fwdbwd": (rows_in + g_out + H * K * 4 + part_bytes,
+                       B * (4 * H * K + 4 * H * d + (win + 1) * 2 * H * d), "mfma"),
+        }
+    m["sort"] = (N * 16 * passes, 0, "hbm")
+    m["update"] = (N * (8 + d * 4) + 2 * st["U"] * d * 4 + part_bytes + 2 * dense, N * d, "alu")
+    m["segfix"] = (st["partials"] * d * 4 + 2 * st["long_rows"] * d * 4, st["partials"] * d, "alu")
     return m
 
 
@@ -123,6 +147,45 @@ def roofline(nbytes, nflops, engine, ms):
 
 
 # ---------------------------------------------------------------------------
+# HBM traffic from the committed rocprofv3 counter summaries.
+
+def source_digest():
+    """sha256 over the HIP sources (file names and contents, sorted by name)."""
+    import hashlib
+    h = hashlib.sha256()
+    src = os.path.join(ROOT, "paper_1404_1521_amd", "csrc")
+    for name in sorted(os.listdir(src)):
+        if name.endswith((".hip", ".h")):
+            h.update(name.encode())
+            with open(os.path.join(src, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def counter_traffic(summary, kernel):
+    """HBM bytes per launch (per call for the scatter-add entries) of `kernel`
+    from the summary's FETCH_SIZE and WRITE_SIZE averages, each scaled by the
+    ratio of known bytes to counted bytes of a plain device copy profiled the
+    same way.  None if the summary is missing, lacks the kernel, or was taken
+    from kernel sources other than the ones built here."""
+    import re
+    try:
+        with open(COUNTERS.format(summary)) as f:
+            text = f.read()
+    except OSError:
+        return None
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if not m:
+        return None
+    data = json.loads(m.group(1))
+    k = data.get("kernels", {}).get(kernel)
+    if data.get("source_sha256") != source_digest() or not k:
+        return None
+    cal = data["copy"]
+    f_scale = cal["bytes_read"] / (cal["fetch_kib"] * 1024.0)
+    w_scale = cal["bytes_written"] / (cal["write_kib"] * 1024.0)
+    return int(round(k["fetch_kib"] * 1024.0 * f_scale + k["write_kib"] * 1024.0 * w_scale))
+
 
 def cpu_model_name():
     try:
@@ -196,8 +259,9 @@ def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
             ctx.gather(E, dw, dc, X, Xc)
         ms, n = ctx.kernel_times()["gather"]
         nbytes = w.B * ((w.win + 1) * 4 + 2 * (w.win + 1) * w.d * 4)
-        out["gather"] = dict(roofline(nbytes, 0, "hbm", ms / n), avg_launch_us=round(ms / n * 1e3, 3),
-                             bytes_per_launch=nbytes, workload=f"B={w.B} V={w.V} d={w.d} win={w.win}")
+        out["gather"] = dict(roofline(nbytes, 0, "hbm", ms / n), traffic=counter_traffic("kernels", "gather"),
+                             avg_launch_us=round(ms / n * 1e3, 3), bytes_per_launch=nbytes,
+                             workload=f"B={w.B} V={w.V} d={w.d} win={w.win}")
 
         table0, idx, Y = workloads.scatter_inputs(sw)
         T = torch.from_numpy(table0).cuda()
@@ -215,7 +279,8 @@ def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
                 ctx.scatter_add(T, I, Yd, 1.0, mode)
             ms, n = ctx.kernel_times()["scatter"]
             ctx.set_timing(False)
-            out[name] = dict(roofline(nbytes, 0, "hbm", call_ms), avg_call_us=round(call_ms * 1e3, 3),
+            out[name] = dict(roofline(nbytes, 0, "hbm", call_ms), traffic=counter_traffic("kernels", name),
+                             avg_call_us=round(call_ms * 1e3, 3),
                              kernel_us_per_call=round(ms / reps * 1e3, 3),
                              launches_per_call=n // reps, bytes_per_call=nbytes,
                              workload=f"{sw.N} rows Zipf({sw.zipf_s}) into {sw.rows}x{sw.d}, U={U}")
@@ -249,6 +314,14 @@ def main():
 
     import paper_1404_1521_amd as pg
     import workloads
+
+    if args.only_kernels:
+        torch.cuda.set_device(0)
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            kernel_rooflines(torch, np, pg, workloads, stream)
+        torch.cuda.synchronize()
+        return
 
     w = workloads.PRESETS[args.workload]
     B, K, Wm = w.B, args.steps, args.warmup
@@ -309,7 +382,7 @@ def main():
         ctx.close()
 
     # structure of the timed batches (sampled) for the byte model
-    small = N <= 8192
+    small = N <= 8192 and w.H <= 64
     samp = [batch_structure(wins[s], cors[s], seg_chunk(N)) for s in range(Wm + K, Wm + K + min(K, 8))]
     st = {k: float(np.mean([x[k] for x in samp])) for k in samp[0]}
     key_bits = max(1, int(w.V - 1).bit_length())
@@ -319,17 +392,25 @@ def main():
     nt = -(-w.H // 16)
     n_parts = min(-(-B // 16), 256 if (w.d, w.win, nt) in ((64, 5, 2), (16, 5, 1)) else 512)
     model = step_model(w, B, st, passes, n_parts)
+    model_flops = sum(v[1] for v in model.values())
     per = {k: (v[0] / v[1], v[1] / K) for k, v in kt.items() if v[1]}
     dom = max(per, key=lambda k: per[k][0] * per[k][1])
     dms = per[dom][0]
+    # the model is per step; a kernel id with several launches per step (the
+    # sort: histogram + one launch per radix pass) is priced per launch
     nbytes, nflops, engine = model[dom]
+    nbytes, nflops = nbytes / per[dom][1], nflops / per[dom][1]
     roof = roofline(nbytes, nflops, engine, dms)
-    roof["traffic"] = None
+    roof["traffic"] = counter_traffic(args.workload, dom) if args.mode == "sorted" else None
+    roof["traffic_unit"] = "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["kernel"] = dom
+    roof["launches_per_step"] = round(per[dom][1], 3)
     roof["avg_launch_us"] = round(dms * 1e3, 3)
     roof["bytes_per_launch"] = int(nbytes)
     roof["flops_per_launch"] = int(nflops)
     roof["kernels_us_per_step"] = {k: round(v[0] * v[1] * 1e3, 3) for k, v in per.items()}
+    # every contraction of the step over the step time (all kernels, gaps included)
+    roof["step_tflops"] = round(model_flops / (ms / K * 1e-3) / 1e12, 3)
 
     value = B * K / (ms * 1e-3)
     out = {

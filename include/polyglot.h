@@ -140,14 +140,17 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
 int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int32_t* count);
 
 /* Kernel ids reported by polyglot_kernel_times. */
-#define POLYGLOT_K_FWDBWD 0   /* fused gather + forward + hinge + backward (+ sort start) */
+#define POLYGLOT_K_FWDBWD 0   /* fused gather + forward + hinge + backward (+ sort start);
+                                 wide layers: gather + forward + hinge + per-window dz */
 #define POLYGLOT_K_SORT 1     /* radix passes of the entry sort (large batches) */
 #define POLYGLOT_K_UPDATE 2   /* embedding segmented update + dense SGD */
 #define POLYGLOT_K_GATHER 3   /* polyglot_gather */
 #define POLYGLOT_K_SCATTER 4  /* polyglot_scatter_add (all of its launches) */
 #define POLYGLOT_K_SCORE 5    /* polyglot_score */
 #define POLYGLOT_K_SEGFIX 6   /* rows whose sorted entries span several chunks */
-#define POLYGLOT_NKERNELS 7
+#define POLYGLOT_K_WIDE_DW1 7 /* wide layers: dW1 partials over window slices */
+#define POLYGLOT_K_WIDE_G 8   /* wide layers: per-entry embedding gradient rows */
+#define POLYGLOT_NKERNELS 9
 
 /* Per-kernel timing for measurement.  With enable != 0 every later kernel
  * launch of this context (outside graph capture) gets a start/stop event

@@ -30,7 +30,8 @@ EXPORTS = ("polyglot_init", "polyglot_destroy", "polyglot_set_stream", "polyglot
            "polyglot_train_steps", "polyglot_score", "polyglot_gather", "polyglot_scatter_add",
            "polyglot_touched_rows", "polyglot_status", "polyglot_last_error",
            "polyglot_set_timing", "polyglot_kernel_times")
-KERNEL_NAMES = ("fwdbwd", "sort", "update", "gather", "scatter", "score", "segfix")
+KERNEL_NAMES = ("fwdbwd", "sort", "update", "gather", "scatter", "score", "segfix", "wide_dw1",
+                "wide_g")
 
 
 class PolyglotError(RuntimeError):

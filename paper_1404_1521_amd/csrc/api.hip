@@ -289,8 +289,14 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
     {
       Timed tm(ctx, POLYGLOT_K_FWDBWD);
       e = launch_large_fwd(la, 0, tm.L);
-      if (e == hipSuccess) e = launch_large_dw1(la, tm.L);
-      if (e == hipSuccess) e = launch_large_g(la, tm.L);
+    }
+    if (e == hipSuccess) {
+      Timed tm(ctx, POLYGLOT_K_WIDE_DW1);
+      e = launch_large_dw1(la, tm.L);
+    }
+    if (e == hipSuccess) {
+      Timed tm(ctx, POLYGLOT_K_WIDE_G);
+      e = launch_large_g(la, tm.L);
     }
   } else {
     FwdArgs fa{};
