@@ -142,10 +142,12 @@ int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int
 /* Kernel ids reported by polyglot_kernel_times. */
 #define POLYGLOT_K_FWDBWD 0   /* fused gather + forward + hinge + backward (+ sort start);
                                  wide layers: gather + forward + hinge + per-window dz */
-#define POLYGLOT_K_SORT 1     /* radix passes of the entry sort (large batches) */
+#define POLYGLOT_K_SORT 1     /* entry sort launches of a step (large batches) or of
+                                 polyglot_scatter_add */
 #define POLYGLOT_K_UPDATE 2   /* embedding segmented update + dense SGD */
 #define POLYGLOT_K_GATHER 3   /* polyglot_gather */
-#define POLYGLOT_K_SCATTER 4  /* polyglot_scatter_add (all of its launches) */
+#define POLYGLOT_K_SCATTER 4  /* polyglot_scatter_add's table update (atomic mode: and the id
+                                 check); its sort and fix-up count under SORT and SEGFIX */
 #define POLYGLOT_K_SCORE 5    /* polyglot_score */
 #define POLYGLOT_K_SEGFIX 6   /* rows whose sorted entries span several chunks */
 #define POLYGLOT_K_WIDE_DW1 7 /* wide layers: dW1 partials over window slices */
@@ -159,8 +161,8 @@ int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int
  * the host enqueue.  polyglot_kernel_times() synchronises the streams,
  * writes the summed elapsed milliseconds and the launch count of each kernel
  * id into ms[POLYGLOT_NKERNELS] and launches[POLYGLOT_NKERNELS] (host
- * arrays), and resets the sums.  POLYGLOT_K_SCATTER and POLYGLOT_K_SORT sum
- * every launch of their call. */
+ * arrays), and resets the sums.  An id with several launches in one call
+ * (the sort: histogram and radix passes) sums all of them. */
 int polyglot_set_timing(polyglot_ctx* ctx, int enable);
 int polyglot_kernel_times(polyglot_ctx* ctx, double* ms, int32_t* launches);
 

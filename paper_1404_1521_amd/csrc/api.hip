@@ -695,15 +695,24 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
   aa.n_e = table_workgroups(aa.s, aa.mode);
   aa.n_d = 0;
   hipError_t e;
-  Timed tm(ctx, POLYGLOT_K_SCATTER);
   if (aa.mode == 0) {
     // the sort validates the indices (sticky flag) and clears the task list
     aa.zero = sort_zero_ranges(ctx, plan, 0);
     const int n_z = plan.small ? 0 : 16;
-    e = launch_sort_idx(kf, N, plan, sort_bufs(ctx, 0), ctx->ws.long_count, tm.L);
-    if (e == hipSuccess) e = launch_apply_idx(aa, kf, aa.n_e + n_z, tm.L);
-    if (e == hipSuccess) e = launch_segfix(aa.s, segfix_workgroups(aa.s), tm.L);
+    {
+      Timed tm(ctx, POLYGLOT_K_SORT);
+      e = launch_sort_idx(kf, N, plan, sort_bufs(ctx, 0), ctx->ws.long_count, tm.L);
+    }
+    if (e == hipSuccess) {
+      Timed tm(ctx, POLYGLOT_K_SCATTER);
+      e = launch_apply_idx(aa, kf, aa.n_e + n_z, tm.L);
+    }
+    if (e == hipSuccess) {
+      Timed tm(ctx, POLYGLOT_K_SEGFIX);
+      e = launch_segfix(aa.s, segfix_workgroups(aa.s), tm.L);
+    }
   } else {
+    Timed tm(ctx, POLYGLOT_K_SCATTER);
     e = launch_check_idx(idx, N, rows, ctx->ws.flag, tm.L);
     if (e == hipSuccess) e = launch_apply_idx(aa, kf, aa.n_e, tm.L);
   }

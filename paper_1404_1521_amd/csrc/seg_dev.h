@@ -53,17 +53,26 @@ __device__ __forceinline__ ChunkInfo chunk_info(const int32_t* __restrict__ sk,
                                                 int ch) {
   ChunkInfo ci;
   const int lane = lane_id();
-  ci.i0 = chunk * ch;
-  ci.nact = min(ch, N - ci.i0);
+  ci.i0 = __builtin_amdgcn_readfirstlane(chunk * ch);
+  ci.nact = __builtin_amdgcn_readfirstlane(min(ch, N - ci.i0));
   const bool act = lane < ci.nact;
   ci.key = act ? sk[ci.i0 + lane] : -1;
   ci.ent = act ? sv[ci.i0 + lane] : 0;
-  const int32_t before = (ci.i0 > 0) ? sk[ci.i0 - 1] : -1;
-  const int32_t after = (ci.i0 + ch < N) ? sk[ci.i0 + ch] : -2;
+  // the chunk's structure is wave-uniform: held in scalar registers, so the
+  // per-row tests built from it compile to scalar branches
+  const int32_t before =
+      __builtin_amdgcn_readfirstlane((ci.i0 > 0) ? sk[ci.i0 - 1] : -1);
+  const int32_t after =
+      __builtin_amdgcn_readfirstlane((ci.i0 + ch < N) ? sk[ci.i0 + ch] : -2);
   int32_t prev = __shfl_up(ci.key, 1);
   if (lane == 0) prev = before;
-  ci.heads = __ballot(act && ci.key != prev);
-  const int32_t last_key = __shfl(ci.key, ci.nact - 1);
+  const uint64_t hb = __ballot(act && ci.key != prev);
+  // (readfirstlane returns int: go through uint32_t so bit 31 does not
+  // sign-extend into the high word)
+  const uint32_t hlo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)hb);
+  const uint32_t hhi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(hb >> 32));
+  ci.heads = ((uint64_t)hhi << 32) | (uint64_t)hlo;
+  const int32_t last_key = __builtin_amdgcn_readlane(ci.key, ci.nact - 1);
   ci.cont_first = !(ci.heads & 1ull);
   ci.open_last = (after == last_key);
   return ci;
@@ -97,26 +106,42 @@ __device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
   for (int c0 = 0; c0 < a.d; c0 += kWave) {
     const int col = c0 + lane;
     const bool cok = col < a.d;
-    // every row of the chunk in flight at once (lane = column)
+    // Every lane stays active so that every test below is a wave-uniform
+    // scalar branch.  Lanes past the row end (d not a multiple of 64) work on
+    // the row's last column and add -0.0 there, which leaves any float
+    // unchanged.
+    const int colc = cok ? col : a.d - 1;
+    // every row of the chunk in flight at once (lane = column), issued
+    // without branches: rows past the chunk's end read entry 0's row (lanes
+    // beyond nact hold entry 0), whose values no piece uses
     float v[CH];
 #pragma unroll
     for (int r = 0; r < CH; ++r) {
       const int ent = __builtin_amdgcn_readlane(ci.ent, r);
-      v[r] = (r < nact && cok) ? a.Y[(size_t)ent * a.d + col] : 0.f;
+      v[r] = a.Y[(size_t)ent * a.d + colc];
     }
-    // running sum in entry order, closed at every piece end; completed
-    // pieces go straight to their rows
+    // running sum in entry order, closed at every piece end (tail);
+    // completed pieces go straight to their rows
+    const float alpha = cok ? a.alpha : 0.f;
     float acc = 0.f, first_sum = 0.f, last_sum = 0.f;
 #pragma unroll
     for (int r = 0; r < CH; ++r) {
       acc += v[r];
-      if (r == first_tail) first_sum = acc;
-      if (r == nact - 1) last_sum = acc;
-      if (((complete >> r) & 1ull) && cok) {
-        const int32_t key = __builtin_amdgcn_readlane(ci.key, r);
-        unsafeAtomicAdd(a.table + (size_t)key * a.d + col, a.alpha * acc);
+      // the row's bits are taken from the masks here, in scalar registers:
+      // the empty asm keeps the compiler from computing all CH conditions
+      // ahead of the loads and parking them in vector lanes
+      uint32_t tw = (uint32_t)(tails >> (r & 32)), cw = (uint32_t)(complete >> (r & 32));
+      int ft = first_tail, lt = nact - 1;
+      asm volatile("" : "+s"(tw), "+s"(cw), "+s"(ft), "+s"(lt));
+      if ((tw >> (r & 31)) & 1u) {
+        if (r == ft) first_sum = acc;
+        if (r == lt) last_sum = acc;
+        if ((cw >> (r & 31)) & 1u) {
+          const int32_t key = __builtin_amdgcn_readlane(ci.key, r);
+          unsafeAtomicAdd(a.table + (size_t)key * a.d + colc, cok ? alpha * acc : -0.f);
+        }
+        acc = 0.f;
       }
-      if ((tails >> r) & 1ull) acc = 0.f;
     }
     if (cok) {
       if (ci.cont_first) a.seg_part[((size_t)chunk * 2 + 0) * a.seg_stride + col] = first_sum;

@@ -77,7 +77,7 @@ __device__ void dense_sgd(const DenseArgs& a, int gid, int nthreads, bool bad) {
 }
 
 template <int CH, class KeyFn>
-__global__ __launch_bounds__(kBlock) void k_apply(ApplyArgs a, KeyFn kf) {
+__global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
   const int t = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const bool bad = (*reinterpret_cast<const volatile uint32_t*>(a.s.flag)) != 0u;

@@ -149,6 +149,64 @@ def test_scatter_add_matches_oracle(mode, rows, d, N, s):
     assert np.array_equal(got[untouched], t0[untouched])
 
 
+def _run_lengths_covering_every_lane(rng, N):
+    """Keys whose sorted runs have every length 1..70 (shuffled), so piece
+    heads fall on every lane of a 64-entry chunk, runs cross chunk ends, and
+    a run starting at lane 31 continues past lane 32."""
+    lens = []
+    while sum(lens) < N:
+        lens.extend(rng.permutation(np.arange(1, 71)).tolist())
+    keys = np.repeat(np.arange(len(lens)), lens)[:N]
+    return keys.astype(np.int32)
+
+
+@pytest.mark.parametrize("pattern", ["every_lane", "head_at_lane_31"])
+@pytest.mark.parametrize("d", [64, 80])
+def test_scatter_add_long_chunks_piece_structure(pattern, d):
+    """Lists above 131072 entries use 64-entry chunks; these key layouts put
+    piece boundaries on each lane (including both halves of the 64-bit lane
+    masks) and rows of 80 floats take a second, partial column block."""
+    rng = np.random.default_rng(7)
+    N = 140_000
+    if pattern == "every_lane":
+        keys = _run_lengths_covering_every_lane(rng, N)
+    else:  # runs of 64 whose heads all sit at lane 31 of their chunk
+        keys = ((np.arange(N) + 33) // 64).astype(np.int32)
+    rows = int(keys.max()) + 5
+    idx = keys[rng.permutation(N)]  # the sort regroups the runs
+    t0 = rng.normal(0, 0.01, (rows, d)).astype(np.float32)
+    Y = rng.normal(0, 1e-3, (N, d)).astype(np.float32)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    td = dev(t0)
+    ctx.scatter_add(td, dev(idx), dev(Y), -0.5, pg().SCATTER_SORTED)
+    assert ctx.status() == pg().OK
+    got = host(td)
+    ref = t0.copy()
+    oracle.scatter_add(ref, idx, Y, -0.5)
+    err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    assert np.all(err <= scatter_bound(t0, idx, Y, -0.5))
+    untouched = np.setdiff1d(np.arange(rows), idx)
+    assert np.array_equal(got[untouched], t0[untouched])
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_scatter_add_full_size_zipf12(mode):
+    """327,680 Zipf(1.2) rows into a 100000 x 64 table, the standalone
+    scatter-add workload, against the oracle."""
+    table, idx, Y = workloads.scatter_inputs()
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=idx.size, max_rows=table.shape[0])
+    td = dev(table)
+    ctx.scatter_add(td, dev(idx), dev(Y), 1.0, mode)
+    assert ctx.status() == pg().OK
+    got = host(td)
+    ref = table.copy()
+    oracle.scatter_add(ref, idx, Y, 1.0)
+    err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    assert np.all(err <= scatter_bound(table, idx, Y, 1.0))
+    untouched = np.setdiff1d(np.arange(table.shape[0]), idx)
+    assert np.array_equal(got[untouched], table[untouched])
+
+
 def test_scatter_add_sorted_is_deterministic():
     table, idx, Y = workloads.scatter_inputs(N=100_000)
     ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=idx.size, max_rows=table.shape[0])
