@@ -30,7 +30,7 @@ struct SegArgs {
   const int32_t* sk;        // sorted keys [N]
   const int32_t* sv;        // entry ids in sorted order [N]
   float* seg_part;          // [chunks][2][seg_stride]
-  int32_t* long_list;       // start chunks of segments that cross chunks
+  int2* long_list;          // (start chunk, row) of segments that cross chunks
   uint32_t* long_count;     // cleared by the sort launch of the same call
   int32_t* seg_end;         // [rows]: end chunk of a crossing segment, by key
   const uint32_t* flag;     // sticky error bits: nonzero voids the update
@@ -44,6 +44,7 @@ struct ChunkInfo {
   int32_t key;      // this lane's sorted key (-1 beyond the chunk)
   int32_t ent;      // this lane's entry id (0 beyond the chunk)
   uint64_t heads;   // lanes that start a piece
+  int32_t last_key; // key of the chunk's last row
   bool cont_first;  // the first piece continues a segment from the previous chunk
   bool open_last;   // the last piece continues into the next chunk
 };
@@ -72,9 +73,9 @@ __device__ __forceinline__ ChunkInfo chunk_info(const int32_t* __restrict__ sk,
   const uint32_t hlo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)hb);
   const uint32_t hhi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(hb >> 32));
   ci.heads = ((uint64_t)hhi << 32) | (uint64_t)hlo;
-  const int32_t last_key = __builtin_amdgcn_readlane(ci.key, ci.nact - 1);
+  ci.last_key = __builtin_amdgcn_readlane(ci.key, ci.nact - 1);
   ci.cont_first = !(ci.heads & 1ull);
-  ci.open_last = (after == last_key);
+  ci.open_last = (after == ci.last_key);
   return ci;
 }
 
@@ -85,8 +86,13 @@ __host__ __device__ inline int seg_chunk_size(int N) { return N <= 131072 ? 16 :
 // One wave applies chunk `chunk` of the sorted list (see the file comment).
 template <int CH>
 __device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
+  static_assert(CH % 8 == 0 && CH <= kWave, "rows are walked in blocks of 8");
   const int lane = lane_id();
+  // the error flag (set by an earlier launch) is read beside the chunk's
+  // keys, and tested before any write
+  const uint32_t flag = *a.flag;
   const ChunkInfo ci = chunk_info(a.sk, a.sv, a.N, chunk, CH);
+  if (__builtin_amdgcn_readfirstlane(flag) != 0u) return;  // a bad id voids the update
   const int nact = ci.nact;
   const uint64_t act = nact >= 64 ? ~0ull : ((1ull << nact) - 1ull);
   // piece ends: the lane before every later head, and the last active lane
@@ -99,7 +105,7 @@ __device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
   const bool starts_long = ci.open_last && !(ci.cont_first && single);
   const bool ends_long = ci.cont_first && !(ci.open_last && single);
   if (lane == 0) {
-    if (starts_long) a.long_list[atomicAdd(a.long_count, 1u)] = chunk;
+    if (starts_long) a.long_list[atomicAdd(a.long_count, 1u)] = make_int2(chunk, ci.last_key);
     if (ends_long) a.seg_end[ci.key] = chunk;  // lane 0 holds the first piece's key
   }
 
@@ -125,22 +131,30 @@ __device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
     const float alpha = cok ? a.alpha : 0.f;
     float acc = 0.f, first_sum = 0.f, last_sum = 0.f;
 #pragma unroll
-    for (int r = 0; r < CH; ++r) {
-      acc += v[r];
-      // the row's bits are taken from the masks here, in scalar registers:
-      // the empty asm keeps the compiler from computing all CH conditions
-      // ahead of the loads and parking them in vector lanes
-      uint32_t tw = (uint32_t)(tails >> (r & 32)), cw = (uint32_t)(complete >> (r & 32));
-      int ft = first_tail, lt = nact - 1;
+    for (int r0 = 0; r0 < CH; r0 += 8) {
+      // this block's bits, taken from the masks here in scalar registers:
+      // the empty asm keeps the compiler from computing every row's
+      // condition ahead of the loads and parking them in vector lanes
+      uint32_t tw = (uint32_t)(tails >> r0) & 0xffu, cw = (uint32_t)(complete >> r0) & 0xffu;
+      int ft = first_tail - r0, lt = nact - 1 - r0;
       asm volatile("" : "+s"(tw), "+s"(cw), "+s"(ft), "+s"(lt));
-      if ((tw >> (r & 31)) & 1u) {
-        if (r == ft) first_sum = acc;
-        if (r == lt) last_sum = acc;
-        if ((cw >> (r & 31)) & 1u) {
-          const int32_t key = __builtin_amdgcn_readlane(ci.key, r);
-          unsafeAtomicAdd(a.table + (size_t)key * a.d + colc, cok ? alpha * acc : -0.f);
+      if (tw == 0u) {  // no piece ends in these rows
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc += v[r0 + u];
+      } else {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          acc += v[r0 + u];
+          if ((tw >> u) & 1u) {
+            if (u == ft) first_sum = acc;
+            if (u == lt) last_sum = acc;
+            if ((cw >> u) & 1u) {
+              const int32_t key = __builtin_amdgcn_readlane(ci.key, r0 + u);
+              unsafeAtomicAdd(a.table + (size_t)key * a.d + colc, cok ? alpha * acc : -0.f);
+            }
+            acc = 0.f;
+          }
         }
-        acc = 0.f;
       }
     }
     if (cok) {
@@ -165,13 +179,17 @@ __device__ void seg_fix_row(const SegArgs& a, int li, float* red /* [waves][kMax
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const int q = lane & 15, gq = lane >> 4;
-  const int cs = a.long_list[li];
-  const int32_t key = a.sk[(size_t)cs * a.ch + a.ch - 1];
+  const int2 rec = a.long_list[li];
+  const int cs = rec.x;
+  const int32_t key = rec.y;
   const int m = a.seg_end[key] - cs + 1;  // partials of this segment
   constexpr int G = kSegfixWaves * 4;     // lane groups per workgroup
   for (int c0 = 0; c0 < a.d; c0 += 64) {
     const int col = c0 + 4 * q;
     const bool cok = col < a.d;
+    float* tr = a.table + (size_t)key * a.d + col;
+    const bool owner = w == 0 && gq == 0 && cok;
+    const f4 row = owner ? ld4(tr) : kZero4;  // in flight beside the partials
     f4 acc = kZero4;
     for (int base = 0; base < m; base += G * kSegfixUnroll) {
       f4 x[kSegfixUnroll];
@@ -192,12 +210,11 @@ __device__ void seg_fix_row(const SegArgs& a, int li, float* red /* [waves][kMax
     __syncthreads();  // red of the previous column block is no longer read
     if (gq == 0) st4(red + w * kMaxD + 4 * q, acc);
     __syncthreads();
-    if (w == 0 && gq == 0 && cok) {
+    if (owner) {
       f4 s = ld4(red + 4 * q);
 #pragma unroll
       for (int v = 1; v < kSegfixWaves; ++v) s += ld4(red + v * kMaxD + 4 * q);
-      float* tr = a.table + (size_t)key * a.d + col;
-      st4(tr, ld4(tr) + a.alpha * s);
+      st4(tr, row + a.alpha * s);
     }
   }
 }

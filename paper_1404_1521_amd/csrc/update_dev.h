@@ -80,18 +80,20 @@ template <int CH, class KeyFn>
 __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
   const int t = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
-  const bool bad = (*reinterpret_cast<const volatile uint32_t*>(a.s.flag)) != 0u;
   if ((int)blockIdx.x < a.n_e) {
-    if (bad) return;  // all-or-nothing: an out-of-range id voids the update
+    // all-or-nothing: an out-of-range id voids the update (the segmented
+    // apply tests the flag itself, once its loads are in flight)
     if (a.mode == 0) {
       const int nchunks = ceil_div(a.s.N, CH);
       for (int c = blockIdx.x * kWavesPerBlock + w; c < nchunks; c += a.n_e * kWavesPerBlock)
         seg_apply_chunk<CH>(a.s, c);
     } else {
+      if (*reinterpret_cast<const volatile uint32_t*>(a.s.flag)) return;
       atomic_rows(a.s, kf, blockIdx.x, a.n_e);
     }
     return;
   }
+  const bool bad = (*reinterpret_cast<const volatile uint32_t*>(a.s.flag)) != 0u;
   const int gid = (blockIdx.x - a.n_e) * kBlock + t;
   const int nthreads = (gridDim.x - a.n_e) * kBlock;
   if (a.n_d > 0) dense_sgd(a.dn, gid, nthreads, bad);
@@ -101,8 +103,9 @@ __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
 // Rows whose sorted entries cross chunks: one workgroup per row.
 __global__ __launch_bounds__(kSegfixThreads) void k_segfix(SegArgs a) {
   __shared__ float red[kSegfixWaves * kMaxD];
-  if (*reinterpret_cast<const volatile uint32_t*>(a.flag)) return;
-  const uint32_t cnt = *a.long_count;
+  // both read together; the task count is only used if the flag is clear
+  const uint32_t flag = *a.flag, cnt = *a.long_count;
+  if (flag) return;
   for (uint32_t li = blockIdx.x; li < cnt; li += gridDim.x) seg_fix_row(a, (int)li, red);
 }
 
