@@ -217,8 +217,12 @@ hipError_t launch_large_fwd(const LargeArgs& a, int score_only, const Launch& L)
 }
 
 hipError_t launch_large_dw1(const LargeArgs& a, const Launch& L) {
-  return pg_launch(k_large_dw1, dim3(a.H / 64, a.K / 64, ceil_div(a.B, kLgSlice)), dim3(kBlock), 0,
-                   L, a);
+  // 128-column blocks when they stay inside one window position
+  if (a.d % 128 == 0)
+    return pg_launch(k_large_dw1<128>, dim3(a.H / 64, a.K / 128, ceil_div(a.B, kLgSlice)),
+                     dim3(kBlock), 0, L, a);
+  return pg_launch(k_large_dw1<64>, dim3(a.H / 64, a.K / 64, ceil_div(a.B, kLgSlice)), dim3(kBlock),
+                   0, L, a);
 }
 
 hipError_t launch_large_g(const LargeArgs& a, const Launch& L) {

@@ -11,7 +11,8 @@
 //                 mode it writes s(x) instead.
 //   k_large_dw1   dW1 partials: dW1[h][k] = sum_b V_b[h] x_b[k] (centre block:
 //                 dz e_c + dz~ e~) over 1024-window slices; a workgroup owns a
-//                 64 x 64 block of dW1 and one slice.
+//                 64 x KT block of dW1 (KT = 128 when d allows, else 64) and
+//                 one slice, its operands staged through LDS.
 //   k_large_g     G[e][:] = W1_j^T V for entry e = b(win+1) + j (context
 //                 positions dz + dz~, the true centre dz, the corrupt entry dz~
 //                 through block c); a workgroup owns 64 windows of one entry
@@ -227,59 +228,118 @@ __global__ __launch_bounds__(HW * kWave) void k_large_fwd(LargeArgs a, int score
   }
 }
 
-// dW1 partial of a 64 x 64 block (hidden h0.., columns k0..) over one slice
-// of windows; wave w owns hidden rows h0 + 16w .. +15.
+// dW1 partial of a 64 x KT block (hidden h0.., columns k0.. inside one
+// window position j) over one 1024-window slice.  The operands go through
+// LDS in 16-window blocks, row-major (one window per row):
+//   Vs[w][h]   = the window's vector for this position (dz + dz~ for a
+//                context position; dz, then dz~ in a second phase, for the
+//                centre, whose rows are the true centre and the corrupt word)
+//   Xs[w][col] = E[id(w, j)][off0 + col]
+// MFMA q of a block contracts windows {q, 4+q, 8+q, 12+q}: lane (i, g)
+// supplies Vs[4g+q][16rt+i] and Xs[4g+q][16ct+i].  Row strides are 4 mod 8
+// floats, so the two row groups a half-wave reads sit on disjoint banks,
+// and a row is stored with float4 writes.  Wave w owns columns
+// [w*KT/4, (w+1)*KT/4) and all 64 hidden rows.  The slice's row ids are
+// staged in LDS first; rows two blocks ahead are in flight in registers.
+template <int KT>
 __global__ __launch_bounds__(kBlock) void k_large_dw1(LargeArgs a) {
+  constexpr int CT = KT / 64;          // 16-column tiles per wave
+  constexpr int XF = 16 * KT / 4;      // float4 of one block's rows
+  constexpr int XPT = XF / kBlock;     // ... per thread
+  constexpr int XS = KT + 4, VS = 64 + 4;
+  __shared__ __align__(16) float Vs[2][16][VS];
+  __shared__ __align__(16) float Xs[2][16][XS];
+  __shared__ int32_t ids_s[2][kLgSlice];  // row ids of the slice, per phase
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const int i = lane & 15, g = lane >> 4;
-  const int h0 = blockIdx.x * 64, k0 = blockIdx.y * 64, sl = blockIdx.z;
-  const int d = a.d, j = k0 / d, off0 = k0 - j * d;  // 64 columns inside one position
-  const bool ctr = j == a.c;
-  const int b_lo = sl * kLgSlice, b_hi = min(a.B, b_lo + kLgSlice);
-  const int hA = h0 + 16 * w + i;  // A operand hidden unit of this lane
-  f4 acc[4];
-#pragma unroll
-  for (int cb = 0; cb < 4; ++cb) acc[cb] = kZero4;
-  for (int b0 = b_lo; b0 < b_hi; b0 += 16) {
-    // windows of this chunk for k-index g: b0 + 4g + q
-    float av[4], ac[4], x[4][4], xc[4][4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int b = b0 + 4 * g + q;
-      const bool ok = b < b_hi;
-      int32_t id = ok ? a.windows[(size_t)b * a.win + j] : 0;
-      id = (uint32_t)id < (uint32_t)a.V_rows ? id : 0;
-      const float* vr = a.V + (size_t)b * 3 * a.H + hA;
-      av[q] = ok ? vr[ctr ? a.H : 0] : 0.f;
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb) x[cb][q] = a.E[(size_t)id * d + off0 + 16 * cb + i];
-      if (ctr) {
-        int32_t ic = ok ? a.corrupt[b] : 0;
-        ic = (uint32_t)ic < (uint32_t)a.V_rows ? ic : 0;
-        ac[q] = ok ? vr[2 * a.H] : 0.f;
-#pragma unroll
-        for (int cb = 0; cb < 4; ++cb) xc[cb][q] = a.E[(size_t)ic * d + off0 + 16 * cb + i];
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb) acc[cb] = lg_mfma(av[q], x[cb][q], acc[cb]);
-    if (ctr) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int cb = 0; cb < 4; ++cb) acc[cb] = lg_mfma(ac[q], xc[cb][q], acc[cb]);
+  const int h0 = blockIdx.x * 64, k0 = blockIdx.y * KT, sl = blockIdx.z;
+  const int d = a.d, j = k0 / d, off0 = k0 - j * d;
+  const int phases = (j == a.c) ? 2 : 1;
+  const int b_lo = sl * kLgSlice, b_hi = min(a.B, b_lo + kLgSlice), nb = b_hi - b_lo;
+  const int nblk = (nb + 15) / 16, total = phases * nblk;
+
+  // every row id of the slice up front, so a block's row loads depend on LDS only
+  for (int x = t; x < nb; x += kBlock) {
+    const int32_t id0 = a.windows[(size_t)(b_lo + x) * a.win + j];
+    ids_s[0][x] = (uint32_t)id0 < (uint32_t)a.V_rows ? id0 : 0;
+    if (phases == 2) {
+      const int32_t id1 = a.corrupt[b_lo + x];
+      ids_s[1][x] = (uint32_t)id1 < (uint32_t)a.V_rows ? id1 : 0;
     }
   }
-  // lane (i, g), component q: hidden h0 + 16w + 4g + q, column k0 + 16cb + i
+  __syncthreads();
+
+  // this thread's share of a block: XPT float4 of rows (window xw[u], float4
+  // column xc), one float4 of vectors (window t/16, hidden 4*(t%16))
+  const int xc = t % (KT / 4);
+  int xw[XPT];
+#pragma unroll
+  for (int u = 0; u < XPT; ++u) xw[u] = (t + u * kBlock) / (KT / 4);
+  const int vw = t / 16, vh = 4 * (t % 16);
+  auto load = [&](int bi, f4 (&X)[XPT], f4& Vv) {
+    const int ph = bi / nblk, r0 = (bi - ph * nblk) * 16;
+    const int slot = (phases == 1) ? 0 : 1 + ph;
+#pragma unroll
+    for (int u = 0; u < XPT; ++u) {
+      const int r = r0 + xw[u];
+      const int32_t id = r < nb ? ids_s[ph][r] : 0;
+      X[u] = ld4(a.E + (size_t)id * d + off0 + 4 * xc);
+    }
+    const int r = r0 + vw;
+    Vv = r < nb ? ld4(a.V + (size_t)(b_lo + r) * 3 * a.H + (size_t)slot * a.H + h0 + vh) : kZero4;
+  };
+  auto store = [&](int buf, const f4 (&X)[XPT], const f4& Vv) {
+#pragma unroll
+    for (int u = 0; u < XPT; ++u) st4(&Xs[buf][xw[u]][4 * xc], X[u]);
+    st4(&Vs[buf][vw][vh], Vv);
+  };
+  f4 acc[4][CT];
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) acc[rt][ct] = kZero4;
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float A[4], Bm[CT];
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) A[rt] = Vs[buf][4 * g + q][16 * rt + i];
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) Bm[ct] = Xs[buf][4 * g + q][16 * (w * CT + ct) + i];
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[rt][ct] = lg_mfma(A[rt], Bm[ct], acc[rt][ct]);
+    }
+  };
+
+  // two register sets: the rows of block bi+2 are loaded while blocks bi and
+  // bi+1 are contracted.  One barrier per block: the LDS buffer written at
+  // block bi was last read at block bi-2, before block bi-1's barrier.
+  f4 XA[XPT], VA, XB[XPT], VB;
+  if (total > 0) load(0, XA, VA);
+  if (total > 1) load(1, XB, VB);
+  for (int bi = 0; bi < total; bi += 2) {
+    store(0, XA, VA);
+    if (bi + 2 < total) load(bi + 2, XA, VA);
+    __syncthreads();
+    compute(0);
+    if (bi + 1 >= total) break;
+    store(1, XB, VB);
+    if (bi + 3 < total) load(bi + 3, XB, VB);
+    __syncthreads();
+    compute(1);
+  }
+  // lane (i, g), component r: hidden h0 + 16rt + 4g + r, column k0 + 16(w*CT + ct) + i
   float* P = a.part + (size_t)sl * a.H * a.K;
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb)
+  for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      P[(size_t)(h0 + 16 * w + 4 * g + q) * a.K + k0 + 16 * cb + i] = acc[cb][q];
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        P[(size_t)(h0 + 16 * rt + 4 * g + r) * a.K + k0 + 16 * (w * CT + ct) + i] = acc[rt][ct][r];
 }
 
 // G rows of 64 windows at entry position j = blockIdx.y; wave w owns
