@@ -118,6 +118,7 @@ SortBufs sort_bufs(polyglot_ctx* ctx, int set) {
   sb.status = ctx->ws.status[set];
   sb.tile_ctr = ctx->ws.tile_ctr[set];
   sb.epoch = ctx->ws.epoch[set];
+  sb.part_off = ctx->ws.part_off[set];
   sb.max_tiles = ctx->max_tiles;
   sb.flag = ctx->ws.flag;
   return sb;
@@ -379,13 +380,23 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   aa.dn.lr = lr;
   aa.dn.invB = 1.0f / (float)B;
   if (sorted) aa.zero = sort_zero_ranges(ctx, plan, set);  // counters of this set, now read
-  {
+  if (sorted && plan.small) {
+    // partition-sorted: one workgroup per partition completes every segment,
+    // so no fix-up launch follows
+    aa.part_off = ctx->ws.part_off[set];
+    aa.n_part = 1 << plan.part_bits;
+    aa.n_d = ceil_div(aa.n_d * kBlock, kPartApplyThreads);
     Timed tm(ctx, POLYGLOT_K_UPDATE);
-    e = launch_apply_step(aa, kf, aa.n_e + aa.n_d, tm.L);
-  }
-  if (e == hipSuccess && sorted) {
-    Timed tm(ctx, POLYGLOT_K_SEGFIX);
-    e = launch_segfix(aa.s, segfix_workgroups(aa.s), tm.L);
+    e = launch_apply_part(aa, aa.n_part + aa.n_d, tm.L);
+  } else {
+    {
+      Timed tm(ctx, POLYGLOT_K_UPDATE);
+      e = launch_apply_step(aa, kf, aa.n_e + aa.n_d, tm.L);
+    }
+    if (e == hipSuccess && sorted) {
+      Timed tm(ctx, POLYGLOT_K_SEGFIX);
+      e = launch_segfix(aa.s, segfix_workgroups(aa.s), tm.L);
+    }
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "update launch");
 
@@ -510,6 +521,7 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
     if (e == hipSuccess) e = alloc(ctx, &ws.status[k], nstatus);
     if (e == hipSuccess) e = alloc(ctx, &ws.tile_ctr[k], (size_t)kMaxPasses);
     if (e == hipSuccess) e = alloc(ctx, &ws.epoch[k], 1);
+    if (e == hipSuccess) e = alloc(ctx, &ws.part_off[k], (size_t)(1 << kPartBits) + 1);
   }
   if (e == hipSuccess) e = alloc(ctx, &ws.G, (size_t)c.max_batch * (c.win + 1) * c.d);
   if (large) {
@@ -703,13 +715,20 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
       Timed tm(ctx, POLYGLOT_K_SORT);
       e = launch_sort_idx(kf, N, plan, sort_bufs(ctx, 0), ctx->ws.long_count, tm.L);
     }
-    if (e == hipSuccess) {
+    if (e == hipSuccess && plan.small) {  // partition-wise: no fix-up launch
+      aa.part_off = ctx->ws.part_off[0];
+      aa.n_part = 1 << plan.part_bits;
       Timed tm(ctx, POLYGLOT_K_SCATTER);
-      e = launch_apply_idx(aa, kf, aa.n_e + n_z, tm.L);
-    }
-    if (e == hipSuccess) {
-      Timed tm(ctx, POLYGLOT_K_SEGFIX);
-      e = launch_segfix(aa.s, segfix_workgroups(aa.s), tm.L);
+      e = launch_apply_part(aa, aa.n_part, tm.L);
+    } else if (e == hipSuccess) {
+      {
+        Timed tm(ctx, POLYGLOT_K_SCATTER);
+        e = launch_apply_idx(aa, kf, aa.n_e + n_z, tm.L);
+      }
+      if (e == hipSuccess) {
+        Timed tm(ctx, POLYGLOT_K_SEGFIX);
+        e = launch_segfix(aa.s, segfix_workgroups(aa.s), tm.L);
+      }
     }
   } else {
     Timed tm(ctx, POLYGLOT_K_SCATTER);

@@ -55,6 +55,7 @@ struct Workspace {
   unsigned long long* status[2];  // [kMaxPasses][max_tiles][kMaxBins] look-back words
   uint32_t* tile_ctr[2];    // [kMaxPasses] tile id counters
   uint32_t* epoch[2];       // sort epoch of each set
+  int32_t* part_off[2];     // [2^kPartBits + 1] partitioned sort: where each partition starts
   // step
   float* G;                 // [max_batch*(win+1)][d] per-entry embedding gradients
   float* part;              // dense-gradient partials: [max_parts][part_stride], or

@@ -53,7 +53,8 @@ __global__ __launch_bounds__(kBlock, (NT == 1 || (NT == 2 && CPW <= 5)) ? 2 : 1)
   if ((int)blockIdx.x < a.n_sort) {  // small batches: the step's sort, partition blockIdx.x
     const StepKeys kf = step_keys(a.windows, a.corrupt, a.win, a.V);
     part_sort<kBlock>(kf, a.N, a.plan, blockIdx.x, a.sb.keys[a.plan.passes & 1],
-                      a.sb.vals[a.plan.passes & 1], a.flag, reinterpret_cast<uint32_t*>(lds_f));
+                      a.sb.vals[a.plan.passes & 1], a.sb.part_off, a.flag,
+                      reinterpret_cast<uint32_t*>(lds_f));
     return;
   }
   fwdbwd_wg<NT, CPW, D, WIN>(a, blockIdx.x - a.n_sort, lds_f);
@@ -67,7 +68,7 @@ __global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {
   if ((int)blockIdx.x < a.n_sort) {
     const StepKeys kf = step_keys(a.windows, a.corrupt, a.win, a.V);
     part_sort<kF8Threads>(kf, a.N, a.plan, blockIdx.x, a.sb.keys[a.plan.passes & 1],
-                          a.sb.vals[a.plan.passes & 1], a.flag,
+                          a.sb.vals[a.plan.passes & 1], a.sb.part_off, a.flag,
                           reinterpret_cast<uint32_t*>(lds_f));
     return;
   }
@@ -84,7 +85,7 @@ __global__ __launch_bounds__(kPartSortThreads) void k_sort_part(KeyFn kf, int N,
   extern __shared__ uint32_t lds[];
   if (long_count && blockIdx.x == 0 && threadIdx.x == 0) *long_count = 0u;
   part_sort<kPartSortThreads>(kf, N, plan, blockIdx.x, sb.keys[plan.passes & 1],
-                              sb.vals[plan.passes & 1], sb.flag, lds);
+                              sb.vals[plan.passes & 1], sb.part_off, sb.flag, lds);
 }
 
 // Digit totals of a large list (clears the segment task list when given one).
@@ -180,6 +181,10 @@ hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, c
 
 hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, const Launch& L) {
   return launch_apply(a, kf, grid, L);
+}
+
+hipError_t launch_apply_part(const ApplyArgs& a, int grid, const Launch& L) {
+  return pg_launch(k_apply_part, dim3(grid), dim3(kPartApplyThreads), 0, L, a);
 }
 
 hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L) {

@@ -110,6 +110,8 @@ struct ApplyArgs {
   int mode;  // 0 sorted segments, 1 atomic
   int n_e;
   int n_d;
+  const int32_t* part_off;  // partition-wise update: partition starts (n_part + 1)
+  int n_part;
   DenseArgs dn;
   ZeroRanges zero;
 };
@@ -156,6 +158,7 @@ hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const
 hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, const Launch& L);
 hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, const Launch& L);
 hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L);
+hipError_t launch_apply_part(const ApplyArgs& a, int grid, const Launch& L);
 hipError_t launch_check_idx(const int32_t* idx, int N, int rows, uint32_t* flag, const Launch& L);
 hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, const Launch& L);
 hipError_t launch_gather(const GatherArgs& a, const Launch& L);

@@ -49,13 +49,14 @@ struct ChunkInfo {
   bool open_last;   // the last piece continues into the next chunk
 };
 
+// Entries [i0, min(i0 + ch, end)) of a sorted list that ends at `end`.
 __device__ __forceinline__ ChunkInfo chunk_info(const int32_t* __restrict__ sk,
-                                                const int32_t* __restrict__ sv, int N, int chunk,
+                                                const int32_t* __restrict__ sv, int end, int i0,
                                                 int ch) {
   ChunkInfo ci;
   const int lane = lane_id();
-  ci.i0 = __builtin_amdgcn_readfirstlane(chunk * ch);
-  ci.nact = __builtin_amdgcn_readfirstlane(min(ch, N - ci.i0));
+  ci.i0 = __builtin_amdgcn_readfirstlane(i0);
+  ci.nact = __builtin_amdgcn_readfirstlane(min(ch, end - ci.i0));
   const bool act = lane < ci.nact;
   ci.key = act ? sk[ci.i0 + lane] : -1;
   ci.ent = act ? sv[ci.i0 + lane] : 0;
@@ -64,7 +65,7 @@ __device__ __forceinline__ ChunkInfo chunk_info(const int32_t* __restrict__ sk,
   const int32_t before =
       __builtin_amdgcn_readfirstlane((ci.i0 > 0) ? sk[ci.i0 - 1] : -1);
   const int32_t after =
-      __builtin_amdgcn_readfirstlane((ci.i0 + ch < N) ? sk[ci.i0 + ch] : -2);
+      __builtin_amdgcn_readfirstlane((ci.i0 + ch < end) ? sk[ci.i0 + ch] : -2);
   int32_t prev = __shfl_up(ci.key, 1);
   if (lane == 0) prev = before;
   const uint64_t hb = __ballot(act && ci.key != prev);
@@ -83,15 +84,25 @@ __device__ __forceinline__ ChunkInfo chunk_info(const int32_t* __restrict__ sk,
 // batches over more waves; long chunks keep partials few for large ones.
 __host__ __device__ inline int seg_chunk_size(int N) { return N <= 131072 ? 16 : 64; }
 
-// One wave applies chunk `chunk` of the sorted list (see the file comment).
-template <int CH>
-__device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
+// Where a chunk's open pieces go: GLOBAL, the chunk-indexed partials and the
+// task list of the fix-up launch; LOCAL, a wave's slots in LDS (first piece,
+// last piece, and the chunk's flags and keys) for the workgroup to combine.
+struct ChunkSink {
+  float* first;  // LOCAL: [d] sum of the chunk's first piece when it continues a segment
+  float* last;   // LOCAL: [d] sum of the chunk's last piece when it opens one
+  int* meta;     // LOCAL: cont_first, open_last, single, first key, last key
+};
+
+// One wave applies entries [i0, min(i0 + CH, end)) of the sorted list, chunk
+// number `chunk` (see the file comment).
+template <int CH, bool LOCAL>
+__device__ void seg_apply_rows(const SegArgs& a, int i0, int end, int chunk, const ChunkSink& sink) {
   static_assert(CH % 8 == 0 && CH <= kWave, "rows are walked in blocks of 8");
   const int lane = lane_id();
   // the error flag (set by an earlier launch) is read beside the chunk's
   // keys, and tested before any write
   const uint32_t flag = *a.flag;
-  const ChunkInfo ci = chunk_info(a.sk, a.sv, a.N, chunk, CH);
+  const ChunkInfo ci = chunk_info(a.sk, a.sv, end, i0, CH);
   if (__builtin_amdgcn_readfirstlane(flag) != 0u) return;  // a bad id voids the update
   const int nact = ci.nact;
   const uint64_t act = nact >= 64 ? ~0ull : ((1ull << nact) - 1ull);
@@ -105,10 +116,17 @@ __device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
   const bool starts_long = ci.open_last && !(ci.cont_first && single);
   const bool ends_long = ci.cont_first && !(ci.open_last && single);
   if (lane == 0) {
-    if (starts_long) a.long_list[atomicAdd(a.long_count, 1u)] = make_int2(chunk, ci.last_key);
-    if (ends_long) a.seg_end[ci.key] = chunk;  // lane 0 holds the first piece's key
+    if (LOCAL) {
+      sink.meta[0] = ci.cont_first;
+      sink.meta[1] = ci.open_last;
+      sink.meta[2] = single;
+      sink.meta[3] = ci.key;  // lane 0 holds the first piece's key
+      sink.meta[4] = ci.last_key;
+    } else {
+      if (starts_long) a.long_list[atomicAdd(a.long_count, 1u)] = make_int2(chunk, ci.last_key);
+      if (ends_long) a.seg_end[ci.key] = chunk;
+    }
   }
-
   for (int c0 = 0; c0 < a.d; c0 += kWave) {
     const int col = c0 + lane;
     const bool cok = col < a.d;
@@ -158,9 +176,82 @@ __device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
       }
     }
     if (cok) {
-      if (ci.cont_first) a.seg_part[((size_t)chunk * 2 + 0) * a.seg_stride + col] = first_sum;
-      if (starts_long) a.seg_part[((size_t)chunk * 2 + 1) * a.seg_stride + col] = last_sum;
+      if (LOCAL) {
+        if (ci.cont_first) sink.first[col] = first_sum;
+        if (starts_long) sink.last[col] = last_sum;
+      } else {
+        if (ci.cont_first) a.seg_part[((size_t)chunk * 2 + 0) * a.seg_stride + col] = first_sum;
+        if (starts_long) a.seg_part[((size_t)chunk * 2 + 1) * a.seg_stride + col] = last_sum;
+      }
     }
+  }
+}
+
+template <int CH>
+__device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
+  seg_apply_rows<CH, false>(a, chunk * CH, a.N, chunk, ChunkSink{});
+}
+
+// Threads of a partition workgroup: 16 waves, so one round covers 1024
+// entries in 64-entry chunks.
+constexpr int kPartApplyThreads = 1024;
+constexpr int kPartApplyWaves = kPartApplyThreads / kWave;
+constexpr int kPartApplyChunk = 64;
+
+// Segmented apply of one partition of a partitioned sort, entries [s, e):
+// no key has entries in two partitions, so every segment that crosses a
+// chunk is completed inside the workgroup.  Each round, wave w applies
+// chunk r0 + w and leaves its open pieces in LDS; after a barrier wave 0
+// walks the round's chunks in order, adding the pieces of every crossing
+// segment (carried over from earlier rounds when it started there) and
+// applying the row once the segment closes.  The order of every sum is
+// fixed, so the result does not depend on scheduling.
+__device__ void seg_apply_partition(const SegArgs& a, int s, int e,
+                                    float (*F)[kMaxD], float (*Lp)[kMaxD], int (*meta)[5]) {
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
+  constexpr int CB = kMaxD / kWave;  // column blocks of the widest row
+  const int nch = (e - s + kPartApplyChunk - 1) / kPartApplyChunk;
+  float open[CB];                    // wave 0: the segment still open, by column block
+  int open_key = 0;
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) open[cb] = 0.f;
+  for (int r0 = 0; r0 < nch; r0 += kPartApplyWaves) {
+    const int c = r0 + w;
+    if (c < nch)
+      seg_apply_rows<kPartApplyChunk, true>(a, s + c * kPartApplyChunk, e, c,
+                                            ChunkSink{F[w], Lp[w], meta[w]});
+    __syncthreads();  // the round's open pieces are in LDS
+    if (w == 0) {
+      const int nc = min(kPartApplyWaves, nch - r0);
+      for (int k = 0; k < nc; ++k) {
+        const int cf = meta[k][0], ol = meta[k][1], sg = meta[k][2];
+        if (cf) {  // the chunk's first piece continues the open segment
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) {
+            const int col = cb * kWave + lane;
+            if (col < a.d) open[cb] += F[k][col];
+          }
+          if (!(sg && ol)) {  // ... and closes it: apply the row
+            const int key = open_key;
+#pragma unroll
+            for (int cb = 0; cb < CB; ++cb) {
+              const int col = cb * kWave + lane;
+              if (col < a.d) unsafeAtomicAdd(a.table + (size_t)key * a.d + col, a.alpha * open[cb]);
+            }
+          }
+        }
+        if (ol && !(sg && cf)) {  // the chunk's last piece opens a segment
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) {
+            const int col = cb * kWave + lane;
+            open[cb] = col < a.d ? Lp[k][col] : 0.f;
+          }
+          open_key = meta[k][4];
+        }
+      }
+    }
+    __syncthreads();  // the slots are reused by the next round
   }
 }
 

@@ -247,7 +247,8 @@ __host__ __device__ constexpr size_t part_sort_lds_words(int nth) {
 
 template <int NTH, class KeyFn>
 __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part,
-                          int32_t* out_keys, int32_t* out_vals, uint32_t* flag, uint32_t* lds) {
+                          int32_t* out_keys, int32_t* out_vals, int32_t* part_off, uint32_t* flag,
+                          uint32_t* lds) {
   constexpr int NW = NTH / kWave, UMAX = kSmallSortN / NTH;
   static_assert(NW + 1 <= kPartSortMisc, "scan scratch too small");
   uint32_t* bufA = lds;
@@ -301,6 +302,10 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
   __syncthreads();
   const uint32_t tot = misc[NW];
   const int M = (int)(tot & 0xffffu), off = (int)(tot >> 16);
+  if (t == 0) {  // the partition's place in the output (for the partition-wise update)
+    part_off[part] = off;
+    if (part == (int)pmask) part_off[part + 1] = off + M;
+  }
   __syncthreads();  // misc and hist are reused by the passes
 
   uint32_t* res = lds_lsd_passes<NTH>(bufA, bufB, M, plan, vb, rank16, hist, misc);
@@ -345,6 +350,7 @@ struct SortBufs {
   unsigned long long* status;       // [kMaxPasses][max_tiles][kMaxBins] look-back words
   uint32_t* tile_ctr;               // [kMaxPasses] next tile id of each pass
   uint32_t* epoch;                  // [1] advanced by every histogram launch
+  int32_t* part_off;                // [partitions + 1] partitioned sort: where each partition starts
   int max_tiles;
   uint32_t* flag;                   // sticky error bits
 };

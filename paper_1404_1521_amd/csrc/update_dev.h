@@ -100,6 +100,29 @@ __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
   zero_ranges(a.zero, gid, nthreads);
 }
 
+// Sorted update of a partition-sorted list: workgroup p < n_part applies
+// partition p, whose segments never leave it, so no fix-up launch follows;
+// the remaining workgroups run the dense SGD and clearing roles.
+__global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
+  __shared__ float F[kPartApplyWaves][kMaxD];
+  __shared__ float Lp[kPartApplyWaves][kMaxD];
+  __shared__ int meta[kPartApplyWaves][5];
+  const int t = threadIdx.x;
+  if ((int)blockIdx.x < a.n_part) {
+    // the flag was set (or not) by an earlier launch: every wave reads the
+    // same value, so the whole workgroup leaves together
+    if (__builtin_amdgcn_readfirstlane(*a.s.flag) != 0u) return;
+    const int p = blockIdx.x;
+    seg_apply_partition(a.s, a.part_off[p], a.part_off[p + 1], F, Lp, meta);
+    return;
+  }
+  const bool bad = (*reinterpret_cast<const volatile uint32_t*>(a.s.flag)) != 0u;
+  const int gid = (blockIdx.x - a.n_part) * kPartApplyThreads + t;
+  const int nthreads = (gridDim.x - a.n_part) * kPartApplyThreads;
+  if (a.n_d > 0) dense_sgd(a.dn, gid, nthreads, bad);
+  zero_ranges(a.zero, gid, nthreads);
+}
+
 // Rows whose sorted entries cross chunks: one workgroup per row.
 __global__ __launch_bounds__(kSegfixThreads) void k_segfix(SegArgs a) {
   __shared__ float red[kSegfixWaves * kMaxD];
