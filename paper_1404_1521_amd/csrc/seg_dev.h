@@ -213,7 +213,7 @@ __device__ void seg_apply_partition(const SegArgs& a, int s, int e,
   constexpr int CB = kMaxD / kWave;  // column blocks of the widest row
   const int nch = (e - s + kPartApplyChunk - 1) / kPartApplyChunk;
   float open[CB];                    // wave 0: the segment still open, by column block
-  int open_key = 0;
+  int open_key = 0, open_key_next = 0;
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) open[cb] = 0.f;
   for (int r0 = 0; r0 < nch; r0 += kPartApplyWaves) {
@@ -224,32 +224,45 @@ __device__ void seg_apply_partition(const SegArgs& a, int s, int e,
     __syncthreads();  // the round's open pieces are in LDS
     if (w == 0) {
       const int nc = min(kPartApplyWaves, nch - r0);
-      for (int k = 0; k < nc; ++k) {
-        const int cf = meta[k][0], ol = meta[k][1], sg = meta[k][2];
-        if (cf) {  // the chunk's first piece continues the open segment
+      // every chunk's flags and keys at once (lane k reads chunk k), then
+      // taken as wave-uniform values
+      int mk[5];
 #pragma unroll
-          for (int cb = 0; cb < CB; ++cb) {
-            const int col = cb * kWave + lane;
-            if (col < a.d) open[cb] += F[k][col];
+      for (int x = 0; x < 5; ++x) mk[x] = lane < nc ? meta[lane][x] : 0;
+      const uint64_t cfm = __ballot(mk[0] != 0), olm = __ballot(mk[1] != 0),
+                     sgm = __ballot(mk[2] != 0);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        const int col = cb * kWave + lane;
+        if (cb * kWave >= a.d) break;
+        const bool cok = col < a.d;
+        // the round's open pieces of this column block, all reads in flight
+        float fv[kPartApplyWaves], lv[kPartApplyWaves];
+#pragma unroll
+        for (int k = 0; k < kPartApplyWaves; ++k) {
+          fv[k] = (k < nc && cok) ? F[k][col] : 0.f;
+          lv[k] = (k < nc && cok) ? Lp[k][col] : 0.f;
+        }
+        float o = open[cb];
+        int okey = open_key;
+#pragma unroll
+        for (int k = 0; k < kPartApplyWaves; ++k) {
+          if (k >= nc) break;
+          const bool cf = (cfm >> k) & 1ull, ol = (olm >> k) & 1ull, sg = (sgm >> k) & 1ull;
+          if (cf) {  // the chunk's first piece continues the open segment
+            o += fv[k];
+            if (!(sg && ol) && cok)  // ... and closes it: apply the row
+              unsafeAtomicAdd(a.table + (size_t)okey * a.d + col, a.alpha * o);
           }
-          if (!(sg && ol)) {  // ... and closes it: apply the row
-            const int key = open_key;
-#pragma unroll
-            for (int cb = 0; cb < CB; ++cb) {
-              const int col = cb * kWave + lane;
-              if (col < a.d) unsafeAtomicAdd(a.table + (size_t)key * a.d + col, a.alpha * open[cb]);
-            }
+          if (ol && !(sg && cf)) {  // the chunk's last piece opens a segment
+            o = lv[k];
+            okey = __builtin_amdgcn_readlane(mk[4], k);
           }
         }
-        if (ol && !(sg && cf)) {  // the chunk's last piece opens a segment
-#pragma unroll
-          for (int cb = 0; cb < CB; ++cb) {
-            const int col = cb * kWave + lane;
-            open[cb] = col < a.d ? Lp[k][col] : 0.f;
-          }
-          open_key = meta[k][4];
-        }
+        open[cb] = o;
+        if (cb == 0) open_key_next = okey;
       }
+      open_key = open_key_next;
     }
     __syncthreads();  // the slots are reused by the next round
   }
