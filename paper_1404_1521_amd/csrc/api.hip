@@ -104,7 +104,9 @@ SortPlan make_plan(int key_range, int N) {
       sh += pl.bits[p];
     }
   }
-  pl.ntiles = ceil_div(N, kSortTileKeys);
+  // short lists: smaller tiles, so a pass has more, shorter workgroups
+  pl.tile_keys = N <= kShortTileLimit ? kSortTileKeysShort : kSortTileKeys;
+  pl.ntiles = ceil_div(N, pl.tile_keys);
   return pl;
 }
 
@@ -497,7 +499,8 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   ctx->Hp = 16 * ctx->NT;
   ctx->cpw = ceil_div(ctx->K / 16, kWavesPerBlock);
   ctx->max_entries = std::max({c.max_batch * (c.win + 1), c.max_scatter, 1});
-  ctx->max_tiles = ceil_div(ctx->max_entries, kSortTileKeys);
+  ctx->max_tiles = std::max(ceil_div(std::min(ctx->max_entries, kShortTileLimit), kSortTileKeysShort),
+                            ceil_div(ctx->max_entries, kSortTileKeys));
   ctx->max_parts = std::min(ceil_div(c.max_batch, kTileRows), 512);
   // most chunks any call can cut (short chunks apply up to 131072 entries)
   ctx->max_chunks = std::max(ceil_div(std::min(ctx->max_entries, 131072), 16),

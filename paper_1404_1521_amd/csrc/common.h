@@ -21,7 +21,9 @@ constexpr int kMaxD = 256;
 constexpr int kMaxLdsBytes = 160 * 1024;  // LDS per workgroup on gfx950
 
 // Radix sort of (row id, entry) pairs.
-constexpr int kSortTileKeys = 4096;                // multi-tile sort: keys per tile
+constexpr int kSortTileKeys = 4096;                // multi-tile sort: keys per tile (long lists)
+constexpr int kSortTileKeysShort = 1024;           // ... and for lists up to kShortTileLimit
+constexpr int kShortTileLimit = 131072;
 constexpr int kMaxDigitBits = 9;
 constexpr int kMaxBins = 1 << kMaxDigitBits;
 constexpr int kMaxPasses = 4;                      // 31-bit keys at most
@@ -37,7 +39,8 @@ struct SortPlan {
   int passes;               // 0 when N <= 1 (nothing to order)
   int shift[kMaxPasses];
   int bits[kMaxPasses];
-  int ntiles;               // multi-tile path: tiles of kSortTileKeys keys
+  int ntiles;               // multi-tile path: tiles of tile_keys keys
+  int tile_keys;            // kSortTileKeysShort or kSortTileKeys
   int small;                // 1: partitioned sort (one launch, 2^part_bits workgroups)
   int val_bits;             // small path packs (key >> part_bits) << val_bits | entry
   int part_bits;            // small path: partitions by the low key bits

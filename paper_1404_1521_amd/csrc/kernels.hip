@@ -98,11 +98,11 @@ __global__ __launch_bounds__(kBlock) void k_os_hist(KeyFn kf, int N, SortPlan pl
 }
 
 // One radix pass over the tiles of a large list.
-template <class KeyFn>
+template <int R, class KeyFn>
 __global__ __launch_bounds__(kOsThreads) void k_os_pass(KeyFn kf, int N, SortPlan plan,
                                                         SortBufs sb, int p) {
   extern __shared__ uint32_t lds[];
-  os_pass(kf, N, plan, sb, p, lds);
+  os_pass<R>(kf, N, plan, sb, p, lds);
 }
 
 template <class KeyFn>
@@ -110,9 +110,14 @@ static hipError_t launch_tiled_sort(const KeyFn& kf, int N, const SortPlan& plan
                                     const SortBufs& sb, uint32_t* long_count, const Launch& L) {
   hipError_t e = pg_launch(k_os_hist<KeyFn>, dim3(ceil_div(N, kBlock * kOsHistIpt)), dim3(kBlock),
                            kOsHistLdsWords * 4, L, kf, N, plan, sb, long_count);
-  for (int p = 0; p < plan.passes && e == hipSuccess; ++p)
-    e = pg_launch(k_os_pass<KeyFn>, dim3(plan.ntiles), dim3(kOsThreads), kOsPassLdsWords * 4, L,
-                  kf, N, plan, sb, p);
+  for (int p = 0; p < plan.passes && e == hipSuccess; ++p) {
+    if (plan.tile_keys == kSortTileKeysShort)
+      e = pg_launch(k_os_pass<kSortTileKeysShort / kOsThreads, KeyFn>, dim3(plan.ntiles),
+                    dim3(kOsThreads), kOsPassLdsWords * 4, L, kf, N, plan, sb, p);
+    else
+      e = pg_launch(k_os_pass<kSortTileKeys / kOsThreads, KeyFn>, dim3(plan.ntiles),
+                    dim3(kOsThreads), kOsPassLdsWords * 4, L, kf, N, plan, sb, p);
+  }
   return e;
 }
 

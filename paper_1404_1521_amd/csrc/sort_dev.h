@@ -392,17 +392,17 @@ __device__ void os_hist(const KeyFn& kf, int N, const SortPlan& plan, const Sort
   }
 }
 
-// One radix pass: a workgroup of kOsThreads threads per 4096-key tile.
+// One radix pass: a workgroup of kOsThreads threads per tile of R * 1024 keys.
 constexpr int kOsThreads = 1024;
 constexpr int kOsWaves = kOsThreads / kWave;
 // LDS of a pass: counters [kMaxBins][waves + 1], digit bases, scan scratch,
 // the tile id.
 constexpr int kOsPassLdsWords = kMaxBins * (kOsWaves + 1) + kMaxBins + 2 * kOsWaves + 1;
 
-template <class KeyFn>
+template <int R, class KeyFn>
 __device__ void os_pass(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb, int p,
                         uint32_t* lds) {
-  constexpr int NW = kOsWaves, CS = NW + 1, R = kSortTileKeys / kOsThreads;
+  constexpr int NW = kOsWaves, CS = NW + 1, TK = R * kOsThreads;
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   uint32_t* hist = lds;                      // [kMaxBins][CS]: counts, then wave offsets
@@ -430,7 +430,7 @@ __device__ void os_pass(const KeyFn& kf, int N, const SortPlan& plan, const Sort
   uint32_t key[R], dg[R], loc[R];
   int32_t val[R];
   uint64_t act[R];
-  const int wbase = tile * kSortTileKeys + w * (R * kWave);
+  const int wbase = tile * TK + w * (R * kWave);
   if (p == 0) {
     load_keys<R>(kf, N, wbase + lane, kWave, key, sb.flag);
 #pragma unroll
