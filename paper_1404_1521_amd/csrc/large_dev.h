@@ -342,42 +342,87 @@ __global__ __launch_bounds__(kBlock) void k_large_dw1(LargeArgs a) {
         P[(size_t)(h0 + 16 * rt + 4 * g + r) * a.K + k0 + 16 * (w * CT + ct) + i] = acc[rt][ct][r];
 }
 
-// G rows of 64 windows at entry position j = blockIdx.y; wave w owns
-// windows b0 + 16w .. +15 and all DQ column blocks of the row.
+// G rows of 64 windows at entry position j = blockIdx.y:
+// G[b(win+1)+j][:] = W1_jj^T v_b (jj = c for the corrupt entry).  The
+// contraction over hidden units goes in 16-unit steps through LDS,
+// row-major: Vs[w][h] (the window's vector for this position) and
+// Ws[h][col] (W1 rows hc.. of column block jj).  MFMA q of a step contracts
+// units {q, 4+q, 8+q, 12+q}: lane (i, g) supplies Vs[16w'+i][4g+q] (one
+// 128-bit read for all four) and Ws[4g+q][16ct+i]; Ws rows are 4 mod 8
+// floats long, so a half-wave's two rows sit on disjoint banks.  Wave w'
+// owns windows 16w'.. and all DQ column blocks; the rows of step s+2 are in
+// flight in registers while steps s and s+1 are contracted.
 template <int DQ>
 __global__ __launch_bounds__(kBlock) void k_large_g(LargeArgs a) {
+  constexpr int D = 16 * DQ, WS = D + 4, VS = 16 + 4;
+  constexpr int WF = 16 * D / 4;                     // float4 of a step's W1 rows
+  constexpr int WPT = (WF + kBlock - 1) / kBlock;    // ... per thread
+  __shared__ __align__(16) float Vs[2][kLgGRows][VS];
+  __shared__ __align__(16) float Ws[2][16][WS];
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const int i = lane & 15, g = lane >> 4;
-  const int j = blockIdx.y, b0 = blockIdx.x * kLgGRows + 16 * w;
+  const int j = blockIdx.y, b0 = blockIdx.x * kLgGRows;
   const int ty = (j == a.win) ? 2 : (j == a.c ? 1 : 0);
   const int jj = (j == a.win) ? a.c : j;
-  const int bA = b0 + i;  // A operand window of this lane
-  const float* vr = a.V + (size_t)bA * 3 * a.H + (size_t)ty * a.H + 4 * g;
-  const float* wc = a.W1 + (size_t)jj * a.d + i;
+  const int nsteps = a.H / 16;
+  // this thread's share of a step: one float4 of vectors (window t/4, units
+  // 4*(t%4)), WPT float4 of W1 rows (row x / (D/4), float4 column x % (D/4))
+  const int vw = t / 4, vh = 4 * (t % 4);
+  const bool vok = b0 + vw < a.B;
+  const float* vsrc = a.V + (size_t)(vok ? b0 + vw : 0) * 3 * a.H + (size_t)ty * a.H + vh;
+  auto load = [&](int st, f4& Vv, f4 (&Wv)[WPT]) {
+    const int hc = st * 16;
+    Vv = vok ? ld4(vsrc + hc) : kZero4;
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int x = t + u * kBlock;
+      if (x < WF) {
+        const int r = x / (D / 4), c4 = x % (D / 4);
+        Wv[u] = ld4(a.W1 + (size_t)(hc + r) * a.K + (size_t)jj * D + 4 * c4);
+      }
+    }
+  };
+  auto store = [&](int buf, const f4& Vv, const f4 (&Wv)[WPT]) {
+    st4(&Vs[buf][vw][vh], Vv);
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int x = t + u * kBlock;
+      if (x < WF) st4(&Ws[buf][x / (D / 4)][4 * (x % (D / 4))], Wv[u]);
+    }
+  };
   f4 acc[DQ];
 #pragma unroll
-  for (int cb = 0; cb < DQ; ++cb) acc[cb] = kZero4;
-  for (int hc = 0; hc < a.H; hc += 16) {
-    const f4 av = bA < a.B ? ld4(vr + hc) : kZero4;
-    float bv[DQ][4];
+  for (int ct = 0; ct < DQ; ++ct) acc[ct] = kZero4;
+  auto compute = [&](int buf) {
+    const f4 av = ld4(&Vs[buf][16 * w + i][4 * g]);
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int cb = 0; cb < DQ; ++cb) bv[cb][q] = wc[(size_t)(hc + 4 * g + q) * a.K + 16 * cb];
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int cb = 0; cb < DQ; ++cb) acc[cb] = lg_mfma(av[q], bv[cb][q], acc[cb]);
+      for (int ct = 0; ct < DQ; ++ct) acc[ct] = lg_mfma(av[q], Ws[buf][4 * g + q][16 * ct + i], acc[ct]);
+  };
+  f4 VA, WA[WPT], VB, WB[WPT];
+  load(0, VA, WA);
+  if (nsteps > 1) load(1, VB, WB);
+  for (int st = 0; st < nsteps; st += 2) {
+    store(0, VA, WA);
+    if (st + 2 < nsteps) load(st + 2, VA, WA);
+    __syncthreads();
+    compute(0);
+    if (st + 1 >= nsteps) break;
+    store(1, VB, WB);
+    if (st + 3 < nsteps) load(st + 3, VB, WB);
+    __syncthreads();
+    compute(1);
   }
-  // lane (i, g), component q: window b0 + 4g + q, column 16cb + i
+  // lane (i, g), component q: window b0 + 16w + 4g + q, column 16ct + i
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int b = b0 + 4 * g + q;
+    const int b = b0 + 16 * w + 4 * g + q;
     if (b < a.B) {
       float* gr = a.G + ((size_t)b * (a.win + 1) + j) * a.d + i;
 #pragma unroll
-      for (int cb = 0; cb < DQ; ++cb) gr[16 * cb] = acc[cb][q];
+      for (int ct = 0; ct < DQ; ++ct) gr[16 * ct] = acc[ct][q];
     }
   }
 }
