@@ -66,35 +66,66 @@ __global__ __launch_bounds__(HW * kWave) void k_large_fwd(LargeArgs a, int score
     for (int cb = 0; cb < 4; ++cb) Z[rb][cb] = D[rb][cb] = kZero4;
   const int cpb = d / 16;  // 16-column chunks per embedding row
   const int nch = K / 16;
-  const float* wrow[4];
+  // Chunk kc (16 columns of x) goes through LDS, row-major with 16-byte
+  // rows padded to 20 floats: Xs (the 32 windows' rows), Ts (the corrupt
+  // rows, centre block only) and Ws (W1 rows of all H units).  Lane (i, g)
+  // reads Xs[16rb+i][4g] and Ws[64w+16cb+i][4g] as float4: its operands of
+  // the four MFMAs (q) of the chunk.  The 256 float4 of Xs and Ts (item x:
+  // Xs for x < 128, else Ts; row (x&127)/4, column 4(x&3)) and the 64*HW*4
+  // float4 of Ws are spread over the workgroup's threads.
+  constexpr int NT = HW * kWave, XP = 20;
+  constexpr int XPT = (256 + NT - 1) / NT;  // float4 of Xs / Ts per thread
+  constexpr int WPT = (64 * HW * 4) / NT;   // float4 of W1 rows per thread (= 4)
+  __shared__ __align__(16) float Xs[2][kLgRows][XP];
+  __shared__ __align__(16) float Ts[2][kLgRows][XP];
+  __shared__ __align__(16) float Ws[2][64 * HW][XP];
+  auto load = [&](int kc, f4 (&Xv)[XPT], f4 (&Wv)[WPT]) {
+    const int jb = kc / cpb, off = (kc - jb * cpb) * 16;
+    const bool ctr = jb == a.c && !score_only;
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb) wrow[cb] = a.W1 + (size_t)(64 * w + 16 * cb + i) * K + 4 * g;
-  // operands of chunk kc: A = X rows (lane: row 16rb + i, k = 16kc + 4g..+3),
-  // B = W1 rows (lane: hidden 64w + 16cb + i)
-  auto load = [&](int kc, f4 (&A)[2], f4 (&Bv)[4], f4 (&At)[2]) {
-    const int j = kc / cpb, off = (kc - j * cpb) * 16 + 4 * g;
+    for (int u = 0; u < XPT; ++u) {
+      const int x = t + u * NT;
+      const int xr = (x & 127) / 4, xc = 4 * (x & 3);
+      if (x < 128) Xv[u] = ld4(a.E + (size_t)ids[xr][jb] * d + off + xc);
+      else if (x < 256 && ctr) Xv[u] = ld4(a.E + (size_t)ids[xr][a.win] * d + off + xc);
+    }
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) A[rb] = ld4(a.E + (size_t)ids[16 * rb + i][j] * d + off);
-#pragma unroll
-    for (int cb = 0; cb < 4; ++cb) Bv[cb] = ld4(wrow[cb] + 16 * kc);
-    if (j == a.c && !score_only) {
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) At[rb] = ld4(a.E + (size_t)ids[16 * rb + i][a.win] * d + off);
+    for (int u = 0; u < WPT; ++u) {
+      const int x = t + u * NT;
+      Wv[u] = ld4(a.W1 + (size_t)(x / 4) * K + 16 * kc + 4 * (x & 3));
     }
   };
-  f4 A[2], Bv[4], At[2];
-  load(0, A, Bv, At);
-  for (int kc = 0; kc < nch; ++kc) {
-    f4 An[2], Bn[4], Atn[2];
-    if (kc + 1 < nch) load(kc + 1, An, Bn, Atn);  // next chunk in flight
+  auto store = [&](int buf, int kc, const f4 (&Xv)[XPT], const f4 (&Wv)[WPT]) {
     const bool ctr = kc / cpb == a.c && !score_only;
+#pragma unroll
+    for (int u = 0; u < XPT; ++u) {
+      const int x = t + u * NT;
+      const int xr = (x & 127) / 4, xc = 4 * (x & 3);
+      if (x < 128) st4(&Xs[buf][xr][xc], Xv[u]);
+      else if (x < 256 && ctr) st4(&Ts[buf][xr][xc], Xv[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int x = t + u * NT;
+      st4(&Ws[buf][x / 4][4 * (x & 3)], Wv[u]);
+    }
+  };
+  auto compute = [&](int buf, int kc) {
+    f4 A[2], Bv[4];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) A[rb] = ld4(&Xs[buf][16 * rb + i][4 * g]);
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) Bv[cb] = ld4(&Ws[buf][64 * w + 16 * cb + i][4 * g]);
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
       for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
         for (int cb = 0; cb < 4; ++cb) Z[rb][cb] = lg_mfma(A[rb][q], Bv[cb][q], Z[rb][cb]);
-    if (ctr) {
+    if (kc / cpb == a.c && !score_only) {  // D = (e~ - e_c) W1_c^T
+      f4 At[2];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) At[rb] = ld4(&Ts[buf][16 * rb + i][4 * g]);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -104,15 +135,25 @@ __global__ __launch_bounds__(HW * kWave) void k_large_fwd(LargeArgs a, int score
           for (int cb = 0; cb < 4; ++cb) D[rb][cb] = lg_mfma(dx, Bv[cb][q], D[rb][cb]);
         }
     }
-    if (kc + 1 < nch) {
+  };
+  // two register sets: chunk kc+2 is loaded while chunks kc and kc+1 are
+  // contracted; one barrier per chunk (the buffer written at chunk kc was
+  // last read at chunk kc-2, before chunk kc-1's barrier)
+  f4 XA[XPT], WA[WPT], XB[XPT], WB[WPT];
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        A[rb] = An[rb];
-        At[rb] = Atn[rb];
-      }
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb) Bv[cb] = Bn[cb];
-    }
+  for (int u = 0; u < XPT; ++u) XA[u] = XB[u] = kZero4;
+  load(0, XA, WA);
+  if (nch > 1) load(1, XB, WB);
+  for (int kc = 0; kc < nch; kc += 2) {
+    store(0, kc, XA, WA);
+    if (kc + 2 < nch) load(kc + 2, XA, WA);
+    __syncthreads();
+    compute(0, kc);
+    if (kc + 1 >= nch) break;
+    store(1, kc + 1, XB, WB);
+    if (kc + 3 < nch) load(kc + 3, XB, WB);
+    __syncthreads();
+    compute(1, kc + 1);
   }
 
   // ---- epilogue.  Lane (i, g), component q of Z[rb][cb]: row 16rb + 4g + q,
