@@ -189,6 +189,48 @@ def test_scatter_add_long_chunks_piece_structure(pattern, d):
     assert np.array_equal(got[untouched], t0[untouched])
 
 
+@pytest.mark.parametrize("keys_kind,d", [("one_key", 16), ("one_key", 80), ("three_keys", 64),
+                                          ("zipf_small_table", 80)])
+def test_scatter_add_partition_rounds(keys_kind, d):
+    """Lists of at most 8192 entries take the partitioned sort and the
+    partition-wise update (one workgroup per partition, 1024 entries per
+    round): these put several rounds into one partition, so segments carry
+    over from round to round, and rows of 80 floats add a partial column
+    block."""
+    rng = np.random.default_rng(11)
+    N = 8192
+    if keys_kind == "one_key":
+        rows, idx = 5, np.full(N, 3, np.int32)
+    elif keys_kind == "three_keys":  # 0, 128, 256 share partition 0 of 7 key bits
+        rows = 300
+        idx = rng.choice(np.array([0, 128, 256], np.int32), N, p=[0.6, 0.3, 0.1]).astype(np.int32)
+    else:
+        rows = 40
+        idx = workloads.zipf_ids(rng, rows, 1.5, N)
+    t0 = rng.normal(0, 0.01, (rows, d)).astype(np.float32)
+    Y = rng.normal(0, 1e-3, (N, d)).astype(np.float32)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    td = dev(t0)
+    ctx.scatter_add(td, dev(idx), dev(Y), 0.5, pg().SCATTER_SORTED)
+    assert ctx.status() == pg().OK
+    got = host(td)
+    ref = t0.copy()
+    oracle.scatter_add(ref, idx, Y, 0.5)
+    err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    assert np.all(err <= scatter_bound(t0, idx, Y, 0.5))
+    untouched = np.setdiff1d(np.arange(rows), idx)
+    assert np.array_equal(got[untouched], t0[untouched])
+
+
+def test_small_vocabulary_step_partition_rounds():
+    """A 64-word vocabulary at B = 1365 (8190 entries, the largest list the
+    partitioned sort takes): each partition holds one word, the most frequent
+    with about 1800 entries, so the partition-wise update runs two rounds."""
+    w = workloads.Workload("v64_b1365", V=64, d=16, win=5, H=8, B=1365, lr=0.05, steps=3,
+                           zipf_s=1.0, seed=31)
+    run_both(w, w.steps, w.B, 0)
+
+
 @pytest.mark.parametrize("mode", [0, 1])
 def test_scatter_add_full_size_zipf12(mode):
     """327,680 Zipf(1.2) rows into a 100000 x 64 table, the standalone
