@@ -481,10 +481,19 @@ def test_sorted_mode_is_deterministic():
         assert np.array_equal(outs[0][k], outs[1][k]), k
 
 
-def test_train_steps_graph_equals_single_steps():
+GRAPH_CASES = [
+    (PRESETS["sweep_1024"], 1024, 6),   # sort fused into the step kernel, partition-wise update
+    (PRESETS["sweep_1024"], 4096, 4),   # one-sweep sort on the side stream, fix-up launch
+    (LARGE_SHAPES[0], 100, 4),          # wide layers: partitioned sort on the side stream
+    (LARGE_SHAPES[1], 1030, 3),         # wide layers, two dW1 slices
+]
+
+
+@pytest.mark.parametrize("w,B,S", GRAPH_CASES, ids=[f"{c[0].name}_B{c[1]}" for c in GRAPH_CASES])
+def test_train_steps_graph_equals_single_steps(w, B, S):
+    """S steps recorded into one HIP graph (and replayed) leave bit-identical
+    parameters and losses to S single-step calls."""
     m = pg()
-    w = PRESETS["sweep_1024"]
-    S, B = 6, 1024
     batches = [workloads.batch(w, s, B) for s in range(S)]
     wall = dev(np.stack([b[0] for b in batches]))
     call = dev(np.stack([b[1] for b in batches]))
