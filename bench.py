@@ -149,16 +149,28 @@ def roofline(nbytes, nflops, engine, ms):
 # ---------------------------------------------------------------------------
 # HBM traffic from the committed rocprofv3 counter summaries.
 
-def source_digest():
-    """sha256 over the HIP sources (file names and contents, sorted by name)."""
+def code_text(text):
+    """C++ source without comments and without whitespace runs: the part of a
+    file that the compiler sees (string literals here contain no comment
+    markers)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
+def source_digest(src=None):
+    """sha256 over the HIP sources' code (file names and comment-free text,
+    sorted by name): a comment edit keeps the counters valid, a code edit
+    does not."""
     import hashlib
     h = hashlib.sha256()
-    src = os.path.join(ROOT, "paper_1404_1521_amd", "csrc")
+    src = src or os.path.join(ROOT, "paper_1404_1521_amd", "csrc")
     for name in sorted(os.listdir(src)):
         if name.endswith((".hip", ".h")):
             h.update(name.encode())
-            with open(os.path.join(src, name), "rb") as f:
-                h.update(f.read())
+            with open(os.path.join(src, name), encoding="utf-8") as f:
+                h.update(code_text(f.read()).encode())
     return h.hexdigest()
 
 

@@ -252,9 +252,9 @@ hipError_t enqueue_sort(polyglot_ctx* ctx, const int32_t* windows, const int32_t
   return launch_sort_step(kf, N, make_plan(cf.V, N), sort_bufs(ctx, set), nullptr, tm.L);
 }
 
-// The fused kernel, then (after `sorted_ev`, if any) the table update and
-// the long-segment fix-up of one step, on the main stream; sorted mode reads
-// sort set `set`.
+// The forward/backward launch(es), then (after `sorted_ev`, if any) the
+// table update and, for a list sorted as a whole, the long-segment fix-up of
+// one step, on the main stream; sorted mode reads sort set `set`.
 int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
                     const int32_t* windows, const int32_t* corrupt, int B, float lr,
                     float* loss_dev, int set, hipEvent_t sorted_ev) {

@@ -6,17 +6,21 @@
 //
 // The sorted entry list is cut into chunks of CH entries (16 or 64), one per
 // wave.  A wave loads the Y rows of its whole chunk at once (lane = column)
-// and walks them with a running sum that closes at each piece end (a "piece" is a maximal run of
-// equal keys inside the chunk).  Pieces whose segment lies wholly inside the
-// chunk are added to their table rows by that wave, the rows' only writer,
-// with one float add per element performed at the L2 (no read round trip;
-// one add per element, so the result does not depend on scheduling).  Few
-// registers per wave keep every wave of a large launch resident at once.
+// and walks them with a running sum that closes at each piece end (a
+// "piece" is a maximal run of equal keys inside the chunk).  Pieces whose
+// segment lies wholly inside the chunk are added to their table rows by that
+// wave, the rows' only writer, with one float add per element performed at
+// the L2 (no read round trip; one add per element, so the result does not
+// depend on scheduling).  Few registers per wave keep every wave of a large
+// launch resident at once.
 // A segment that crosses chunk boundaries (a heavy Zipf row) leaves one
 // partial per spanned chunk (slot 1: the open last piece of the chunk where
-// it starts; slot 0: the first piece of every later spanned chunk).  Its
-// start chunk goes to a task list and its end chunk is recorded by key; the
-// fix-up launch adds the partials in a fixed order and applies the row.
+// it starts; slot 0: the first piece of every later spanned chunk).  On the
+// whole list, its start chunk goes to a task list and its end chunk is
+// recorded by key; the fix-up launch adds the partials in a fixed order and
+// applies the row.  After a partitioned sort, where no key spans two
+// partitions, one workgroup per partition keeps the partials in LDS and
+// completes every segment itself (seg_apply_partition).
 // Sums never depend on scheduling, no row is written twice and no wave
 // waits on another workgroup.
 #pragma once

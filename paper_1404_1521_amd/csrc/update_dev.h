@@ -1,7 +1,8 @@
 // Table update of the embedding gradients (the advanced-indexing increment
 // of §4.2/§4.3) and the dense SGD of one training step, in one launch with
-// roles; the standalone scatter-add uses the same launch without the dense
-// role.
+// roles: k_apply (chunks of the whole sorted list, or the atomic variant)
+// and k_apply_part (one workgroup per partition of a partitioned sort).  The
+// standalone scatter-add uses the same launches without the dense role.
 #pragma once
 #include "common.h"
 #include "launch.h"
