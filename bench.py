@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="sweep_1024")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="windows per step instead of the workload's own (same model and inputs)")
     ap.add_argument("--mode", choices=("sorted", "atomic"), default="sorted")
     ap.add_argument("--eager", action="store_true",
                     help="one library call per step instead of one captured graph of all steps")
@@ -347,6 +349,8 @@ def main():
         return
 
     w = workloads.PRESETS[args.workload]
+    if args.batch:
+        w = w.with_batch(args.batch)
     B, K, Wm = w.B, args.steps, args.warmup
     N = B * (w.win + 1)
     mode = pg.SCATTER_SORTED if args.mode == "sorted" else pg.SCATTER_ATOMIC
@@ -431,7 +435,9 @@ def main():
     nbytes, nflops, engine = model[dom]
     nbytes, nflops = nbytes / per[dom][1], nflops / per[dom][1]
     roof = roofline(nbytes, nflops, engine, dms)
-    roof["traffic"] = counter_traffic(args.workload, dom) if args.mode == "sorted" else None
+    # the committed counters are per workload at its own batch size
+    own = not args.batch or args.batch == workloads.PRESETS[args.workload].B
+    roof["traffic"] = counter_traffic(args.workload, dom) if args.mode == "sorted" and own else None
     roof["traffic_unit"] = "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["kernel"] = dom
     roof["launches_per_step"] = round(per[dom][1], 3)

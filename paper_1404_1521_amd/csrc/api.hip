@@ -238,8 +238,8 @@ int table_workgroups(const SegArgs& s, int mode) {
   return std::max(1, std::min(units, mode == 0 ? 2048 : 8192));
 }
 
-int segfix_workgroups(const SegArgs& s) {
-  return std::max(1, std::min(ceil_div(s.N, s.ch), 2048));
+int segfix_workgroups(const SegArgs& s) {  // kSegfixWaves tasks per workgroup and round
+  return std::max(1, std::min(ceil_div(ceil_div(s.N, s.ch), kSegfixWaves), 2048));
 }
 
 // The sort of one step's entries into sort set `set`, on the side stream.

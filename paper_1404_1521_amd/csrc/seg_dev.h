@@ -272,25 +272,55 @@ __device__ void seg_apply_partition(const SegArgs& a, int s, int e,
   }
 }
 
-// Threads of the fix-up workgroup: one workgroup per crossing segment.
+// Fix-up workgroups: each takes kSegfixWaves crossing segments at a time,
+// one per wave; a segment with more than kSegfixLight partials (a heavy Zipf
+// row) is summed by the whole workgroup instead.
 constexpr int kSegfixThreads = 512;
 constexpr int kSegfixWaves = kSegfixThreads / kWave;
 constexpr int kSegfixUnroll = 16;
+constexpr int kSegfixLight = 16;
 
-// Adds the partials of crossing segment li and applies its row.  Lane group
-// gq = lane/16 of wave w takes partials i = G*u + 4*w + gq, G = 4 * waves (i = 0 is
-// the open piece of the start chunk, i >= 1 the first piece of chunk cs+i),
-// each lane four consecutive columns; group sums are combined by a fixed
-// butterfly and the wave sums in wave order, so the result is independent
-// of scheduling.
-__device__ void seg_fix_row(const SegArgs& a, int li, float* red /* [waves][kMaxD] */) {
+// One wave adds the m <= kSegfixLight partials of a crossing segment
+// starting at chunk cs and applies row `key`: lane group gq = lane/16 sums
+// partials gq, gq+4, ... in order (each lane four consecutive columns), the
+// four group sums are combined by a fixed butterfly.
+__device__ void seg_fix_row_wave(const SegArgs& a, int cs, int32_t key, int m) {
+  const int lane = lane_id(), q = lane & 15, gq = lane >> 4;
+  for (int c0 = 0; c0 < a.d; c0 += 64) {
+    const int col = c0 + 4 * q;
+    const bool cok = col < a.d;
+    float* tr = a.table + (size_t)key * a.d + col;
+    const f4 row = (gq == 0 && cok) ? ld4(tr) : kZero4;  // in flight beside the partials
+    f4 x[kSegfixLight / 4];
+#pragma unroll
+    for (int u = 0; u < kSegfixLight / 4; ++u) {
+      const int i = 4 * u + gq;
+      const size_t slot = i == 0 ? (size_t)cs * 2 + 1 : (size_t)(cs + i) * 2;
+      x[u] = (i < m && cok) ? ld4(a.seg_part + slot * a.seg_stride + col) : kZero4;
+    }
+    f4 acc = kZero4;
+#pragma unroll
+    for (int u = 0; u < kSegfixLight / 4; ++u) acc += x[u];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      acc[k] += __shfl_xor(acc[k], 16);
+      acc[k] += __shfl_xor(acc[k], 32);
+    }
+    if (gq == 0 && cok) st4(tr, row + a.alpha * acc);
+  }
+}
+
+// The whole workgroup adds the m partials of crossing segment (cs, key) and
+// applies its row.  Lane group gq = lane/16 of wave w takes partials
+// i = G*u + 4*w + gq, G = 4 * waves (i = 0 is the open piece of the start
+// chunk, i >= 1 the first piece of chunk cs+i), each lane four consecutive
+// columns; group sums are combined by a fixed butterfly and the wave sums in
+// wave order, so the result is independent of scheduling.
+__device__ void seg_fix_row(const SegArgs& a, int cs, int32_t key, int m,
+                            float* red /* [waves][kMaxD] */) {
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const int q = lane & 15, gq = lane >> 4;
-  const int2 rec = a.long_list[li];
-  const int cs = rec.x;
-  const int32_t key = rec.y;
-  const int m = a.seg_end[key] - cs + 1;  // partials of this segment
   constexpr int G = kSegfixWaves * 4;     // lane groups per workgroup
   for (int c0 = 0; c0 < a.d; c0 += 64) {
     const int col = c0 + 4 * q;
