@@ -220,7 +220,6 @@ SegArgs seg_args(polyglot_ctx* ctx, float* table, const float* Y, const SortPlan
   a.sv = ctx->ws.vals[2 * set + (plan.passes & 1)];
   a.seg_part = ctx->ws.seg_part;
   a.long_list = ctx->ws.long_list;
-  a.long_count = ctx->ws.long_count;
   a.seg_end = ctx->ws.seg_end;
   a.flag = ctx->ws.flag;
   a.N = N;
@@ -249,7 +248,7 @@ hipError_t enqueue_sort(polyglot_ctx* ctx, const int32_t* windows, const int32_t
   const int N = B * (cf.win + 1);
   const StepKeys kf = step_keys(windows, corrupt, cf.win, cf.V);
   Timed tm(ctx, POLYGLOT_K_SORT, ctx->side);
-  return launch_sort_step(kf, N, make_plan(cf.V, N), sort_bufs(ctx, set), nullptr, tm.L);
+  return launch_sort_step(kf, N, make_plan(cf.V, N), sort_bufs(ctx, set), tm.L);
 }
 
 // The forward/backward launch(es), then (after `sorted_ev`, if any) the
@@ -280,7 +279,6 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
     la.part = ctx->ws.part;
     la.G = ctx->ws.G;
     la.flag = ctx->ws.flag;
-    la.long_count = ctx->ws.long_count;
     la.V_rows = cf.V;
     la.d = cf.d;
     la.win = cf.win;
@@ -312,7 +310,6 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
     fa.corrupt = corrupt;
     fa.G = ctx->ws.G;
     fa.part = ctx->ws.part;
-    fa.long_count = ctx->ws.long_count;
     fa.flag = ctx->ws.flag;
     fa.V = cf.V;
     fa.d = cf.d;
@@ -539,7 +536,6 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_end, (size_t)std::max(c.V, c.max_rows));
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_part, (size_t)ctx->max_chunks * 2 * ctx->seg_stride);
   if (e == hipSuccess) e = alloc(ctx, &ws.long_list, (size_t)ctx->max_chunks);
-  if (e == hipSuccess) e = alloc(ctx, &ws.long_count, 1);
   if (e == hipSuccess) e = alloc(ctx, &ws.flag, 1);
   if (e == hipSuccess) e = alloc(ctx, &ws.scratch_loss, 1);
   for (int k = 0; k < 2; ++k) {
@@ -549,7 +545,6 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
     if (e == hipSuccess) e = hipMemset(ws.tile_ctr[k], 0, sizeof(uint32_t) * kMaxPasses);
     if (e == hipSuccess) e = hipMemset(ws.epoch[k], 0, sizeof(uint32_t));
   }
-  if (e == hipSuccess) e = hipMemset(ws.long_count, 0, sizeof(uint32_t));
   if (e == hipSuccess) e = hipMemset(ws.flag, 0, sizeof(uint32_t));
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);
   for (hipEvent_t* ev : {&ctx->ev_fork, &ctx->ev_sorted[0], &ctx->ev_sorted[1], &ctx->ev_done[0],
@@ -711,12 +706,12 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
   aa.n_d = 0;
   hipError_t e;
   if (aa.mode == 0) {
-    // the sort validates the indices (sticky flag) and clears the task list
+    // the sort validates the indices (sticky flag)
     aa.zero = sort_zero_ranges(ctx, plan, 0);
     const int n_z = plan.small ? 0 : 16;
     {
       Timed tm(ctx, POLYGLOT_K_SORT);
-      e = launch_sort_idx(kf, N, plan, sort_bufs(ctx, 0), ctx->ws.long_count, tm.L);
+      e = launch_sort_idx(kf, N, plan, sort_bufs(ctx, 0), tm.L);
     }
     if (e == hipSuccess && plan.small) {  // partition-wise: no fix-up launch
       aa.part_off = ctx->ws.part_off[0];

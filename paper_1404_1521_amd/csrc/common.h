@@ -67,8 +67,8 @@ struct Workspace {
   float* vbuf;              // three-contraction path: [max_batch][3][H] dz + dz~, dz, dz~
   // segmented update
   float* seg_part;          // [max_chunks][2][seg_stride] partial sums of long segments
-  int2* long_list;          // [max_chunks] (start chunk, row) of segments spanning chunks
-  uint32_t* long_count;     // number of entries in long_list
+  int2* long_list;          // [max_chunks] by chunk: (chunk, row) if a segment crossing
+                            // chunks starts there, else (-1, 0)
   int32_t* seg_end;         // [max(V, max_rows)] end chunk of a long segment, by row id
   uint32_t* flag;           // sticky error bits
   float* scratch_loss;      // loss slot used when the caller passes no loss pointer

@@ -147,7 +147,6 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   const float b1v = hn < a.H ? a.b1[hn] : 0.f;
   const float w2v = hn < a.H ? a.w2[hn] : 0.f;
   const float b2v = a.b2[0];
-  if (wg == 0 && t == 0) *a.long_count = 0u;  // read only by this step's later launches
 
   f4 accW[CPW];
 #pragma unroll
@@ -292,13 +291,14 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int row = row0 + 4 * g + i;
-          if (row < a.B) a.G[((size_t)row * W1P + j) * D + cb * 16 + n16] = acc[i];
+          if (row < a.B) __builtin_nontemporal_store(acc[i], &a.G[((size_t)row * W1P + j) * D + cb * 16 + n16]);
         }
       }
     }
   }
 
-  // ---- this workgroup's partial of the dense gradients.  Slot layout:
+  // ---- this workgroup's partial of the dense gradients (streaming stores,
+  // like the G rows above: the next kernel reads them once).  Slot layout:
   // dW1 [Hp][K], db1 [Hp], dw2 [Hp], loss, db2.
   float* P = a.part + (size_t)wg * a.part_stride;
 #pragma unroll
@@ -306,7 +306,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
     const int kc = kq + KW * ci;
     if (kc < NCH) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) P[(nt_w * 16 + 4 * g + i) * K + kc * 16 + n16] = accW[ci][i];
+      for (int i = 0; i < 4; ++i) __builtin_nontemporal_store(accW[ci][i], &P[(nt_w * 16 + 4 * g + i) * K + kc * 16 + n16]);
     }
   }
   // db1, dw2 (per hidden unit: the two row halves of the wave, then the

@@ -139,7 +139,6 @@ __device__ void fwdbwd_wg(const FwdArgs& a, int wg, float* lds) {
     w2v[nt] = n < a.H ? a.w2[n] : 0.f;
   }
   const float b2v = a.b2[0];
-  if (wg == 0 && t == 0) *a.long_count = 0u;  // read only by this step's later launches
   store_ids(0, idv);
   __syncthreads();                            // W1 and the first tile's ids staged
 

@@ -77,23 +77,19 @@ __global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {
 
 // =============================================================== sort
 
-// Partitioned sort of a small list, partition blockIdx.x (clears the segment
-// task list when given one).
+// Partitioned sort of a small list, partition blockIdx.x.
 template <class KeyFn>
 __global__ __launch_bounds__(kPartSortThreads) void k_sort_part(KeyFn kf, int N, SortPlan plan,
-                                                                SortBufs sb, uint32_t* long_count) {
+                                                                SortBufs sb) {
   extern __shared__ uint32_t lds[];
-  if (long_count && blockIdx.x == 0 && threadIdx.x == 0) *long_count = 0u;
   part_sort<kPartSortThreads>(kf, N, plan, blockIdx.x, sb.keys[plan.passes & 1],
                               sb.vals[plan.passes & 1], sb.part_off, sb.flag, lds);
 }
 
-// Digit totals of a large list (clears the segment task list when given one).
+// Digit totals of a large list.
 template <class KeyFn>
-__global__ __launch_bounds__(kBlock) void k_os_hist(KeyFn kf, int N, SortPlan plan, SortBufs sb,
-                                                    uint32_t* long_count) {
+__global__ __launch_bounds__(kBlock) void k_os_hist(KeyFn kf, int N, SortPlan plan, SortBufs sb) {
   extern __shared__ uint32_t lds[];
-  if (long_count && blockIdx.x == 0 && threadIdx.x == 0) *long_count = 0u;
   os_hist(kf, N, plan, sb, blockIdx.x, lds);
 }
 
@@ -107,9 +103,9 @@ __global__ __launch_bounds__(kOsThreads) void k_os_pass(KeyFn kf, int N, SortPla
 
 template <class KeyFn>
 static hipError_t launch_tiled_sort(const KeyFn& kf, int N, const SortPlan& plan,
-                                    const SortBufs& sb, uint32_t* long_count, const Launch& L) {
+                                    const SortBufs& sb, const Launch& L) {
   hipError_t e = pg_launch(k_os_hist<KeyFn>, dim3(ceil_div(N, kBlock * kOsHistIpt)), dim3(kBlock),
-                           kOsHistLdsWords * 4, L, kf, N, plan, sb, long_count);
+                           kOsHistLdsWords * 4, L, kf, N, plan, sb);
   for (int p = 0; p < plan.passes && e == hipSuccess; ++p) {
     if (plan.tile_keys == kSortTileKeysShort)
       e = pg_launch(k_os_pass<kSortTileKeysShort / kOsThreads, KeyFn>, dim3(plan.ntiles),
@@ -123,11 +119,11 @@ static hipError_t launch_tiled_sort(const KeyFn& kf, int N, const SortPlan& plan
 
 template <class KeyFn>
 static hipError_t launch_sort(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                              uint32_t* long_count, const Launch& L) {
+                              const Launch& L) {
   if (plan.small)
     return pg_launch(k_sort_part<KeyFn>, dim3(1 << plan.part_bits), dim3(kPartSortThreads),
-                     part_sort_lds_words(kPartSortThreads) * 4, L, kf, N, plan, sb, long_count);
-  return launch_tiled_sort(kf, N, plan, sb, long_count, L);
+                     part_sort_lds_words(kPartSortThreads) * 4, L, kf, N, plan, sb);
+  return launch_tiled_sort(kf, N, plan, sb, L);
 }
 
 // =============================================================== launchers
@@ -165,13 +161,13 @@ hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_
 }
 
 hipError_t launch_sort_step(const StepKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                            uint32_t* long_count, const Launch& L) {
-  return launch_sort(kf, N, plan, sb, long_count, L);
+                            const Launch& L) {
+  return launch_sort(kf, N, plan, sb, L);
 }
 
 hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                           uint32_t* long_count, const Launch& L) {
-  return launch_sort(kf, N, plan, sb, long_count, L);
+                           const Launch& L) {
+  return launch_sort(kf, N, plan, sb, L);
 }
 
 template <class KeyFn>

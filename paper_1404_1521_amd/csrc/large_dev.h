@@ -41,7 +41,6 @@ __global__ __launch_bounds__(HW * kWave) void k_large_fwd(LargeArgs a, int score
   const int i = lane & 15, g = lane >> 4;
   const int r0 = blockIdx.x * kLgRows;
   const int W1p = a.win + 1, d = a.d, K = a.K;
-  if (blockIdx.x == 0 && t == 0 && a.long_count) *a.long_count = 0u;
   if (t < kLgRows) badrow[t] = 0;
   __syncthreads();
   for (int k = t; k < kLgRows * W1p; k += HW * kWave) {

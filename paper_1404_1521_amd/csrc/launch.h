@@ -46,7 +46,6 @@ struct FwdArgs {
   const int32_t* corrupt;
   float* G;          // [B*(win+1)][d] per-entry embedding gradients
   float* part;       // [workgroups][part_stride] dense partials
-  uint32_t* long_count;  // segment task list of this step, cleared here
   uint32_t* flag;
   int V, d, win, H, Hp, K, c, B, N;
   // sort role: workgroups [0, n_sort) run the partitioned small sort
@@ -78,7 +77,6 @@ struct LargeArgs {
   float* G;          // [B*(win+1)][d]
   float* scores;     // score-only mode: s(x) [B]
   uint32_t* flag;
-  uint32_t* long_count;
   int V_rows, d, win, H, K, c, B;
   float invB;
 };
@@ -150,11 +148,11 @@ constexpr int kF8MaxWorkgroups = 256;         // one workgroup per CU
 hipError_t launch_step_fwdbwd8(const FwdArgs& a, int shape, int grid, size_t lds,
                                const Launch& L);
 // First sort launch (whole small sort, or pass-0 tile counts) and, for
-// multi-tile plans, every later pass; clears *long_count if not NULL.
+// multi-tile plans, every later pass.
 hipError_t launch_sort_step(const StepKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                            uint32_t* long_count, const Launch& L);
+                            const Launch& L);
 hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
-                           uint32_t* long_count, const Launch& L);
+                           const Launch& L);
 hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, const Launch& L);
 hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, const Launch& L);
 hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L);

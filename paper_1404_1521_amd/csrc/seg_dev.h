@@ -16,8 +16,8 @@
 // A segment that crosses chunk boundaries (a heavy Zipf row) leaves one
 // partial per spanned chunk (slot 1: the open last piece of the chunk where
 // it starts; slot 0: the first piece of every later spanned chunk).  On the
-// whole list, its start chunk goes to a task list and its end chunk is
-// recorded by key; the fix-up launch adds the partials in a fixed order and
+// whole list, the chunk where it starts records it in its own slot of the
+// segment list (no shared counter) and its end chunk is recorded by key; the fix-up launch adds the partials in a fixed order and
 // applies the row.  After a partitioned sort, where no key spans two
 // partitions, one workgroup per partition keeps the partials in LDS and
 // completes every segment itself (seg_apply_partition).
@@ -34,8 +34,8 @@ struct SegArgs {
   const int32_t* sk;        // sorted keys [N]
   const int32_t* sv;        // entry ids in sorted order [N]
   float* seg_part;          // [chunks][2][seg_stride]
-  int2* long_list;          // (start chunk, row) of segments that cross chunks
-  uint32_t* long_count;     // cleared by the sort launch of the same call
+  int2* long_list;          // [chunks] by chunk: (chunk, row) if a segment that crosses
+                            // chunks starts in it, else (-1, 0); every chunk writes its slot
   int32_t* seg_end;         // [rows]: end chunk of a crossing segment, by key
   const uint32_t* flag;     // sticky error bits: nonzero voids the update
   int N, d, ch, seg_stride;
@@ -89,7 +89,7 @@ __device__ __forceinline__ ChunkInfo chunk_info(const int32_t* __restrict__ sk,
 __host__ __device__ inline int seg_chunk_size(int N) { return N <= 131072 ? 16 : 64; }
 
 // Where a chunk's open pieces go: GLOBAL, the chunk-indexed partials and the
-// task list of the fix-up launch; LOCAL, a wave's slots in LDS (first piece,
+// chunk's slot of the fix-up launch's segment list; LOCAL, a wave's slots in LDS (first piece,
 // last piece, and the chunk's flags and keys) for the workgroup to combine.
 struct ChunkSink {
   float* first;  // LOCAL: [d] sum of the chunk's first piece when it continues a segment
@@ -127,7 +127,7 @@ __device__ void seg_apply_rows(const SegArgs& a, int i0, int end, int chunk, con
       sink.meta[3] = ci.key;  // lane 0 holds the first piece's key
       sink.meta[4] = ci.last_key;
     } else {
-      if (starts_long) a.long_list[atomicAdd(a.long_count, 1u)] = make_int2(chunk, ci.last_key);
+      a.long_list[chunk] = starts_long ? make_int2(chunk, ci.last_key) : make_int2(-1, 0);
       if (ends_long) a.seg_end[ci.key] = chunk;
     }
   }

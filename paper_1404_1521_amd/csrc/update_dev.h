@@ -124,36 +124,38 @@ __global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
   zero_ranges(a.zero, gid, nthreads);
 }
 
-// Rows whose sorted entries cross chunks.  A workgroup takes kSegfixWaves
-// tasks at a time: a light segment is finished by its wave, a heavy one is
-// listed and then summed by the whole workgroup.  Every row is a different
-// segment's, so the order in which heavy ones are taken does not matter.
+// Rows whose sorted entries cross chunks.  Task li is chunk li's slot of the
+// segment list (empty unless a crossing segment starts in that chunk).  A
+// workgroup takes kSegfixWaves slots at a time: a light segment is finished
+// by its wave, a heavy one is listed and then summed by the whole workgroup.
+// Every row is a different segment's, so the order in which heavy ones are
+// taken does not matter.
 __global__ __launch_bounds__(kSegfixThreads) void k_segfix(SegArgs a) {
   __shared__ float red[kSegfixWaves * kMaxD];
   __shared__ int heavy[kSegfixWaves][3];  // (start chunk, row, partials)
   __shared__ int nheavy;
-  // both read together; the task count is only used if the flag is clear
-  const uint32_t flag = *a.flag, cnt = *a.long_count;
-  if (flag) return;
+  if (*a.flag) return;
+  const uint32_t cnt = (uint32_t)((a.N + a.ch - 1) / a.ch);
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
-  // task li of a round goes to workgroup li % gridDim.x, so the tasks of
-  // neighbouring heavy rows (appended next to each other) land in different
-  // workgroups
+  // slot li of a round goes to workgroup li % gridDim.x, so the segments of
+  // heavy rows that start in nearby chunks land in different workgroups
   for (uint32_t base = 0; base + blockIdx.x < cnt; base += gridDim.x * kSegfixWaves) {
     if (t == 0) nheavy = 0;
     __syncthreads();
     const uint32_t li = base + (uint32_t)w * gridDim.x + blockIdx.x;
     if (li < cnt) {
       const int2 rec = a.long_list[li];
-      const int m = a.seg_end[rec.y] - rec.x + 1;  // partials of this segment
-      if (m <= kSegfixLight) {
-        seg_fix_row_wave(a, rec.x, rec.y, m);
-      } else if (lane == 0) {
-        const int h = atomicAdd(&nheavy, 1);
-        heavy[h][0] = rec.x;
-        heavy[h][1] = rec.y;
-        heavy[h][2] = m;
+      if (rec.x >= 0) {
+        const int m = a.seg_end[rec.y] - rec.x + 1;  // partials of this segment
+        if (m <= kSegfixLight) {
+          seg_fix_row_wave(a, rec.x, rec.y, m);
+        } else if (lane == 0) {
+          const int h = atomicAdd(&nheavy, 1);
+          heavy[h][0] = rec.x;
+          heavy[h][1] = rec.y;
+          heavy[h][2] = m;
+        }
       }
     }
     __syncthreads();
