@@ -119,7 +119,6 @@ SortBufs sort_bufs(polyglot_ctx* ctx, int set) {
   sb.totals = ctx->ws.totals[set];
   sb.status = ctx->ws.status[set];
   sb.tile_ctr = ctx->ws.tile_ctr[set];
-  sb.epoch = ctx->ws.epoch[set];
   sb.part_off = ctx->ws.part_off[set];
   sb.max_tiles = ctx->max_tiles;
   sb.flag = ctx->ws.flag;
@@ -127,7 +126,7 @@ SortBufs sort_bufs(polyglot_ctx* ctx, int set) {
 }
 
 // Counters a multi-tile sort accumulates atomically (the look-back words are
-// told apart by the sort epoch and need no clearing).
+// cleared by the sort's histogram launch).
 ZeroRanges sort_zero_ranges(polyglot_ctx* ctx, const SortPlan& plan, int set) {
   ZeroRanges z{};
   if (plan.small) return z;
@@ -520,7 +519,6 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
     if (e == hipSuccess) e = alloc(ctx, &ws.totals[k], (size_t)kMaxPasses * kMaxBins);
     if (e == hipSuccess) e = alloc(ctx, &ws.status[k], nstatus);
     if (e == hipSuccess) e = alloc(ctx, &ws.tile_ctr[k], (size_t)kMaxPasses);
-    if (e == hipSuccess) e = alloc(ctx, &ws.epoch[k], 1);
     if (e == hipSuccess) e = alloc(ctx, &ws.part_off[k], (size_t)(1 << kPartBits) + 1);
   }
   if (e == hipSuccess) e = alloc(ctx, &ws.G, (size_t)c.max_batch * (c.win + 1) * c.d);
@@ -541,9 +539,8 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   for (int k = 0; k < 2; ++k) {
     if (e == hipSuccess)
       e = hipMemset(ws.totals[k], 0, sizeof(uint32_t) * kMaxPasses * kMaxBins);
-    if (e == hipSuccess) e = hipMemset(ws.status[k], 0, sizeof(unsigned long long) * nstatus);
+    if (e == hipSuccess) e = hipMemset(ws.status[k], 0, sizeof(uint32_t) * nstatus);
     if (e == hipSuccess) e = hipMemset(ws.tile_ctr[k], 0, sizeof(uint32_t) * kMaxPasses);
-    if (e == hipSuccess) e = hipMemset(ws.epoch[k], 0, sizeof(uint32_t));
   }
   if (e == hipSuccess) e = hipMemset(ws.flag, 0, sizeof(uint32_t));
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);

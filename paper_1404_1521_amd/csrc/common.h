@@ -28,7 +28,7 @@ constexpr int kMaxDigitBits = 9;
 constexpr int kMaxBins = 1 << kMaxDigitBits;
 constexpr int kMaxPasses = 4;                      // 31-bit keys at most
 constexpr int kSmallSortN = 8192;                  // partitioned LDS sort up to this N
-constexpr int kSmallDigitBits = 10;                // digit width of the partitioned sort's passes
+constexpr int kSmallDigitBits = 7;                 // widest digit of the partitioned sort's passes
 constexpr int kSmallBins = 1 << kSmallDigitBits;
 
 // Sticky device error bits.
@@ -55,9 +55,8 @@ struct Workspace {
   int32_t* keys[4];         // sorted keys [max_entries]
   int32_t* vals[4];         // entry ids   [max_entries]
   uint32_t* totals[2];      // [kMaxPasses][kMaxBins] global digit counts
-  unsigned long long* status[2];  // [kMaxPasses][max_tiles][kMaxBins] look-back words
+  uint32_t* status[2];      // [kMaxPasses][max_tiles][kMaxBins] look-back words
   uint32_t* tile_ctr[2];    // [kMaxPasses] tile id counters
-  uint32_t* epoch[2];       // sort epoch of each set
   int32_t* part_off[2];     // [2^kPartBits + 1] partitioned sort: where each partition starts
   // step
   float* G;                 // [max_batch*(win+1)][d] per-entry embedding gradients

@@ -280,27 +280,35 @@ constexpr int kSegfixWaves = kSegfixThreads / kWave;
 constexpr int kSegfixUnroll = 16;
 constexpr int kSegfixLight = 16;
 
-// One wave adds the m <= kSegfixLight partials of a crossing segment
-// starting at chunk cs and applies row `key`: lane group gq = lane/16 sums
-// partials gq, gq+4, ... in order (each lane four consecutive columns), the
-// four group sums are combined by a fixed butterfly.
-__device__ void seg_fix_row_wave(const SegArgs& a, int cs, int32_t key, int m) {
+// One wave finishes crossing segment (cs, key) when it has at most
+// kSegfixLight partials, m = seg_end[key] - cs + 1, and returns m; a heavier
+// segment is left alone (the caller hands it to the whole workgroup).  The
+// kSegfixLight candidate partials (chunks below nchunks) and the row are read
+// together with seg_end, then masked by m, so the segment costs one round of
+// loads after its slot.  Lane group gq = lane/16 sums partials gq, gq+4, ...
+// in order (each lane four consecutive columns), and the four group sums are
+// combined by a fixed butterfly.
+__device__ int seg_fix_row_wave(const SegArgs& a, int cs, int32_t key, int nchunks) {
   const int lane = lane_id(), q = lane & 15, gq = lane >> 4;
+  const int ce = a.seg_end[key];
   for (int c0 = 0; c0 < a.d; c0 += 64) {
     const int col = c0 + 4 * q;
     const bool cok = col < a.d;
     float* tr = a.table + (size_t)key * a.d + col;
-    const f4 row = (gq == 0 && cok) ? ld4(tr) : kZero4;  // in flight beside the partials
+    const f4 row = (gq == 0 && cok) ? ld4(tr) : kZero4;
     f4 x[kSegfixLight / 4];
 #pragma unroll
     for (int u = 0; u < kSegfixLight / 4; ++u) {
       const int i = 4 * u + gq;
       const size_t slot = i == 0 ? (size_t)cs * 2 + 1 : (size_t)(cs + i) * 2;
-      x[u] = (i < m && cok) ? ld4(a.seg_part + slot * a.seg_stride + col) : kZero4;
+      x[u] = (cs + i < nchunks && cok) ? ld4(a.seg_part + slot * a.seg_stride + col) : kZero4;
     }
+    const int m = __builtin_amdgcn_readfirstlane(ce) - cs + 1;
+    if (m > kSegfixLight) return m;
     f4 acc = kZero4;
 #pragma unroll
-    for (int u = 0; u < kSegfixLight / 4; ++u) acc += x[u];
+    for (int u = 0; u < kSegfixLight / 4; ++u)
+      if (4 * u + gq < m) acc += x[u];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       acc[k] += __shfl_xor(acc[k], 16);
@@ -308,6 +316,7 @@ __device__ void seg_fix_row_wave(const SegArgs& a, int cs, int32_t key, int m) {
     }
     if (gq == 0 && cok) st4(tr, row + a.alpha * acc);
   }
+  return __builtin_amdgcn_readfirstlane(ce) - cs + 1;
 }
 
 // The whole workgroup adds the m partials of crossing segment (cs, key) and

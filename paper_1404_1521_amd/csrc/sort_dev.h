@@ -322,8 +322,8 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
 // 256 * IPT keys, one launch per pass plus one histogram launch.
 //   histogram   every workgroup counts the digits of all passes for a share
 //               of the keys (LDS) and adds them into the digit totals; it
-//               also resets the per-pass tile counters and advances the
-//               sort set's epoch;
+//               also resets the per-pass tile counters and clears the
+//               status words of this call's tiles;
 //   pass p      a workgroup takes the next tile id from an atomic counter
 //               (so every tile it waits for below is already running),
 //               ranks its keys stably in LDS, publishes the tile's digit
@@ -331,33 +331,31 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
 //               tiles by looking back over their published counts: a tile
 //               publishes its count first and, once its own prefix is
 //               known, its inclusive prefix, so a look-back stops at the
-//               first prefix it meets.  Keys and entry ids are then
-//               scattered to digit start + earlier tiles + rank.
-// Status words carry the epoch of the sort that wrote them, so no clearing
-// is needed between calls (graph replays included).  A look-back that
-// waits implausibly long raises kFlagInternal and stops (the update is then
-// voided), so a library bug cannot hang the device.
+//               first prefix it meets.  Two threads per digit read
+//               2 * kOsHalf earlier tiles per step, so at these list sizes
+//               one round of loads usually finds the prefix.  Keys and entry
+//               ids are then scattered to digit start + earlier tiles + rank.
+// A look-back that waits implausibly long raises kFlagInternal and stops
+// (the update is then voided), so a library bug cannot hang the device.
 constexpr uint32_t kOsAgg = 1u;     // status: the tile's own digit count
 constexpr uint32_t kOsPrefix = 2u;  // status: inclusive count over tiles 0..tile
 constexpr int kOsHistIpt = 16;      // keys per thread of a histogram workgroup
 constexpr uint32_t kOsSpinLimit = 1u << 22;
-constexpr int kOsWindow = 32;       // earlier tiles read per look-back step
+constexpr int kOsHalf = 64;         // earlier tiles read by each thread of a digit per step
 
 struct SortBufs {
   int32_t* keys[2];
   int32_t* vals[2];
   uint32_t* totals;                 // [kMaxPasses][kMaxBins] digit totals
-  unsigned long long* status;       // [kMaxPasses][max_tiles][kMaxBins] look-back words
+  uint32_t* status;                 // [kMaxPasses][max_tiles][kMaxBins] look-back words:
+                                    // flag (2 bits: 0 none, kOsAgg, kOsPrefix) | count (30)
   uint32_t* tile_ctr;               // [kMaxPasses] next tile id of each pass
-  uint32_t* epoch;                  // [1] advanced by every histogram launch
   int32_t* part_off;                // [partitions + 1] partitioned sort: where each partition starts
   int max_tiles;
   uint32_t* flag;                   // sticky error bits
 };
 
-__device__ __forceinline__ unsigned long long os_word(uint32_t epoch, uint32_t fl, uint32_t v) {
-  return ((unsigned long long)epoch << 32) | ((unsigned long long)fl << 30) | v;
-}
+__device__ __forceinline__ uint32_t os_word(uint32_t fl, uint32_t v) { return (fl << 30) | v; }
 
 constexpr int kOsHistLdsWords = kMaxPasses * kMaxBins;
 
@@ -367,7 +365,11 @@ __device__ void os_hist(const KeyFn& kf, int N, const SortPlan& plan, const Sort
                         uint32_t* lds) {
   const int t = threadIdx.x;
   if (blk == 0 && t < kMaxPasses) sb.tile_ctr[t] = 0u;
-  if (blk == 0 && t == 0) sb.epoch[0] = sb.epoch[0] + 1u;
+  // the status words of this call's tiles start unpublished
+  const size_t rows = (size_t)plan.ntiles * kMaxBins;
+  for (int p = 0; p < plan.passes; ++p)
+    for (size_t i = (size_t)blk * kBlock + t; i < rows; i += (size_t)gridDim.x * kBlock)
+      sb.status[(size_t)p * sb.max_tiles * kMaxBins + i] = 0u;
   for (int i = t; i < plan.passes * kMaxBins; i += kBlock) lds[i] = 0;
   const int base = blk * kBlock * kOsHistIpt;
   uint32_t key[kOsHistIpt];
@@ -395,9 +397,11 @@ __device__ void os_hist(const KeyFn& kf, int N, const SortPlan& plan, const Sort
 // One radix pass: a workgroup of kOsThreads threads per tile of R * 1024 keys.
 constexpr int kOsThreads = 1024;
 constexpr int kOsWaves = kOsThreads / kWave;
-// LDS of a pass: counters [kMaxBins][waves + 1], digit bases, scan scratch,
-// the tile id.
-constexpr int kOsPassLdsWords = kMaxBins * (kOsWaves + 1) + kMaxBins + 2 * kOsWaves + 1;
+// LDS of a pass: counters [kMaxBins][waves + 1], digit bases (the look-back's
+// next tile per digit before that), scan scratch, the tile id, and the
+// look-back's exchange between the two threads of a digit [2][kMaxBins].
+constexpr int kOsPassLdsWords = kMaxBins * (kOsWaves + 1) + kMaxBins + 2 * kOsWaves + 1 + 2 * kMaxBins;
+static_assert(kOsThreads == 2 * kMaxBins, "the look-back takes two threads per digit");
 
 template <int R, class KeyFn>
 __device__ void os_pass(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb, int p,
@@ -409,11 +413,12 @@ __device__ void os_pass(const KeyFn& kf, int N, const SortPlan& plan, const Sort
   uint32_t* base = hist + kMaxBins * CS;     // [kMaxBins] start of the digit's keys of this tile
   uint32_t* misc = base + kMaxBins;          // scan scratch
   uint32_t* tid_s = misc + 2 * NW;
+  uint32_t* lb_sum = tid_s + 1;              // [kMaxBins] look-back: upper half's sum
+  uint32_t* lb_res = lb_sum + kMaxBins;      // [kMaxBins] ... its outcome and stop tile
   const int bits = plan.bits[p], shift = plan.shift[p], bins = 1 << bits;
   if (t == 0) tid_s[0] = atomicAdd(&sb.tile_ctr[p], 1u);
   // digit total of digit t (complete: written by the histogram launch)
   const uint32_t tot = t < bins ? sb.totals[p * kMaxBins + t] : 0u;
-  const uint32_t epoch = sb.epoch[0];
   uint32_t* mycol = hist + w;
   for (int d = lane; d < bins; d += kWave) {
     mycol[d * CS] = 0;
@@ -466,44 +471,78 @@ __device__ void os_pass(const KeyFn& kf, int N, const SortPlan& plan, const Sort
   }
 
   // publish this tile's digit counts, look back over earlier tiles, publish
-  // the inclusive prefix; thread t < bins takes digit t.  A look-back step
-  // reads a window of kOsWindow earlier tiles at once and adds them from the
-  // nearest down to the first inclusive prefix; a tile that has not
-  // published yet ends the step (it is read again in the next one).
-  unsigned long long* st = sb.status + (size_t)p * sb.max_tiles * kMaxBins;
+  // the inclusive prefix.  Digit bd has two threads, h = 0 (thread bd, which
+  // holds the count) and h = 1 (thread bd + kMaxBins).  From the digit's next
+  // unread tile c, thread h reads tiles c - h*kOsHalf - i, i < kOsHalf, all at
+  // once, and adds them nearest first until it meets an inclusive prefix (or
+  // the first tile), an unpublished tile, or the end of its range.  Thread
+  // h = 0 then combines: its own sum, and the upper half's only if its range
+  // held aggregates alone.  An unpublished tile is read again next step.
+  uint32_t* st = sb.status + (size_t)p * sb.max_tiles * kMaxBins;
+  const int bd = t & (kMaxBins - 1), h = t / kMaxBins;
+  int32_t* lb_cur = reinterpret_cast<int32_t*>(base);  // next unread tile per digit, -1: done
   uint32_t excl = 0u;
-  int cur = mine ? tile - 1 : -1;  // next earlier tile to read; -1: done
   if (mine)
-    __hip_atomic_store(&st[(size_t)tile * kMaxBins + t],
-                       os_word(epoch, tile == 0 ? kOsPrefix : kOsAgg, cnt), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-  for (uint32_t spins = 0; cur >= 0; ++spins) {
+    __hip_atomic_store(&st[(size_t)tile * kMaxBins + t], os_word(tile == 0 ? kOsPrefix : kOsAgg, cnt),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (h == 0) lb_cur[bd] = (mine && tile > 0) ? tile - 1 : -1;
+  __syncthreads();
+  for (uint32_t spins = 0;; ++spins) {
     if (spins > kOsSpinLimit) {  // never expected: give up, void the update
-      atomicOr(sb.flag, kFlagInternal);
+      if (t == 0) atomicOr(sb.flag, kFlagInternal);
       break;
     }
-    unsigned long long sw[kOsWindow];
+    const int c = lb_cur[bd];
+    const int top = c - h * kOsHalf;
+    uint32_t sw[kOsHalf];
 #pragma unroll
-    for (int i = 0; i < kOsWindow; ++i)
-      sw[i] = cur - i >= 0 ? __hip_atomic_load(&st[(size_t)(cur - i) * kMaxBins + t],
-                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                           : 0ull;
-    bool stop = false;
+    for (int i = 0; i < kOsHalf; ++i)
+      sw[i] = (c >= 0 && top - i >= 0)
+                  ? __hip_atomic_load(&st[(size_t)(top - i) * kMaxBins + bd], __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT)
+                  : 0u;
+    // outcome: 0 all aggregates (continue below the range), 1 unpublished
+    // tile `stop`, 2 complete (a prefix or the first tile reached)
+    uint32_t ps = 0u;
+    int res = 0, stop = top - kOsHalf;
 #pragma unroll
-    for (int i = 0; i < kOsWindow; ++i) {
-      if (stop || cur < 0) continue;
-      const uint32_t ep = (uint32_t)(sw[i] >> 32), fl = (uint32_t)(sw[i] >> 30) & 3u;
-      if (ep != epoch || fl == 0u) {  // not published yet: read it again next step
-        stop = true;
+    for (int i = 0; i < kOsHalf; ++i) {
+      if (res != 0) continue;
+      if (top - i < 0) {
+        res = 2;
         continue;
       }
-      excl += (uint32_t)sw[i] & 0x3fffffffu;
-      cur = (fl == kOsPrefix || cur == 0) ? -1 : cur - 1;
+      const uint32_t fl = sw[i] >> 30;
+      if (fl == 0u) {
+        res = 1;
+        stop = top - i;
+        continue;
+      }
+      ps += sw[i] & 0x3fffffffu;
+      if (fl == kOsPrefix) res = 2;
     }
+    if (h == 1) {
+      lb_sum[bd] = ps;
+      lb_res[bd] = (uint32_t)res | ((uint32_t)(stop + 1) << 2);
+    }
+    __syncthreads();
+    bool more = false;
+    if (h == 0 && c >= 0) {
+      excl += ps;
+      int next = res == 2 ? -1 : stop;
+      if (res == 0) {  // this range held aggregates only: the upper half counts
+        const uint32_t r1 = lb_res[bd];
+        excl += lb_sum[bd];
+        next = (r1 & 3u) == 2u ? -1 : (int)(r1 >> 2) - 1;
+      }
+      lb_cur[bd] = next;
+      more = next >= 0;
+    }
+    if (!__syncthreads_or(more)) break;
   }
   if (mine) {
     if (tile > 0)
-      __hip_atomic_store(&st[(size_t)tile * kMaxBins + t], os_word(epoch, kOsPrefix, excl + cnt),
+      __hip_atomic_store(&st[(size_t)tile * kMaxBins + t], os_word(kOsPrefix, excl + cnt),
                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   // digit starts of the pass: exclusive scan of the totals over digits

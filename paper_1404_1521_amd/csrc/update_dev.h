@@ -147,10 +147,8 @@ __global__ __launch_bounds__(kSegfixThreads) void k_segfix(SegArgs a) {
     if (li < cnt) {
       const int2 rec = a.long_list[li];
       if (rec.x >= 0) {
-        const int m = a.seg_end[rec.y] - rec.x + 1;  // partials of this segment
-        if (m <= kSegfixLight) {
-          seg_fix_row_wave(a, rec.x, rec.y, m);
-        } else if (lane == 0) {
+        const int m = seg_fix_row_wave(a, rec.x, rec.y, (int)cnt);  // partials of the segment
+        if (m > kSegfixLight && lane == 0) {
           const int h = atomicAdd(&nheavy, 1);
           heavy[h][0] = rec.x;
           heavy[h][1] = rec.y;

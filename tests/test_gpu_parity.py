@@ -249,6 +249,28 @@ def test_scatter_add_full_size_zipf12(mode):
     assert np.array_equal(got[untouched], table[untouched])
 
 
+@pytest.mark.parametrize("s", [1.2, 0.0])
+def test_scatter_add_many_sort_tiles(s):
+    """700,000 rows, 171 sort tiles of 4096 keys: more earlier tiles than one
+    look-back step reads (128), so late tiles continue below their first
+    window.  Zipf(1.2) and uniform ids; sorted against the oracle, and two
+    calls bit-identical."""
+    sw = dataclasses.replace(workloads.SCATTER_ISO, d=16, N=700_000, zipf_s=s, seed=41)
+    table, idx, Y = workloads.scatter_inputs(sw)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=idx.size, max_rows=table.shape[0])
+    outs = []
+    for _ in range(2):
+        td = dev(table)
+        ctx.scatter_add(td, dev(idx), dev(Y), 1.0, pg().SCATTER_SORTED)
+        assert ctx.status() == pg().OK
+        outs.append(host(td))
+    ref = table.copy()
+    oracle.scatter_add(ref, idx, Y, 1.0)
+    err = np.abs(outs[0].astype(np.float64) - ref.astype(np.float64))
+    assert np.all(err <= scatter_bound(table, idx, Y, 1.0))
+    assert np.array_equal(outs[0], outs[1])
+
+
 def test_scatter_add_sorted_is_deterministic():
     table, idx, Y = workloads.scatter_inputs(N=100_000)
     ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=idx.size, max_rows=table.shape[0])
