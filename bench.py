@@ -317,6 +317,25 @@ def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
     return out
 
 
+def copy_ceiling(torch, mib=256, reps=10):
+    """Streaming-copy ceiling measured on this device: a plain device-to-device
+    copy of `mib` MiB, timed with events on the current stream; bytes read +
+    bytes written per second, in GB/s."""
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    t1.record()
+    t1.synchronize()
+    gbs = 2 * n * 4 * reps / (t0.elapsed_time(t1) * 1e-3) / 1e9
+    del src, dst
+    return round(gbs, 1)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -407,6 +426,7 @@ def main():
             raise RuntimeError("non-finite loss")
         kern = None if args.no_kernels else kernel_rooflines(torch, np, pg, workloads, stream)
         ctx.close()
+        ceiling = copy_ceiling(torch)
 
     # structure of the timed batches (sampled) for the byte model
     small = N <= 8192 and w.H <= 64
@@ -447,7 +467,17 @@ def main():
     roof["kernels_us_per_step"] = {k: round(v[0] * v[1] * 1e3, 3) for k, v in per.items()}
     # every contraction of the step over the step time (all kernels, gaps included)
     roof["step_tflops"] = round(model_flops / (ms / K * 1e-3) / 1e12, 3)
+    # the HBM denominator measured here, beside the 8 TB/s of the data sheet
+    roof["copy_ceiling_gbs"] = ceiling
+    roof["frac_of_copy"] = round(roof["achieved"] / ceiling, 5) if roof["unit"] == "GB/s" else None
+    # kernel time per step over step time (above 1 when the side-stream sort
+    # overlaps the main stream)
+    roof["gpu_busy"] = round(sum(step_us.values()) / (ms / K), 3)  # both in ms
 
+    if kern is not None:
+        for kr in kern.values():
+            if kr.get("unit") == "GB/s":
+                kr["frac_of_copy"] = round(kr["achieved"] / ceiling, 5)
     value = B * K / (ms * 1e-3)
     out = {
         "metric": "training windows/sec (fwd+bwd+update) at V=100k,d=64,win=5,B=1024; HBM GB/s",

@@ -1,5 +1,5 @@
 // Fused gather + forward + hinge + backward for compile-time shapes, one
-// workgroup of 8 waves per group of consecutive 16-window tiles (16x16x4 f32
+// workgroup of 16 waves per group of consecutive 16-window tiles (16x16x4 f32
 // MFMA), ending in the per-entry embedding gradient rows G.
 //
 // Per tile of 16 windows (rows r), with V = dz + dz~, dz or dz~ (per window,
@@ -11,10 +11,10 @@
 //             are loaded into registers while tile k computes, and the ids
 //             of tile k+2 are loaded at the same time;
 //   forward   Z = X W1^T: wave w takes hidden block nt = w % NT and the
-//             K-chunks kc = w / NT + (8 / NT) i; the corrupted copy only
+//             K-chunks kc = w / NT + (16 / NT) i; the corrupted copy only
 //             differs in block c, so z~ = z - zctr + zcor (§1 model, x~);
 //   epilogue  tanh, both scores, hinge mask, dz, dz~ and their sum; a lane
-//             takes one hidden unit of one row;
+//             of waves 0-7 takes one hidden unit of one row;
 //   dW1       dW1 += V^T X for the wave's (nt, chunks), held in registers
 //             across the workgroup's tiles and written once as its partial;
 //   G         G[e][:] = W1_j^T V for entry e = b(win+1) + j: context
@@ -198,8 +198,9 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
     }
     __syncthreads();  // forward partials written
 
-    // ---- epilogue: lane (hn, rsel) takes hidden unit hn of row 2w + rsel
-    {
+    // ---- epilogue: lane (hn, rsel) of wave w < 8 takes hidden unit hn of
+    // row 2w + rsel
+    if (w < kTileRows / 2) {
       const int r = 2 * w + rsel;
       const int row = row0 + r;
       const int nt = hn >> 4, src = (hn & 15) + 16 * (r >> 2), comp = r & 3;
@@ -271,7 +272,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       }
     }
 
-    // ---- G: output tiles ot = w + 8u (position j = ot / DQ, columns cb*16).
+    // ---- G: output tiles ot = w + 16u (position j = ot / DQ, columns cb*16).
     // A operand: lane (r = n16, g) holds V_ty[r][4q + g]; B operand: lane
     // (col = n16, g) holds W1[4q + g][jj*D + cb*16 + col].
 #pragma unroll

@@ -60,7 +60,7 @@ __global__ __launch_bounds__(kBlock, (NT == 1 || (NT == 2 && CPW <= 5)) ? 2 : 1)
   fwdbwd_wg<NT, CPW, D, WIN>(a, blockIdx.x - a.n_sort, lds_f);
 }
 
-// The same step for the compile-time shapes, 8 waves per workgroup; the
+// The same step for the compile-time shapes, 16 waves per workgroup; the
 // sort role (small batches) runs in 512-thread workgroups.
 template <int D, int WIN, int NT>
 __global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {

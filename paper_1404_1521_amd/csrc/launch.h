@@ -138,11 +138,11 @@ struct GatherArgs {
 
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
                               const Launch& L);
-// 8-wave fused kernel for the compile-time shapes: fwdbwd8_shape() gives the
+// 16-wave fused kernel for the compile-time shapes: fwdbwd8_shape() gives the
 // shape id (0: not covered), fwdbwd8_lds_bytes() its LDS.
 int fwdbwd8_shape(int d, int win, int NT);
 size_t fwdbwd8_lds_bytes(int shape);
-constexpr int kF8Waves = 8;
+constexpr int kF8Waves = 16;
 constexpr int kF8Threads = kF8Waves * kWave;  // 512
 constexpr int kF8MaxWorkgroups = 256;         // one workgroup per CU
 hipError_t launch_step_fwdbwd8(const FwdArgs& a, int shape, int grid, size_t lds,
