@@ -71,10 +71,14 @@ def _load():
         lib.oracle_touched_rows.argtypes = [i32] * 3 + [p, p, p, ctypes.c_int32, p]
         lib.oracle_scatter_add_f32.argtypes = [i32, i32, p, p, p, lng, dbl]
         lib.oracle_scatter_add_f64.argtypes = [i32, i32, p, p, p, lng, dbl]
+        lib.oracle_scatter_add_ex.argtypes = [i32, i32, p, i32, p, i32, p, lng, dbl, i32]
+        lib.oracle_encode.argtypes = [i32, p, lng, p]
+        lib.oracle_decode.argtypes = [i32, p, lng, p]
         for name in ("oracle_train_step_f32", "oracle_train_step_f64", "oracle_gradients_f64",
                      "oracle_loss_f64", "oracle_score_f32", "oracle_score_f64",
                      "oracle_gather_f32", "oracle_touched_rows", "oracle_scatter_add_f32",
-                     "oracle_scatter_add_f64"):
+                     "oracle_scatter_add_f64", "oracle_scatter_add_ex", "oracle_encode",
+                     "oracle_decode"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -215,3 +219,60 @@ def scatter_add(table, idx, Y, alpha: float = 1.0) -> None:
     fn = _load().oracle_scatter_add_f32 if dt == np.float32 else _load().oracle_scatter_add_f64
     rc = fn(rows, d, _ptr(table), _ptr(idx), _ptr(Y), N, float(alpha))
     _check(rc, "scatter_add")
+
+
+# storage formats and ops of the general advanced-indexing op
+F32, BF16, F16 = 0, 1, 2
+OP_INC, OP_SET = 0, 1
+
+
+def _dtype_code(arr, bf16):
+    if bf16:
+        if arr.dtype != np.uint16:
+            raise ValueError("bfloat16 arrays are passed as their uint16 bit patterns")
+        return BF16
+    if arr.dtype == np.float32:
+        return F32
+    if arr.dtype == np.float16:
+        return F16
+    raise ValueError("table must be float32, float16, or bfloat16 bits (uint16, bf16=True)")
+
+
+def scatter_add_ex(table, idx, Y, alpha: float = 1.0, op: int = OP_INC, bf16: bool = False) -> None:
+    """In place, the general op: op=OP_INC does table[idx[k]] += alpha*Y[k]
+    for k in order (rows carried in float64, rounded once to the storage
+    format, to nearest even); op=OP_SET does table[idx[k]] = Y[k] (last
+    wins).  table/Y: float32, float16, or bfloat16 bit patterns as uint16 with
+    bf16=True; idx: int32 or int64."""
+    code = _dtype_code(table, bf16)
+    if Y.dtype != table.dtype:
+        raise ValueError("Y must have the table's storage format")
+    if not (table.flags.c_contiguous and Y.flags.c_contiguous):
+        raise ValueError("table and Y must be C-contiguous")
+    idx = np.ascontiguousarray(idx)
+    if idx.dtype not in (np.int32, np.int64):
+        raise ValueError("idx must be int32 or int64")
+    rows, d = table.shape
+    N = idx.shape[0]
+    if Y.shape != (N, d):
+        raise ValueError("Y must be [len(idx)][d]")
+    rc = _load().oracle_scatter_add_ex(rows, d, _ptr(table), code, _ptr(idx), idx.dtype.itemsize,
+                                       _ptr(Y), N, float(alpha), int(op))
+    _check(rc, "scatter_add_ex")
+
+
+def encode(x, dtype: int) -> np.ndarray:
+    """float64 values rounded to a storage format (F32 -> float32 array,
+    BF16 / F16 -> uint16 bit patterns)."""
+    x = np.ascontiguousarray(x, np.float64)
+    out = np.empty(x.shape, np.float32 if dtype == F32 else np.uint16)
+    _check(_load().oracle_encode(int(dtype), _ptr(x), x.size, _ptr(out)), "encode")
+    return out
+
+
+def decode(a, dtype: int) -> np.ndarray:
+    """Storage-format values (as produced by encode) to float64."""
+    a = np.ascontiguousarray(a)
+    x = np.empty(a.shape, np.float64)
+    _check(_load().oracle_decode(int(dtype), _ptr(a), a.size, _ptr(x)), "decode")
+    return x

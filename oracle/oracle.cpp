@@ -292,9 +292,142 @@ int scatter_add(int rows, int d, S* table, const int32_t* idx, const S* Y, long 
   return ORACLE_OK;
 }
 
+/* ---- The general advanced-indexing op (§4.3 names it; the library form
+   the paper contributes takes any table, any index vector and either an
+   increment or an assignment).  Storage formats: IEEE binary32, bfloat16
+   (the upper half of a binary32: 8 significant bits, binary32's exponent
+   range) and IEEE binary16 (11 significant bits, exponents -14..15).
+   Decoding is exact; encoding rounds the double to nearest, ties to even,
+   in one step (no intermediate binary32). */
+enum { ORACLE_F32 = 0, ORACLE_BF16 = 1, ORACLE_F16 = 2 };
+enum { ORACLE_OP_INC = 0, ORACLE_OP_SET = 1 };
+
+/* x rounded to p significant bits with the exponent of the leading bit
+   clamped below at emin (gradual underflow) and overflow to infinity above
+   2^(emax+1); the default rounding mode is to nearest, ties to even. */
+double round_to_format(double x, int p, int emin, int emax) {
+  if (x == 0.0 || !std::isfinite(x)) return x;
+  int e;
+  std::frexp(x, &e);  // |x| in [2^(e-1), 2^e)
+  const int lead = std::max(e - 1, emin);
+  const double q = std::ldexp(1.0, lead - (p - 1));  // spacing of the format at x
+  const double r = std::nearbyint(x / q) * q;        // both scalings are exact
+  if (std::fabs(r) >= std::ldexp(1.0, emax + 1)) return std::copysign(INFINITY, x);
+  return r;
+}
+
+double decode_elem(const void* base, size_t i, int dtype) {
+  if (dtype == ORACLE_F32) return (double)static_cast<const float*>(base)[i];
+  const uint16_t h = static_cast<const uint16_t*>(base)[i];
+  if (dtype == ORACLE_BF16) {
+    const uint32_t u = (uint32_t)h << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return (double)f;
+  }
+  const int sign = h >> 15, ex = (h >> 10) & 31, man = h & 1023;
+  double v;
+  if (ex == 0) v = std::ldexp((double)man, -24);
+  else if (ex == 31) v = man ? NAN : INFINITY;
+  else v = std::ldexp(1.0 + man / 1024.0, ex - 15);
+  return sign ? -v : v;
+}
+
+void encode_elem(void* base, size_t i, int dtype, double x) {
+  if (dtype == ORACLE_F32) {
+    static_cast<float*>(base)[i] = (float)round_to_format(x, 24, -126, 127);
+    return;
+  }
+  uint16_t h;
+  if (dtype == ORACLE_BF16) {
+    const float f = std::isnan(x) ? NAN : (float)round_to_format(x, 8, -126, 127);  // exact
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    h = std::isnan(x) ? (uint16_t)0x7fc0 : (uint16_t)(u >> 16);
+  } else {
+    const double r = std::isnan(x) ? x : round_to_format(x, 11, -14, 15);
+    const uint16_t sign = std::signbit(r) ? 0x8000 : 0;
+    const double a = std::fabs(r);
+    if (std::isnan(r)) h = 0x7e00;
+    else if (std::isinf(r)) h = sign | 0x7c00;
+    else if (a < std::ldexp(1.0, -14)) h = sign | (uint16_t)(a * std::ldexp(1.0, 24));  // subnormal or 0
+    else {
+      int e;
+      std::frexp(a, &e);
+      const int ex = e - 1 + 15;
+      const uint16_t man = (uint16_t)((a / std::ldexp(1.0, e - 1) - 1.0) * 1024.0);
+      h = sign | (uint16_t)(ex << 10) | man;
+    }
+  }
+  static_cast<uint16_t*>(base)[i] = h;
+}
+
+/* op = inc: for k in order, table[idx[k]] += alpha * Y[k], each touched row
+   carried in double from its stored value and rounded to the storage format
+   once at the end.  op = set: for k in order, table[idx[k]] = Y[k] (the
+   last entry of a row wins; alpha is unused).  Indices are int32 or int64;
+   any index outside [0, rows) rejects the whole call before a write. */
+int scatter_add_ex(int rows, int d, void* table, int dtype, const void* idx, int idx_bytes,
+                   const void* Y, long N, double alpha, int op) {
+  if (rows <= 0 || d <= 0 || N < 0) return ORACLE_EINVAL;
+  if (dtype < ORACLE_F32 || dtype > ORACLE_F16 || (idx_bytes != 4 && idx_bytes != 8))
+    return ORACLE_EINVAL;
+  if (op != ORACLE_OP_INC && op != ORACLE_OP_SET) return ORACLE_EINVAL;
+  if (op == ORACLE_OP_INC && !std::isfinite(alpha)) return ORACLE_EINVAL;
+  if (N > 0 && (!table || !idx || !Y)) return ORACLE_ENULL;
+  std::vector<int64_t> id(N);
+  for (long k = 0; k < N; ++k) {
+    id[k] = idx_bytes == 4 ? (int64_t) static_cast<const int32_t*>(idx)[k]
+                           : static_cast<const int64_t*>(idx)[k];
+    if (id[k] < 0 || id[k] >= rows) return ORACLE_EID;
+  }
+  if (op == ORACLE_OP_SET) {
+    const size_t es = dtype == ORACLE_F32 ? 4 : 2;
+    for (long k = 0; k < N; ++k)
+      std::memcpy(static_cast<char*>(table) + (size_t)id[k] * d * es,
+                  static_cast<const char*>(Y) + (size_t)k * d * es, d * es);
+    return ORACLE_OK;
+  }
+  std::vector<long> slot_of(rows, -1);
+  std::vector<int64_t> touched;
+  std::vector<double> acc;
+  for (long k = 0; k < N; ++k) {
+    const int64_t r = id[k];
+    if (slot_of[r] < 0) {
+      slot_of[r] = (long)touched.size();
+      touched.push_back(r);
+      for (int t = 0; t < d; ++t) acc.push_back(decode_elem(table, (size_t)r * d + t, dtype));
+    }
+    double* a = &acc[(size_t)slot_of[r] * d];
+    for (int t = 0; t < d; ++t) a[t] += alpha * decode_elem(Y, (size_t)k * d + t, dtype);
+  }
+  for (size_t u = 0; u < touched.size(); ++u)
+    for (int t = 0; t < d; ++t) encode_elem(table, (size_t)touched[u] * d + t, dtype, acc[u * d + t]);
+  return ORACLE_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+int oracle_scatter_add_ex(int rows, int d, void* table, int dtype, const void* idx, int idx_bytes,
+                          const void* Y, long N, double alpha, int op) {
+  return scatter_add_ex(rows, d, table, dtype, idx, idx_bytes, Y, N, alpha, op);
+}
+
+/* the storage formats' rounding alone, for pinning against other
+   implementations: n doubles encoded into `out` (binary32 or 16-bit words) */
+int oracle_encode(int dtype, const double* x, long n, void* out) {
+  if (dtype < ORACLE_F32 || dtype > ORACLE_F16 || n < 0) return ORACLE_EINVAL;
+  for (long i = 0; i < n; ++i) encode_elem(out, (size_t)i, dtype, x[i]);
+  return ORACLE_OK;
+}
+
+int oracle_decode(int dtype, const void* in, long n, double* x) {
+  if (dtype < ORACLE_F32 || dtype > ORACLE_F16 || n < 0) return ORACLE_EINVAL;
+  for (long i = 0; i < n; ++i) x[i] = decode_elem(in, (size_t)i, dtype);
+  return ORACLE_OK;
+}
 
 int oracle_train_step_f32(int V, int d, int win, int H, int B, float* E, float* W1, float* b1,
                           float* w2, float* b2, const int32_t* windows, const int32_t* corrupt,

@@ -360,3 +360,114 @@ def test_zipf_generator_head_mass():
     hv = np.sum(1.0 / np.arange(1, V + 1))
     assert np.mean(ids == 0) == pytest.approx(1 / hv, rel=0.03)
     assert np.mean(ids == 1) == pytest.approx(0.5 / hv, rel=0.05)
+
+
+# ------------------------------------------- the general advanced-indexing op
+
+def _probe_doubles(rng, n):
+    """Doubles over the interesting ranges of the 16-bit formats: normal,
+    subnormal, near overflow, exact halfway points, both signs."""
+    x = np.concatenate([
+        rng.standard_normal(n) * 10.0 ** rng.uniform(-9, 5, n),
+        np.ldexp(rng.integers(1, 2048, n).astype(np.float64) + 0.5, -24),  # fp16 halfway points
+        np.ldexp(rng.integers(256, 512, n).astype(np.float64) + 0.5, rng.integers(-20, 20, n) - 8),
+        [0.0, -0.0, 65504.0, 65519.99, 65520.0, 2.0 ** -24, 2.0 ** -25, 3 * 2.0 ** -26, 1e300],
+    ])
+    return x * np.where(rng.random(x.size) < 0.5, -1.0, 1.0)
+
+
+def test_f16_rounding_matches_numpy():
+    """binary16 encoding is numpy's float64 -> float16 cast (round to nearest even)."""
+    x = _probe_doubles(np.random.default_rng(11), 4000)
+    with np.errstate(over="ignore"):
+        ref = x.astype(np.float16).view(np.uint16)
+    assert np.array_equal(oracle.encode(x, oracle.F16), ref)
+    finite = np.isfinite(ref.view(np.float16))
+    assert np.array_equal(oracle.decode(ref[finite], oracle.F16),
+                          ref[finite].view(np.float16).astype(np.float64))
+
+
+def test_f32_rounding_matches_numpy():
+    x = _probe_doubles(np.random.default_rng(12), 4000)
+    with np.errstate(over="ignore"):
+        ref = x.astype(np.float32)
+    assert np.array_equal(oracle.encode(x, oracle.F32).view(np.uint32), ref.view(np.uint32))
+
+
+def test_bf16_rounding_is_nearest_even_by_brute_force():
+    """Each bfloat16 code is the nearest representable value to x (compared
+    exactly in float64 against both neighbours of the code), and on a tie the
+    one with an even last mantissa bit; decoding is the upper half of a
+    binary32."""
+    x = _probe_doubles(np.random.default_rng(13), 3000)
+    x = x[np.abs(x) < 3e38]
+    h = oracle.encode(x, oracle.BF16)
+    v = oracle.decode(h, oracle.BF16)
+    assert np.array_equal(v, (h.astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+    for hk, xk, vk in zip(h, x, v):
+        mag = int(hk) & 0x7FFF
+        sign = int(hk) & 0x8000
+        nbrs = [sign | m for m in (mag - 1, mag + 1) if 0 <= m < 0x7F80]
+        dv = abs(vk - xk)
+        for nb in nbrs:
+            dn = abs(oracle.decode(np.array([nb], np.uint16), oracle.BF16)[0] - xk)
+            assert dv <= dn
+            if dv == dn:
+                assert mag % 2 == 0
+
+
+def test_scatter_add_ex_f32_inc_is_scatter_add():
+    rng = np.random.default_rng(14)
+    t0 = rng.normal(0, 0.01, (50, 7)).astype(np.float32)
+    idx = workloads.zipf_ids(rng, 50, 1.2, 400)
+    Y = rng.normal(0, 1e-3, (400, 7)).astype(np.float32)
+    a, b = t0.copy(), t0.copy()
+    oracle.scatter_add(a, idx, Y, -0.3)
+    oracle.scatter_add_ex(b, idx.astype(np.int64), Y, -0.3, oracle.OP_INC)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_scatter_add_ex_set_last_entry_wins():
+    rng = np.random.default_rng(15)
+    for dt in (np.float32, np.float16):
+        t0 = rng.normal(0, 1, (30, 5)).astype(dt)
+        idx = rng.integers(0, 30, 200).astype(np.int32)
+        Y = rng.normal(0, 1, (200, 5)).astype(dt)
+        got = t0.copy()
+        oracle.scatter_add_ex(got, idx, Y, 0.0, oracle.OP_SET)
+        ref = t0.copy()
+        last = {}
+        for k, r in enumerate(idx):
+            last[int(r)] = k
+        for r, k in last.items():
+            ref[r] = Y[k]
+        assert np.array_equal(got.view(np.uint16 if dt == np.float16 else np.uint32),
+                              ref.view(np.uint16 if dt == np.float16 else np.uint32))
+
+
+def test_scatter_add_ex_rounds_each_row_once():
+    """bfloat16 has 8 significant bits: 1 + 2^-9 rounds back to 1, so adding
+    2^-9 three times entry by entry would leave 1.0; the op carries the row
+    exactly and rounds 1 + 3*2^-9 once, to 1 + 2^-7.  binary16 likewise with
+    2^-12 steps on 1.0 (spacing 2^-10)."""
+    for code, step, want in ((oracle.BF16, 2.0 ** -9, 1 + 2.0 ** -7),
+                             (oracle.F16, 2.0 ** -12, 1 + 2.0 ** -10)):
+        t = oracle.encode(np.array([[1.0, -2.0]]), code)
+        Y = oracle.encode(np.full((3, 2), step), code)
+        if code == oracle.F16:
+            t, Y = t.view(np.float16), Y.view(np.float16)
+        oracle.scatter_add_ex(t, np.zeros(3, np.int64), Y, 1.0, oracle.OP_INC,
+                              bf16=code == oracle.BF16)
+        got = oracle.decode(t.view(np.uint16) if code == oracle.F16 else t, code)
+        assert got[0, 0] == want
+        assert got[0, 1] == oracle.decode(oracle.encode(np.array([-2.0 + 3 * step]), code), code)[0]
+
+
+def test_scatter_add_ex_rejects_bad_ids_before_writing():
+    t0 = np.ones((4, 2), np.float32)
+    for idx in (np.array([0, 4], np.int32), np.array([1, -1], np.int64),
+                np.array([2, 1 << 33], np.int64)):
+        t = t0.copy()
+        with pytest.raises(oracle.OracleError):
+            oracle.scatter_add_ex(t, idx, np.ones((2, 2), np.float32), 1.0)
+        assert np.array_equal(t, t0)
