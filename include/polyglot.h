@@ -133,6 +133,38 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
                          const int32_t* idx, const float* Y, int32_t N, float alpha,
                          int32_t mode);
 
+/* Storage formats and operations of polyglot_scatter_update. */
+#define POLYGLOT_F32 0  /* IEEE binary32 */
+#define POLYGLOT_BF16 1 /* bfloat16: the upper 16 bits of a binary32 */
+#define POLYGLOT_F16 2  /* IEEE binary16 */
+#define POLYGLOT_OP_INC 0 /* table[idx[k]] += alpha * Y[k] */
+#define POLYGLOT_OP_SET 1 /* table[idx[k]] = Y[k]; alpha unused */
+
+/* The general advanced-indexing op of §4.3 (the increment the paper
+ * rewrites, in the library form it contributes: any table format, any
+ * index vector, increment or assignment).
+ *   table[rows][d] and Y[N][d]: device, row-major, both in storage format
+ *     dtype; d in [1, 256]; aligned to their element size.
+ *   idx[N]: device, int32 (idx_bytes 4) or int64 (idx_bytes 8), each in
+ *     [0, rows); aligned to idx_bytes.
+ *   op POLYGLOT_OP_INC: for every k, table[idx[k]] += alpha * Y[k];
+ *     repeated indices accumulate.  Sorted mode adds each row's entries in
+ *     float32 in entry order and rounds the row to its format once (round
+ *     to nearest even).  Atomic mode: float32 tables only, one float atomic
+ *     per element.
+ *   op POLYGLOT_OP_SET: for every k in order, table[idx[k]] = Y[k]; for a
+ *     repeated index the largest k wins (sorted mode only).
+ * N <= max_scatter and rows <= max_rows of the context.  Float32 increments
+ * take the same kernels as polyglot_scatter_add.  The caller owns every
+ * buffer; the call is asynchronous on the context stream.  Returns
+ * POLYGLOT_EINVAL for a bad format, op, mode, width or alignment or an
+ * unsupported mode combination, POLYGLOT_ENULL, POLYGLOT_EBATCH; an index
+ * outside [0, rows) leaves the table untouched and raises the sticky flag
+ * (POLYGLOT_EID from polyglot_status). */
+int polyglot_scatter_update(polyglot_ctx* ctx, void* table, int32_t dtype, int32_t rows,
+                            int32_t d, const void* idx, int32_t idx_bytes, const void* Y,
+                            int32_t N, float alpha, int32_t op, int32_t mode);
+
 /* Host copy of the sorted distinct row ids touched by the last sorted-mode
  * train step (ids of the windows and the corrupt ids).  Synchronises the
  * stream.  Writes at most cap ids to ids_host and the total to *count.

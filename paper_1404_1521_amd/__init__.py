@@ -22,12 +22,15 @@ LIB_PATH = os.path.join(_HERE, "libpolyglot.so")
 
 OK, EINVAL, ENULL, EBATCH, EHIP, EID, ESTATE = 0, -1, -2, -3, -4, -5, -6
 SCATTER_SORTED, SCATTER_ATOMIC = 0, 1
+F32, BF16, F16 = 0, 1, 2      # storage formats of scatter_update
+OP_INC, OP_SET = 0, 1         # its operations
 _CODE_NAMES = {EINVAL: "EINVAL", ENULL: "ENULL", EBATCH: "EBATCH", EHIP: "EHIP", EID: "EID",
                ESTATE: "ESTATE"}
 
 # Every entry point declared in include/polyglot.h.
 EXPORTS = ("polyglot_init", "polyglot_destroy", "polyglot_set_stream", "polyglot_train_step",
            "polyglot_train_steps", "polyglot_score", "polyglot_gather", "polyglot_scatter_add",
+           "polyglot_scatter_update",
            "polyglot_touched_rows", "polyglot_status", "polyglot_last_error",
            "polyglot_set_timing", "polyglot_kernel_times")
 KERNEL_NAMES = ("fwdbwd", "sort", "update", "gather", "scatter", "score", "segfix", "wide_dw1",
@@ -68,6 +71,7 @@ def load_library():
         "polyglot_score": [p] + [p] * 6 + [i32, p],
         "polyglot_gather": [p, p, p, p, i32, p, p],
         "polyglot_scatter_add": [p, p, i32, i32, p, p, i32, f32, i32],
+        "polyglot_scatter_update": [p, p, i32, i32, i32, p, i32, p, i32, f32, i32, i32],
         "polyglot_touched_rows": [p, p, i32, p],
         "polyglot_status": [p],
         "polyglot_last_error": [p],
@@ -181,6 +185,24 @@ class Context:
             self._h, _dev_tensor(table, torch.float32, "table"), rows, d,
             _dev_tensor(idx, torch.int32, "idx", (N,)),
             _dev_tensor(Y, torch.float32, "Y", (N, d)), N, alpha, mode), "scatter_add")
+
+    def scatter_update(self, table, idx, Y, alpha: float = 1.0, op: int = OP_INC,
+                       mode: int = SCATTER_SORTED) -> None:
+        """The general advanced-indexing op on a float32, bfloat16 or float16
+        table (Y in the same dtype) with int32 or int64 indices: op=OP_INC
+        adds alpha * Y[k] into row idx[k]; op=OP_SET assigns Y[k] (the last
+        k of a row wins)."""
+        codes = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
+        if table.dtype not in codes:
+            raise TypeError(f"table must be float32, bfloat16 or float16, got {table.dtype}")
+        if idx.dtype not in (torch.int32, torch.int64):
+            raise TypeError(f"idx must be int32 or int64, got {idx.dtype}")
+        rows, d = table.shape
+        N = idx.shape[0]
+        self._check(self._lib.polyglot_scatter_update(
+            self._h, _dev_tensor(table, table.dtype, "table"), codes[table.dtype], rows, d,
+            _dev_tensor(idx, idx.dtype, "idx", (N,)), idx.element_size(),
+            _dev_tensor(Y, table.dtype, "Y", (N, d)), N, alpha, op, mode), "scatter_update")
 
     def touched_rows(self):
         n = ctypes.c_int32()

@@ -459,6 +459,11 @@ int check_step_args(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   return POLYGLOT_OK;
 }
 
+// The float32 scatter-add once the arguments are valid: sorted segments
+// (partition-wise for short lists) or one atomic per element.
+int scatter_add_f32(polyglot_ctx* ctx, float* table, int32_t rows, int32_t d, const int32_t* idx,
+                    const float* Y, int32_t N, float alpha, int32_t mode);
+
 }  // namespace
 
 extern "C" {
@@ -534,6 +539,7 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_end, (size_t)std::max(c.V, c.max_rows));
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_part, (size_t)ctx->max_chunks * 2 * ctx->seg_stride);
   if (e == hipSuccess) e = alloc(ctx, &ws.long_list, (size_t)ctx->max_chunks);
+  if (e == hipSuccess) e = alloc(ctx, &ws.idx32, (size_t)c.max_scatter);
   if (e == hipSuccess) e = alloc(ctx, &ws.flag, 1);
   if (e == hipSuccess) e = alloc(ctx, &ws.scratch_loss, 1);
   for (int k = 0; k < 2; ++k) {
@@ -694,6 +700,94 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
   if (!std::isfinite(alpha)) return fail(ctx, POLYGLOT_EINVAL, "scatter_add: alpha not finite");
   if (mode != POLYGLOT_SCATTER_SORTED && mode != POLYGLOT_SCATTER_ATOMIC)
     return fail(ctx, POLYGLOT_EINVAL, "scatter_add: bad mode");
+  return scatter_add_f32(ctx, table, rows, d, idx, Y, N, alpha, mode);
+}
+
+int polyglot_scatter_update(polyglot_ctx* ctx, void* table, int32_t dtype, int32_t rows,
+                            int32_t d, const void* idx, int32_t idx_bytes, const void* Y,
+                            int32_t N, float alpha, int32_t op, int32_t mode) {
+  if (!ctx) return POLYGLOT_ENULL;
+  if (!table || !idx || !Y) return fail(ctx, POLYGLOT_ENULL, "scatter_update: NULL pointer");
+  if (N <= 0 || N > ctx->cfg.max_scatter)
+    return fail(ctx, POLYGLOT_EBATCH, "scatter_update: N must be in [1, max_scatter]");
+  if (rows <= 0 || rows > ctx->cfg.max_rows || d <= 0 || d > kMaxD)
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_update: bad rows or d");
+  if (dtype != POLYGLOT_F32 && dtype != POLYGLOT_BF16 && dtype != POLYGLOT_F16)
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_update: bad storage format");
+  if (idx_bytes != 4 && idx_bytes != 8)
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_update: indices must be 4 or 8 bytes");
+  if (op != POLYGLOT_OP_INC && op != POLYGLOT_OP_SET)
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_update: bad op");
+  if (mode != POLYGLOT_SCATTER_SORTED && mode != POLYGLOT_SCATTER_ATOMIC)
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_update: bad mode");
+  if (op == POLYGLOT_OP_INC && !std::isfinite(alpha))
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_update: alpha not finite");
+  const size_t es = dtype == POLYGLOT_F32 ? 4 : 2;
+  if (reinterpret_cast<uintptr_t>(table) % es || reinterpret_cast<uintptr_t>(Y) % es ||
+      reinterpret_cast<uintptr_t>(idx) % idx_bytes)
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_update: misaligned pointer");
+  if (mode == POLYGLOT_SCATTER_ATOMIC && (dtype != POLYGLOT_F32 || op != POLYGLOT_OP_INC))
+    return fail(ctx, POLYGLOT_EINVAL, "scatter_update: the atomic mode takes float32 increments only");
+  hipError_t e = hipSuccess;
+  const int32_t* keys = static_cast<const int32_t*>(idx);
+  if (idx_bytes == 8) {  // narrowed (and range-checked) into the context's key buffer
+    Timed tm(ctx, POLYGLOT_K_SORT);
+    e = launch_keys_from_i64(static_cast<const int64_t*>(idx), N, rows, ctx->ws.idx32,
+                             ctx->ws.flag, tm.L);
+    if (e != hipSuccess) return hip_fail(ctx, e, "scatter_update: key launch");
+    keys = ctx->ws.idx32;
+  }
+  // float32 increments take the scatter-add kernels (their fix-up reads rows
+  // as 16-byte vectors, so the sorted mode wants d % 4 == 0 and aligned rows)
+  if (dtype == POLYGLOT_F32 && op == POLYGLOT_OP_INC &&
+      (mode == POLYGLOT_SCATTER_ATOMIC || (d % 4 == 0 && aligned16(table) && aligned16(Y))))
+    return scatter_add_f32(ctx, static_cast<float*>(table), rows, d, keys,
+                           static_cast<const float*>(Y), N, alpha, mode);
+  const SortPlan plan = make_plan(rows, N);
+  const IdxKeys kf{keys, rows};
+  {
+    Timed tm(ctx, POLYGLOT_K_SORT);
+    e = launch_sort_idx(kf, N, plan, sort_bufs(ctx, 0), tm.L);
+  }
+  GenCall c{};
+  c.table = table;
+  c.Y = Y;
+  c.sk = ctx->ws.keys[plan.passes & 1];
+  c.sv = ctx->ws.vals[plan.passes & 1];
+  c.seg_part = ctx->ws.seg_part;
+  c.long_list = ctx->ws.long_list;
+  c.seg_end = ctx->ws.seg_end;
+  c.flag = ctx->ws.flag;
+  c.N = N;
+  c.d = d;
+  c.ch = seg_chunk_size(N);
+  c.seg_stride = ctx->seg_stride;
+  c.alpha = alpha;
+  c.zero = sort_zero_ranges(ctx, plan, 0);
+  c.dtype = dtype;
+  c.op = op;
+  c.n_e = std::max(1, std::min(ceil_div(ceil_div(N, op == POLYGLOT_OP_SET ? kWave : c.ch),
+                                        kWavesPerBlock), 2048));
+  c.n_z = plan.small ? 0 : 16;
+  if (e == hipSuccess) {
+    Timed tm(ctx, POLYGLOT_K_SCATTER);
+    e = launch_gen_update(c, tm.L);
+  }
+  if (e == hipSuccess && op == POLYGLOT_OP_INC) {
+    Timed tm(ctx, POLYGLOT_K_SEGFIX);
+    e = launch_gen_fix(c, std::max(1, std::min(ceil_div(ceil_div(N, c.ch), kSegfixWaves), 2048)),
+                       tm.L);
+  }
+  ctx->have_sorted = false;  // the sort buffers now hold this call's order
+  return e == hipSuccess ? POLYGLOT_OK : hip_fail(ctx, e, "scatter_update launch");
+}
+
+}  // extern "C"
+
+namespace {
+
+int scatter_add_f32(polyglot_ctx* ctx, float* table, int32_t rows, int32_t d, const int32_t* idx,
+                    const float* Y, int32_t N, float alpha, int32_t mode) {
   const SortPlan plan = make_plan(rows, N);
   const IdxKeys kf{idx, rows};
   ApplyArgs aa{};
@@ -733,6 +827,10 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
   ctx->have_sorted = false;  // the sort buffers now hold this call's order
   return e == hipSuccess ? POLYGLOT_OK : hip_fail(ctx, e, "scatter_add launch");
 }
+
+}  // namespace
+
+extern "C" {
 
 int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int32_t* count) {
   if (!ctx || !count) return POLYGLOT_ENULL;

@@ -71,6 +71,7 @@ struct Workspace {
   int32_t* seg_end;         // [max(V, max_rows)] end chunk of a long segment, by row id
   uint32_t* flag;           // sticky error bits
   float* scratch_loss;      // loss slot used when the caller passes no loss pointer
+  int32_t* idx32;           // [max_scatter] int64 indices narrowed to int32 keys
 };
 
 __host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }

@@ -41,6 +41,7 @@
 #include "large_dev.h"
 #include "update_dev.h"
 #include "aux_dev.h"
+#include "general_dev.h"
 
 namespace pg {
 
@@ -190,6 +191,54 @@ hipError_t launch_apply_part(const ApplyArgs& a, int grid, const Launch& L) {
 
 hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L) {
   return pg_launch(k_segfix, dim3(grid), dim3(kSegfixThreads), 0, L, a);
+}
+
+template <class T>
+static GenArgs<T> gen_args(const GenCall& c) {
+  GenArgs<T> a{};
+  a.table = static_cast<T*>(c.table);
+  a.Y = static_cast<const T*>(c.Y);
+  a.sk = c.sk;
+  a.sv = c.sv;
+  a.seg_part = c.seg_part;
+  a.long_list = c.long_list;
+  a.seg_end = c.seg_end;
+  a.flag = c.flag;
+  a.N = c.N;
+  a.d = c.d;
+  a.ch = c.ch;
+  a.seg_stride = c.seg_stride;
+  a.alpha = c.alpha;
+  a.zero = c.zero;
+  return a;
+}
+
+template <class T>
+static hipError_t launch_gen_update_t(const GenCall& c, const Launch& L) {
+  const dim3 grid(c.n_e + c.n_z), block(kBlock);
+  if (c.op == 1) return pg_launch(k_gen_set<T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
+  if (c.ch == 16) return pg_launch(k_gen_apply<16, T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
+  return pg_launch(k_gen_apply<64, T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
+}
+
+hipError_t launch_gen_update(const GenCall& c, const Launch& L) {
+  if (c.dtype == 1) return launch_gen_update_t<BF16>(c, L);
+  if (c.dtype == 2) return launch_gen_update_t<F16>(c, L);
+  return launch_gen_update_t<float>(c, L);
+}
+
+hipError_t launch_gen_fix(const GenCall& c, int grid, const Launch& L) {
+  if (c.dtype == 1)
+    return pg_launch(k_gen_segfix<BF16>, dim3(grid), dim3(kSegfixThreads), 0, L, gen_args<BF16>(c));
+  if (c.dtype == 2)
+    return pg_launch(k_gen_segfix<F16>, dim3(grid), dim3(kSegfixThreads), 0, L, gen_args<F16>(c));
+  return pg_launch(k_gen_segfix<float>, dim3(grid), dim3(kSegfixThreads), 0, L, gen_args<float>(c));
+}
+
+hipError_t launch_keys_from_i64(const int64_t* idx, int N, int rows, int32_t* keys,
+                                uint32_t* flag, const Launch& L) {
+  const int g = std::min(std::max(ceil_div(N, kBlock), 1), 1024);
+  return pg_launch(k_keys_from_i64, dim3(g), dim3(kBlock), 0, L, idx, N, rows, keys, flag);
 }
 
 hipError_t launch_check_idx(const int32_t* idx, int N, int rows, uint32_t* flag, const Launch& L) {

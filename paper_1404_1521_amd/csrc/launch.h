@@ -156,6 +156,31 @@ hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const
 hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, const Launch& L);
 hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, const Launch& L);
 hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L);
+
+// The general advanced-indexing op (any storage format, increment or
+// assignment) over a sorted entry list; pointers as in SegArgs, the table
+// and Y in format `dtype` (0 float32, 1 bfloat16, 2 binary16).
+struct GenCall {
+  void* table;
+  const void* Y;
+  const int32_t* sk;
+  const int32_t* sv;
+  float* seg_part;
+  int2* long_list;
+  int32_t* seg_end;
+  const uint32_t* flag;
+  int N, d, ch, seg_stride;
+  float alpha;
+  ZeroRanges zero;
+  int dtype;  // 0 float32, 1 bfloat16, 2 binary16
+  int op;     // 0 increment, 1 assignment
+  int n_e;    // workgroups of the apply / assignment role
+  int n_z;    // workgroups clearing the sort counters
+};
+hipError_t launch_gen_update(const GenCall& c, const Launch& L);
+hipError_t launch_gen_fix(const GenCall& c, int grid, const Launch& L);
+hipError_t launch_keys_from_i64(const int64_t* idx, int N, int rows, int32_t* keys,
+                                uint32_t* flag, const Launch& L);
 hipError_t launch_apply_part(const ApplyArgs& a, int grid, const Launch& L);
 hipError_t launch_check_idx(const int32_t* idx, int N, int rows, uint32_t* flag, const Launch& L);
 hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, const Launch& L);

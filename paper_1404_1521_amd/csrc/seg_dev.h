@@ -97,10 +97,19 @@ struct ChunkSink {
   int* meta;     // LOCAL: cont_first, open_last, single, first key, last key
 };
 
+// Element access of the float32 table: a row's entries are read as floats;
+// a completed piece is added with one float atomic per element at the L2
+// (lanes past the row end add -0.0, which changes nothing).
+__device__ __forceinline__ float seg_load(const SegArgs& a, size_t i) { return a.Y[i]; }
+__device__ __forceinline__ void seg_add(const SegArgs& a, size_t i, bool cok, float v) {
+  unsafeAtomicAdd(a.table + i, cok ? v : -0.f);
+}
+
 // One wave applies entries [i0, min(i0 + CH, end)) of the sorted list, chunk
-// number `chunk` (see the file comment).
-template <int CH, bool LOCAL>
-__device__ void seg_apply_rows(const SegArgs& a, int i0, int end, int chunk, const ChunkSink& sink) {
+// number `chunk` (see the file comment).  A is SegArgs or another argument
+// set with the same fields and its own seg_load / seg_add.
+template <int CH, bool LOCAL, class A>
+__device__ void seg_apply_rows(const A& a, int i0, int end, int chunk, const ChunkSink& sink) {
   static_assert(CH % 8 == 0 && CH <= kWave, "rows are walked in blocks of 8");
   const int lane = lane_id();
   // the error flag (set by an earlier launch) is read beside the chunk's
@@ -146,7 +155,7 @@ __device__ void seg_apply_rows(const SegArgs& a, int i0, int end, int chunk, con
 #pragma unroll
     for (int r = 0; r < CH; ++r) {
       const int ent = __builtin_amdgcn_readlane(ci.ent, r);
-      v[r] = a.Y[(size_t)ent * a.d + colc];
+      v[r] = seg_load(a, (size_t)ent * a.d + colc);
     }
     // running sum in entry order, closed at every piece end (tail);
     // completed pieces go straight to their rows
@@ -172,7 +181,7 @@ __device__ void seg_apply_rows(const SegArgs& a, int i0, int end, int chunk, con
             if (u == lt) last_sum = acc;
             if ((cw >> u) & 1u) {
               const int32_t key = __builtin_amdgcn_readlane(ci.key, r0 + u);
-              unsafeAtomicAdd(a.table + (size_t)key * a.d + colc, cok ? alpha * acc : -0.f);
+              seg_add(a, (size_t)key * a.d + colc, cok, alpha * acc);
             }
             acc = 0.f;
           }

@@ -583,3 +583,138 @@ def test_score_matches_oracle(name, B):
     s = host(ctx.score(params_dev(p), dev(win)))
     r = oracle.score(p, win)
     np.testing.assert_allclose(s, r, rtol=1e-5, atol=1e-6 * np.max(np.abs(r)))
+
+
+# --------------------------------------------- the general advanced-indexing op
+
+_FMT = {"f32": (np.float32, 0), "bf16": (np.uint16, 1), "f16": (np.float16, 2)}
+
+
+def _to_dev(a, fmt):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if fmt == "bf16":
+        t = t.view(torch.int16).view(torch.bfloat16)
+    return t.cuda()
+
+
+def _to_host(t, fmt):
+    torch.cuda.synchronize()
+    if fmt == "bf16":
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.cpu().numpy()
+
+
+def _format_inputs(rng, fmt, rows, d, N, s, idx_dtype):
+    code = _FMT[fmt][1]
+    t64 = rng.normal(0, 0.01, (rows, d))
+    y64 = rng.normal(0, 1e-3, (N, d))
+    if fmt == "f32":
+        t0, Y = t64.astype(np.float32), y64.astype(np.float32)
+    elif fmt == "f16":
+        t0, Y = t64.astype(np.float16), y64.astype(np.float16)
+    else:
+        t0, Y = oracle.encode(t64, code), oracle.encode(y64, code)
+    idx = workloads.zipf_ids(rng, rows, s, N).astype(idx_dtype)
+    return t0, Y, idx
+
+
+def _format_bound(fmt, t0, idx, Y, alpha, ref_vals):
+    """One unit in the last place of the storage format at the reference
+    value (the once-per-row rounding may land on the other side of a
+    rounding boundary) plus the float32 accumulation bound of the sums."""
+    code = _FMT[fmt][1]
+    tv = oracle.decode(t0, code) if fmt == "bf16" else t0.astype(np.float64)
+    yv = oracle.decode(Y, code) if fmt == "bf16" else Y.astype(np.float64)
+    acc = scatter_bound(tv, idx, yv, alpha)
+    a = np.abs(ref_vals).astype(np.float32)
+    if fmt == "bf16":
+        ulp = np.spacing(a).astype(np.float64) * 2.0 ** 16
+    elif fmt == "f16":
+        ulp = np.spacing(np.abs(ref_vals).astype(np.float16)).astype(np.float64)
+    else:
+        ulp = np.zeros_like(acc)
+    return ulp + acc
+
+
+@pytest.mark.parametrize("fmt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("op", [0, 1])
+@pytest.mark.parametrize("rows,d,N,s,idx_dtype", [
+    (50, 8, 400, 1.2, np.int32), (1000, 33, 5000, 1.2, np.int64), (100_000, 64, 20_000, 1.2, np.int32),
+    (3, 4, 1, 1.0, np.int64), (7, 256, 3000, 1.5, np.int32), (100_000, 1, 9000, 1.1, np.int64),
+    (20_000, 17, 140_000, 1.2, np.int64),
+])
+def test_scatter_update_matches_oracle(fmt, op, rows, d, N, s, idx_dtype):
+    """Every storage format and op, int32 and int64 indices, widths that are
+    not multiples of 4, the partition-sorted (N <= 8192) and the chunked list
+    (64-entry chunks above 131072, with heavy rows in the fix-up)."""
+    rng = np.random.default_rng(rows * 7 + N + d)
+    t0, Y, idx = _format_inputs(rng, fmt, rows, d, N, s, idx_dtype)
+    alpha = -0.75
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    td = _to_dev(t0, fmt)
+    ctx.scatter_update(td, dev(idx), _to_dev(Y, fmt), alpha, op)
+    assert ctx.status() == pg().OK
+    got = _to_host(td, fmt)
+    ref = t0.copy()
+    oracle.scatter_add_ex(ref, idx, Y, alpha, op, bf16=fmt == "bf16")
+    untouched = np.setdiff1d(np.arange(rows), idx)
+    assert np.array_equal(got[untouched], t0[untouched])
+    if op == 1:  # assignment copies bits
+        assert np.array_equal(got, ref)
+        return
+    code = _FMT[fmt][1]
+    gv = oracle.decode(got, code) if fmt == "bf16" else got.astype(np.float64)
+    rv = oracle.decode(ref, code) if fmt == "bf16" else ref.astype(np.float64)
+    assert np.all(np.abs(gv - rv) <= _format_bound(fmt, t0, idx, Y, alpha, rv))
+
+
+def test_scatter_update_bf16_full_size_and_deterministic():
+    """The standalone scatter-add workload (327,680 Zipf(1.2) rows into
+    100000 x 64) on a bfloat16 table: against the oracle, and two calls
+    bit-identical."""
+    table, idx, Y = workloads.scatter_inputs()
+    t0 = oracle.encode(table.astype(np.float64), 1)
+    Yb = oracle.encode(Y.astype(np.float64), 1)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=idx.size, max_rows=table.shape[0])
+    outs = []
+    for _ in range(2):
+        td = _to_dev(t0, "bf16")
+        ctx.scatter_update(td, dev(idx.astype(np.int64)), _to_dev(Yb, "bf16"), 1.0)
+        assert ctx.status() == pg().OK
+        outs.append(_to_host(td, "bf16"))
+    assert np.array_equal(outs[0], outs[1])
+    ref = t0.copy()
+    oracle.scatter_add_ex(ref, idx, Yb, 1.0, 0, bf16=True)
+    rv = oracle.decode(ref, 1)
+    assert np.all(np.abs(oracle.decode(outs[0], 1) - rv) <= _format_bound("bf16", t0, idx, Yb, 1.0, rv))
+
+
+def test_scatter_update_bad_int64_index_leaves_table_untouched():
+    m = pg()
+    rng = np.random.default_rng(3)
+    t0 = rng.normal(0, 1, (10, 3)).astype(np.float16)
+    Y = np.ones((3, 3), np.float16)
+    ctx = m.Context(1000, 16, 5, 8, max_batch=1, max_scatter=3, max_rows=10)
+    for bad in (10, -1, 1 << 33):
+        for op in (m.OP_INC, m.OP_SET):
+            td = _to_dev(t0, "f16")
+            ctx.scatter_update(td, dev(np.array([1, bad, 2], np.int64)), _to_dev(Y, "f16"), 1.0, op)
+            assert ctx.status() == m.EID
+            assert np.array_equal(_to_host(td, "f16"), t0)
+            assert ctx.status() == m.OK
+
+
+def test_scatter_update_rejects_unsupported_combinations():
+    m = pg()
+    ctx = m.Context(1000, 16, 5, 8, max_batch=1, max_scatter=4, max_rows=10)
+    idx = dev(np.zeros(4, np.int32))
+    tb = torch.zeros(10, 8, dtype=torch.bfloat16, device="cuda")
+    Yb = torch.zeros(4, 8, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(m.PolyglotError):
+        ctx.scatter_update(tb, idx, Yb, 1.0, m.OP_INC, m.SCATTER_ATOMIC)
+    tf = torch.zeros(10, 8, dtype=torch.float32, device="cuda")
+    Yf = torch.zeros(4, 8, dtype=torch.float32, device="cuda")
+    with pytest.raises(m.PolyglotError):
+        ctx.scatter_update(tf, idx, Yf, 1.0, m.OP_SET, m.SCATTER_ATOMIC)
+    ctx.scatter_update(tf, idx, Yf, 1.0, m.OP_INC, m.SCATTER_ATOMIC)
+    assert ctx.status() == m.OK
