@@ -310,6 +310,33 @@ def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
                              bytes_per_call=nbytes,
                              workload=f"{sw.N} rows Zipf({sw.zipf_s}) into {sw.rows}x{sw.d}, U={U}")
         ctx.set_timing(False)
+        # the general op on the same workload: a bfloat16 table with int64
+        # indices (increment), and a float16 table (assignment).  Roofline of
+        # the table kernels: increment 4 B sorted key + 2d B of Y per entry and
+        # 2 * 2d B per distinct row; assignment 8 B (key, entry) per entry and
+        # 2 * 2d B per distinct row (one Y row read, one table row written)
+        I64 = I.to(torch.int64)
+        for name, dt, ix, op, gbytes in (
+                ("update_bf16_inc", torch.bfloat16, I64, pg.OP_INC,
+                 sw.N * (4 + 2 * sw.d) + 2 * U * sw.d * 2),
+                ("update_f16_set", torch.float16, I, pg.OP_SET, sw.N * 8 + 2 * U * sw.d * 2)):
+            Tg, Yg = T.to(dt), Yd.to(dt)
+            call_ms = time_events(torch, stream, lambda: ctx.scatter_update(Tg, ix, Yg, 1.0, op), reps)
+            ctx.set_timing(True)
+            for _ in range(reps):
+                ctx.scatter_update(Tg, ix, Yg, 1.0, op)
+            kt = ctx.kernel_times()
+            ctx.set_timing(False)
+            us = {k: kt.get(k, (0.0, 0))[0] / reps * 1e3 for k in ("sort", "scatter", "segfix")}
+            table_ms = (us["scatter"] + us["segfix"]) * 1e-3
+            out[name] = dict(roofline(gbytes, 0, "hbm", table_ms),
+                             table_kernels_us=round(table_ms * 1e3, 3),
+                             sort_us_per_call=round(us["sort"], 3),
+                             apply_us_per_call=round(us["scatter"], 3),
+                             fixup_us_per_call=round(us["segfix"], 3),
+                             avg_call_us=round(call_ms * 1e3, 3), bytes_per_call=gbytes,
+                             workload=f"{sw.N} rows Zipf({sw.zipf_s}) into {sw.rows}x{sw.d} {dt}, "
+                                      f"{'int64' if ix.dtype == torch.int64 else 'int32'} ids")
         if ctx.status() != pg.OK:
             raise RuntimeError("device error flag raised in the kernel measurements")
     finally:

@@ -8,8 +8,10 @@
 // order of the entries (the radix sort of the step, stable by entry): inc
 // accumulates each row's entries in float32 in entry order and rounds the
 // row to the storage format once, so a row never loses small increments to
-// per-entry rounding; set copies, for each row, the entry that ends its
-// sorted segment.  Results do not depend on scheduling.
+// per-entry rounding (a segment that crosses chunks is finished by the
+// float32 fix-up, k_segfix, through this format's row access); set copies,
+// for each row, the entry that ends its sorted segment.  Results do not
+// depend on scheduling.
 #pragma once
 #include "common.h"
 #include "launch.h"
@@ -73,6 +75,8 @@ struct GenArgs {
   int N, d, ch, seg_stride;
   float alpha;
   ZeroRanges zero;          // sort counters cleared by the apply launch
+  // a row update is a load and a store: deferred past the walk (seg_add_rows)
+  static constexpr bool kDeferred = true;
 };
 
 template <class T>
@@ -83,6 +87,34 @@ __device__ __forceinline__ float seg_load(const GenArgs<T>& a, size_t i) {
 template <class T>
 __device__ __forceinline__ void seg_add(const GenArgs<T>& a, size_t i, bool cok, float v) {
   if (cok) a.table[i] = Elem<T>::put(Elem<T>::get(a.table[i]) + v);
+}
+
+// The completed pieces of a chunk, after its walk: v[r] holds the sum of the
+// piece ending at row r for every bit r of `complete`.  Rows are updated 16
+// at a time with their 16 loads in flight together, so a chunk of many short
+// pieces (the Zipf tail) waits for four round trips, not one per piece.
+// (Reading all of a chunk's rows before the walk, beside the entries, needs
+// 64 more registers per lane and measured slower for the lost occupancy.)
+template <int CH, class T>
+__device__ void seg_add_rows(const GenArgs<T>& a, const ChunkInfo& ci, uint64_t complete,
+                             const float (&v)[CH], int colc, bool cok) {
+  constexpr int RB = 16;
+#pragma unroll
+  for (int r0 = 0; r0 < CH; r0 += RB) {
+    uint32_t cw = (uint32_t)(complete >> r0) & ((1u << RB) - 1u);
+    asm volatile("" : "+s"(cw));
+    if (cw == 0u) continue;
+    T old[RB];
+#pragma unroll
+    for (int u = 0; u < RB; ++u)
+      if ((cw >> u) & 1u)
+        old[u] = a.table[(size_t)__builtin_amdgcn_readlane(ci.key, r0 + u) * a.d + colc];
+#pragma unroll
+    for (int u = 0; u < RB; ++u)
+      if (((cw >> u) & 1u) && cok)
+        a.table[(size_t)__builtin_amdgcn_readlane(ci.key, r0 + u) * a.d + colc] =
+            Elem<T>::put(Elem<T>::get(old[u]) + v[r0 + u]);
+  }
 }
 
 // Increment: one wave per chunk of CH sorted entries (seg_apply_rows), the
@@ -100,100 +132,29 @@ __global__ __launch_bounds__(kBlock) void k_gen_apply(GenArgs<T> a, int n_e) {
               (size_t)(gridDim.x - n_e) * kBlock);
 }
 
-// Fix-up of crossing segments (as k_segfix): light segments (at most
-// kSegfixLight partials) by one wave, lane = column, partials added in
-// chunk order; heavy ones by the whole workgroup, wave v adding a contiguous
-// run of the partials in order and wave 0 adding the eight run sums in order.
+// Row access of the fix-up (seg_fix_row_wave / seg_fix_row, launched as
+// k_segfix<GenArgs<T>>): four consecutive columns at element i, n of them
+// inside the row, converted to and from float.  The fix-up is the row's only
+// writer.
 template <class T>
-__device__ int gen_fix_row_wave(const GenArgs<T>& a, int cs, int32_t key, int nchunks) {
-  const int lane = lane_id();
-  const int m = __builtin_amdgcn_readfirstlane(a.seg_end[key]) - cs + 1;
-  if (m > kSegfixLight) return m;
-  for (int c0 = 0; c0 < a.d; c0 += kWave) {
-    const int col = c0 + lane;
-    const bool cok = col < a.d;
-    float x[kSegfixLight];
+__device__ __forceinline__ f4 seg_row4(const GenArgs<T>& a, size_t i, int n) {
+  f4 r = kZero4;
 #pragma unroll
-    for (int i = 0; i < kSegfixLight; ++i) {
-      const size_t slot = i == 0 ? (size_t)cs * 2 + 1 : (size_t)(cs + i) * 2;
-      x[i] = (i < m && cs + i < nchunks && cok) ? a.seg_part[slot * a.seg_stride + col] : 0.f;
-    }
-    float acc = 0.f;
-#pragma unroll
-    for (int i = 0; i < kSegfixLight; ++i) acc += x[i];
-    seg_add(a, (size_t)key * a.d + col, cok, a.alpha * acc);
-  }
-  return m;
+  for (int k = 0; k < 4; ++k)
+    if (k < n) r[k] = Elem<T>::get(a.table[i + k]);
+  return r;
 }
-
 template <class T>
-__device__ void gen_fix_row(const GenArgs<T>& a, int cs, int32_t key, int m, float* red) {
-  const int t = threadIdx.x, lane = t & (kWave - 1);
-  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
-  const int per = ceil_div(m, kSegfixWaves);
-  const int i0 = w * per, i1 = min(m, i0 + per);
-  constexpr int U = 8;
-  for (int c0 = 0; c0 < a.d; c0 += kWave) {
-    const int col = c0 + lane;
-    const bool cok = col < a.d;
-    float acc = 0.f;
-    for (int i = i0; i < i1; i += U) {
-      float x[U];
+__device__ __forceinline__ void seg_put4(const GenArgs<T>& a, size_t i, int n, f4 v) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int j = i + u;
-        const size_t slot = j == 0 ? (size_t)cs * 2 + 1 : (size_t)(cs + j) * 2;
-        x[u] = (j < i1 && cok) ? a.seg_part[slot * a.seg_stride + col] : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) acc += x[u];
-    }
-    __syncthreads();  // red of the previous column block is no longer read
-    red[w * kWave + lane] = acc;
-    __syncthreads();
-    if (w == 0) {
-      float s = 0.f;
-      for (int v = 0; v < kSegfixWaves; ++v) s += red[v * kWave + lane];
-      seg_add(a, (size_t)key * a.d + col, cok, a.alpha * s);
-    }
-  }
-}
-
-template <class T>
-__global__ __launch_bounds__(kSegfixThreads) void k_gen_segfix(GenArgs<T> a) {
-  __shared__ float red[kSegfixWaves * kWave];
-  __shared__ int heavy[kSegfixWaves][3];
-  __shared__ int nheavy;
-  if (*a.flag) return;
-  const uint32_t cnt = (uint32_t)((a.N + a.ch - 1) / a.ch);
-  const int t = threadIdx.x, lane = t & (kWave - 1);
-  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
-  for (uint32_t base = 0; base + blockIdx.x < cnt; base += gridDim.x * kSegfixWaves) {
-    if (t == 0) nheavy = 0;
-    __syncthreads();
-    const uint32_t li = base + (uint32_t)w * gridDim.x + blockIdx.x;
-    if (li < cnt) {
-      const int2 rec = a.long_list[li];
-      if (rec.x >= 0) {
-        const int m = gen_fix_row_wave(a, rec.x, rec.y, (int)cnt);
-        if (m > kSegfixLight && lane == 0) {
-          const int h = atomicAdd(&nheavy, 1);
-          heavy[h][0] = rec.x;
-          heavy[h][1] = rec.y;
-          heavy[h][2] = m;
-        }
-      }
-    }
-    __syncthreads();
-    const int nh = nheavy;
-    for (int h = 0; h < nh; ++h) gen_fix_row(a, heavy[h][0], heavy[h][1], heavy[h][2], red);
-    __syncthreads();
-  }
+  for (int k = 0; k < 4; ++k)
+    if (k < n) a.table[i + k] = Elem<T>::put(v[k]);
 }
 
 // Assignment: one wave per 64 sorted entries; an entry whose successor has
 // another key (or that is the last) ends its row's segment, so it is the
-// row's last entry in index order, and its Y row is copied (lane = column).
+// row's last entry in index order, and its Y row is copied (lane = column),
+// 16 rows at a time.
 // The extra workgroups clear the sort counters.
 template <class T>
 __global__ __launch_bounds__(kBlock) void k_gen_set(GenArgs<T> a, int n_e) {
@@ -206,6 +167,7 @@ __global__ __launch_bounds__(kBlock) void k_gen_set(GenArgs<T> a, int n_e) {
   }
   if (__builtin_amdgcn_readfirstlane(*a.flag) != 0u) return;
   const int ngroups = ceil_div(a.N, kWave);
+  constexpr int RB = 16;  // rows copied together, their loads in flight at once
   for (int gi = blockIdx.x * kWavesPerBlock + w; gi < ngroups; gi += n_e * kWavesPerBlock) {
     const int i = gi * kWave + lane;
     const bool act = i < a.N;
@@ -214,13 +176,29 @@ __global__ __launch_bounds__(kBlock) void k_gen_set(GenArgs<T> a, int n_e) {
     const int32_t ent = act ? a.sv[i] : 0;
     uint64_t tails = __ballot(act && key != nxt);
     while (tails) {
-      const int src = __ffsll((unsigned long long)tails) - 1;
-      tails &= tails - 1;
-      const int32_t k = __builtin_amdgcn_readlane(key, src);
-      const int32_t e = __builtin_amdgcn_readlane(ent, src);
+      int src[RB];
+      int n = 0;
+#pragma unroll
+      for (int j = 0; j < RB; ++j) {
+        src[j] = 0;
+        if (tails) {
+          src[j] = __ffsll((unsigned long long)tails) - 1;
+          tails &= tails - 1;
+          n = j + 1;
+        }
+      }
       for (int c0 = 0; c0 < a.d; c0 += kWave) {
         const int col = c0 + lane;
-        if (col < a.d) a.table[(size_t)k * a.d + col] = a.Y[(size_t)e * a.d + col];
+        const bool cok = col < a.d;
+        T v[RB];
+#pragma unroll
+        for (int j = 0; j < RB; ++j)
+          if (j < n && cok)
+            v[j] = a.Y[(size_t)__builtin_amdgcn_readlane(ent, src[j]) * a.d + col];
+#pragma unroll
+        for (int j = 0; j < RB; ++j)
+          if (j < n && cok)
+            a.table[(size_t)__builtin_amdgcn_readlane(key, src[j]) * a.d + col] = v[j];
       }
     }
   }

@@ -190,7 +190,7 @@ hipError_t launch_apply_part(const ApplyArgs& a, int grid, const Launch& L) {
 }
 
 hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L) {
-  return pg_launch(k_segfix, dim3(grid), dim3(kSegfixThreads), 0, L, a);
+  return pg_launch(k_segfix<SegArgs>, dim3(grid), dim3(kSegfixThreads), 0, L, a);
 }
 
 template <class T>
@@ -229,10 +229,13 @@ hipError_t launch_gen_update(const GenCall& c, const Launch& L) {
 
 hipError_t launch_gen_fix(const GenCall& c, int grid, const Launch& L) {
   if (c.dtype == 1)
-    return pg_launch(k_gen_segfix<BF16>, dim3(grid), dim3(kSegfixThreads), 0, L, gen_args<BF16>(c));
+    return pg_launch(k_segfix<GenArgs<BF16>>, dim3(grid), dim3(kSegfixThreads), 0, L,
+                     gen_args<BF16>(c));
   if (c.dtype == 2)
-    return pg_launch(k_gen_segfix<F16>, dim3(grid), dim3(kSegfixThreads), 0, L, gen_args<F16>(c));
-  return pg_launch(k_gen_segfix<float>, dim3(grid), dim3(kSegfixThreads), 0, L, gen_args<float>(c));
+    return pg_launch(k_segfix<GenArgs<F16>>, dim3(grid), dim3(kSegfixThreads), 0, L,
+                     gen_args<F16>(c));
+  return pg_launch(k_segfix<GenArgs<float>>, dim3(grid), dim3(kSegfixThreads), 0, L,
+                   gen_args<float>(c));
 }
 
 hipError_t launch_keys_from_i64(const int64_t* idx, int N, int rows, int32_t* keys,

@@ -40,6 +40,8 @@ struct SegArgs {
   const uint32_t* flag;     // sticky error bits: nonzero voids the update
   int N, d, ch, seg_stride;
   float alpha;
+  // completed pieces are added as they close (float atomics), not deferred
+  static constexpr bool kDeferred = false;
 };
 
 // Piece structure of one chunk, computed by the whole wave (lanes < ch).
@@ -158,7 +160,9 @@ __device__ void seg_apply_rows(const A& a, int i0, int end, int chunk, const Chu
       v[r] = seg_load(a, (size_t)ent * a.d + colc);
     }
     // running sum in entry order, closed at every piece end (tail);
-    // completed pieces go straight to their rows
+    // completed pieces go straight to their rows, or (argument sets whose
+    // row update is a load and a store) replace their tail row's value and
+    // are applied after the walk
     const float alpha = cok ? a.alpha : 0.f;
     float acc = 0.f, first_sum = 0.f, last_sum = 0.f;
 #pragma unroll
@@ -180,14 +184,19 @@ __device__ void seg_apply_rows(const A& a, int i0, int end, int chunk, const Chu
             if (u == ft) first_sum = acc;
             if (u == lt) last_sum = acc;
             if ((cw >> u) & 1u) {
-              const int32_t key = __builtin_amdgcn_readlane(ci.key, r0 + u);
-              seg_add(a, (size_t)key * a.d + colc, cok, alpha * acc);
+              if constexpr (A::kDeferred) {
+                v[r0 + u] = alpha * acc;
+              } else {
+                const int32_t key = __builtin_amdgcn_readlane(ci.key, r0 + u);
+                seg_add(a, (size_t)key * a.d + colc, cok, alpha * acc);
+              }
             }
             acc = 0.f;
           }
         }
       }
     }
+    if constexpr (A::kDeferred) seg_add_rows<CH>(a, ci, complete, v, colc, cok);
     if (cok) {
       if (LOCAL) {
         if (ci.cont_first) sink.first[col] = first_sum;
@@ -289,6 +298,16 @@ constexpr int kSegfixWaves = kSegfixThreads / kWave;
 constexpr int kSegfixUnroll = 16;
 constexpr int kSegfixLight = 16;
 
+// Row access of the fix-up, four consecutive columns at element i of the
+// table (n of them inside the row; the float32 table has d % 4 == 0 and
+// aligned rows, so n is 4 or 0): read as floats, written back.
+__device__ __forceinline__ f4 seg_row4(const SegArgs& a, size_t i, int n) {
+  return n > 0 ? ld4(a.table + i) : kZero4;
+}
+__device__ __forceinline__ void seg_put4(const SegArgs& a, size_t i, int n, f4 v) {
+  if (n > 0) st4(a.table + i, v);
+}
+
 // One wave finishes crossing segment (cs, key) when it has at most
 // kSegfixLight partials, m = seg_end[key] - cs + 1, and returns m; a heavier
 // segment is left alone (the caller hands it to the whole workgroup).  The
@@ -296,15 +315,19 @@ constexpr int kSegfixLight = 16;
 // together with seg_end, then masked by m, so the segment costs one round of
 // loads after its slot.  Lane group gq = lane/16 sums partials gq, gq+4, ...
 // in order (each lane four consecutive columns), and the four group sums are
-// combined by a fixed butterfly.
-__device__ int seg_fix_row_wave(const SegArgs& a, int cs, int32_t key, int nchunks) {
+// combined by a fixed butterfly.  Partial rows are read four columns at a
+// time up to the next multiple of 4 (inside the partial slot's stride); the
+// row access masks the columns past d.
+template <class A>
+__device__ int seg_fix_row_wave(const A& a, int cs, int32_t key, int nchunks) {
   const int lane = lane_id(), q = lane & 15, gq = lane >> 4;
   const int ce = a.seg_end[key];
   for (int c0 = 0; c0 < a.d; c0 += 64) {
     const int col = c0 + 4 * q;
     const bool cok = col < a.d;
-    float* tr = a.table + (size_t)key * a.d + col;
-    const f4 row = (gq == 0 && cok) ? ld4(tr) : kZero4;
+    const size_t tr = (size_t)key * a.d + col;
+    const int nrow = (gq == 0 && cok) ? min(4, a.d - col) : 0;
+    const f4 row = seg_row4(a, tr, nrow);
     f4 x[kSegfixLight / 4];
 #pragma unroll
     for (int u = 0; u < kSegfixLight / 4; ++u) {
@@ -323,7 +346,7 @@ __device__ int seg_fix_row_wave(const SegArgs& a, int cs, int32_t key, int nchun
       acc[k] += __shfl_xor(acc[k], 16);
       acc[k] += __shfl_xor(acc[k], 32);
     }
-    if (gq == 0 && cok) st4(tr, row + a.alpha * acc);
+    seg_put4(a, tr, nrow, row + a.alpha * acc);
   }
   return __builtin_amdgcn_readfirstlane(ce) - cs + 1;
 }
@@ -334,7 +357,8 @@ __device__ int seg_fix_row_wave(const SegArgs& a, int cs, int32_t key, int nchun
 // chunk, i >= 1 the first piece of chunk cs+i), each lane four consecutive
 // columns; group sums are combined by a fixed butterfly and the wave sums in
 // wave order, so the result is independent of scheduling.
-__device__ void seg_fix_row(const SegArgs& a, int cs, int32_t key, int m,
+template <class A>
+__device__ void seg_fix_row(const A& a, int cs, int32_t key, int m,
                             float* red /* [waves][kMaxD] */) {
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -343,9 +367,10 @@ __device__ void seg_fix_row(const SegArgs& a, int cs, int32_t key, int m,
   for (int c0 = 0; c0 < a.d; c0 += 64) {
     const int col = c0 + 4 * q;
     const bool cok = col < a.d;
-    float* tr = a.table + (size_t)key * a.d + col;
+    const size_t tr = (size_t)key * a.d + col;
     const bool owner = w == 0 && gq == 0 && cok;
-    const f4 row = owner ? ld4(tr) : kZero4;  // in flight beside the partials
+    const int nrow = owner ? min(4, a.d - col) : 0;
+    const f4 row = seg_row4(a, tr, nrow);  // in flight beside the partials
     f4 acc = kZero4;
     for (int base = 0; base < m; base += G * kSegfixUnroll) {
       f4 x[kSegfixUnroll];
@@ -370,7 +395,7 @@ __device__ void seg_fix_row(const SegArgs& a, int cs, int32_t key, int m,
       f4 s = ld4(red + 4 * q);
 #pragma unroll
       for (int v = 1; v < kSegfixWaves; ++v) s += ld4(red + v * kMaxD + 4 * q);
-      st4(tr, row + a.alpha * s);
+      seg_put4(a, tr, nrow, row + a.alpha * s);
     }
   }
 }

@@ -130,7 +130,8 @@ __global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
 // by its wave, a heavy one is listed and then summed by the whole workgroup.
 // Every row is a different segment's, so the order in which heavy ones are
 // taken does not matter.
-__global__ __launch_bounds__(kSegfixThreads) void k_segfix(SegArgs a) {
+template <class A>
+__global__ __launch_bounds__(kSegfixThreads) void k_segfix(A a) {
   __shared__ float red[kSegfixWaves * kMaxD];
   __shared__ int heavy[kSegfixWaves][3];  // (start chunk, row, partials)
   __shared__ int nheavy;
