@@ -329,7 +329,7 @@ def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
             ctx.set_timing(False)
             us = {k: kt.get(k, (0.0, 0))[0] / reps * 1e3 for k in ("sort", "scatter", "segfix")}
             table_ms = (us["scatter"] + us["segfix"]) * 1e-3
-            out[name] = dict(roofline(gbytes, 0, "hbm", table_ms),
+            out[name] = dict(roofline(gbytes, 0, "hbm", table_ms), traffic=counter_traffic("kernels", name),
                              table_kernels_us=round(table_ms * 1e3, 3),
                              sort_us_per_call=round(us["sort"], 3),
                              apply_us_per_call=round(us["scatter"], 3),
