@@ -718,3 +718,37 @@ def test_scatter_update_rejects_unsupported_combinations():
         ctx.scatter_update(tf, idx, Yf, 1.0, m.OP_SET, m.SCATTER_ATOMIC)
     ctx.scatter_update(tf, idx, Yf, 1.0, m.OP_INC, m.SCATTER_ATOMIC)
     assert ctx.status() == m.OK
+
+
+def test_scatter_update_host_validation_enqueues_nothing():
+    """Bad storage format, index width, row width, op, mode, N, and
+    misaligned pointers are refused on the host (EINVAL / EBATCH / ENULL)
+    and leave the table untouched."""
+    m = pg()
+    lib = m.load_library()
+    ctx = m.Context(1000, 16, 5, 8, max_batch=1, max_scatter=8, max_rows=10)
+    t = torch.zeros(10 * 8 + 1, dtype=torch.float16, device="cuda")
+    Y = torch.ones(8 * 8 + 1, dtype=torch.float16, device="cuda")
+    idx = torch.zeros(9, dtype=torch.int64, device="cuda")
+    tp, yp, ip = t.data_ptr(), Y.data_ptr(), idx.data_ptr()
+    good = dict(table=tp, dtype=m.F16, rows=10, d=8, idx=ip, idx_bytes=8, Y=yp, N=8, alpha=1.0,
+                op=m.OP_INC, mode=m.SCATTER_SORTED)
+    bad = [({"dtype": 3}, m.EINVAL), ({"idx_bytes": 2}, m.EINVAL), ({"d": 0}, m.EINVAL),
+           ({"d": 257}, m.EINVAL), ({"rows": 11}, m.EINVAL), ({"op": 2}, m.EINVAL),
+           ({"mode": 2}, m.EINVAL), ({"N": 9}, m.EBATCH), ({"N": 0}, m.EBATCH),
+           ({"table": tp + 1}, m.EINVAL), ({"Y": yp + 1}, m.EINVAL), ({"idx": ip + 4}, m.EINVAL),
+           ({"alpha": float("inf")}, m.EINVAL), ({"table": None}, m.ENULL),
+           ({"mode": m.SCATTER_ATOMIC}, m.EINVAL)]
+    for change, code in bad:
+        a = dict(good, **change)
+        rc = lib.polyglot_scatter_update(ctx._h, a["table"], a["dtype"], a["rows"], a["d"], a["idx"],
+                                         a["idx_bytes"], a["Y"], a["N"], a["alpha"], a["op"],
+                                         a["mode"])
+        assert rc == code, (change, rc)
+    assert ctx.status() == m.OK
+    assert torch.count_nonzero(t).item() == 0
+    # the same arguments unchanged are accepted
+    rc = lib.polyglot_scatter_update(ctx._h, tp, m.F16, 10, 8, ip, 8, yp, 8, 1.0, m.OP_INC,
+                                     m.SCATTER_SORTED)
+    assert rc == m.OK and ctx.status() == m.OK
+    assert torch.count_nonzero(t).item() == 8
