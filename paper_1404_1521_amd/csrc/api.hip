@@ -503,9 +503,11 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   ctx->max_tiles = std::max(ceil_div(std::min(ctx->max_entries, kShortTileLimit), kSortTileKeysShort),
                             ceil_div(ctx->max_entries, kSortTileKeys));
   ctx->max_parts = std::min(ceil_div(c.max_batch, kTileRows), 512);
-  // most chunks any call can cut (short chunks apply up to 131072 entries)
-  ctx->max_chunks = std::max(ceil_div(std::min(ctx->max_entries, 131072), 16),
-                             ceil_div(ctx->max_entries, seg_chunk_size(ctx->max_entries)));
+  // most chunks any call can cut (short chunks apply up to 131072 entries;
+  // the general op cuts longer lists into gen_chunk_size chunks)
+  ctx->max_chunks = std::max({ceil_div(std::min(ctx->max_entries, 131072), 16),
+                              ceil_div(ctx->max_entries, seg_chunk_size(ctx->max_entries)),
+                              ceil_div(c.max_scatter, gen_chunk_size(c.max_scatter))});
   ctx->seg_stride = std::max(c.d, c.max_scatter > 0 ? kMaxD : 0);
   ctx->part_stride = ctx->Hp * ctx->K + 2 * ctx->Hp + 2;
 
@@ -760,7 +762,7 @@ int polyglot_scatter_update(polyglot_ctx* ctx, void* table, int32_t dtype, int32
   c.flag = ctx->ws.flag;
   c.N = N;
   c.d = d;
-  c.ch = seg_chunk_size(N);
+  c.ch = gen_chunk_size(N);
   c.seg_stride = ctx->seg_stride;
   c.alpha = alpha;
   c.zero = sort_zero_ranges(ctx, plan, 0);

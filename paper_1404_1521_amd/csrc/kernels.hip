@@ -218,7 +218,7 @@ static hipError_t launch_gen_update_t(const GenCall& c, const Launch& L) {
   const dim3 grid(c.n_e + c.n_z), block(kBlock);
   if (c.op == 1) return pg_launch(k_gen_set<T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
   if (c.ch == 16) return pg_launch(k_gen_apply<16, T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
-  return pg_launch(k_gen_apply<64, T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
+  return pg_launch(k_gen_apply<32, T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
 }
 
 hipError_t launch_gen_update(const GenCall& c, const Launch& L) {

@@ -89,6 +89,11 @@ __device__ __forceinline__ ChunkInfo chunk_info(const int32_t* __restrict__ sk,
 // Chunk size of a sorted list of N entries: short chunks spread small
 // batches over more waves; long chunks keep partials few for large ones.
 __host__ __device__ inline int seg_chunk_size(int N) { return N <= 131072 ? 16 : 64; }
+// The general op's typed increments defer their row updates past the walk
+// (a load and a store per row, 16 rows per round of loads), so shorter
+// chunks on long lists pay off there: fewer rounds and more resident waves
+// (bfloat16, 327,680 entries: apply 27 -> 16 us, fix-up 8.6 -> 11.5 us).
+__host__ __device__ inline int gen_chunk_size(int N) { return N <= 131072 ? 16 : 32; }
 
 // Where a chunk's open pieces go: GLOBAL, the chunk-indexed partials and the
 // chunk's slot of the fix-up launch's segment list; LOCAL, a wave's slots in LDS (first piece,
