@@ -440,6 +440,17 @@ def main():
         ms = e0.elapsed_time(e1)
         if ctx.status() != pg.OK:
             raise RuntimeError("device error flag raised during the benchmark")
+        # spread: the same K steps replayed five more times, each timed alone
+        # (value above is the first timed replay)
+        reps = []
+        for _ in range(5):
+            e0.record(stream)
+            run(Wm, Wm + K)
+            e1.record(stream)
+            e1.synchronize()
+            reps.append(e0.elapsed_time(e1) / K)
+        if ctx.status() != pg.OK:
+            raise RuntimeError("device error flag raised during the repeats")
 
         # per-kernel durations: K more steps, one call each, HIP events around
         # every launch on the library stream
@@ -525,6 +536,8 @@ def main():
                    "global_batch": B, "parallelism": "single-gpu",
                    "distinct_rows_per_step": round(st["U"], 1)},
         "roofline": roof,
+        "repeats": {"n": len(reps), "ms_per_step_mean": round(float(np.mean(reps)), 5),
+                    "ms_per_step_std": round(float(np.std(reps, ddof=1)), 5)},
         "wall_s": round(wall, 4),
     }
     if kern is not None:
