@@ -23,7 +23,8 @@
 //             16 columns) round-robin over the waves.
 // W1 is staged once per workgroup in LDS (row stride K + 4 floats, rows
 // >= H zero) and read from there as the B operand of the forward and of G.
-// A tile takes three workgroup barriers: X staged, forward partials, V.
+// A tile takes two workgroup barriers: the tiles are software-pipelined so
+// that dW1 and G of one tile share a phase with the forward of the next.
 #pragma once
 #include "common.h"
 #include "launch.h"
@@ -153,18 +154,8 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   for (int ci = 0; ci < CPW; ++ci) accW[ci] = kZero4;
   float db1a = 0.f, dw2a = 0.f, lossa = 0.f;
 
-  for (int tt = 0; tt < ntl; ++tt) {
-    const int tile = tile0 + tt;
-    const int row0 = tile * kTileRows;
-    const int buf = tt & 1;
-    const float* X = xl + buf * Sh::kX;
-    store_x(buf, xr);
-    __syncthreads();  // X of this tile (and W1) staged
-    if (tt + 1 < ntl) {
-      load_x(ids[(tt + 1) & 1], xr);                           // rows of the next tile
-      if (tt + 2 < ntl) load_ids(tile + 2, ids[tt & 1]);       // ids two tiles ahead
-    }
-
+  // ---- forward of the tile in X: split-K partials into zp
+  auto forward = [&](const float* X) {
     // ---- forward: wave (nt_w, kq) over chunks kc = kq + KW ci; common
     // blocks, true centre and corrupt centre accumulate separately
     f4 zc = kZero4, zctr = kZero4, zcor = kZero4;
@@ -196,8 +187,10 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       zp[(((kq * 3 + 1) * NT + nt_w) * 4 + i) * kWave + lane] = zctr[i];
       zp[(((kq * 3 + 2) * NT + nt_w) * 4 + i) * kWave + lane] = zcor[i];
     }
-    __syncthreads();  // forward partials written
-
+  };
+  // ---- epilogue of the tile starting at row0: zp -> V (vt) and the
+  // accumulators
+  auto epilogue = [&](int row0) {
     // ---- epilogue: lane (hn, rsel) of wave w < 8 takes hidden unit hn of
     // row 2w + rsel
     if (w < kTileRows / 2) {
@@ -241,8 +234,9 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       dw2a -= gst * hmh;  // -(m/B) h + (m/B) h~
       if (hn == 0) lossa += on ? mg : 0.f;
     }
-    __syncthreads();  // V written
-
+  };
+  // ---- dW1 and G of the tile in X starting at row0 (reads vt)
+  auto backward = [&](const float* X, int row0) {
     // ---- dW1 += V^T X for this wave's (nt, chunks).  A operand: lane (n16,
     // g) holds V[4ii+g][nt*16 + n16]; B operand: X[4ii+g][16kc + n16].
     {
@@ -296,6 +290,36 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
         }
       }
     }
+  };
+
+  // Software pipeline, two barriers per tile: the epilogue of tile t runs
+  // beside the staging of tile t+1's rows (into the other X buffer), then
+  // dW1 and G of tile t run in one phase with the forward of tile t+1.
+  // Between a buffer's last reader and its next writer there is always a
+  // barrier: zp (forward t+1 after the epilogue of t), vt (epilogue t+1
+  // after dW1/G of t), X[t&1] (rows of t+2 after dW1 of t).
+  store_x(0, xr);
+  if (ntl > 1) {
+    load_x(ids[1], xr);                                  // rows of tile 1
+    if (ntl > 2) load_ids(tile0 + 2, ids[0]);            // ids of tile 2
+  }
+  __syncthreads();  // X of tile 0 and W1 staged
+  forward(xl);
+  __syncthreads();  // forward partials of tile 0 written
+  for (int tt = 0; tt < ntl; ++tt) {
+    const int row0 = (tile0 + tt) * kTileRows;
+    epilogue(row0);
+    if (tt + 1 < ntl) {
+      store_x((tt + 1) & 1, xr);                         // rows of tile tt+1
+      if (tt + 2 < ntl) {
+        load_x(ids[tt & 1], xr);                         // rows of tile tt+2
+        if (tt + 3 < ntl) load_ids(tile0 + tt + 3, ids[(tt + 1) & 1]);
+      }
+    }
+    __syncthreads();  // V of tile tt and X of tile tt+1 written
+    backward(xl + (tt & 1) * Sh::kX, row0);
+    if (tt + 1 < ntl) forward(xl + ((tt + 1) & 1) * Sh::kX);
+    __syncthreads();  // forward partials of tile tt+1 written; vt, X[tt&1] free
   }
 
   // ---- this workgroup's partial of the dense gradients (streaming stores,
