@@ -53,7 +53,12 @@ struct F8Shape {
   static constexpr int S = K + 4;            // W1 row stride in LDS
   // LDS, in floats
   static constexpr int kW1 = HP * S;
-  static constexpr int kX = XF4 * 4;                       // one X buffer
+  // one X buffer: [position][column quad] blocks of 16 windows x 4 floats,
+  // each padded to 72 floats (8 mod 32 banks), so the dW1 operand read, whose
+  // four lane groups take four column quads of one window, hits 32 distinct
+  // banks per half-wave
+  static constexpr int kXq = 4 * kTileRows + 8;
+  static constexpr int kX = W1P * QD * kXq;
   static constexpr int kZp = kF8Waves * 3 * 4 * kWave;     // forward split-K partials
   static constexpr int kVt = 3 * kTileRows * (HP + 1);
   static constexpr int kRed = kF8Waves * (2 * HP + 2);
@@ -116,7 +121,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
 #pragma unroll
     for (int p = 0; p < XPT; ++p) {
       const int pi = t + kF8Threads * p;
-      if (pi < XF4) st4(xl + buf * Sh::kX + 4 * pi, xr[p]);
+      if (pi < XF4) st4(xl + buf * Sh::kX + (pi / kTileRows) * Sh::kXq + 4 * (pi % kTileRows), xr[p]);
     }
   };
 
@@ -164,13 +169,13 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       const int kc = kq + KW * ci;
       if (kc < NCH) {
         const int j = kc / DQ, qq = 4 * (kc % DQ) + g;
-        const f4 xa = ld4(X + 4 * ((j * QD + qq) * kTileRows + n16));
+        const f4 xa = ld4(X + (j * QD + qq) * Sh::kXq + 4 * n16);
         const f4 wb = ld4(w1s + (nt_w * 16 + n16) * S + kc * 16 + 4 * g);
         if (j != C) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) zc = mfma16x4(xa[q], wb[q], zc);
         } else {
-          const f4 xt = ld4(X + 4 * ((WIN * QD + qq) * kTileRows + n16));
+          const f4 xt = ld4(X + (WIN * QD + qq) * Sh::kXq + 4 * n16);
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             zctr = mfma16x4(xa[q], wb[q], zctr);
@@ -253,11 +258,11 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
           const int j = kc / DQ, qq = 4 * (kc % DQ) + (n16 >> 2);
 #pragma unroll
           for (int ii = 0; ii < 4; ++ii) {
-            const float xb = X[4 * ((j * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
+            const float xb = X[(j * QD + qq) * Sh::kXq + 4 * (4 * ii + g) + (n16 & 3)];
             if (j != C) {
               accW[ci] = mfma16x4(vc[0][ii], xb, accW[ci]);
             } else {
-              const float xc = X[4 * ((WIN * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
+              const float xc = X[(WIN * QD + qq) * Sh::kXq + 4 * (4 * ii + g) + (n16 & 3)];
               accW[ci] = mfma16x4(vc[1][ii], xb, accW[ci]);
               accW[ci] = mfma16x4(vc[2][ii], xc, accW[ci]);
             }
