@@ -23,8 +23,9 @@
 //             16 columns) round-robin over the waves.
 // W1 is staged once per workgroup in LDS (row stride K + 4 floats, rows
 // >= H zero) and read from there as the B operand of the forward and of G.
-// A tile takes two workgroup barriers: the tiles are software-pipelined so
-// that dW1 and G of one tile share a phase with the forward of the next.
+// A workgroup with several tiles takes two barriers per tile: the tiles are
+// software-pipelined so that dW1 and G of one tile share a phase with the
+// forward of the next (a single tile takes three, in a plain sequence).
 #pragma once
 #include "common.h"
 #include "launch.h"
@@ -53,12 +54,7 @@ struct F8Shape {
   static constexpr int S = K + 4;            // W1 row stride in LDS
   // LDS, in floats
   static constexpr int kW1 = HP * S;
-  // one X buffer: [position][column quad] blocks of 16 windows x 4 floats,
-  // each padded to 72 floats (8 mod 32 banks), so the dW1 operand read, whose
-  // four lane groups take four column quads of one window, hits 32 distinct
-  // banks per half-wave
-  static constexpr int kXq = 4 * kTileRows + 8;
-  static constexpr int kX = W1P * QD * kXq;
+  static constexpr int kX = XF4 * 4;                       // one X buffer
   static constexpr int kZp = kF8Waves * 3 * 4 * kWave;     // forward split-K partials
   static constexpr int kVt = 3 * kTileRows * (HP + 1);
   static constexpr int kRed = kF8Waves * (2 * HP + 2);
@@ -67,7 +63,7 @@ struct F8Shape {
   static_assert(HP <= 32, "one hidden unit per lane of each 32-lane row half");
 };
 
-template <int D, int WIN, int NT>
+template <int D, int WIN, int NT, bool PIPE>
 __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   using Sh = F8Shape<D, WIN, NT>;
   constexpr int HP = Sh::HP, K = Sh::K, C = Sh::C, W1P = Sh::W1P, DQ = Sh::DQ, QD = Sh::QD;
@@ -121,7 +117,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
 #pragma unroll
     for (int p = 0; p < XPT; ++p) {
       const int pi = t + kF8Threads * p;
-      if (pi < XF4) st4(xl + buf * Sh::kX + (pi / kTileRows) * Sh::kXq + 4 * (pi % kTileRows), xr[p]);
+      if (pi < XF4) st4(xl + buf * Sh::kX + 4 * pi, xr[p]);
     }
   };
 
@@ -159,6 +155,156 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   for (int ci = 0; ci < CPW; ++ci) accW[ci] = kZero4;
   float db1a = 0.f, dw2a = 0.f, lossa = 0.f;
 
+  if constexpr (!PIPE) {
+  // Tiles one after another, three barriers each (X staged, forward
+  // partials, V).  Used when a workgroup has a single tile: the pipelined
+  // form below measured 0.3 us slower there.
+  for (int tt = 0; tt < ntl; ++tt) {
+    const int tile = tile0 + tt;
+    const int row0 = tile * kTileRows;
+    const int buf = tt & 1;
+    const float* X = xl + buf * Sh::kX;
+    store_x(buf, xr);
+    __syncthreads();  // X of this tile (and W1) staged
+    if (tt + 1 < ntl) {
+      load_x(ids[(tt + 1) & 1], xr);                           // rows of the next tile
+      if (tt + 2 < ntl) load_ids(tile + 2, ids[tt & 1]);       // ids two tiles ahead
+    }
+
+    // ---- forward: wave (nt_w, kq) over chunks kc = kq + KW ci; common
+    // blocks, true centre and corrupt centre accumulate separately
+    f4 zc = kZero4, zctr = kZero4, zcor = kZero4;
+#pragma unroll
+    for (int ci = 0; ci < CPW; ++ci) {
+      const int kc = kq + KW * ci;
+      if (kc < NCH) {
+        const int j = kc / DQ, qq = 4 * (kc % DQ) + g;
+        const f4 xa = ld4(X + 4 * ((j * QD + qq) * kTileRows + n16));
+        const f4 wb = ld4(w1s + (nt_w * 16 + n16) * S + kc * 16 + 4 * g);
+        if (j != C) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) zc = mfma16x4(xa[q], wb[q], zc);
+        } else {
+          const f4 xt = ld4(X + 4 * ((WIN * QD + qq) * kTileRows + n16));
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            zctr = mfma16x4(xa[q], wb[q], zctr);
+            zcor = mfma16x4(xt[q], wb[q], zcor);
+          }
+        }
+      }
+    }
+    // partials [kq][type][nt][component][lane] (component-major: a reader of
+    // one component of every lane touches consecutive words)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      zp[(((kq * 3 + 0) * NT + nt_w) * 4 + i) * kWave + lane] = zc[i];
+      zp[(((kq * 3 + 1) * NT + nt_w) * 4 + i) * kWave + lane] = zctr[i];
+      zp[(((kq * 3 + 2) * NT + nt_w) * 4 + i) * kWave + lane] = zcor[i];
+    }
+    __syncthreads();  // forward partials written
+
+    // ---- epilogue: lane (hn, rsel) of wave w < 8 takes hidden unit hn of
+    // row 2w + rsel
+    if (w < kTileRows / 2) {
+      const int r = 2 * w + rsel;
+      const int row = row0 + r;
+      const int nt = hn >> 4, src = (hn & 15) + 16 * (r >> 2), comp = r & 3;
+      float Zc = 0.f, Zctr = 0.f, Zcor = 0.f;
+      if (hn < HP) {
+#pragma unroll
+        for (int v = 0; v < KW; ++v) {
+          Zc += zp[(((v * 3 + 0) * NT + nt) * 4 + comp) * kWave + src];
+          Zctr += zp[(((v * 3 + 1) * NT + nt) * 4 + comp) * kWave + src];
+          Zcor += zp[(((v * 3 + 2) * NT + nt) * 4 + comp) * kWave + src];
+        }
+      }
+      const float z = b1v + (Zc + Zctr);
+      const float zt = b1v + (Zc + Zcor);
+      const float h = tanh_fast(z), ht = tanh_fast(zt);
+      // h - h~ = tanh(z - z~) (1 - h h~), z - z~ = zctr - zcor without
+      // cancellation against the common part
+      const float hmh = tanh_fast(Zctr - Zcor) * (1.f - h * ht);
+      float ps = w2v * h, pst = w2v * ht;
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) {
+        ps += __shfl_xor(ps, o);
+        pst += __shfl_xor(pst, o);
+      }
+      const float mg = 1.f - (b2v + ps) + (b2v + pst);
+      const bool on = row < a.B && mg > 0.f;  // hinge active (derivative 0 at margin 0)
+      const float gst = on ? a.invB : 0.f;    // d loss/d s~ = m/B, d loss/d s = -m/B
+      const float gw = gst * w2v;
+      const float dz = -gw * (1.f - h * h);
+      const float dzt = gw * (1.f - ht * ht);
+      const float dsum = gw * hmh * (h + ht);  // dz + dz~ = g w2 (h - h~)(h + h~)
+      if (hn < HP) {
+        vt[(0 * kTileRows + r) * (HP + 1) + hn] = dsum;
+        vt[(1 * kTileRows + r) * (HP + 1) + hn] = dz;
+        vt[(2 * kTileRows + r) * (HP + 1) + hn] = dzt;
+      }
+      db1a += dsum;
+      dw2a -= gst * hmh;  // -(m/B) h + (m/B) h~
+      if (hn == 0) lossa += on ? mg : 0.f;
+    }
+    __syncthreads();  // V written
+
+    // ---- dW1 += V^T X for this wave's (nt, chunks).  A operand: lane (n16,
+    // g) holds V[4ii+g][nt*16 + n16]; B operand: X[4ii+g][16kc + n16].
+    {
+      float vc[3][4];
+#pragma unroll
+      for (int ty = 0; ty < 3; ++ty)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii)
+          vc[ty][ii] = vt[(ty * kTileRows + 4 * ii + g) * (HP + 1) + nt_w * 16 + n16];
+#pragma unroll
+      for (int ci = 0; ci < CPW; ++ci) {
+        const int kc = kq + KW * ci;
+        if (kc < NCH) {
+          const int j = kc / DQ, qq = 4 * (kc % DQ) + (n16 >> 2);
+#pragma unroll
+          for (int ii = 0; ii < 4; ++ii) {
+            const float xb = X[4 * ((j * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
+            if (j != C) {
+              accW[ci] = mfma16x4(vc[0][ii], xb, accW[ci]);
+            } else {
+              const float xc = X[4 * ((WIN * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
+              accW[ci] = mfma16x4(vc[1][ii], xb, accW[ci]);
+              accW[ci] = mfma16x4(vc[2][ii], xc, accW[ci]);
+            }
+          }
+        }
+      }
+    }
+
+    // ---- G: output tiles ot = w + 16u (position j = ot / DQ, columns cb*16).
+    // A operand: lane (r = n16, g) holds V_ty[r][4q + g]; B operand: lane
+    // (col = n16, g) holds W1[4q + g][jj*D + cb*16 + col].
+#pragma unroll
+    for (int u = 0; u < GPW; ++u) {
+      const int ot = w + kF8Waves * u;
+      if (ot < NGT) {
+        const int j = ot / DQ, cb = ot - (ot / DQ) * DQ;
+        const int ty = (j == WIN) ? 2 : (j == C ? 1 : 0);
+        const int jj = (j == WIN) ? C : j;
+        f4 acc = kZero4;
+#pragma unroll
+        for (int q = 0; q < HP / 4; ++q) {
+          const float av = vt[(ty * kTileRows + n16) * (HP + 1) + 4 * q + g];
+          const float bv = w1s[(4 * q + g) * S + jj * D + cb * 16 + n16];
+          acc = mfma16x4(av, bv, acc);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = row0 + 4 * g + i;
+          if (row < a.B) __builtin_nontemporal_store(acc[i], &a.G[((size_t)row * W1P + j) * D + cb * 16 + n16]);
+        }
+      }
+    }
+  }
+
+  } else {
   // ---- forward of the tile in X: split-K partials into zp
   auto forward = [&](const float* X) {
     // ---- forward: wave (nt_w, kq) over chunks kc = kq + KW ci; common
@@ -169,13 +315,13 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       const int kc = kq + KW * ci;
       if (kc < NCH) {
         const int j = kc / DQ, qq = 4 * (kc % DQ) + g;
-        const f4 xa = ld4(X + (j * QD + qq) * Sh::kXq + 4 * n16);
+        const f4 xa = ld4(X + 4 * ((j * QD + qq) * kTileRows + n16));
         const f4 wb = ld4(w1s + (nt_w * 16 + n16) * S + kc * 16 + 4 * g);
         if (j != C) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) zc = mfma16x4(xa[q], wb[q], zc);
         } else {
-          const f4 xt = ld4(X + (WIN * QD + qq) * Sh::kXq + 4 * n16);
+          const f4 xt = ld4(X + 4 * ((WIN * QD + qq) * kTileRows + n16));
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             zctr = mfma16x4(xa[q], wb[q], zctr);
@@ -258,11 +404,11 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
           const int j = kc / DQ, qq = 4 * (kc % DQ) + (n16 >> 2);
 #pragma unroll
           for (int ii = 0; ii < 4; ++ii) {
-            const float xb = X[(j * QD + qq) * Sh::kXq + 4 * (4 * ii + g) + (n16 & 3)];
+            const float xb = X[4 * ((j * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
             if (j != C) {
               accW[ci] = mfma16x4(vc[0][ii], xb, accW[ci]);
             } else {
-              const float xc = X[(WIN * QD + qq) * Sh::kXq + 4 * (4 * ii + g) + (n16 & 3)];
+              const float xc = X[4 * ((WIN * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
               accW[ci] = mfma16x4(vc[1][ii], xb, accW[ci]);
               accW[ci] = mfma16x4(vc[2][ii], xc, accW[ci]);
             }
@@ -323,8 +469,12 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
     }
     __syncthreads();  // V of tile tt and X of tile tt+1 written
     backward(xl + (tt & 1) * Sh::kX, row0);
-    if (tt + 1 < ntl) forward(xl + ((tt + 1) & 1) * Sh::kX);
-    __syncthreads();  // forward partials of tile tt+1 written; vt, X[tt&1] free
+    if (tt + 1 < ntl) {  // (uniform: every wave takes the same branch)
+      forward(xl + ((tt + 1) & 1) * Sh::kX);
+      __syncthreads();  // forward partials of tile tt+1 written; vt, X[tt&1] free
+    }
+  }
+
   }
 
   // ---- this workgroup's partial of the dense gradients (streaming stores,

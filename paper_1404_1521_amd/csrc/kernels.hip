@@ -61,9 +61,10 @@ __global__ __launch_bounds__(kBlock, (NT == 1 || (NT == 2 && CPW <= 5)) ? 2 : 1)
   fwdbwd_wg<NT, CPW, D, WIN>(a, blockIdx.x - a.n_sort, lds_f);
 }
 
-// The same step for the compile-time shapes, 16 waves per workgroup; the
-// sort role (small batches) runs in 512-thread workgroups.
-template <int D, int WIN, int NT>
+// The same step for the compile-time shapes, 16 waves per workgroup (the
+// sort role of small batches too); PIPE: software-pipelined tiles, for
+// workgroups with more than one tile.
+template <int D, int WIN, int NT, bool PIPE>
 __global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {
   extern __shared__ float lds_f[];
   if ((int)blockIdx.x < a.n_sort) {
@@ -73,7 +74,7 @@ __global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {
                           reinterpret_cast<uint32_t*>(lds_f));
     return;
   }
-  fwdbwd8_wg<D, WIN, NT>(a, blockIdx.x - a.n_sort, lds_f);
+  fwdbwd8_wg<D, WIN, NT, PIPE>(a, blockIdx.x - a.n_sort, lds_f);
 }
 
 // =============================================================== sort
@@ -149,9 +150,12 @@ size_t fwdbwd8_lds_bytes(int shape) {
 
 hipError_t launch_step_fwdbwd8(const FwdArgs& a, int shape, int grid, size_t lds,
                                const Launch& L) {
+  const dim3 g(grid), b(kF8Threads);
   if (shape == 1)
-    return pg_launch(k_step_fwdbwd8<64, 5, 2>, dim3(grid), dim3(kF8Threads), lds, L, a);
-  return pg_launch(k_step_fwdbwd8<16, 5, 1>, dim3(grid), dim3(kF8Threads), lds, L, a);
+    return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<64, 5, 2, true>, g, b, lds, L, a)
+                              : pg_launch(k_step_fwdbwd8<64, 5, 2, false>, g, b, lds, L, a);
+  return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<16, 5, 1, true>, g, b, lds, L, a)
+                            : pg_launch(k_step_fwdbwd8<16, 5, 1, false>, g, b, lds, L, a);
 }
 
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
