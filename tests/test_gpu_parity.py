@@ -752,3 +752,25 @@ def test_scatter_update_host_validation_enqueues_nothing():
                                      m.SCATTER_SORTED)
     assert rc == m.OK and ctx.status() == m.OK
     assert torch.count_nonzero(t).item() == 8
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "f16"])
+def test_scatter_update_widest_rows_long_list(fmt):
+    """d = 256 (four column blocks per row) on a 140,000-entry list: the
+    32-entry-chunk apply and the fix-up of heavy rows, every column block."""
+    rows, d, N = 3000, 256, 140_000
+    rng = np.random.default_rng(77)
+    t0, Y, idx = _format_inputs(rng, fmt, rows, d, N, 1.1, np.int32)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    td = _to_dev(t0, fmt)
+    ctx.scatter_update(td, dev(idx), _to_dev(Y, fmt), 0.5)
+    assert ctx.status() == pg().OK
+    got = _to_host(td, fmt)
+    ref = t0.copy()
+    oracle.scatter_add_ex(ref, idx, Y, 0.5, 0, bf16=fmt == "bf16")
+    code = _FMT[fmt][1]
+    gv = oracle.decode(got, code) if fmt == "bf16" else got.astype(np.float64)
+    rv = oracle.decode(ref, code) if fmt == "bf16" else ref.astype(np.float64)
+    assert np.all(np.abs(gv - rv) <= _format_bound(fmt, t0, idx, Y, 0.5, rv))
+    untouched = np.setdiff1d(np.arange(rows), idx)
+    assert np.array_equal(got[untouched], t0[untouched])
