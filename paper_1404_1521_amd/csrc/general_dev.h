@@ -83,16 +83,12 @@ template <class T>
 __device__ __forceinline__ float seg_load(const GenArgs<T>& a, size_t i) {
   return Elem<T>::get(a.Y[i]);
 }
-// a completed piece: the chunk's wave is the row's only writer in this launch
-template <class T>
-__device__ __forceinline__ void seg_add(const GenArgs<T>& a, size_t i, bool cok, float v) {
-  if (cok) a.table[i] = Elem<T>::put(Elem<T>::get(a.table[i]) + v);
-}
 
 // The completed pieces of a chunk, after its walk: v[r] holds the sum of the
-// piece ending at row r for every bit r of `complete`.  Rows are updated 16
-// at a time with their 16 loads in flight together, so a chunk of many short
-// pieces (the Zipf tail) waits for four round trips, not one per piece.
+// piece ending at row r for every bit r of `complete`.  The chunk's wave is
+// the only writer of these rows in this launch.  Rows are updated 16 at a
+// time with their 16 loads in flight together, so a chunk of many short
+// pieces (the Zipf tail) waits for CH / 16 round trips, not one per piece.
 // (Reading all of a chunk's rows before the walk, beside the entries, needs
 // 64 more registers per lane and measured slower for the lost occupancy.)
 template <int CH, class T>
