@@ -324,6 +324,19 @@ def test_sweep_batches(B, steps):
     run_both(w, steps, B, 0)
 
 
+@pytest.mark.parametrize("B", [4100, 8215, 8231])
+def test_pipelined_tiles_ragged(B):
+    """More than 256 tiles, so workgroups take several tiles through the
+    pipelined loop, and the last workgroup fewer: 257 tiles at two per
+    workgroup (the last has one), 514 and 515 tiles at three per workgroup
+    (the last has one or two); the last tile holds 4, 7 or 7 windows."""
+    ntiles = -(-B // 16)
+    per = -(-ntiles // 256)
+    assert per > 1 and ntiles % per != 0
+    w = PRESETS["sweep_1024"].with_batch(B)
+    run_both(w, 2, B, 0)
+
+
 @pytest.mark.parametrize("mode", [0, 1])
 def test_full_size_batch_65536_one_step(mode):
     w = PRESETS["sweep_65536"]
@@ -506,6 +519,7 @@ def test_sorted_mode_is_deterministic():
 GRAPH_CASES = [
     (PRESETS["sweep_1024"], 1024, 6),   # sort fused into the step kernel, partition-wise update
     (PRESETS["sweep_1024"], 4096, 4),   # one-sweep sort on the side stream, fix-up launch
+    (PRESETS["sweep_1024"], 8192, 3),   # two tiles per workgroup: the pipelined tile loop
     (LARGE_SHAPES[0], 100, 4),          # wide layers: partitioned sort on the side stream
     (LARGE_SHAPES[1], 1030, 3),         # wide layers, two dW1 slices
 ]
