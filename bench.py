@@ -48,6 +48,12 @@ def parse():
     ap.add_argument("--only-kernels", action="store_true",
                     help="run only the standalone gather / scatter-add measurements (no step, "
                          "no JSON line): isolates their dispatches under a counter profiler")
+    ap.add_argument("--convergence", action="store_true",
+                    help="batch size vs convergence on the planted synthetic task (one JSON line)")
+    ap.add_argument("--conv-budget", type=int, default=8_000_000,
+                    help="training windows per run of the convergence study")
+    ap.add_argument("--conv-target", type=float, default=0.05,
+                    help="held-out ranking error that ends a run of the convergence study")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device copies of MIB MiB (calibrates the HBM byte "
                          "counters: each copy reads and writes exactly MIB MiB) and exit")
@@ -344,6 +350,65 @@ def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
     return out
 
 
+def convergence_study(torch, np, pg, workloads, budget, target):
+    """Batch size against convergence (the paper's §4.6 question, on the
+    planted task of workloads.PLANTED): for each batch size and learning-rate
+    schedule, train until the held-out ranking error reaches `target` or
+    `budget` windows are spent; report windows, steps and GPU seconds (the
+    train_steps calls only, between stream synchronisations; data generation
+    and evaluation excluded)."""
+    task = workloads.PLANTED
+    ew, ewc = task.held_out()
+    dew, dewc = torch.from_numpy(ew).cuda(), torch.from_numpy(ewc).cuda()
+    s_true = torch.empty(ew.shape[0], device="cuda")
+    s_cor = torch.empty(ew.shape[0], device="cuda")
+    chunk = 65536  # training windows between evaluations
+    runs = []
+    for sched, lr_of in (("lr 1.0", lambda B: 1.0),
+                         ("lr 0.25*sqrt(B/16)", lambda B: 0.25 * (B / 16) ** 0.5)):
+        for B in (16, 64, 256, 1024, 4096):
+            lr = lr_of(B)
+            pd = {k: torch.from_numpy(v).cuda()
+                  for k, v in workloads.init_params(task.workload(B, lr)).items()}
+            ctx = pg.Context(task.V, task.d, task.win, task.H, max_batch=max(B, ew.shape[0]))
+            S = max(1, chunk // B)
+            dw = torch.empty(S, B, task.win, dtype=torch.int32, device="cuda")
+            dc = torch.empty(S, B, dtype=torch.int32, device="cuda")
+            losses = torch.zeros(S, device="cuda")
+            rng = np.random.default_rng([task.seed, 4, B])
+            seen = steps = 0
+            gpu_s, err, curve = 0.0, 1.0, []
+            while seen < budget:
+                w, c = task.batch(rng, S * B)
+                dw.copy_(torch.from_numpy(w.reshape(S, B, task.win)))
+                dc.copy_(torch.from_numpy(c.reshape(S, B)))
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                ctx.train_steps(pd, dw, dc, lr, losses)  # same buffers: the cached graph replays
+                torch.cuda.synchronize()
+                gpu_s += time.perf_counter() - t0
+                seen += S * B
+                steps += S
+                ctx.score(pd, dew, s_true)
+                ctx.score(pd, dewc, s_cor)
+                err = float((s_true <= s_cor).float().mean())
+                curve.append([seen, round(err, 4)])
+                if err <= target:
+                    break
+            if ctx.status() != pg.OK:
+                raise RuntimeError("device error flag raised in the convergence study")
+            ctx.close()
+            runs.append({"schedule": sched, "B": B, "lr": round(lr, 4), "reached": err <= target,
+                         "windows": seen, "steps": steps, "gpu_s": round(gpu_s, 4),
+                         "final_error": round(err, 4), "final_loss": round(float(losses.mean()), 4),
+                         "curve": curve if len(curve) <= 24 else curve[::len(curve) // 24] + [curve[-1]]})
+    return {"study": "batch size vs convergence on the planted synthetic task",
+            "task": {"V": task.V, "d": task.d, "win": task.win, "H": task.H, "zipf_s": task.zipf_s,
+                     "noise": task.noise, "held_out": int(ew.shape[0])},
+            "target_error": target, "budget_windows": budget, "eval_every_windows": chunk,
+            "runs": runs}
+
+
 def copy_ceiling(torch, mib=256, reps=10):
     """Streaming-copy ceiling measured on this device: a plain device-to-device
     copy of `mib` MiB, timed with events on the current stream; bytes read +
@@ -385,6 +450,12 @@ def main():
 
     import paper_1404_1521_amd as pg
     import workloads
+
+    if args.convergence:
+        torch.cuda.set_device(0)
+        print(json.dumps(convergence_study(torch, np, pg, workloads, args.conv_budget,
+                                           args.conv_target)), flush=True)
+        return
 
     if args.only_kernels:
         torch.cuda.set_device(0)

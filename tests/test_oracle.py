@@ -471,3 +471,21 @@ def test_scatter_add_ex_rejects_bad_ids_before_writing():
         with pytest.raises(oracle.OracleError):
             oracle.scatter_add_ex(t, idx, np.ones((2, 2), np.float32), 1.0)
         assert np.array_equal(t, t0)
+
+
+def test_planted_task_generator():
+    """The planted rule holds for the expected share of training windows and
+    for every held-out window; ids stay in range; the corrupted held-out copy
+    differs only in the centre."""
+    t = workloads.PLANTED
+    rule = t.rule()
+    assert sorted(rule.tolist()) == list(range(t.V))
+    c = t.win // 2
+    w, cor = t.batch(np.random.default_rng(0), 20000)
+    assert w.dtype == np.int32 and cor.dtype == np.int32
+    assert w.min() >= 0 and w.max() < t.V and cor.min() >= 0 and cor.max() < t.V
+    hold = np.mean(w[:, c] == rule[w[:, c - 1]])
+    assert abs(hold - (1 - t.noise)) < 0.02 + 1.0 / t.V * 5
+    hw, hwc = t.held_out(512)
+    assert np.all(hw[:, c] == rule[hw[:, c - 1]])
+    assert np.array_equal(np.delete(hw, c, axis=1), np.delete(hwc, c, axis=1))

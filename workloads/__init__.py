@@ -121,3 +121,50 @@ def scatter_inputs(sw: ScatterWorkload = SCATTER_ISO, N: int | None = None):
     idx = zipf_ids(rng, sw.rows, sw.zipf_s, N)
     Y = rng.standard_normal((N, sw.d), dtype=np.float32) * np.float32(sw.y_std)
     return table, idx, Y
+
+
+# ------------------------------------------------ planted structure (convergence study)
+
+@dataclass(frozen=True)
+class PlantedTask:
+    """Synthetic windows with a learnable rule: ids ~ Zipf(zipf_s) over V, and
+    with probability 1 - noise the centre word is a fixed random permutation
+    of its left neighbour.  Corrupt centres are uniform.  A held-out set with
+    no noise measures the ranking error (fraction of windows that do not
+    score above their corrupted copy), the stand-in for the paper's
+    unspecified error level."""
+    V: int = 1000
+    d: int = 64
+    win: int = 5
+    H: int = 32
+    zipf_s: float = 1.0
+    noise: float = 0.1
+    seed: int = 11
+    init_std: float = 0.01
+
+    def workload(self, B: int, lr: float) -> Workload:
+        return Workload("planted", V=self.V, d=self.d, win=self.win, H=self.H, B=B, lr=lr,
+                        steps=0, zipf_s=self.zipf_s, seed=self.seed, init_std=self.init_std)
+
+    def rule(self) -> np.ndarray:
+        return np.random.default_rng([self.seed, 2]).permutation(self.V).astype(np.int32)
+
+    def batch(self, rng: np.random.Generator, n: int, noise: float | None = None):
+        """n windows [n][win] int32 and n corrupt centre ids [n] int32."""
+        noise = self.noise if noise is None else noise
+        c = self.win // 2
+        w = zipf_ids(rng, self.V, self.zipf_s, (n, self.win))
+        keep = rng.random(n) >= noise
+        w[:, c] = np.where(keep, self.rule()[w[:, c - 1]], w[:, c])
+        cor = rng.integers(0, self.V, n).astype(np.int32)
+        return w, cor
+
+    def held_out(self, n: int = 8192):
+        """Noise-free windows and the same windows with the corrupt centre."""
+        w, cor = self.batch(np.random.default_rng([self.seed, 3]), n, noise=0.0)
+        wc = w.copy()
+        wc[:, self.win // 2] = cor
+        return w, wc
+
+
+PLANTED = PlantedTask()
