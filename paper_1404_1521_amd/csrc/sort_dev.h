@@ -239,6 +239,10 @@ __device__ uint32_t* lds_lsd_passes(uint32_t* src, uint32_t* dst, int M, const S
 // contiguous and in entry order -- what the segmented sum needs; the order
 // between distinct keys is fixed by the keys alone.
 constexpr int kPartBits = 7;
+// Partitions of at most this many entries are ranked by counting smaller
+// words (quadratic in the partition: measured faster than the two LDS radix
+// passes up to about 540 entries, slower at 720).
+constexpr int kRankSortMax = 512;
 constexpr int kPartSortThreads = 1024;  // one workgroup of 16 waves per partition
 constexpr int kPartSortMisc = 32;       // scan scratch: wave sums, then the partition total
 __host__ __device__ constexpr size_t part_sort_lds_words(int nth) {
@@ -308,7 +312,39 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
   }
   __syncthreads();  // misc and hist are reused by the passes
 
-  uint32_t* res = lds_lsd_passes<NTH>(bufA, bufB, M, plan, vb, rank16, hist, misc);
+  // The words (key bits above the partition bits, then the entry id) are
+  // distinct, so a word's place in the sorted partition is the number of
+  // smaller words: up to kRankSortMax words are ranked by one pass of
+  // broadcast LDS reads, one thread per word (the same order as the stable
+  // radix passes, which larger partitions take).
+  uint32_t* res;
+  if (M <= kRankSortMax && M <= NTH) {
+    if (t < M) {
+      const uint32_t wv = bufA[t];
+      uint32_t r = 0u;
+      int j = 0;
+      for (; j + 16 <= M; j += 16) {  // four reads in flight per step
+        uint4 q[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) q[u] = *reinterpret_cast<const uint4*>(bufA + j + 4 * u);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          r += (q[u].x < wv ? 1u : 0u) + (q[u].y < wv ? 1u : 0u) + (q[u].z < wv ? 1u : 0u) +
+               (q[u].w < wv ? 1u : 0u);
+      }
+      for (; j + 4 <= M; j += 4) {
+        const uint4 q = *reinterpret_cast<const uint4*>(bufA + j);
+        r += (q.x < wv ? 1u : 0u) + (q.y < wv ? 1u : 0u) + (q.z < wv ? 1u : 0u) +
+             (q.w < wv ? 1u : 0u);
+      }
+      for (; j < M; ++j) r += bufA[j] < wv ? 1u : 0u;
+      bufB[r] = wv;
+    }
+    __syncthreads();
+    res = bufB;
+  } else {
+    res = lds_lsd_passes<NTH>(bufA, bufB, M, plan, vb, rank16, hist, misc);
+  }
   const uint32_t vmask = (1u << vb) - 1u;
   for (int i = t; i < M; i += NTH) {
     const uint32_t word = res[i];
