@@ -222,6 +222,34 @@ def test_scatter_add_partition_rounds(keys_kind, d):
     assert np.array_equal(got[untouched], t0[untouched])
 
 
+@pytest.mark.parametrize("M", [1, 2, 255, 256, 257, 511, 512, 513, 700, 1024, 2000])
+def test_scatter_add_partition_sizes_exact(M):
+    """Partition 0 (ids that are multiples of 128) holds exactly M entries
+    over eight ids, the rest of the 6000 entries fall in other partitions:
+    sizes on both sides of where the partitioned sort switches from ranking
+    by counting to its radix passes.  Y holds small integers and the table
+    starts at zero, so every order of summation gives the same float32 and
+    the result must equal the oracle's exactly: an entry lost or taken twice
+    by the ranking shows."""
+    rng = np.random.default_rng(1000 + M)
+    rows, N, d = 1024, 6000, 24
+    hot = rng.choice(np.arange(0, rows, 128, dtype=np.int32), M)
+    other = rng.integers(0, rows, 4 * N).astype(np.int32)
+    other = other[other % 128 != 0][: N - M]
+    idx = rng.permutation(np.concatenate([hot, other])).astype(np.int32)
+    assert idx.size == N and np.count_nonzero(idx % 128 == 0) == M
+    Y = rng.integers(-8, 9, (N, d)).astype(np.float32)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    t0 = np.zeros((rows, d), np.float32)
+    ref = t0.astype(np.float64)
+    oracle.scatter_add(ref, idx, Y.astype(np.float64), 0.5)
+    for mode in (pg().SCATTER_SORTED, pg().SCATTER_ATOMIC):
+        td = dev(t0)
+        ctx.scatter_add(td, dev(idx), dev(Y), 0.5, mode)
+        assert ctx.status() == pg().OK
+        assert np.array_equal(host(td), ref.astype(np.float32)), mode
+
+
 def test_small_vocabulary_step_partition_rounds():
     """A 64-word vocabulary at B = 1365 (8190 entries, the largest list the
     partitioned sort takes): each partition holds one word, the most frequent
