@@ -89,13 +89,21 @@ def batch_structure(wins, cors, ch):
 
 
 def step_model(w, B, st, passes, n_parts):
-    """{kernel: (bytes, flops, engine)} of one step.
+    """({kernel: (bytes, flops, engine)}, {kernel: overhead bytes}) of one step.
+
+    The first map holds the method's own bytes and flops per step: what the
+    operation must read, write and compute whatever the implementation.  The
+    second holds the traffic this implementation adds on top (the dense
+    gradient partials that one kernel writes and the next reads back), which
+    is reported beside the roofline, never inside it.
 
     Hidden layers of at most 64 units (one fused kernel):
     fwdbwd: ids + every window row and corrupt row read once (the gather),
       the per-entry gradient rows G written ((win+1) rows of d floats per
-      window), W1 read once, dense partials written; flops = forward 2HK +
-      2Hd (corrupted centre block), dW1 2HK + 2Hd, G (win+1) 2Hd per window.
+      window), W1 read once: (win+1)(4 + 8d) B per window, 3,096 B at d 64,
+      window 5; flops = forward 2HK + 2Hd (corrupted centre block), dW1
+      2HK + 2Hd, G (win+1) 2Hd per window: 73,728 at H 32 (plus O(H)
+      elementwise work, not counted).  Overhead: the dense partial slots.
     Wider layers (three contractions):
     fwdbwd: ids and rows read, W1 read, the per-window vectors (3H floats)
       and the db1/dw2/loss partials written; flops 2HK + 2Hd per window.
@@ -105,8 +113,8 @@ def step_model(w, B, st, passes, n_parts):
       (win+1) 2Hd per window.
     sort: 16 B per entry per radix pass (keys and values, read and written).
     update: sorted keys+values and every G row read once, every distinct row
-      of E read and written, dense partials read, W1/b1/w2/b2 read and
-      written; flops = one add per G element.
+      of E read and written, W1/b1/w2/b2 read and written; flops = one add
+      per G element.  Overhead: the dense partials read back.
     segfix: the chunk partials of long rows (d floats each) read, their rows
       read and written.
     """
@@ -131,13 +139,16 @@ def step_model(w, B, st, passes, n_parts):
         part_stride = Hp * K + 2 * Hp + 2
         part_bytes = n_parts * part_stride * 4
         m = {
-            "fwdbwd": (rows_in + g_out + H * K * 4 + part_bytes,
+            "fwdbwd": (rows_in + g_out + H * K * 4,
                        B * (4 * H * K + 4 * H * d + (win + 1) * 2 * H * d), "mfma"),
         }
     m["sort"] = (N * 16 * passes, 0, "hbm")
-    m["update"] = (N * (8 + d * 4) + 2 * st["U"] * d * 4 + part_bytes + 2 * dense, N * d, "alu")
+    m["update"] = (N * (8 + d * 4) + 2 * st["U"] * d * 4 + 2 * dense, N * d, "alu")
     m["segfix"] = (st["partials"] * d * 4 + 2 * st["long_rows"] * d * 4, st["partials"] * d, "alu")
-    return m
+    over = {"fwdbwd": part_bytes, "update": part_bytes}
+    if H > 64:
+        over = {"wide_dw1": slices * H * K * 4, "update": part_bytes}
+    return m, over
 
 
 def roofline(nbytes, nflops, engine, ms):
@@ -224,19 +235,27 @@ def cpu_baseline(w, seconds):
     import workloads
     p = workloads.init_params(w)
     steps, busy = 0, 0.0
-    while busy < seconds:
-        win, cor = workloads.batch(w, steps, w.B)
-        a = time.perf_counter()
-        oracle.train_step(p, win, cor, w.lr)
-        busy += time.perf_counter() - a
-        steps += 1
+    # pinned to one core of those this process may use, for the timed steps
+    allowed = sorted(os.sched_getaffinity(0))
+    core = allowed[0]
+    os.sched_setaffinity(0, {core})
+    try:
+        while busy < seconds:
+            win, cor = workloads.batch(w, steps, w.B)
+            a = time.perf_counter()
+            oracle.train_step(p, win, cor, w.lr)
+            busy += time.perf_counter() - a
+            steps += 1
+    finally:
+        os.sched_setaffinity(0, set(allowed))
     return {
         "value": round(w.B * steps / busy, 1),
         "unit": "windows/s",
         "cores": 1,
         "kind": "oracle",
         "sample": f"first {steps} steps of {w.name} (B={w.B}): float32 storage, float64 "
-                  f"arithmetic C++ oracle, 1 thread of {os.cpu_count()} on {cpu_model_name()}, "
+                  f"arithmetic C++ oracle, 1 thread pinned to core {core} ({len(allowed)} cores "
+                  f"allowed, {os.cpu_count()} in the machine) on {cpu_model_name()}, "
                   f"{busy:.1f} s of step time",
     }
 
@@ -261,28 +280,52 @@ def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
     roofline covers its table-update kernels (the sort is reported separately,
     as its bytes are not the operation's); whole calls are timed end to end on
     the stream as well."""
+    out = {}
+    # The gather, twice: over the stress table (1M x 128 floats, 512 MB,
+    # twice the 256 MB Infinity Cache) and over the 100k x 64 table (25.6 MB,
+    # cache-resident).  Algorithmic bytes: the ids, every DISTINCT row read
+    # once (a repeated row is read from cache, not from HBM) and X and Xc
+    # written; the per-window figure that counts every row read is given
+    # beside it.
+    for key, name in (("gather", "stress"), ("gather_cache_resident", "sweep_65536")):
+        w = workloads.PRESETS[name]
+        gctx = pg.Context(w.V, w.d, w.win, w.H, max_batch=w.B, stream=stream)
+        try:
+            p = workloads.init_params(w)
+            E = torch.from_numpy(p["E"]).cuda()
+            del p
+            wins, cors = workloads.batch(w, 0, w.B)
+            dw, dc = torch.from_numpy(wins).cuda(), torch.from_numpy(cors).cuda()
+            X = torch.empty(w.B, w.K, device="cuda")
+            Xc = torch.empty(w.B, w.d, device="cuda")
+            gctx.gather(E, dw, dc, X, Xc)
+            stream.synchronize()
+            gctx.set_timing(True)
+            for _ in range(reps):
+                gctx.gather(E, dw, dc, X, Xc)
+            ms, n = gctx.kernel_times()["gather"]
+            if gctx.status() != pg.OK:
+                raise RuntimeError("device error flag raised in the gather measurement")
+        finally:
+            gctx.close()
+        U = int(np.unique(np.concatenate([wins.ravel(), cors])).size)
+        ids_b = w.B * (w.win + 1) * 4
+        out_b = w.B * (w.win + 1) * w.d * 4
+        nbytes = ids_b + U * w.d * 4 + out_b
+        out[key] = dict(roofline(nbytes, 0, "hbm", ms / n),
+                        traffic=counter_traffic("kernels", key),
+                        avg_launch_us=round(ms / n * 1e3, 3), bytes_per_launch=nbytes,
+                        bytes_per_launch_every_row=ids_b + 2 * out_b, distinct_rows=U,
+                        table_mb=round(w.V * w.d * 4 / 1e6, 1),
+                        workload=f"B={w.B} V={w.V} d={w.d} win={w.win} Zipf({w.zipf_s})")
+        del E, dw, dc, X, Xc
+    torch.cuda.empty_cache()
+
     w = workloads.PRESETS["sweep_65536"]
     sw = workloads.SCATTER_ISO
-    out = {}
     ctx = pg.Context(w.V, w.d, w.win, w.H, max_batch=w.B, max_scatter=sw.N, max_rows=sw.rows,
                      stream=stream)
     try:
-        p = workloads.init_params(w)
-        E = torch.from_numpy(p["E"]).cuda()
-        wins, cors = workloads.batch(w, 0, w.B)
-        dw, dc = torch.from_numpy(wins).cuda(), torch.from_numpy(cors).cuda()
-        X = torch.empty(w.B, w.K, device="cuda")
-        Xc = torch.empty(w.B, w.d, device="cuda")
-        ctx.gather(E, dw, dc, X, Xc)
-        stream.synchronize()
-        ctx.set_timing(True)
-        for _ in range(reps):
-            ctx.gather(E, dw, dc, X, Xc)
-        ms, n = ctx.kernel_times()["gather"]
-        nbytes = w.B * ((w.win + 1) * 4 + 2 * (w.win + 1) * w.d * 4)
-        out["gather"] = dict(roofline(nbytes, 0, "hbm", ms / n), traffic=counter_traffic("kernels", "gather"),
-                             avg_launch_us=round(ms / n * 1e3, 3), bytes_per_launch=nbytes,
-                             workload=f"B={w.B} V={w.V} d={w.d} win={w.win}")
 
         table0, idx, Y = workloads.scatter_inputs(sw)
         T = torch.from_numpy(table0).cuda()
@@ -547,7 +590,7 @@ def main():
     # for the compile-time shapes d 64 / d 16 with window 5, 512 otherwise)
     nt = -(-w.H // 16)
     n_parts = min(-(-B // 16), 256 if (w.d, w.win, nt) in ((64, 5, 2), (16, 5, 1)) else 512)
-    model = step_model(w, B, st, passes, n_parts)
+    model, overhead = step_model(w, B, st, passes, n_parts)
     model_flops = sum(v[1] for v in model.values())
     per = {k: (v[0] / v[1], v[1] / K) for k, v in kt.items() if v[1]}
     step_us = {k: v[0] * v[1] for k, v in per.items()}
@@ -573,6 +616,11 @@ def main():
     roof["avg_launch_us"] = round(dms * 1e3, 3)
     roof["bytes_per_launch"] = int(nbytes)
     roof["flops_per_launch"] = int(nflops)
+    roof["intensity_flop_per_byte"] = round(nflops / nbytes, 3) if nbytes else None
+    # traffic this implementation adds beyond the method's bytes (not in `achieved`)
+    ob = overhead.get(dom, 0) / per[dom][1]
+    roof["overhead_bytes_per_launch"] = int(ob)
+    roof["overhead_ratio"] = round((nbytes + ob) / nbytes, 4) if nbytes else None
     roof["kernels_us_per_step"] = {k: round(v[0] * v[1] * 1e3, 3) for k, v in per.items()}
     # every contraction of the step over the step time (all kernels, gaps included)
     roof["step_tflops"] = round(model_flops / (ms / K * 1e-3) / 1e12, 3)

@@ -102,6 +102,20 @@ int polyglot_train_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float
                         const int32_t* windows, const int32_t* corrupt, int32_t B, float lr,
                         float* loss_dev);
 
+/* polyglot_train_step followed by a synchronisation: the step is enqueued on
+ * the context's stream with its loss in a library-owned device slot, the
+ * stream is synchronised, and the mean hinge loss (the quantity of the
+ * model above, at the pre-step parameters) is written to *loss_host (host
+ * memory, caller-owned).  Returns what polyglot_train_step returns for the
+ * arguments (nothing is enqueued on such an error and *loss_host is left
+ * unchanged); POLYGLOT_EHIP if the synchronisation fails; POLYGLOT_EID if a
+ * device error word is raised once the step has run, in which case the step
+ * changed no parameter and *loss_host is NaN.  The error words stay raised
+ * (every later step is void) until polyglot_status() clears them. */
+int polyglot_train_step_sync(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2,
+                             float* b2, const int32_t* windows, const int32_t* corrupt,
+                             int32_t B, float lr, float* loss_host);
+
 /* S consecutive SGD steps, step s using windows + s*B*win and corrupt + s*B,
  * exactly as S calls of polyglot_train_step.  losses_dev[S] (device, may be
  * NULL) receives each step's loss.  The launches of the S steps are recorded
@@ -111,15 +125,22 @@ int polyglot_train_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, floa
                          float* b2, const int32_t* windows, const int32_t* corrupt, int32_t S,
                          int32_t B, float lr, float* losses_dev);
 
-/* Scores s(x) = w2 . tanh(W1 x + b1) + b2 of the B windows into
- * scores_dev[B] (NaN for a window holding an out-of-range id). */
+/* The score of the ranking model of §1 Introduction (the SENNA-like
+ * network the paper trains), s(x) = w2 . tanh(W1 x + b1) + b2, of each of
+ * the B windows: x = concat_j E[windows[b][j]].  windows[B][win] int32
+ * (device), scores_dev[B] float32 (device, written).  A window holding an
+ * out-of-range id scores NaN and raises the sticky flag.  1 <= B <= max_batch;
+ * E and W1 16-byte aligned (else POLYGLOT_EINVAL). */
 int polyglot_score(polyglot_ctx* ctx, const float* E, const float* W1, const float* b1,
                    const float* w2, const float* b2, const int32_t* windows, int32_t B,
                    float* scores_dev);
 
-/* The window gather on its own: X[B][win*d] = concat_j E[windows[b][j]] and
- * Xc[B][d] = E[corrupt[b]] (bit-exact copies; a row with an out-of-range id
- * is written as NaN and raises the sticky flag). */
+/* The window gather on its own: the input vector x of the §1 Introduction
+ * model, the concatenation of the window's embedding rows, for every
+ * window, X[B][win*d] = concat_j E[windows[b][j]], and the corrupted centre
+ * rows Xc[B][d] = E[corrupt[b]] (bit-exact copies; a row with an
+ * out-of-range id is written as NaN and raises the sticky flag).  All
+ * pointers device; E, X and Xc 16-byte aligned; 1 <= B <= max_batch. */
 int polyglot_gather(polyglot_ctx* ctx, const float* E, const int32_t* windows,
                     const int32_t* corrupt, int32_t B, float* X, float* Xc);
 
@@ -165,10 +186,13 @@ int polyglot_scatter_update(polyglot_ctx* ctx, void* table, int32_t dtype, int32
                             int32_t d, const void* idx, int32_t idx_bytes, const void* Y,
                             int32_t N, float alpha, int32_t op, int32_t mode);
 
-/* Host copy of the sorted distinct row ids touched by the last sorted-mode
- * train step (ids of the windows and the corrupt ids).  Synchronises the
- * stream.  Writes at most cap ids to ids_host and the total to *count.
- * POLYGLOT_ESTATE if no sorted-mode step has run. */
+/* The distinct values of the index vector I of the §4.2 increment
+ * W[I[k]] += Y[k] in the last sorted-mode train step: the rows of E the step
+ * updated (ids of the windows and the corrupt ids), ascending.  Synchronises
+ * the stream.  ids_host: host array of cap ints (may be NULL with cap 0);
+ * at most cap ids are written and the total to *count (host).
+ * POLYGLOT_ESTATE if no sorted-mode step has run, or if a scatter-add has
+ * reused the sort buffers since. */
 int polyglot_touched_rows(polyglot_ctx* ctx, int32_t* ids_host, int32_t cap, int32_t* count);
 
 /* Kernel ids reported by polyglot_kernel_times. */

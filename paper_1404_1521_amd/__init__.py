@@ -29,7 +29,7 @@ _CODE_NAMES = {EINVAL: "EINVAL", ENULL: "ENULL", EBATCH: "EBATCH", EHIP: "EHIP",
 
 # Every entry point declared in include/polyglot.h.
 EXPORTS = ("polyglot_init", "polyglot_destroy", "polyglot_set_stream", "polyglot_train_step",
-           "polyglot_train_steps", "polyglot_score", "polyglot_gather", "polyglot_scatter_add",
+           "polyglot_train_step_sync", "polyglot_train_steps", "polyglot_score", "polyglot_gather", "polyglot_scatter_add",
            "polyglot_scatter_update",
            "polyglot_touched_rows", "polyglot_status", "polyglot_last_error",
            "polyglot_set_timing", "polyglot_kernel_times")
@@ -67,6 +67,7 @@ def load_library():
         "polyglot_destroy": [p],
         "polyglot_set_stream": [p, p],
         "polyglot_train_step": [p] + [p] * 7 + [i32, f32, p],
+        "polyglot_train_step_sync": [p] + [p] * 7 + [i32, f32, ctypes.POINTER(f32)],
         "polyglot_train_steps": [p] + [p] * 7 + [i32, i32, f32, p],
         "polyglot_score": [p] + [p] * 6 + [i32, p],
         "polyglot_gather": [p, p, p, p, i32, p, p],
@@ -142,6 +143,18 @@ class Context:
         c = _dev_tensor(corrupt, torch.int32, "corrupt", (B,))
         lo = None if loss_out is None else _dev_tensor(loss_out, torch.float32, "loss_out")
         self._check(self._lib.polyglot_train_step(self._h, *args, w, c, B, lr, lo), "train_step")
+
+    def train_step_sync(self, params: dict, windows, corrupt, lr: float) -> float:
+        """One SGD step in place on params; synchronises the context stream and
+        returns the step's mean loss as a Python float."""
+        B = windows.shape[0]
+        args = self._params(params)
+        w = _dev_tensor(windows, torch.int32, "windows", (B, self.win))
+        c = _dev_tensor(corrupt, torch.int32, "corrupt", (B,))
+        loss = ctypes.c_float(0.0)
+        self._check(self._lib.polyglot_train_step_sync(self._h, *args, w, c, B, lr,
+                                                       ctypes.byref(loss)), "train_step_sync")
+        return loss.value
 
     def train_steps(self, params: dict, windows, corrupt, lr: float, losses_out=None) -> None:
         """S steps over windows[S][B][win], corrupt[S][B] (graph-replayed)."""

@@ -125,6 +125,12 @@ SortBufs sort_bufs(polyglot_ctx* ctx, int set) {
   return sb;
 }
 
+// The error word of a training step's side-stream sort into set `set`.  The
+// sort of step s+1 runs while step s updates its parameters, so it raises a
+// word of its own: step s's update reads word 0 and its own set's word, never
+// the other set's.  polyglot_status reports all three words.
+uint32_t* set_flag(polyglot_ctx* ctx, int set) { return ctx->ws.flag + 1 + set; }
+
 // Counters a multi-tile sort accumulates atomically (the look-back words are
 // cleared by the sort's histogram launch).
 ZeroRanges sort_zero_ranges(polyglot_ctx* ctx, const SortPlan& plan, int set) {
@@ -211,7 +217,7 @@ struct Timed {
 };
 
 SegArgs seg_args(polyglot_ctx* ctx, float* table, const float* Y, const SortPlan& plan, int set,
-                 int N, int d, float alpha) {
+                 int N, int d, float alpha, bool step) {
   SegArgs a{};
   a.table = table;
   a.Y = Y;
@@ -221,6 +227,7 @@ SegArgs seg_args(polyglot_ctx* ctx, float* table, const float* Y, const SortPlan
   a.long_list = ctx->ws.long_list;
   a.seg_end = ctx->ws.seg_end;
   a.flag = ctx->ws.flag;
+  a.flag2 = step ? set_flag(ctx, set) : ctx->ws.flag;
   a.N = N;
   a.d = d;
   a.ch = seg_chunk_size(N);
@@ -247,7 +254,9 @@ hipError_t enqueue_sort(polyglot_ctx* ctx, const int32_t* windows, const int32_t
   const int N = B * (cf.win + 1);
   const StepKeys kf = step_keys(windows, corrupt, cf.win, cf.V);
   Timed tm(ctx, POLYGLOT_K_SORT, ctx->side);
-  return launch_sort_step(kf, N, make_plan(cf.V, N), sort_bufs(ctx, set), tm.L);
+  SortBufs sb = sort_bufs(ctx, set);
+  sb.flag = set_flag(ctx, set);
+  return launch_sort_step(kf, N, make_plan(cf.V, N), sb, tm.L);
 }
 
 // The forward/backward launch(es), then (after `sorted_ev`, if any) the
@@ -349,7 +358,7 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   }
 
   ApplyArgs aa{};
-  aa.s = seg_args(ctx, E, ctx->ws.G, plan, set, N, cf.d, -lr);
+  aa.s = seg_args(ctx, E, ctx->ws.G, plan, set, N, cf.d, -lr, true);
   aa.mode = sorted ? 0 : 1;
   aa.n_e = table_workgroups(aa.s, aa.mode);
   aa.n_d = ceil_div(ctx->part_stride * kDenseSlices, kBlock);
@@ -542,7 +551,7 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_part, (size_t)ctx->max_chunks * 2 * ctx->seg_stride);
   if (e == hipSuccess) e = alloc(ctx, &ws.long_list, (size_t)ctx->max_chunks);
   if (e == hipSuccess) e = alloc(ctx, &ws.idx32, (size_t)c.max_scatter);
-  if (e == hipSuccess) e = alloc(ctx, &ws.flag, 1);
+  if (e == hipSuccess) e = alloc(ctx, &ws.flag, 3);
   if (e == hipSuccess) e = alloc(ctx, &ws.scratch_loss, 1);
   for (int k = 0; k < 2; ++k) {
     if (e == hipSuccess)
@@ -550,7 +559,7 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
     if (e == hipSuccess) e = hipMemset(ws.status[k], 0, sizeof(uint32_t) * nstatus);
     if (e == hipSuccess) e = hipMemset(ws.tile_ctr[k], 0, sizeof(uint32_t) * kMaxPasses);
   }
-  if (e == hipSuccess) e = hipMemset(ws.flag, 0, sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMemset(ws.flag, 0, 3 * sizeof(uint32_t));
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking);
   for (hipEvent_t* ev : {&ctx->ev_fork, &ctx->ev_sorted[0], &ctx->ev_sorted[1], &ctx->ev_done[0],
                          &ctx->ev_done[1]})
@@ -587,6 +596,30 @@ int polyglot_train_step(polyglot_ctx* ctx, float* E, float* W1, float* b1, float
   const int rc = check_step_args(ctx, E, W1, b1, w2, b2, windows, corrupt, B, lr);
   if (rc) return rc;
   return enqueue_steps(ctx, E, W1, b1, w2, b2, windows, corrupt, 1, B, lr, loss_dev);
+}
+
+int polyglot_train_step_sync(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2,
+                             float* b2, const int32_t* windows, const int32_t* corrupt,
+                             int32_t B, float lr, float* loss_host) {
+  if (!ctx) return POLYGLOT_ENULL;
+  if (!loss_host) return fail(ctx, POLYGLOT_ENULL, "train_step_sync: NULL loss_host");
+  int rc = check_step_args(ctx, E, W1, b1, w2, b2, windows, corrupt, B, lr);
+  if (rc) return rc;
+  rc = enqueue_steps(ctx, E, W1, b1, w2, b2, windows, corrupt, 1, B, lr, ctx->ws.scratch_loss);
+  if (rc) return rc;
+  float loss = 0.f;
+  uint32_t w[3] = {0, 0, 0};
+  hipError_t e = hipMemcpyAsync(&loss, ctx->ws.scratch_loss, sizeof(loss), hipMemcpyDeviceToHost,
+                                ctx->stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(w, ctx->ws.flag, sizeof(w), hipMemcpyDeviceToHost, ctx->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "train_step_sync: loss copy");
+  *loss_host = loss;
+  if (w[0] | w[1] | w[2])
+    return fail(ctx, (w[0] | w[1] | w[2]) & kFlagBadId ? POLYGLOT_EID : POLYGLOT_EHIP,
+                "train_step_sync: a device error word is raised; the step changed nothing");
+  return POLYGLOT_OK;
 }
 
 int polyglot_train_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2,
@@ -793,7 +826,7 @@ int scatter_add_f32(polyglot_ctx* ctx, float* table, int32_t rows, int32_t d, co
   const SortPlan plan = make_plan(rows, N);
   const IdxKeys kf{idx, rows};
   ApplyArgs aa{};
-  aa.s = seg_args(ctx, table, Y, plan, 0, N, d, alpha);
+  aa.s = seg_args(ctx, table, Y, plan, 0, N, d, alpha, false);
   aa.mode = mode == POLYGLOT_SCATTER_SORTED ? 0 : 1;
   aa.n_e = table_workgroups(aa.s, aa.mode);
   aa.n_d = 0;
@@ -859,11 +892,12 @@ int polyglot_status(polyglot_ctx* ctx) {
   if (!ctx) return POLYGLOT_ENULL;
   hipError_t e = hipStreamSynchronize(ctx->stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "status: sync");
-  uint32_t f = 0;
-  e = hipMemcpy(&f, ctx->ws.flag, sizeof(f), hipMemcpyDeviceToHost);
+  uint32_t w[3] = {0, 0, 0};
+  e = hipMemcpy(w, ctx->ws.flag, sizeof(w), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(ctx, e, "status: read flag");
+  const uint32_t f = w[0] | w[1] | w[2];
   if (f) {
-    e = hipMemset(ctx->ws.flag, 0, sizeof(uint32_t));
+    e = hipMemset(ctx->ws.flag, 0, sizeof(w));
     if (e != hipSuccess) return hip_fail(ctx, e, "status: clear flag");
     if (f & kFlagBadId) return fail(ctx, POLYGLOT_EID, "an id was outside its table");
     return fail(ctx, POLYGLOT_EHIP, "internal: sort position outside the entry range");

@@ -69,7 +69,9 @@ struct Workspace {
   int2* long_list;          // [max_chunks] by chunk: (chunk, row) if a segment crossing
                             // chunks starts there, else (-1, 0)
   int32_t* seg_end;         // [max(V, max_rows)] end chunk of a long segment, by row id
-  uint32_t* flag;           // sticky error bits
+  uint32_t* flag;           // sticky error bits [3]: word 0 raised by every launch except a
+                            // training step's side-stream sort, word 1 + q by the side-stream
+                            // sort of sort set q (read only by that set's update)
   float* scratch_loss;      // loss slot used when the caller passes no loss pointer
   int32_t* idx32;           // [max_scatter] int64 indices narrowed to int32 keys
 };

@@ -72,6 +72,7 @@ struct GenArgs {
   int2* long_list;          // by chunk, as in SegArgs
   int32_t* seg_end;         // [rows]
   const uint32_t* flag;     // sticky error bits: nonzero voids the update
+  const uint32_t* flag2;    // same word as flag (the general op has one sort of its own)
   int N, d, ch, seg_stride;
   float alpha;
   ZeroRanges zero;          // sort counters cleared by the apply launch
@@ -161,7 +162,7 @@ __global__ __launch_bounds__(kBlock) void k_gen_set(GenArgs<T> a, int n_e) {
                 (size_t)(gridDim.x - n_e) * kBlock);
     return;
   }
-  if (__builtin_amdgcn_readfirstlane(*a.flag) != 0u) return;
+  if (__builtin_amdgcn_readfirstlane(void_bits(a)) != 0u) return;
   const int ngroups = ceil_div(a.N, kWave);
   constexpr int RB = 16;  // rows copied together, their loads in flight at once
   for (int gi = blockIdx.x * kWavesPerBlock + w; gi < ngroups; gi += n_e * kWavesPerBlock) {

@@ -208,6 +208,7 @@ static GenArgs<T> gen_args(const GenCall& c) {
   a.long_list = c.long_list;
   a.seg_end = c.seg_end;
   a.flag = c.flag;
+  a.flag2 = c.flag;
   a.N = c.N;
   a.d = c.d;
   a.ch = c.ch;

@@ -38,6 +38,8 @@ struct SegArgs {
                             // chunks starts in it, else (-1, 0); every chunk writes its slot
   int32_t* seg_end;         // [rows]: end chunk of a crossing segment, by key
   const uint32_t* flag;     // sticky error bits: nonzero voids the update
+  const uint32_t* flag2;    // the error word of this list's sort (a training step's sort
+                            // set raises its own word; otherwise the same as flag)
   int N, d, ch, seg_stride;
   float alpha;
   // completed pieces are added as they close (float atomics), not deferred
@@ -86,6 +88,13 @@ __device__ __forceinline__ ChunkInfo chunk_info(const int32_t* __restrict__ sk,
   return ci;
 }
 
+// Nonzero when an earlier launch raised an error that voids this update.
+template <class A>
+__device__ __forceinline__ uint32_t void_bits(const A& a) {
+  return *reinterpret_cast<const volatile uint32_t*>(a.flag) |
+         *reinterpret_cast<const volatile uint32_t*>(a.flag2);
+}
+
 // Chunk size of a sorted list of N entries: short chunks spread small
 // batches over more waves; long chunks keep partials few for large ones.
 __host__ __device__ inline int seg_chunk_size(int N) { return N <= 131072 ? 16 : 64; }
@@ -119,9 +128,9 @@ template <int CH, bool LOCAL, class A>
 __device__ void seg_apply_rows(const A& a, int i0, int end, int chunk, const ChunkSink& sink) {
   static_assert(CH % 8 == 0 && CH <= kWave, "rows are walked in blocks of 8");
   const int lane = lane_id();
-  // the error flag (set by an earlier launch) is read beside the chunk's
+  // the error words (set by earlier launches) are read beside the chunk's
   // keys, and tested before any write
-  const uint32_t flag = *a.flag;
+  const uint32_t flag = *a.flag | *a.flag2;
   const ChunkInfo ci = chunk_info(a.sk, a.sv, end, i0, CH);
   if (__builtin_amdgcn_readfirstlane(flag) != 0u) return;  // a bad id voids the update
   const int nact = ci.nact;

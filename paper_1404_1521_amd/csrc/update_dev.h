@@ -89,12 +89,12 @@ __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
       for (int c = blockIdx.x * kWavesPerBlock + w; c < nchunks; c += a.n_e * kWavesPerBlock)
         seg_apply_chunk<CH>(a.s, c);
     } else {
-      if (*reinterpret_cast<const volatile uint32_t*>(a.s.flag)) return;
+      if (void_bits(a.s)) return;
       atomic_rows(a.s, kf, blockIdx.x, a.n_e);
     }
     return;
   }
-  const bool bad = (*reinterpret_cast<const volatile uint32_t*>(a.s.flag)) != 0u;
+  const bool bad = void_bits(a.s) != 0u;
   const int gid = (blockIdx.x - a.n_e) * kBlock + t;
   const int nthreads = (gridDim.x - a.n_e) * kBlock;
   if (a.n_d > 0) dense_sgd(a.dn, gid, nthreads, bad);
@@ -110,14 +110,14 @@ __global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
   __shared__ int meta[kPartApplyWaves][5];
   const int t = threadIdx.x;
   if ((int)blockIdx.x < a.n_part) {
-    // the flag was set (or not) by an earlier launch: every wave reads the
-    // same value, so the whole workgroup leaves together
-    if (__builtin_amdgcn_readfirstlane(*a.s.flag) != 0u) return;
+    // the error words were set (or not) by earlier launches: every wave
+    // reads the same value, so the whole workgroup leaves together
+    if (__builtin_amdgcn_readfirstlane(void_bits(a.s)) != 0u) return;
     const int p = blockIdx.x;
     seg_apply_partition(a.s, a.part_off[p], a.part_off[p + 1], F, Lp, meta);
     return;
   }
-  const bool bad = (*reinterpret_cast<const volatile uint32_t*>(a.s.flag)) != 0u;
+  const bool bad = void_bits(a.s) != 0u;
   const int gid = (blockIdx.x - a.n_part) * kPartApplyThreads + t;
   const int nthreads = (gridDim.x - a.n_part) * kPartApplyThreads;
   if (a.n_d > 0) dense_sgd(a.dn, gid, nthreads, bad);
@@ -135,7 +135,7 @@ __global__ __launch_bounds__(kSegfixThreads) void k_segfix(A a) {
   __shared__ float red[kSegfixWaves * kMaxD];
   __shared__ int heavy[kSegfixWaves][3];  // (start chunk, row, partials)
   __shared__ int nheavy;
-  if (*a.flag) return;
+  if (void_bits(a)) return;
   const uint32_t cnt = (uint32_t)((a.N + a.ch - 1) / a.ch);
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);

@@ -26,3 +26,17 @@ def pytest_collection_modifyitems(config, items):
         for item in items:
             if "gpu" in item.keywords:
                 item.add_marker(skip)
+
+
+def pytest_sessionfinish(session, exitstatus):
+    """With PG_MARGINS_OUT set, writes the largest error-to-bar ratios that
+    the step parity tests reached (per case and tensor) as JSON lines."""
+    path = os.environ.get("PG_MARGINS_OUT")
+    mod = sys.modules.get("test_gpu_parity") or sys.modules.get("tests.test_gpu_parity")
+    if not path or mod is None or not getattr(mod, "MARGINS", None):
+        return
+    import json
+    with open(path, "w") as f:
+        for case, k, pr, dr in mod.MARGINS:
+            f.write(json.dumps({"case": case, "tensor": k, "param_ratio": round(pr, 4),
+                                "delta_ratio": round(dr, 4)}) + "\n")

@@ -87,6 +87,12 @@ def test_null_context_is_rejected(lib):
     assert lib.polyglot_train_step(None, *([None] * 7), 1, ctypes.c_float(0.1), None) == pg.ENULL
     assert lib.polyglot_train_steps(None, *([None] * 7), 1, 1, ctypes.c_float(0.1),
                                     None) == pg.ENULL
+    loss = ctypes.c_float(7.0)
+    assert lib.polyglot_train_step_sync(None, *([None] * 7), 1, ctypes.c_float(0.1),
+                                        ctypes.byref(loss)) == pg.ENULL
+    assert lib.polyglot_train_step_sync(None, *([None] * 7), 1, ctypes.c_float(0.1),
+                                        None) == pg.ENULL
+    assert loss.value == 7.0
     assert lib.polyglot_score(None, *([None] * 6), 1, None) == pg.ENULL
     assert lib.polyglot_gather(None, None, None, None, 1, None, None) == pg.ENULL
     assert lib.polyglot_scatter_add(None, None, 1, 4, None, None, 1, ctypes.c_float(1.0),

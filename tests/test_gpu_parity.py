@@ -10,6 +10,7 @@ Bars (see the design notes for their derivation):
   * scatter-add: within the worst-case float32 summation bound
     n * 2^-24 * (|t0| + sum |alpha Y|) per element, n = entries of the row + 1.
 """
+import ctypes
 import dataclasses
 
 import numpy as np
@@ -47,11 +48,23 @@ def rms(a):
     return float(np.sqrt(np.mean(a * a))) if a.size else 0.0
 
 
-def assert_params_close(got, ref, init, stores, entries=None):
+MARGINS = []  # (case, tensor, largest err/bar of the parameters, of the deltas)
+
+
+def assert_params_close(got, ref, init, stores, entries=None, rows=None, case=""):
     """stores[k]: per-element count of float32 stores over the run (steps for
     the dense tensors, steps touching the row for E); entries: per-row count
     of scatter entries, given for the atomic variant, which rounds once per
-    entry instead of once per row and step."""
+    entry instead of once per row and step.  rows: if given, E is compared on
+    these rows only (the rest must then be bit-identical to init, which the
+    caller checks)."""
+    if rows is not None:
+        got = dict(got, E=got["E"][rows])
+        ref = dict(ref, E=ref["E"][rows])
+        init = dict(init, E=init["E"][rows])
+        stores = dict(stores, E=np.asarray(stores["E"])[rows])
+        if entries is not None:
+            entries = entries[rows]
     for k in ("E", "W1", "b1", "w2", "b2"):
         g = got[k].astype(np.float64)
         r = ref[k].astype(np.float64)
@@ -68,12 +81,15 @@ def assert_params_close(got, ref, init, stores, entries=None):
         dr = r - init[k]
         derr = np.abs(dg - dr)
         dbar = 2e-3 * np.abs(dr) + 2e-3 * rms(dr) + floor
+        MARGINS.append((case, k, float(np.max(err / bar)), float(np.max(derr / dbar))))
         assert np.all(derr <= dbar), (k, "delta", float(np.max(derr - dbar)), rms(dr))
 
 
-def run_both(w, steps, B, mode=0, lr=None, seed=None, p0=None, batches=None, check=True):
+def run_both(w, steps, B, mode=0, lr=None, seed=None, p0=None, batches=None, check=True,
+             touched_only=False):
     """Runs `steps` SGD steps on the GPU and in the float32-storage oracle and
-    compares losses and parameters."""
+    compares losses and parameters (with touched_only, E on the rows the
+    steps touched, the others bit-identical)."""
     m = pg()
     lr = w.lr if lr is None else lr
     p = workloads.init_params(w, seed) if p0 is None else {k: v.copy() for k, v in p0.items()}
@@ -97,7 +113,13 @@ def run_both(w, steps, B, mode=0, lr=None, seed=None, p0=None, batches=None, che
     if check:
         np.testing.assert_allclose(gl, rl, rtol=1e-5, atol=1e-6)
         stores = {"E": row_steps, "W1": steps, "b1": steps, "w2": steps, "b2": steps}
-        assert_params_close(got, p, init, stores, row_entries if mode == 1 else None)
+        rows = None
+        if touched_only:
+            rows = np.flatnonzero(row_steps)
+            untouched = row_steps == 0
+            assert np.array_equal(got["E"][untouched], init["E"][untouched].astype(np.float32))
+        assert_params_close(got, p, init, stores, row_entries if mode == 1 else None, rows,
+                            f"{w.name} B={B} mode={mode} lr={lr} steps={steps}")
     return got, p, init, gl, rl, ctx
 
 
@@ -459,6 +481,50 @@ def test_stress_full_size_sampled():
     assert np.array_equal(host(pd["b2"]), p["b2"])
 
 
+@pytest.mark.parametrize("mode,steps", [(0, 3), (1, 1)])
+def test_stress_full_size_parity(mode, steps):
+    """The stress workload at its full size (V 1M, d 128, window 11, H 256,
+    B 16384, lr 0.005) against the oracle: per-step losses, W1, b1, w2, b2
+    and the touched rows of E under the parameter and delta bars, the other
+    rows bit-identical.  This is the one shape that runs the wide-layer
+    backward with 16 dW1 slices, the multi-tile sort and 64-entry chunks
+    together."""
+    w = PRESETS["stress"]
+    run_both(w, steps, w.B, mode, touched_only=True)
+
+
+@pytest.mark.parametrize("B,lr,S", [(16, 1.0, 64), (4096, 4.0, 8), (1024, 0.25 * 8.0, 16)])
+def test_planted_task_high_rate_parity(B, lr, S):
+    """The batch-size study's regime (the planted task of the convergence
+    study, learning rates 1.0 to 4.0) through train_steps, the call the
+    study times, against the oracle: per-step losses and the parameters
+    under the same bars as every other step test."""
+    m = pg()
+    task = workloads.PLANTED
+    w = task.workload(B, lr)
+    p = workloads.init_params(w)
+    init = {k: v.astype(np.float64) for k, v in p.items()}
+    rng = np.random.default_rng([task.seed, 4, B])
+    wins, cors = task.batch(rng, S * B)
+    wins, cors = wins.reshape(S, B, task.win), cors.reshape(S, B)
+    st = torch.cuda.Stream()
+    with torch.cuda.stream(st):
+        pd = params_dev(p)
+        ctx = m.Context(task.V, task.d, task.win, task.H, max_batch=B, stream=st)
+        losses = torch.zeros(S, device="cuda")
+        ctx.train_steps(pd, dev(wins), dev(cors), lr, losses)
+        st.synchronize()
+    assert ctx.status() == m.OK
+    ref_losses = [oracle.train_step(p, wins[s], cors[s], lr) for s in range(S)]
+    row_steps = np.zeros(task.V)
+    for s in range(S):
+        row_steps[np.unique(np.concatenate([wins[s].reshape(-1), cors[s]]))] += 1
+    np.testing.assert_allclose(host(losses), ref_losses, rtol=1e-5, atol=1e-6)
+    got = {k: host(v) for k, v in pd.items()}
+    stores = {"E": row_steps, "W1": S, "b1": S, "w2": S, "b2": S}
+    assert_params_close(got, p, init, stores, case=f"planted B={B} lr={lr} S={S}")
+
+
 @pytest.mark.parametrize("name,B", [("tiny", 32), ("poly256", 256), ("poly256", 4096)])
 def test_touched_rows_bit_exact(name, B):
     w = PRESETS[name]
@@ -597,6 +663,88 @@ def test_out_of_range_id_voids_the_step():
         for k in p:
             assert np.array_equal(host(pd[k]), p[k]), k
         assert ctx.status() == m.OK
+
+
+@pytest.mark.parametrize("graph", [False, True])
+@pytest.mark.parametrize("shape", ["sweep", "wide"])
+def test_bad_id_in_next_step_leaves_this_step_intact(shape, graph):
+    """Two steps in one call, a bad id only in the second.  From 12,288
+    entries up (and for every wide layer) the second step's sort runs on a
+    side stream while the first step updates; it raises its own error word,
+    so the first step must equal a single valid step bit for bit and only
+    the second is void."""
+    m = pg()
+    if shape == "sweep":
+        w, B = PRESETS["poly256"], 2048
+    else:
+        w, B = LARGE_SHAPES[1], 1030
+    p0 = workloads.init_params(w)
+    (w0, c0), (w1, c1) = workloads.batch(w, 0, B), workloads.batch(w, 1, B)
+    w1 = w1.copy()
+    w1[B // 2, w.win // 2] = w.V  # out of range, in the second step only
+    st = torch.cuda.Stream() if graph else torch.cuda.current_stream()
+    with torch.cuda.stream(st):
+        a = params_dev(p0)
+        ctx = m.Context(w.V, w.d, w.win, w.H, max_batch=B, stream=st)
+        la = torch.zeros(2, device="cuda")
+        ctx.train_steps(a, dev(np.stack([w0, w1])), dev(np.stack([c0, c1])), 0.5, la)
+        st.synchronize()
+        assert ctx.status() == m.EID
+        assert ctx.status() == m.OK
+        b = params_dev(p0)
+        lb = torch.zeros(1, device="cuda")
+        ctx.train_step(b, dev(w0), dev(c0), 0.5, lb)
+        st.synchronize()
+        assert ctx.status() == m.OK
+    got = host(la)
+    assert got[0] == host(lb)[0]
+    assert np.isnan(got[1])
+    for k in p0:
+        assert np.array_equal(host(a[k]), host(b[k])), k
+
+
+def test_train_step_sync_returns_the_step_loss():
+    m = pg()
+    w = PRESETS["poly256"]
+    p0 = workloads.init_params(w)
+    B = 4096
+    win, cor = workloads.batch(w, 2, B)
+    ctx = m.Context(w.V, w.d, w.win, w.H, max_batch=B)
+    a, b = params_dev(p0), params_dev(p0)
+    la = torch.zeros(1, device="cuda")
+    ctx.train_step(a, dev(win), dev(cor), 0.3, la)
+    lb = ctx.train_step_sync(b, dev(win), dev(cor), 0.3)
+    assert isinstance(lb, float)
+    assert np.float32(lb) == host(la)[0]
+    for k in p0:
+        assert np.array_equal(host(a[k]), host(b[k])), k
+    # host errors: nothing enqueued, the output untouched
+    args = ctx._params(b)
+    wd, cd = dev(win), dev(cor)
+    wp, cp = ctypes.c_void_p(wd.data_ptr()), ctypes.c_void_p(cd.data_ptr())
+    out = ctypes.c_float(7.0)
+    lib = ctx._lib
+    assert lib.polyglot_train_step_sync(ctx._h, *args, wp, cp, B, ctypes.c_float(0.3),
+                                        None) == m.ENULL
+    assert lib.polyglot_train_step_sync(ctx._h, *args, wp, cp, 0, ctypes.c_float(0.3),
+                                        ctypes.byref(out)) == m.EBATCH
+    assert lib.polyglot_train_step_sync(ctx._h, *args, wp, cp, B + 1, ctypes.c_float(0.3),
+                                        ctypes.byref(out)) == m.EBATCH
+    assert lib.polyglot_train_step_sync(ctx._h, *args, wp, cp, B, ctypes.c_float(float("nan")),
+                                        ctypes.byref(out)) == m.EINVAL
+    assert out.value == 7.0
+    for k in p0:
+        assert np.array_equal(host(a[k]), host(b[k])), k
+    # an out-of-range id: EID, a NaN loss, no parameter changed
+    bad = win.copy()
+    bad[3, 0] = -1
+    with pytest.raises(m.PolyglotError) as e:
+        ctx.train_step_sync(b, dev(bad), dev(cor), 0.3)
+    assert e.value.rc == m.EID
+    assert ctx.status() == m.EID
+    assert ctx.status() == m.OK
+    for k in p0:
+        assert np.array_equal(host(a[k]), host(b[k])), k
 
 
 def test_host_errors_enqueue_nothing():
