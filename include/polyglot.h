@@ -154,6 +154,34 @@ int polyglot_scatter_add(polyglot_ctx* ctx, float* table, int32_t rows, int32_t 
                          const int32_t* idx, const float* Y, int32_t N, float alpha,
                          int32_t mode);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the sorted
+ * mode of polyglot_scatter_add -- table[idx[k]] += alpha * Y[k] for every k in
+ * [0, N), repeated indices accumulated in entry order, each touched row
+ * written once -- with no context.  It allocates nothing: its sort buffers
+ * live in a static device array of POLYGLOT_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every GPU it runs on until the process ends.
+ *   table[rows][d], Y[N][d] float32 and idx[N] int32: device pointers owned by
+ *     the caller; table and Y 16-byte aligned; d a multiple of 4 up to 256;
+ *     1 <= rows <= POLYGLOT_NOALLOC_MAX_ROWS.
+ *   1 <= N <= POLYGLOT_NOALLOC_MAX_N, else POLYGLOT_EBATCH.
+ *   status_dev: device int32 (may be NULL), written on the device with
+ *     POLYGLOT_OK, or POLYGLOT_EID when an index is outside [0, rows), in
+ *     which case the call leaves the table untouched.  Nothing is sticky:
+ *     every call starts clean.
+ *   stream: hipStream_t the two launches go on (NULL = the default stream).
+ * Returns POLYGLOT_OK once enqueued, POLYGLOT_ENULL, POLYGLOT_EBATCH,
+ * POLYGLOT_EINVAL (rows, d, alignment, non-finite alpha) before anything is
+ * enqueued, or POLYGLOT_EHIP.  All calls on one GPU share its scratch array:
+ * calls that may overlap in time on one GPU (several streams or host
+ * threads) race and must be serialised by the caller. */
+#define POLYGLOT_NOALLOC_MAX_N 8192
+#define POLYGLOT_NOALLOC_MAX_ROWS (1 << 26)
+#define POLYGLOT_NOALLOC_SCRATCH_BYTES 66816
+int polyglot_scatter_add_noalloc(float* table, int32_t rows, int32_t d, const int32_t* idx,
+                                 const float* Y, int32_t N, float alpha, int32_t* status_dev,
+                                 void* stream);
+
 /* Storage formats and operations of polyglot_scatter_update. */
 #define POLYGLOT_F32 0  /* IEEE binary32 */
 #define POLYGLOT_BF16 1 /* bfloat16: the upper 16 bits of a binary32 */

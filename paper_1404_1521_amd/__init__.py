@@ -30,7 +30,7 @@ _CODE_NAMES = {EINVAL: "EINVAL", ENULL: "ENULL", EBATCH: "EBATCH", EHIP: "EHIP",
 # Every entry point declared in include/polyglot.h.
 EXPORTS = ("polyglot_init", "polyglot_destroy", "polyglot_set_stream", "polyglot_train_step",
            "polyglot_train_step_sync", "polyglot_train_steps", "polyglot_score", "polyglot_gather", "polyglot_scatter_add",
-           "polyglot_scatter_update",
+           "polyglot_scatter_update", "polyglot_scatter_add_noalloc",
            "polyglot_touched_rows", "polyglot_status", "polyglot_last_error",
            "polyglot_set_timing", "polyglot_kernel_times")
 KERNEL_NAMES = ("fwdbwd", "sort", "update", "gather", "scatter", "score", "segfix", "wide_dw1",
@@ -73,6 +73,7 @@ def load_library():
         "polyglot_gather": [p, p, p, p, i32, p, p],
         "polyglot_scatter_add": [p, p, i32, i32, p, p, i32, f32, i32],
         "polyglot_scatter_update": [p, p, i32, i32, i32, p, i32, p, i32, f32, i32, i32],
+        "polyglot_scatter_add_noalloc": [p, i32, i32, p, p, i32, f32, p, p],
         "polyglot_touched_rows": [p, p, i32, p],
         "polyglot_status": [p],
         "polyglot_last_error": [p],
@@ -99,6 +100,28 @@ def _dev_tensor(t, dtype, name, shape=None):
     if shape is not None and tuple(t.shape) != tuple(shape):
         raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
     return ctypes.c_void_p(t.data_ptr())
+
+
+NOALLOC_MAX_N = 8192  # POLYGLOT_NOALLOC_MAX_N
+
+
+def scatter_add_noalloc(table, idx, Y, alpha: float = 1.0, status=None, stream=None) -> None:
+    """table[idx[k]] += alpha * Y[k] (sorted mode) through the entry point that
+    allocates nothing and needs no context (N <= NOALLOC_MAX_N).  status: an
+    optional int32 device tensor of one element that receives OK or EID on
+    the device.  Asynchronous on `stream` (default: torch's current stream)."""
+    lib = load_library()
+    rows, d = table.shape
+    N = idx.shape[0]
+    st = stream if stream is not None else torch.cuda.current_stream()
+    sp = None if status is None else _dev_tensor(status, torch.int32, "status", (1,))
+    rc = lib.polyglot_scatter_add_noalloc(
+        _dev_tensor(table, torch.float32, "table"), rows, d,
+        _dev_tensor(idx, torch.int32, "idx", (N,)),
+        _dev_tensor(Y, torch.float32, "Y", (N, d)), N, alpha, sp,
+        ctypes.c_void_p(st.cuda_stream))
+    if rc != OK:
+        raise PolyglotError(rc, "scatter_add_noalloc")
 
 
 class Context:

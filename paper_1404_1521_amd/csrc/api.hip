@@ -9,6 +9,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -936,3 +937,92 @@ int polyglot_kernel_times(polyglot_ctx* ctx, double* ms, int32_t* launches) {
 const char* polyglot_last_error(const polyglot_ctx* ctx) { return ctx ? ctx->err.c_str() : ""; }
 
 }  // extern "C"
+
+// ------------------------------------------------------------ no-alloc scatter-add
+// polyglot_scatter_add_noalloc keeps its sort buffers in `scratch`, a
+// file-scope device array that every GPU the library runs on holds for the
+// life of the process.  Host code never passes the array's name to a kernel
+// (on the host it is only a stand-in for the symbol): the device address comes
+// from hipGetSymbolAddress, once per device, with that device current.
+namespace {
+
+static_assert(pg::kStatusOk == POLYGLOT_OK && pg::kStatusBadId == POLYGLOT_EID,
+              "device status words must equal the ABI codes");
+constexpr int kNoAllocMaxN = POLYGLOT_NOALLOC_MAX_N;
+constexpr int kNoAllocPartWords = 256;  // partition starts (129 used), one 1 KiB block
+constexpr int kNoAllocFlagWords = 64;   // error flag, then the status word used when the
+                                        // caller passes none, one 256-byte block
+constexpr size_t kNoAllocWords = 2 * (size_t)kNoAllocMaxN + kNoAllocPartWords + kNoAllocFlagWords;
+static_assert(kNoAllocWords * 4 == POLYGLOT_NOALLOC_SCRATCH_BYTES, "scratch size");
+constexpr int kNoAllocMaxDevices = 64;
+
+std::mutex g_noalloc_mu;
+uint32_t* g_noalloc_ptr[kNoAllocMaxDevices];
+
+}  // namespace
+
+// Layout (32-bit words): sorted keys [kNoAllocMaxN], entry ids [kNoAllocMaxN],
+// partition starts [kNoAllocPartWords], error flag and spare status word.
+static __device__ __align__(256) uint32_t scratch[kNoAllocWords];
+
+namespace {
+
+// Device address of this device's copy of `scratch` (null on a HIP error).
+uint32_t* noalloc_scratch() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kNoAllocMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  if (!g_noalloc_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_noalloc_ptr[dev] = static_cast<uint32_t*>(ptr);
+  }
+  return g_noalloc_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" int polyglot_scatter_add_noalloc(float* table, int32_t rows, int32_t d,
+                                            const int32_t* idx, const float* Y, int32_t N,
+                                            float alpha, int32_t* status_dev, void* stream) {
+  if (!table || !idx || !Y) return POLYGLOT_ENULL;
+  if (N <= 0 || N > kNoAllocMaxN) return POLYGLOT_EBATCH;
+  if (rows <= 0 || rows > POLYGLOT_NOALLOC_MAX_ROWS || d <= 0 || d > kMaxD || d % 4 != 0)
+    return POLYGLOT_EINVAL;
+  if (!aligned16(table) || !aligned16(Y) || !std::isfinite(alpha)) return POLYGLOT_EINVAL;
+  const SortPlan plan = make_plan(rows, N);
+  if (!plan.small) return POLYGLOT_EINVAL;  // not reached within the limits above
+  uint32_t* base = noalloc_scratch();
+  if (!base) return POLYGLOT_EHIP;
+  int32_t* keys = reinterpret_cast<int32_t*>(base);
+  int32_t* vals = reinterpret_cast<int32_t*>(base + kNoAllocMaxN);
+  int32_t* part_off = reinterpret_cast<int32_t*>(base + 2 * kNoAllocMaxN);
+  uint32_t* flag = base + 2 * kNoAllocMaxN + kNoAllocPartWords;
+  SortBufs sb{};
+  sb.keys[0] = sb.keys[1] = keys;
+  sb.vals[0] = sb.vals[1] = vals;
+  sb.part_off = part_off;
+  sb.flag = flag;
+  // the sort rewrites the flag (no clearing launch) and the status word
+  sb.fresh_status = status_dev ? status_dev : reinterpret_cast<int32_t*>(flag + 1);
+  ApplyArgs aa{};
+  aa.s.table = table;
+  aa.s.Y = Y;
+  aa.s.sk = keys;
+  aa.s.sv = vals;
+  aa.s.flag = flag;
+  aa.s.flag2 = flag;
+  aa.s.N = N;
+  aa.s.d = d;
+  aa.s.ch = seg_chunk_size(N);
+  aa.s.seg_stride = d;
+  aa.s.alpha = alpha;
+  aa.mode = 0;
+  aa.part_off = part_off;
+  aa.n_part = 1 << plan.part_bits;
+  Launch L;
+  L.s = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_sort_idx(IdxKeys{idx, rows}, N, plan, sb, L);
+  if (e == hipSuccess) e = launch_apply_part(aa, aa.n_part, L);
+  return e == hipSuccess ? POLYGLOT_OK : POLYGLOT_EHIP;
+}

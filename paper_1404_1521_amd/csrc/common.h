@@ -34,6 +34,9 @@ constexpr int kSmallBins = 1 << kSmallDigitBits;
 // Sticky device error bits.
 constexpr uint32_t kFlagBadId = 1u;
 constexpr uint32_t kFlagInternal = 2u;  // a sort position fell outside [0, N): a library bug
+// Status words written on the device (the values of POLYGLOT_OK and POLYGLOT_EID).
+constexpr int32_t kStatusOk = 0;
+constexpr int32_t kStatusBadId = -5;
 
 struct SortPlan {
   int passes;               // 0 when N <= 1 (nothing to order)

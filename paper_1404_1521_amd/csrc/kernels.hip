@@ -85,7 +85,8 @@ __global__ __launch_bounds__(kPartSortThreads) void k_sort_part(KeyFn kf, int N,
                                                                 SortBufs sb) {
   extern __shared__ uint32_t lds[];
   part_sort<kPartSortThreads>(kf, N, plan, blockIdx.x, sb.keys[plan.passes & 1],
-                              sb.vals[plan.passes & 1], sb.part_off, sb.flag, lds);
+                              sb.vals[plan.passes & 1], sb.part_off, sb.flag, lds,
+                              sb.fresh_status);
 }
 
 // Digit totals of a large list.

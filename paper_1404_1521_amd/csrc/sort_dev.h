@@ -249,10 +249,15 @@ __host__ __device__ constexpr size_t part_sort_lds_words(int nth) {
   return 2 * kSmallSortN + kSmallSortN / 2 + (size_t)(nth / kWave + 1) * kSmallBins + kPartSortMisc;
 }
 
+// fresh_status: null for a sort whose error flag is sticky (bad ids OR
+// kFlagBadId into *flag).  Otherwise the flag is rewritten by this sort: every
+// workgroup reads every key, so workgroup 0 alone stores *flag (kFlagBadId or
+// 0) and *fresh_status (kStatusBadId or kStatusOk), and nothing needs
+// clearing between calls.
 template <int NTH, class KeyFn>
 __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part,
                           int32_t* out_keys, int32_t* out_vals, int32_t* part_off, uint32_t* flag,
-                          uint32_t* lds) {
+                          uint32_t* lds, int32_t* fresh_status = nullptr) {
   constexpr int NW = NTH / kWave, UMAX = kSmallSortN / NTH;
   static_assert(NW + 1 <= kPartSortMisc, "scan scratch too small");
   uint32_t* bufA = lds;
@@ -285,7 +290,15 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
     mine += (act && pk == (uint32_t)part) ? 1u : 0u;
     below += (act && pk < (uint32_t)part) ? 1u : 0u;
   }
-  if (bad) atomicOr(flag, kFlagBadId);
+  if (fresh_status) {
+    const int any = __syncthreads_or(bad ? 1 : 0);
+    if (part == 0 && t == 0) {
+      *flag = any ? kFlagBadId : 0u;
+      *fresh_status = any ? kStatusBadId : kStatusOk;
+    }
+  } else if (bad) {
+    atomicOr(flag, kFlagBadId);
+  }
 
   // exclusive prefix over threads of (below << 16 | mine): each thread's
   // first slot in the partition, and at the end the partition's size and
@@ -389,6 +402,7 @@ struct SortBufs {
   int32_t* part_off;                // [partitions + 1] partitioned sort: where each partition starts
   int max_tiles;
   uint32_t* flag;                   // sticky error bits
+  int32_t* fresh_status;            // partitioned sort only: see part_sort (null: sticky flag)
 };
 
 __device__ __forceinline__ uint32_t os_word(uint32_t fl, uint32_t v) { return (fl << 30) | v; }
