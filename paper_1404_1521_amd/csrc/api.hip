@@ -93,6 +93,14 @@ SortPlan make_plan(int key_range, int N) {
   pl.part_bits = std::min(kPartBits, kb);
   pl.small = (N <= kSmallSortN && (kb - pl.part_bits) + pl.val_bits <= 32) ? 1 : 0;
   if (!pl.small) pl.part_bits = 0;
+  pl.key_bits = kb;
+  pl.bucket = (!pl.small && N <= kBkMaxN && kb <= kBkMaxKeyBits) ? 1 : 0;
+  if (pl.bucket) {  // grouped into a second buffer by two launches
+    pl.passes = 1;
+    pl.tile_keys = kBkTileKeys;
+    pl.ntiles = bk_tiles(N);
+    return pl;
+  }
   const int rb = kb - pl.part_bits;  // bits the radix passes rank
   const int digit = pl.small ? kSmallDigitBits : kMaxDigitBits;
   pl.passes = (rb + digit - 1) / digit;
@@ -527,7 +535,10 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   // passes of the largest key range this context sorts
   const int key_bits = bits_for((uint32_t)std::max({c.V, c.max_rows, 2}));
   const int max_passes = (key_bits + kMaxDigitBits - 1) / kMaxDigitBits;
-  const size_t nstatus = (size_t)max_passes * kMaxBins * ctx->max_tiles;
+  // look-back words of the multi-tile sort, or the (bucket, tile) words of the bucketed sort
+  const size_t nstatus =
+      std::max((size_t)max_passes * kMaxBins * ctx->max_tiles,
+               (size_t)kBkBuckets * bk_tiles(std::min(ctx->max_entries, kBkMaxN)));
   for (int k = 0; k < 4; ++k) {
     if (e == hipSuccess) e = alloc(ctx, &ws.keys[k], me);
     if (e == hipSuccess) e = alloc(ctx, &ws.vals[k], me);

@@ -47,6 +47,8 @@ struct SortPlan {
   int small;                // 1: partitioned sort (one launch, 2^part_bits workgroups)
   int val_bits;             // small path packs (key >> part_bits) << val_bits | entry
   int part_bits;            // small path: partitions by the low key bits
+  int bucket;               // 1: bucketed sort (mid-size lists; two launches, passes = 1)
+  int key_bits;             // bits of the key range
 };
 
 // Device workspace owned by a context (all sizes fixed at init).

@@ -120,12 +120,35 @@ static hipError_t launch_tiled_sort(const KeyFn& kf, int N, const SortPlan& plan
   return e;
 }
 
+// Bucketed sort of a mid-size list: tiles by bucket, then buckets.
+template <class KeyFn>
+__global__ __launch_bounds__(kBkThreads) void k_bk_tiles(KeyFn kf, int N, int ntiles, SortBufs sb) {
+  extern __shared__ uint32_t lds[];
+  bk_tiles(kf, N, ntiles, sb, lds);
+}
+
+__global__ __launch_bounds__(kBkSortThreads) void k_bk_buckets(int N, int ntiles, int key_bits,
+                                                               SortBufs sb) {
+  extern __shared__ uint32_t lds[];
+  bk_buckets(N, ntiles, key_bits, sb, lds);
+}
+
+constexpr int kBkTilesLdsWords = kBkBuckets * (kBkThreads / kWave + 1) + kBkScanN + 32;
+
 template <class KeyFn>
 static hipError_t launch_sort(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
                               const Launch& L) {
   if (plan.small)
     return pg_launch(k_sort_part<KeyFn>, dim3(1 << plan.part_bits), dim3(kPartSortThreads),
                      part_sort_lds_words(kPartSortThreads) * 4, L, kf, N, plan, sb);
+  if (plan.bucket) {
+    hipError_t e = pg_launch(k_bk_tiles<KeyFn>, dim3(plan.ntiles), dim3(kBkThreads),
+                             kBkTilesLdsWords * 4, L, kf, N, plan.ntiles, sb);
+    if (e == hipSuccess)
+      e = pg_launch(k_bk_buckets, dim3(bk_grid(N)), dim3(kBkSortThreads), kBkLdsWords * 4, L, N,
+                    plan.ntiles, plan.key_bits, sb);
+    return e;
+  }
   return launch_tiled_sort(kf, N, plan, sb, L);
 }
 

@@ -6,6 +6,7 @@
 #include "common.h"
 #include "seg_dev.h"
 #include "sort_dev.h"
+#include "bsort_dev.h"
 
 namespace pg {
 

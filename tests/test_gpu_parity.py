@@ -12,6 +12,7 @@ Bars (see the design notes for their derivation):
 """
 import ctypes
 import dataclasses
+import zlib
 
 import numpy as np
 import pytest
@@ -318,6 +319,65 @@ def test_scatter_add_many_sort_tiles(s):
     oracle.scatter_add(ref, idx, Y, 1.0)
     err = np.abs(outs[0].astype(np.float64) - ref.astype(np.float64))
     assert np.all(err <= scatter_bound(table, idx, Y, 1.0))
+    assert np.array_equal(outs[0], outs[1])
+
+
+def _bucket_case(kind):
+    rng = np.random.default_rng(zlib.crc32(kind.encode()))
+    if kind == "permuted_zipf":   # heavy rows at random ids: oversize hashed buckets, 1 pass
+        rows, d, N = 100_000, 64, 327_680
+        idx = rng.permutation(rows).astype(np.int32)[workloads.zipf_ids(rng, rows, 1.2, N)]
+    elif kind == "one_key":       # one hashed bucket holds every entry
+        rows, d, N = 100_000, 16, 50_000
+        idx = np.full(N, 77_777, np.int32)
+    elif kind == "wide_keys":     # 24-bit keys: 2 global passes, 3 LDS passes
+        rows, d, N = 1 << 24, 4, 200_000
+        idx = rng.permutation(rows).astype(np.int32)[workloads.zipf_ids(rng, rows, 1.1, N)]
+    elif kind == "few_keys":      # every key has a bucket of its own
+        rows, d, N = 50, 8, 30_000
+        idx = workloads.zipf_ids(rng, rows, 1.0, N)
+    elif kind == "one_key_per_bucket":  # keys below 576: hashed buckets of one or two keys
+        rows, d, N = 600, 32, 100_000
+        idx = rng.integers(0, rows, N).astype(np.int32)
+    elif kind == "uniform_mid":   # hashed buckets of 513..2048 entries: LDS radix passes
+        rows, d, N = 5_000, 8, 700_000
+        idx = rng.integers(0, rows, N).astype(np.int32)
+    else:                         # above 1,048,576 entries: the multi-tile look-back sort
+        rows, d, N = 100_000, 4, 1_200_000
+        idx = workloads.zipf_ids(rng, rows, 1.0, N)
+    t0 = rng.normal(0, 0.01, (rows, d)).astype(np.float32)
+    Y = rng.normal(0, 1e-3, (N, d)).astype(np.float32)
+    return t0, idx, Y
+
+
+@pytest.mark.parametrize("kind", ["permuted_zipf", "one_key", "wide_keys", "few_keys",
+                                  "one_key_per_bucket", "uniform_mid", "look_back"])
+def test_scatter_add_sort_paths(kind):
+    """Lists of 8,192 < N <= 1,048,576 entries take the bucketed sort (64
+    dedicated buckets for the smallest ids, 512 hashed ones for the rest);
+    these inputs reach its less common paths: heavy rows at random ids
+    (hashed buckets above 2,048 entries, ordered through global memory),
+    one key for every entry, 24-bit keys, key ranges inside the dedicated
+    buckets, buckets of one key, and hashed buckets sorted by LDS radix
+    passes; above 1,048,576 entries the multi-tile look-back sort.  Against
+    the oracle, the touched rows, and two calls bit-identical."""
+    t0, idx, Y = _bucket_case(kind)
+    rows, d = t0.shape
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=idx.size, max_rows=rows)
+    outs = []
+    for _ in range(2):
+        td = dev(t0)
+        ctx.scatter_add(td, dev(idx), dev(Y), -0.5, pg().SCATTER_SORTED)
+        assert ctx.status() == pg().OK
+        outs.append(host(td))
+        del td
+    ref = t0.copy()
+    oracle.scatter_add(ref, idx, Y, -0.5)
+    touched = np.zeros(rows, bool)
+    touched[idx] = True
+    err = np.abs(outs[0][touched].astype(np.float64) - ref[touched].astype(np.float64))
+    assert np.all(err <= scatter_bound(t0, idx, Y, -0.5)[touched])
+    assert np.array_equal(outs[0][~touched], t0[~touched])
     assert np.array_equal(outs[0], outs[1])
 
 
