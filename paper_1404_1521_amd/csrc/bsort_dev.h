@@ -143,8 +143,12 @@ constexpr int kBkLdsOff = kBkLdsRun + kBkScanN;           // [kBkMaxTiles] run o
 constexpr int kBkLdsMisc = kBkLdsOff + kBkMaxTiles;       // [kPartSortMisc] scan scratch
 constexpr int kBkLdsSort = kBkLdsMisc + kPartSortMisc;    // sort area
 constexpr int kBkSortNW = kBkSortThreads / kWave;
-// sort area: bufA, bufB [kBkCap], rank16 [kBkCap / 2], ent [kBkCap], hist [kSmallBins][NW+1]
-constexpr int kBkLdsSortWords = 3 * kBkCap + kBkCap / 2 + kSmallBins * (kBkSortNW + 1);
+constexpr int kBkLdsDigit = 8;   // digit of the LDS counting passes
+constexpr int kBkRankMax = 192;  // hashed buckets up to this size are ranked by counting
+// sort area: bufA, bufB [kBkCap], rank16 [kBkCap / 2], ent [kBkCap], hist [256][NW+1]
+constexpr int kBkLdsSortWords =
+    3 * kBkCap + kBkCap / 2 + (1 << kBkLdsDigit) * (kBkSortNW + 1);
+static_assert(kBkRankMax <= kBkSortThreads, "one thread per word");
 // the oversize path's counters [256][NW+1] and digit bases [256] alias the sort area
 static_assert(256 * (kBkSortNW + 1) + 256 <= kBkLdsSortWords, "oversize counters");
 constexpr int kBkLdsWords = kBkLdsSort + kBkLdsSortWords;
@@ -251,6 +255,9 @@ struct BkLoc {
   }
 };
 
+// Workgroup j < kBkHashed orders hashed bucket kBkDedicated + j (known before
+// any load, so its column of (offset, count) words is read beside the
+// totals); the others copy the units of the dedicated buckets in order.
 __device__ void bk_buckets(int N, int ntiles, int key_bits, const SortBufs& sb, uint32_t* lds) {
   constexpr int NTH = kBkSortThreads, P = kBkBuckets;
   uint32_t* tot = lds + kBkLdsTot;
@@ -260,36 +267,59 @@ __device__ void bk_buckets(int N, int ntiles, int key_bits, const SortBufs& sb, 
   uint32_t* misc = lds + kBkLdsMisc;
   uint32_t* sa = lds + kBkLdsSort;
   const int t = threadIdx.x;
-  // bucket totals -> starts; work units -> unit starts
-  for (int d = t; d < kBkScanN; d += NTH) {
-    const uint32_t m = d < P ? sb.totals[d] : 0u;
-    tot[d] = m;
-    uni[d] = m == 0u ? 0u : (d < kBkDedicated ? (m + kBkUnit - 1) / kBkUnit : 1u);
+  const uint32_t j = blockIdx.x;
+  const bool hashed = j < (uint32_t)kBkHashed;
+  int b = kBkDedicated + (int)j;
+  // bucket totals (and a hashed bucket's column), every load in flight at once
+  {
+    const uint32_t* col = sb.status + (size_t)b * ntiles;
+    uint32_t m[2], cw = 0u;
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int d = t + k * NTH;
+      m[k] = d < P ? sb.totals[d] : 0u;
+    }
+    if (hashed && t < ntiles) cw = col[t];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int d = t + k * NTH;
+      tot[d] = m[k];
+      uni[d] = (d < kBkDedicated && m[k]) ? (m[k] + kBkUnit - 1) / kBkUnit : 0u;
+      run[d] = (hashed && d == t && t < ntiles) ? (cw & 0xffffu) : 0u;
+    }
+    if (hashed && t < ntiles) off[t] = cw >> 16;
   }
   __syncthreads();
   block_exclusive_scan<NTH>(tot, kBkScanN, misc);
-  block_exclusive_scan<NTH>(uni, kBkScanN, misc);
-  const uint32_t j = blockIdx.x;
-  if (j >= uni[P]) return;  // past the last unit (uniform over the workgroup)
-  const int b = bk_floor(uni, P, j);
-  const uint32_t sub = j - uni[b];
+  uint32_t sub = 0u;
+  if (hashed) {
+    block_exclusive_scan<NTH>(run, kBkScanN, misc);
+  } else {
+    block_exclusive_scan<NTH>(uni, kBkScanN, misc);
+    const uint32_t u = j - (uint32_t)kBkHashed;
+    if (u >= uni[kBkDedicated]) return;  // past the last unit (uniform over the workgroup)
+    b = bk_floor(uni, kBkDedicated, u);
+    sub = u - uni[b];
+  }
   const uint32_t start = tot[b], M = tot[b + 1] - start;
   if (start + M > (uint32_t)N || tot[P] != (uint32_t)N) {  // inconsistent counters: a library bug
     if (t == 0) atomicOr(sb.flag, kFlagInternal);
     return;
   }
-  // the bucket's run in every tile
-  const uint32_t* col = sb.status + (size_t)b * ntiles;
-  for (int tt = t; tt < kBkScanN; tt += NTH) {
-    const uint32_t wv = tt < ntiles ? col[tt] : 0u;
-    run[tt] = wv & 0xffffu;
-    if (tt < ntiles) off[tt] = wv >> 16;
+  if (M == 0u) return;
+  if (!hashed) {  // the dedicated bucket's run in every tile
+    const uint32_t* col = sb.status + (size_t)b * ntiles;
+    for (int tt = t; tt < kBkScanN; tt += NTH) {
+      const uint32_t wv = tt < ntiles ? col[tt] : 0u;
+      run[tt] = wv & 0xffffu;
+      if (tt < ntiles) off[tt] = wv >> 16;
+    }
+    __syncthreads();
+    block_exclusive_scan<NTH>(run, kBkScanN, misc);
   }
-  __syncthreads();
-  block_exclusive_scan<NTH>(run, kBkScanN, misc);
   const BkLoc loc{sb.keys[1] + start, sb.vals[1] + start, sb.keys[0], sb.vals[0], run, off, ntiles};
 
-  if (b < kBkDedicated) {  // one key: copy this unit's entries, already in entry order
+  if (!hashed) {  // one key: copy this unit's entries, already in entry order
     const uint32_t lo = sub * kBkUnit, hi = min(M, lo + (uint32_t)kBkUnit);
     constexpr int U = kBkUnit / NTH;
     int32_t v[U];
@@ -309,8 +339,8 @@ __device__ void bk_buckets(int N, int ntiles, int key_bits, const SortBufs& sb, 
     return;
   }
 
-  const int hb = max(0, key_bits - kBkHashBits);  // bits of bk_high
-  if (M > (uint32_t)kBkCap) {  // oversize: stable 8-bit passes through global memory
+  if (M > (uint32_t)kBkCap) {
+    const int hb = max(0, key_bits - kBkHashBits);  // bits of bk_high  // oversize: stable 8-bit passes through global memory
     uint32_t* cnt = sa;                               // [256][NW + 1]
     uint32_t* base = sa + 256 * (kBkSortNW + 1);      // [256]
     const int np = (hb + 7) / 8;
@@ -329,7 +359,7 @@ __device__ void bk_buckets(int N, int ntiles, int key_bits, const SortBufs& sb, 
     return;
   }
 
-  // hashed bucket in LDS: words (order, index in the bucket), ranked stably
+  // hashed bucket in LDS: words (order, index in the bucket), distinct
   uint32_t* bufA = sa;
   uint32_t* bufB = bufA + kBkCap;
   uint16_t* rank16 = reinterpret_cast<uint16_t*>(bufB + kBkCap);
@@ -341,26 +371,33 @@ __device__ void bk_buckets(int N, int ntiles, int key_bits, const SortBufs& sb, 
     ent[i] = (uint32_t)loc.tv[s];
     bufA[i] = (bk_high(k) << kBkIdxBits) | (uint32_t)i;
   }
+  for (int i = (int)M + t; i < ((int)M + 15) / 16 * 16; i += NTH) bufA[i] = 0xffffffffu;  // pad
   __syncthreads();
-  uint32_t* res;
-  if (M <= (uint32_t)NTH) {  // distinct words: the place of a word is the count of smaller ones
+  const uint32_t* res;
+  if (M <= (uint32_t)kBkRankMax) {
+    // a word's place is the number of smaller words: one thread per word,
+    // broadcast reads of sixteen words per step (the order of the stable
+    // radix passes, without their scans)
     if (t < (int)M) {
       const uint32_t wv = bufA[t];
       uint32_t r = 0u;
-      int q = 0;
-      for (; q + 4 <= (int)M; q += 4) {
-        const uint4 x = *reinterpret_cast<const uint4*>(bufA + q);
-        r += (x.x < wv ? 1u : 0u) + (x.y < wv ? 1u : 0u) + (x.z < wv ? 1u : 0u) +
-             (x.w < wv ? 1u : 0u);
+      for (int q = 0; q < (int)M; q += 16) {
+        uint4 x[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) x[u] = *reinterpret_cast<const uint4*>(bufA + q + 4 * u);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          r += (x[u].x < wv ? 1u : 0u) + (x[u].y < wv ? 1u : 0u) + (x[u].z < wv ? 1u : 0u) +
+               (x[u].w < wv ? 1u : 0u);
       }
-      for (; q < (int)M; ++q) r += bufA[q] < wv ? 1u : 0u;
       bufB[r] = wv;
     }
     __syncthreads();
     res = bufB;
-  } else {
+  } else {  // stable LDS counting passes of up to 8 bits (one pass below 2^17 rows)
+    const int hb = max(0, key_bits - kBkHashBits);  // bits of bk_high
     SortPlan lp{};
-    lp.passes = (hb + kSmallDigitBits - 1) / kSmallDigitBits;
+    lp.passes = (hb + kBkLdsDigit - 1) / kBkLdsDigit;
     int sh = 0;
     for (int p = 0; p < lp.passes; ++p) {
       lp.bits[p] = hb / lp.passes + (p < hb % lp.passes ? 1 : 0);
