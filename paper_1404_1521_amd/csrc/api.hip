@@ -816,6 +816,10 @@ int polyglot_scatter_update(polyglot_ctx* ctx, void* table, int32_t dtype, int32
   c.n_e = std::max(1, std::min(ceil_div(ceil_div(N, op == POLYGLOT_OP_SET ? kWave : c.ch),
                                         kWavesPerBlock), 2048));
   c.n_z = plan.small ? 0 : 16;
+  // a partitioned (small) list is applied partition-wise, in one launch
+  c.part_off = ctx->ws.part_off[0];
+  c.partitioned = plan.small;
+  c.n_part = 1 << plan.part_bits;  // the partitions this sort wrote
   if (e == hipSuccess) {
     Timed tm(ctx, POLYGLOT_K_SCATTER);
     e = launch_gen_update(c, tm.L);

@@ -76,6 +76,7 @@ struct GenArgs {
   int N, d, ch, seg_stride;
   float alpha;
   ZeroRanges zero;          // sort counters cleared by the apply launch
+  const int32_t* part_off;  // partition starts of a partitioned sort
   // a row update is a load and a store: deferred past the walk (seg_add_rows)
   static constexpr bool kDeferred = true;
 };
@@ -83,6 +84,12 @@ struct GenArgs {
 template <class T>
 __device__ __forceinline__ float seg_load(const GenArgs<T>& a, size_t i) {
   return Elem<T>::get(a.Y[i]);
+}
+// A segment's sum v (alpha applied) added to element i by the row's only
+// writer: one rounding to the storage format.
+template <class T>
+__device__ __forceinline__ void seg_close(const GenArgs<T>& a, size_t i, float v) {
+  a.table[i] = Elem<T>::put(Elem<T>::get(a.table[i]) + v);
 }
 
 // The completed pieces of a chunk, after its walk: v[r] holds the sum of the
@@ -127,6 +134,19 @@ __global__ __launch_bounds__(kBlock) void k_gen_apply(GenArgs<T> a, int n_e) {
   }
   zero_ranges(a.zero, (size_t)(blockIdx.x - n_e) * kBlock + threadIdx.x,
               (size_t)(gridDim.x - n_e) * kBlock);
+}
+
+// Increment after a partitioned sort (N <= kSmallSortN): workgroup p applies
+// partition p, whose segments never leave it, so no fix-up follows; the
+// extra workgroups clear nothing (the small sort keeps no counters).
+template <class T>
+__global__ __launch_bounds__(kPartApplyThreads) void k_gen_apply_part(GenArgs<T> a) {
+  __shared__ float F[kPartApplyWaves][kMaxD];
+  __shared__ float Lp[kPartApplyWaves][kMaxD];
+  __shared__ int meta[kPartApplyWaves][5];
+  if (__builtin_amdgcn_readfirstlane(void_bits(a)) != 0u) return;
+  const int p = blockIdx.x;
+  seg_apply_partition<kPartApplyWaves>(a, a.part_off[p], a.part_off[p + 1], F, Lp, meta);
 }
 
 // Row access of the fix-up (seg_fix_row_wave / seg_fix_row, launched as

@@ -239,6 +239,7 @@ static GenArgs<T> gen_args(const GenCall& c) {
   a.seg_stride = c.seg_stride;
   a.alpha = c.alpha;
   a.zero = c.zero;
+  a.part_off = c.part_off;
   return a;
 }
 
@@ -246,6 +247,9 @@ template <class T>
 static hipError_t launch_gen_update_t(const GenCall& c, const Launch& L) {
   const dim3 grid(c.n_e + c.n_z), block(kBlock);
   if (c.op == 1) return pg_launch(k_gen_set<T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
+  if (c.partitioned)
+    return pg_launch(k_gen_apply_part<T>, dim3(c.n_part), dim3(kPartApplyThreads), 0, L,
+                     gen_args<T>(c));
   if (c.ch == 16) return pg_launch(k_gen_apply<16, T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
   return pg_launch(k_gen_apply<32, T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
 }
@@ -256,15 +260,16 @@ hipError_t launch_gen_update(const GenCall& c, const Launch& L) {
   return launch_gen_update_t<float>(c, L);
 }
 
+template <class T>
+static hipError_t launch_gen_fix_t(const GenCall& c, int grid, const Launch& L) {
+  if (c.partitioned) return hipSuccess;  // the partitions completed every segment
+  return pg_launch(k_segfix<GenArgs<T>>, dim3(grid), dim3(kSegfixThreads), 0, L, gen_args<T>(c));
+}
+
 hipError_t launch_gen_fix(const GenCall& c, int grid, const Launch& L) {
-  if (c.dtype == 1)
-    return pg_launch(k_segfix<GenArgs<BF16>>, dim3(grid), dim3(kSegfixThreads), 0, L,
-                     gen_args<BF16>(c));
-  if (c.dtype == 2)
-    return pg_launch(k_segfix<GenArgs<F16>>, dim3(grid), dim3(kSegfixThreads), 0, L,
-                     gen_args<F16>(c));
-  return pg_launch(k_segfix<GenArgs<float>>, dim3(grid), dim3(kSegfixThreads), 0, L,
-                   gen_args<float>(c));
+  if (c.dtype == 1) return launch_gen_fix_t<BF16>(c, grid, L);
+  if (c.dtype == 2) return launch_gen_fix_t<F16>(c, grid, L);
+  return launch_gen_fix_t<float>(c, grid, L);
 }
 
 hipError_t launch_keys_from_i64(const int64_t* idx, int N, int rows, int32_t* keys,

@@ -177,12 +177,18 @@ struct GenCall {
   int op;     // 0 increment, 1 assignment
   int n_e;    // workgroups of the apply / assignment role
   int n_z;    // workgroups clearing the sort counters
+  // a partitioned (small) list: partition starts; its increments take one
+  // launch, one workgroup per partition, and no fix-up
+  const int32_t* part_off;
+  bool partitioned;
+  int n_part;
 };
 hipError_t launch_gen_update(const GenCall& c, const Launch& L);
 hipError_t launch_gen_fix(const GenCall& c, int grid, const Launch& L);
 hipError_t launch_keys_from_i64(const int64_t* idx, int N, int rows, int32_t* keys,
                                 uint32_t* flag, const Launch& L);
 hipError_t launch_apply_part(const ApplyArgs& a, int grid, const Launch& L);
+
 hipError_t launch_check_idx(const int32_t* idx, int N, int rows, uint32_t* flag, const Launch& L);
 hipError_t launch_score(const ScoreArgs& a, int NT, int cpw, const Launch& L);
 hipError_t launch_gather(const GatherArgs& a, const Launch& L);

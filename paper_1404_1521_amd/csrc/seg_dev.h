@@ -120,6 +120,11 @@ __device__ __forceinline__ float seg_load(const SegArgs& a, size_t i) { return a
 __device__ __forceinline__ void seg_add(const SegArgs& a, size_t i, bool cok, float v) {
   unsafeAtomicAdd(a.table + i, cok ? v : -0.f);
 }
+// A segment's sum v (alpha applied) added to table element i by the row's
+// only writer.
+__device__ __forceinline__ void seg_close(const SegArgs& a, size_t i, float v) {
+  unsafeAtomicAdd(a.table + i, v);
+}
 
 // One wave applies entries [i0, min(i0 + CH, end)) of the sorted list, chunk
 // number `chunk` (see the file comment).  A is SegArgs or another argument
@@ -234,7 +239,8 @@ constexpr int kPartApplyThreads = 1024;
 constexpr int kPartApplyWaves = kPartApplyThreads / kWave;
 constexpr int kPartApplyChunk = 64;
 
-// Segmented apply of one partition of a partitioned sort, entries [s, e):
+// Segmented apply of one partition of a partitioned sort (NW waves per
+// workgroup), entries [s, e):
 // no key has entries in two partitions, so every segment that crosses a
 // chunk is completed inside the workgroup.  Each round, wave w applies
 // chunk r0 + w and leaves its open pieces in LDS; after a barrier wave 0
@@ -242,7 +248,8 @@ constexpr int kPartApplyChunk = 64;
 // segment (carried over from earlier rounds when it started there) and
 // applying the row once the segment closes.  The order of every sum is
 // fixed, so the result does not depend on scheduling.
-__device__ void seg_apply_partition(const SegArgs& a, int s, int e,
+template <int NW, class A>
+__device__ void seg_apply_partition(const A& a, int s, int e,
                                     float (*F)[kMaxD], float (*Lp)[kMaxD], int (*meta)[5]) {
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -252,14 +259,14 @@ __device__ void seg_apply_partition(const SegArgs& a, int s, int e,
   int open_key = 0, open_key_next = 0;
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) open[cb] = 0.f;
-  for (int r0 = 0; r0 < nch; r0 += kPartApplyWaves) {
+  for (int r0 = 0; r0 < nch; r0 += NW) {
     const int c = r0 + w;
     if (c < nch)
       seg_apply_rows<kPartApplyChunk, true>(a, s + c * kPartApplyChunk, e, c,
                                             ChunkSink{F[w], Lp[w], meta[w]});
     __syncthreads();  // the round's open pieces are in LDS
     if (w == 0) {
-      const int nc = min(kPartApplyWaves, nch - r0);
+      const int nc = min(NW, nch - r0);
       // every chunk's flags and keys at once (lane k reads chunk k), then
       // taken as wave-uniform values
       int mk[5];
@@ -273,22 +280,22 @@ __device__ void seg_apply_partition(const SegArgs& a, int s, int e,
         if (cb * kWave >= a.d) break;
         const bool cok = col < a.d;
         // the round's open pieces of this column block, all reads in flight
-        float fv[kPartApplyWaves], lv[kPartApplyWaves];
+        float fv[NW], lv[NW];
 #pragma unroll
-        for (int k = 0; k < kPartApplyWaves; ++k) {
+        for (int k = 0; k < NW; ++k) {
           fv[k] = (k < nc && cok) ? F[k][col] : 0.f;
           lv[k] = (k < nc && cok) ? Lp[k][col] : 0.f;
         }
         float o = open[cb];
         int okey = open_key;
 #pragma unroll
-        for (int k = 0; k < kPartApplyWaves; ++k) {
+        for (int k = 0; k < NW; ++k) {
           if (k >= nc) break;
           const bool cf = (cfm >> k) & 1ull, ol = (olm >> k) & 1ull, sg = (sgm >> k) & 1ull;
           if (cf) {  // the chunk's first piece continues the open segment
             o += fv[k];
             if (!(sg && ol) && cok)  // ... and closes it: apply the row
-              unsafeAtomicAdd(a.table + (size_t)okey * a.d + col, a.alpha * o);
+              seg_close(a, (size_t)okey * a.d + col, a.alpha * o);
           }
           if (ol && !(sg && cf)) {  // the chunk's last piece opens a segment
             o = lv[k];

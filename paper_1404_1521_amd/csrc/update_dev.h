@@ -114,7 +114,7 @@ __global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
     // reads the same value, so the whole workgroup leaves together
     if (__builtin_amdgcn_readfirstlane(void_bits(a.s)) != 0u) return;
     const int p = blockIdx.x;
-    seg_apply_partition(a.s, a.part_off[p], a.part_off[p + 1], F, Lp, meta);
+    seg_apply_partition<kPartApplyWaves>(a.s, a.part_off[p], a.part_off[p + 1], F, Lp, meta);
     return;
   }
   const bool bad = void_bits(a.s) != 0u;
