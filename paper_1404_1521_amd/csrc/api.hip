@@ -240,6 +240,7 @@ SegArgs seg_args(polyglot_ctx* ctx, float* table, const float* Y, const SortPlan
   a.N = N;
   a.d = d;
   a.ch = seg_chunk_size(N);
+  a.rg = a.ch * kWavesPerBlock;
   a.seg_stride = ctx->seg_stride;
   a.alpha = alpha;
   return a;
@@ -253,7 +254,7 @@ int table_workgroups(const SegArgs& s, int mode) {
 }
 
 int segfix_workgroups(const SegArgs& s) {  // kSegfixWaves tasks per workgroup and round
-  return std::max(1, std::min(ceil_div(ceil_div(s.N, s.ch), kSegfixWaves), 2048));
+  return std::max(1, std::min(ceil_div(ceil_div(s.N, s.rg), kSegfixWaves), 2048));
 }
 
 // The sort of one step's entries into sort set `set`, on the side stream.
@@ -808,6 +809,7 @@ int polyglot_scatter_update(polyglot_ctx* ctx, void* table, int32_t dtype, int32
   c.N = N;
   c.d = d;
   c.ch = gen_chunk_size(N);
+  c.rg = c.ch * kWavesPerBlock;
   c.seg_stride = ctx->seg_stride;
   c.alpha = alpha;
   c.zero = sort_zero_ranges(ctx, plan, 0);
@@ -826,7 +828,7 @@ int polyglot_scatter_update(polyglot_ctx* ctx, void* table, int32_t dtype, int32
   }
   if (e == hipSuccess && op == POLYGLOT_OP_INC) {
     Timed tm(ctx, POLYGLOT_K_SEGFIX);
-    e = launch_gen_fix(c, std::max(1, std::min(ceil_div(ceil_div(N, c.ch), kSegfixWaves), 2048)),
+    e = launch_gen_fix(c, std::max(1, std::min(ceil_div(ceil_div(N, c.rg), kSegfixWaves), 2048)),
                        tm.L);
   }
   ctx->have_sorted = false;  // the sort buffers now hold this call's order

@@ -74,6 +74,7 @@ struct GenArgs {
   const uint32_t* flag;     // sticky error bits: nonzero voids the update
   const uint32_t* flag2;    // same word as flag (the general op has one sort of its own)
   int N, d, ch, seg_stride;
+  int rg;                   // entries per range of the apply (the fix-up's slots)
   float alpha;
   ZeroRanges zero;          // sort counters cleared by the apply launch
   const int32_t* part_off;  // partition starts of a partitioned sort
@@ -125,11 +126,14 @@ __device__ void seg_add_rows(const GenArgs<T>& a, const ChunkInfo& ci, uint64_t 
 // extra workgroups clear the sort counters.
 template <int CH, class T>
 __global__ __launch_bounds__(kBlock) void k_gen_apply(GenArgs<T> a, int n_e) {
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  __shared__ float F[kWavesPerBlock][kMaxD];
+  __shared__ float Lp[kWavesPerBlock][kMaxD];
+  __shared__ int meta[kWavesPerBlock][5];
   if ((int)blockIdx.x < n_e) {
-    const int nchunks = ceil_div(a.N, CH);
-    for (int c = blockIdx.x * kWavesPerBlock + w; c < nchunks; c += n_e * kWavesPerBlock)
-      seg_apply_rows<CH, false>(a, c * CH, a.N, c, ChunkSink{});
+    if (__builtin_amdgcn_readfirstlane(void_bits(a)) != 0u) return;
+    const int nranges = ceil_div(a.N, CH * kWavesPerBlock);
+    for (int r = blockIdx.x; r < nranges; r += n_e)
+      seg_apply_range<CH, kWavesPerBlock>(a, r, F, Lp, meta);
     return;
   }
   zero_ranges(a.zero, (size_t)(blockIdx.x - n_e) * kBlock + threadIdx.x,

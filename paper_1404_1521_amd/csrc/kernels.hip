@@ -236,6 +236,7 @@ static GenArgs<T> gen_args(const GenCall& c) {
   a.N = c.N;
   a.d = c.d;
   a.ch = c.ch;
+  a.rg = c.rg;
   a.seg_stride = c.seg_stride;
   a.alpha = c.alpha;
   a.zero = c.zero;

@@ -171,6 +171,7 @@ struct GenCall {
   int32_t* seg_end;
   const uint32_t* flag;
   int N, d, ch, seg_stride;
+  int rg;  // entries per range of the apply (the fix-up's slots)
   float alpha;
   ZeroRanges zero;
   int dtype;  // 0 float32, 1 bfloat16, 2 binary16

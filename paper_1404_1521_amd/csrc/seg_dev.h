@@ -41,6 +41,7 @@ struct SegArgs {
   const uint32_t* flag2;    // the error word of this list's sort (a training step's sort
                             // set raises its own word; otherwise the same as flag)
   int N, d, ch, seg_stride;
+  int rg;                   // entries per range (NW chunks of one workgroup): the fix-up's slots
   float alpha;
   // completed pieces are added as they close (float atomics), not deferred
   static constexpr bool kDeferred = false;
@@ -228,11 +229,6 @@ __device__ void seg_apply_rows(const A& a, int i0, int end, int chunk, const Chu
   }
 }
 
-template <int CH>
-__device__ void seg_apply_chunk(const SegArgs& a, int chunk) {
-  seg_apply_rows<CH, false>(a, chunk * CH, a.N, chunk, ChunkSink{});
-}
-
 // Threads of a partition workgroup: 16 waves, so one round covers 1024
 // entries in 64-entry chunks.
 constexpr int kPartApplyThreads = 1024;
@@ -309,6 +305,90 @@ __device__ void seg_apply_partition(const A& a, int s, int e,
     }
     __syncthreads();  // the slots are reused by the next round
   }
+}
+
+// One range of the whole sorted list: NW consecutive chunks of CH entries,
+// range r = entries [r*NW*CH, (r+1)*NW*CH), one chunk per wave of the
+// workgroup.  The chunks leave their open pieces in LDS; wave 0 walks them in
+// order, completing every segment that crosses a chunk boundary inside the
+// range, and exports at most two partials, by range, with the meaning a
+// chunk's have for the fix-up (seg_fix_row): slot 0 the first piece when it
+// continues a segment from an earlier range, slot 1 the last piece when a
+// segment starts here and continues into the next range (recorded in the
+// range's long_list slot; seg_end[key] = the range where such a segment
+// ends).  So segments crossing chunks inside a workgroup never reach the
+// fix-up, and a heavy row leaves one partial per range instead of one per
+// chunk.  Every sum has a fixed order.  The caller has tested the error flag.
+template <int CH, int NW, class A>
+__device__ void seg_apply_range(const A& a, int r, float (*F)[kMaxD], float (*Lp)[kMaxD],
+                                int (*meta)[5]) {
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
+  const int s = r * NW * CH;
+  const int nch = min(NW, (a.N - s + CH - 1) / CH);
+  if (w < nch)
+    seg_apply_rows<CH, true>(a, s + w * CH, a.N, 0, ChunkSink{F[w], Lp[w], meta[w]});
+  __syncthreads();  // the chunks' open pieces are in LDS
+  if (w == 0) {
+    int mk[5];
+#pragma unroll
+    for (int x = 0; x < 5; ++x) mk[x] = lane < nch ? meta[lane][x] : 0;
+    const uint64_t cfm = __ballot(mk[0] != 0), olm = __ballot(mk[1] != 0),
+                   sgm = __ballot(mk[2] != 0);
+    const bool cf0 = cfm & 1ull;                      // continues from an earlier range
+    const bool olL = (olm >> (nch - 1)) & 1ull;       // continues into the next range
+    const int32_t key0 = __builtin_amdgcn_readlane(mk[3], 0);
+    bool front_open = cf0;                            // (wave-uniform)
+    int32_t okey = 0;
+    for (int c0 = 0; c0 < a.d; c0 += kWave) {
+      const int col = c0 + lane;
+      const bool cok = col < a.d;
+      float fv[NW], lv[NW];
+#pragma unroll
+      for (int k = 0; k < NW; ++k) {
+        fv[k] = (k < nch && cok) ? F[k][col] : 0.f;
+        lv[k] = (k < nch && cok) ? Lp[k][col] : 0.f;
+      }
+      float o = 0.f, first = 0.f;
+      bool front = cf0;
+      int32_t ok = 0;
+#pragma unroll
+      for (int k = 0; k < NW; ++k) {
+        if (k >= nch) break;
+        const bool cf = (cfm >> k) & 1ull, ol = (olm >> k) & 1ull, sg = (sgm >> k) & 1ull;
+        if (cf) {  // the chunk's first piece continues the open segment
+          o += fv[k];
+          if (!(sg && ol)) {  // ... and closes it
+            if (front) {
+              first = o;  // the segment from an earlier range ends here
+              front = false;
+            } else if (cok) {
+              seg_close(a, (size_t)ok * a.d + col, a.alpha * o);
+            }
+          }
+        }
+        if (ol && !(sg && cf)) {  // the chunk's last piece opens a segment
+          o = lv[k];
+          ok = __builtin_amdgcn_readlane(mk[4], k);
+          front = false;
+        }
+      }
+      // the range's exports (front: the segment from an earlier range spans
+      // the whole range; it is then slot 0 and the range records nothing)
+      if (cok) {
+        if (cf0) a.seg_part[((size_t)r * 2 + 0) * a.seg_stride + col] = front ? o : first;
+        if (olL && !front) a.seg_part[((size_t)r * 2 + 1) * a.seg_stride + col] = o;
+      }
+      front_open = front;
+      okey = ok;
+    }
+    if (lane == 0) {
+      const bool starts_long = olL && !front_open;
+      a.long_list[r] = starts_long ? make_int2(r, okey) : make_int2(-1, 0);
+      if (cf0 && !(olL && front_open)) a.seg_end[key0] = r;
+    }
+  }
+  __syncthreads();  // the slots are reused by the workgroup's next range
 }
 
 // Fix-up workgroups: each takes kSegfixWaves crossing segments at a time,

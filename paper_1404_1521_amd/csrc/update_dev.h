@@ -79,15 +79,18 @@ __device__ void dense_sgd(const DenseArgs& a, int gid, int nthreads, bool bad) {
 
 template <int CH, class KeyFn>
 __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
+  __shared__ float F[kWavesPerBlock][kMaxD];
+  __shared__ float Lp[kWavesPerBlock][kMaxD];
+  __shared__ int meta[kWavesPerBlock][5];
   const int t = threadIdx.x;
-  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   if ((int)blockIdx.x < a.n_e) {
-    // all-or-nothing: an out-of-range id voids the update (the segmented
-    // apply tests the flag itself, once its loads are in flight)
+    // all-or-nothing: an out-of-range id voids the update.  The error words
+    // were set (or not) by earlier launches: the workgroup leaves together
     if (a.mode == 0) {
-      const int nchunks = ceil_div(a.s.N, CH);
-      for (int c = blockIdx.x * kWavesPerBlock + w; c < nchunks; c += a.n_e * kWavesPerBlock)
-        seg_apply_chunk<CH>(a.s, c);
+      if (__builtin_amdgcn_readfirstlane(void_bits(a.s)) != 0u) return;
+      const int nranges = ceil_div(a.s.N, CH * kWavesPerBlock);
+      for (int r = blockIdx.x; r < nranges; r += a.n_e)
+        seg_apply_range<CH, kWavesPerBlock>(a.s, r, F, Lp, meta);
     } else {
       if (void_bits(a.s)) return;
       atomic_rows(a.s, kf, blockIdx.x, a.n_e);
@@ -136,7 +139,7 @@ __global__ __launch_bounds__(kSegfixThreads) void k_segfix(A a) {
   __shared__ int heavy[kSegfixWaves][3];  // (start chunk, row, partials)
   __shared__ int nheavy;
   if (void_bits(a)) return;
-  const uint32_t cnt = (uint32_t)((a.N + a.ch - 1) / a.ch);
+  const uint32_t cnt = (uint32_t)((a.N + a.rg - 1) / a.rg);  // ranges of the apply
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   // slot li of a round goes to workgroup li % gridDim.x, so the segments of
