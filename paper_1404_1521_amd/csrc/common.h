@@ -70,10 +70,11 @@ struct Workspace {
   float* vpart;             // three-contraction path: [forward workgroups][2H + 2]
   float* vbuf;              // three-contraction path: [max_batch][3][H] dz + dz~, dz, dz~
   // segmented update
-  float* seg_part;          // [max_chunks][2][seg_stride] partial sums of long segments
-  int2* long_list;          // [max_chunks] by chunk: (chunk, row) if a segment crossing
-                            // chunks starts there, else (-1, 0)
-  int32_t* seg_end;         // [max(V, max_rows)] end chunk of a long segment, by row id
+  float* seg_part;          // [ranges][2][seg_stride] partial sums of long segments (sized
+                            // by chunks: at least the ranges of any call)
+  int2* long_list;          // [ranges] by range: (range, row) if a segment crossing
+                            // ranges starts there, else (-1, 0)
+  int32_t* seg_end;         // [max(V, max_rows)] end range of a long segment, by row id
   uint32_t* flag;           // sticky error bits [3]: word 0 raised by every launch except a
                             // training step's side-stream sort, word 1 + q by the side-stream
                             // sort of sort set q (read only by that set's update)

@@ -68,8 +68,8 @@ struct GenArgs {
   const T* Y;               // [N][d]
   const int32_t* sk;        // sorted keys [N]
   const int32_t* sv;        // entry ids in sorted order [N]
-  float* seg_part;          // [chunks][2][seg_stride] float32 partials
-  int2* long_list;          // by chunk, as in SegArgs
+  float* seg_part;          // [ranges][2][seg_stride] float32 partials
+  int2* long_list;          // by range, as in SegArgs
   int32_t* seg_end;         // [rows]
   const uint32_t* flag;     // sticky error bits: nonzero voids the update
   const uint32_t* flag2;    // same word as flag (the general op has one sort of its own)

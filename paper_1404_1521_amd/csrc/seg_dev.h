@@ -13,14 +13,18 @@
 // the L2 (no read round trip; one add per element, so the result does not
 // depend on scheduling).  Few registers per wave keep every wave of a large
 // launch resident at once.
-// A segment that crosses chunk boundaries (a heavy Zipf row) leaves one
-// partial per spanned chunk (slot 1: the open last piece of the chunk where
-// it starts; slot 0: the first piece of every later spanned chunk).  On the
-// whole list, the chunk where it starts records it in its own slot of the
-// segment list (no shared counter) and its end chunk is recorded by key; the fix-up launch adds the partials in a fixed order and
-// applies the row.  After a partitioned sort, where no key spans two
-// partitions, one workgroup per partition keeps the partials in LDS and
-// completes every segment itself (seg_apply_partition).
+// A segment that crosses chunk boundaries leaves the chunks' open pieces in
+// LDS, and one wave of the workgroup closes every segment that stays inside
+// the workgroup's chunks.  On the whole list a workgroup takes a range of
+// consecutive chunks (seg_apply_range); a segment that crosses ranges (a
+// heavy Zipf row) leaves one partial per spanned range (slot 1: the open
+// last piece of the range where it starts; slot 0: the first piece of every
+// later spanned range); the range where it starts records it in its own slot
+// of the segment list (no shared counter) and its end range is recorded by
+// key; the fix-up launch adds the partials in a fixed order and applies the
+// row.  After a partitioned sort, where no key spans two partitions, one
+// workgroup per partition completes every segment itself
+// (seg_apply_partition).
 // Sums never depend on scheduling, no row is written twice and no wave
 // waits on another workgroup.
 #pragma once
@@ -34,9 +38,9 @@ struct SegArgs {
   const int32_t* sk;        // sorted keys [N]
   const int32_t* sv;        // entry ids in sorted order [N]
   float* seg_part;          // [chunks][2][seg_stride]
-  int2* long_list;          // [chunks] by chunk: (chunk, row) if a segment that crosses
-                            // chunks starts in it, else (-1, 0); every chunk writes its slot
-  int32_t* seg_end;         // [rows]: end chunk of a crossing segment, by key
+  int2* long_list;          // [ranges] by range: (range, row) if a segment that crosses
+                            // ranges starts in it, else (-1, 0); every range writes its slot
+  int32_t* seg_end;         // [rows]: end range of a crossing segment, by key
   const uint32_t* flag;     // sticky error bits: nonzero voids the update
   const uint32_t* flag2;    // the error word of this list's sort (a training step's sort
                             // set raises its own word; otherwise the same as flag)
@@ -105,13 +109,12 @@ __host__ __device__ inline int seg_chunk_size(int N) { return N <= 131072 ? 16 :
 // (bfloat16, 327,680 entries: apply 27 -> 16 us, fix-up 8.6 -> 11.5 us).
 __host__ __device__ inline int gen_chunk_size(int N) { return N <= 131072 ? 16 : 32; }
 
-// Where a chunk's open pieces go: GLOBAL, the chunk-indexed partials and the
-// chunk's slot of the fix-up launch's segment list; LOCAL, a wave's slots in LDS (first piece,
-// last piece, and the chunk's flags and keys) for the workgroup to combine.
+// Where a chunk's open pieces go: the wave's slots in LDS (first piece, last
+// piece, and the chunk's flags and keys) for the workgroup to combine.
 struct ChunkSink {
-  float* first;  // LOCAL: [d] sum of the chunk's first piece when it continues a segment
-  float* last;   // LOCAL: [d] sum of the chunk's last piece when it opens one
-  int* meta;     // LOCAL: cont_first, open_last, single, first key, last key
+  float* first;  // [d] sum of the chunk's first piece when it continues a segment
+  float* last;   // [d] sum of the chunk's last piece when it opens one
+  int* meta;     // cont_first, open_last, single, first key, last key
 };
 
 // Element access of the float32 table: a row's entries are read as floats;
@@ -127,11 +130,11 @@ __device__ __forceinline__ void seg_close(const SegArgs& a, size_t i, float v) {
   unsafeAtomicAdd(a.table + i, v);
 }
 
-// One wave applies entries [i0, min(i0 + CH, end)) of the sorted list, chunk
-// number `chunk` (see the file comment).  A is SegArgs or another argument
-// set with the same fields and its own seg_load / seg_add.
-template <int CH, bool LOCAL, class A>
-__device__ void seg_apply_rows(const A& a, int i0, int end, int chunk, const ChunkSink& sink) {
+// One wave applies entries [i0, min(i0 + CH, end)) of the sorted list (see
+// the file comment).  A is SegArgs or another argument set with the same
+// fields and its own seg_load / seg_add.
+template <int CH, class A>
+__device__ void seg_apply_rows(const A& a, int i0, int end, const ChunkSink& sink) {
   static_assert(CH % 8 == 0 && CH <= kWave, "rows are walked in blocks of 8");
   const int lane = lane_id();
   // the error words (set by earlier launches) are read beside the chunk's
@@ -149,18 +152,12 @@ __device__ void seg_apply_rows(const A& a, int i0, int end, int chunk, const Chu
   if (ci.cont_first) complete &= ~(1ull << first_tail);
   if (ci.open_last) complete &= ~(1ull << (nact - 1));
   const bool starts_long = ci.open_last && !(ci.cont_first && single);
-  const bool ends_long = ci.cont_first && !(ci.open_last && single);
   if (lane == 0) {
-    if (LOCAL) {
-      sink.meta[0] = ci.cont_first;
-      sink.meta[1] = ci.open_last;
-      sink.meta[2] = single;
-      sink.meta[3] = ci.key;  // lane 0 holds the first piece's key
-      sink.meta[4] = ci.last_key;
-    } else {
-      a.long_list[chunk] = starts_long ? make_int2(chunk, ci.last_key) : make_int2(-1, 0);
-      if (ends_long) a.seg_end[ci.key] = chunk;
-    }
+    sink.meta[0] = ci.cont_first;
+    sink.meta[1] = ci.open_last;
+    sink.meta[2] = single;
+    sink.meta[3] = ci.key;  // lane 0 holds the first piece's key
+    sink.meta[4] = ci.last_key;
   }
   for (int c0 = 0; c0 < a.d; c0 += kWave) {
     const int col = c0 + lane;
@@ -218,13 +215,8 @@ __device__ void seg_apply_rows(const A& a, int i0, int end, int chunk, const Chu
     }
     if constexpr (A::kDeferred) seg_add_rows<CH>(a, ci, complete, v, colc, cok);
     if (cok) {
-      if (LOCAL) {
-        if (ci.cont_first) sink.first[col] = first_sum;
-        if (starts_long) sink.last[col] = last_sum;
-      } else {
-        if (ci.cont_first) a.seg_part[((size_t)chunk * 2 + 0) * a.seg_stride + col] = first_sum;
-        if (starts_long) a.seg_part[((size_t)chunk * 2 + 1) * a.seg_stride + col] = last_sum;
-      }
+      if (ci.cont_first) sink.first[col] = first_sum;
+      if (starts_long) sink.last[col] = last_sum;
     }
   }
 }
@@ -258,8 +250,8 @@ __device__ void seg_apply_partition(const A& a, int s, int e,
   for (int r0 = 0; r0 < nch; r0 += NW) {
     const int c = r0 + w;
     if (c < nch)
-      seg_apply_rows<kPartApplyChunk, true>(a, s + c * kPartApplyChunk, e, c,
-                                            ChunkSink{F[w], Lp[w], meta[w]});
+      seg_apply_rows<kPartApplyChunk>(a, s + c * kPartApplyChunk, e,
+                                      ChunkSink{F[w], Lp[w], meta[w]});
     __syncthreads();  // the round's open pieces are in LDS
     if (w == 0) {
       const int nc = min(NW, nch - r0);
@@ -327,7 +319,7 @@ __device__ void seg_apply_range(const A& a, int r, float (*F)[kMaxD], float (*Lp
   const int s = r * NW * CH;
   const int nch = min(NW, (a.N - s + CH - 1) / CH);
   if (w < nch)
-    seg_apply_rows<CH, true>(a, s + w * CH, a.N, 0, ChunkSink{F[w], Lp[w], meta[w]});
+    seg_apply_rows<CH>(a, s + w * CH, a.N, ChunkSink{F[w], Lp[w], meta[w]});
   __syncthreads();  // the chunks' open pieces are in LDS
   if (w == 0) {
     int mk[5];
