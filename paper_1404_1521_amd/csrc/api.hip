@@ -257,16 +257,34 @@ int segfix_workgroups(const SegArgs& s) {  // kSegfixWaves tasks per workgroup a
   return std::max(1, std::min(ceil_div(ceil_div(s.N, s.rg), kSegfixWaves), 2048));
 }
 
-// The sort of one step's entries into sort set `set`, on the side stream.
+// The sort of one step's entries into sort set `set`, on stream `st` (the
+// side stream, or the main stream for the first step of a folded call).
 hipError_t enqueue_sort(polyglot_ctx* ctx, const int32_t* windows, const int32_t* corrupt, int B,
-                        int set) {
+                        int set, hipStream_t st) {
   const polyglot_config& cf = ctx->cfg;
   const int N = B * (cf.win + 1);
   const StepKeys kf = step_keys(windows, corrupt, cf.win, cf.V);
-  Timed tm(ctx, POLYGLOT_K_SORT, ctx->side);
+  Timed tm(ctx, POLYGLOT_K_SORT, st);
   SortBufs sb = sort_bufs(ctx, set);
   sb.flag = set_flag(ctx, set);
   return launch_sort_step(kf, N, make_plan(cf.V, N), sb, tm.L);
+}
+
+// A step's bucketed sort into set `set`, as the extra workgroups of the
+// previous step's update (tiles) and fix-up (buckets).
+NextSort next_sort(polyglot_ctx* ctx, const int32_t* windows, const int32_t* corrupt, int B,
+                   int set) {
+  const polyglot_config& cf = ctx->cfg;
+  NextSort nx{};
+  nx.N = B * (cf.win + 1);
+  const SortPlan plan = make_plan(cf.V, nx.N);
+  nx.kf = step_keys(windows, corrupt, cf.win, cf.V);
+  nx.sb = sort_bufs(ctx, set);
+  nx.sb.flag = set_flag(ctx, set);
+  nx.ntiles = plan.ntiles;
+  nx.key_bits = plan.key_bits;
+  nx.n_wg = plan.ntiles;
+  return nx;
 }
 
 // The forward/backward launch(es), then (after `sorted_ev`, if any) the
@@ -274,7 +292,7 @@ hipError_t enqueue_sort(polyglot_ctx* ctx, const int32_t* windows, const int32_t
 // one step, on the main stream; sorted mode reads sort set `set`.
 int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
                     const int32_t* windows, const int32_t* corrupt, int B, float lr,
-                    float* loss_dev, int set, hipEvent_t sorted_ev) {
+                    float* loss_dev, int set, hipEvent_t sorted_ev, const NextSort& nx) {
   const polyglot_config& cf = ctx->cfg;
   const int N = B * (cf.win + 1);
   const bool sorted = cf.scatter_mode == POLYGLOT_SCATTER_SORTED;
@@ -408,11 +426,19 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   } else {
     {
       Timed tm(ctx, POLYGLOT_K_UPDATE);
-      e = launch_apply_step(aa, kf, aa.n_e + aa.n_d, tm.L);
+      aa.nx = nx;
+      e = nx.n_wg ? launch_apply_step_next(aa, kf, aa.n_e + aa.n_d, tm.L)
+                  : launch_apply_step(aa, kf, aa.n_e + aa.n_d, tm.L);
     }
     if (e == hipSuccess && sorted) {
       Timed tm(ctx, POLYGLOT_K_SEGFIX);
-      e = launch_segfix(aa.s, segfix_workgroups(aa.s), tm.L);
+      if (nx.n_wg) {
+        NextSort nb = nx;
+        nb.n_wg = bk_grid(nx.N);
+        e = launch_segfix_step(aa.s, nb, segfix_workgroups(aa.s), tm.L);
+      } else {
+        e = launch_segfix(aa.s, segfix_workgroups(aa.s), tm.L);
+      }
     }
   }
   if (e != hipSuccess) return hip_fail(ctx, e, "update launch");
@@ -427,19 +453,31 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
 // Enqueues S consecutive steps (arguments already validated), step s using
 // windows + s*B*win and corrupt + s*B.  Sorted mode, small batches: the sort
 // is a role of the fused kernel (extra workgroups, no cross-stream join).
-// Large batches: the sort of step s+1 runs on the side stream while step s
-// computes; it waits for step s-1, the last reader of the same sort set.
+// Bucketed sorts (mid-size lists): the first step's sort runs on the main
+// stream, and the sort of step s+1 runs as extra workgroups of step s's
+// update and fix-up launches, beside their work, with no second stream (the
+// fused kernel holds every CU, so a side-stream sort could not overlap it,
+// and the cross-queue joins cost time of their own).  Other lists (above
+// 1,048,576 entries, or the small sort of wide layers): the sort of step s+1
+// runs on the side stream while step s computes; it waits for step s-1, the
+// last reader of the same sort set.
 int enqueue_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
                   const int32_t* windows, const int32_t* corrupt, int S, int B, float lr,
                   float* losses_dev) {
-  const bool side_sort = ctx->cfg.scatter_mode == POLYGLOT_SCATTER_SORTED &&
-                         (ctx->large || !make_plan(ctx->cfg.V, B * (ctx->cfg.win + 1)).small);
+  const bool sorted = ctx->cfg.scatter_mode == POLYGLOT_SCATTER_SORTED;
+  const SortPlan plan = make_plan(ctx->cfg.V, B * (ctx->cfg.win + 1));
+  const bool fold = sorted && plan.bucket;
+  const bool side_sort = sorted && !fold && (ctx->large || !plan.small);
   const size_t wstride = (size_t)B * ctx->cfg.win;
   hipError_t e = hipSuccess;
+  if (fold) {
+    e = enqueue_sort(ctx, windows, corrupt, B, 0, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "sort launch");
+  }
   if (side_sort) {
     e = hipEventRecord(ctx->ev_fork, ctx->stream);
     if (e == hipSuccess) e = hipStreamWaitEvent(ctx->side, ctx->ev_fork, 0);
-    if (e == hipSuccess) e = enqueue_sort(ctx, windows, corrupt, B, 0);
+    if (e == hipSuccess) e = enqueue_sort(ctx, windows, corrupt, B, 0, ctx->side);
     if (e == hipSuccess) e = hipEventRecord(ctx->ev_sorted[0], ctx->side);
     if (e != hipSuccess) return hip_fail(ctx, e, "sort launch");
   }
@@ -449,14 +487,18 @@ int enqueue_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, 
       if (s >= 1) e = hipStreamWaitEvent(ctx->side, ctx->ev_done[1 - q], 0);
       if (e == hipSuccess)
         e = enqueue_sort(ctx, windows + (s + 1) * wstride, corrupt + (size_t)(s + 1) * B, B,
-                         1 - q);
+                         1 - q, ctx->side);
       if (e == hipSuccess) e = hipEventRecord(ctx->ev_sorted[1 - q], ctx->side);
       if (e != hipSuccess) return hip_fail(ctx, e, "sort launch");
     }
+    const NextSort nx =
+        (fold && s + 1 < S)
+            ? next_sort(ctx, windows + (s + 1) * wstride, corrupt + (size_t)(s + 1) * B, B, 1 - q)
+            : NextSort{};
     const int r = enqueue_compute(ctx, E, W1, b1, w2, b2, windows + s * wstride,
                                   corrupt + (size_t)s * B, B, lr,
                                   losses_dev ? losses_dev + s : nullptr, q,
-                                  side_sort ? ctx->ev_sorted[q] : nullptr);
+                                  side_sort ? ctx->ev_sorted[q] : nullptr, nx);
     if (r) return r;
     if (side_sort) {
       e = hipEventRecord(ctx->ev_done[q], ctx->stream);

@@ -44,8 +44,7 @@ constexpr int kBkDigitBits = 10;                    // bucket ids fit 10 bits
 static_assert(kBkBuckets <= (1 << kBkDigitBits), "bucket ids");
 constexpr int kBkScanN = 1024;                      // padded length of the per-bucket scans
 constexpr int kBkThreads = 512;                     // k_bk_tiles workgroup
-constexpr int kBkR = 4;                             // rounds of 64 keys per wave
-constexpr int kBkTileKeys = kBkThreads * kBkR;      // 2048
+constexpr int kBkTileKeys = 2048;                   // keys per tile
 constexpr int kBkMaxTiles = 512;
 constexpr int kBkMaxN = kBkTileKeys * kBkMaxTiles;  // 1,048,576
 constexpr int kBkMaxKeyBits = 30;                   // hashed words pack (key >> 9) and 11 index bits
@@ -72,16 +71,24 @@ __device__ __forceinline__ uint32_t bk_high(uint32_t key) {
 }
 
 // ------------------------------------------------------------------ tiles
-template <class KeyFn>
-__device__ void bk_tiles(const KeyFn& kf, int N, int ntiles, const SortBufs& sb, uint32_t* lds) {
-  constexpr int NW = kBkThreads / kWave, CS = NW + 1, R = kBkR, P = kBkBuckets;
+// LDS of bk_tiles for NTH threads, in words.
+__host__ __device__ constexpr int bk_tiles_lds_words(int nth) {
+  return kBkBuckets * (nth / kWave + 1) + kBkScanN + 32;
+}
+
+// Tile `tile` of the list, by a workgroup of NTH threads (R = 2048 / NTH
+// rounds of 64 keys per wave).
+template <int NTH, class KeyFn>
+__device__ void bk_tiles(const KeyFn& kf, int N, int ntiles, const SortBufs& sb, int tile,
+                         uint32_t* lds) {
+  constexpr int NW = NTH / kWave, CS = NW + 1, R = kBkTileKeys / NTH, P = kBkBuckets;
+  static_assert(R * NTH == kBkTileKeys && NW + 1 <= 32, "tile shape");
   uint32_t* hist = lds;                 // [P][CS]: per-wave counts, then wave offsets
   uint32_t* loff = hist + P * CS;       // [kBkScanN]: counts, then offsets inside the tile
   uint32_t* misc = loff + kBkScanN;     // scan scratch
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
-  const int tile = blockIdx.x;
-  for (int i = t; i < P * CS; i += kBkThreads) hist[i] = 0u;
+  for (int i = t; i < P * CS; i += NTH) hist[i] = 0u;
   const int wbase = tile * kBkTileKeys + w * (R * kWave);
   uint32_t key[R], dg[R], loc[R];
   uint64_t act[R];
@@ -95,10 +102,12 @@ __device__ void bk_tiles(const KeyFn& kf, int N, int ntiles, const SortBufs& sb,
   wave_rank<R>(dg, act, R, kBkDigitBits, hist + w, loc, CS);
   __syncthreads();
   // bucket d: the tile's count and each wave's offset inside the bucket
-  uint32_t cnt[2] = {0u, 0u};
+  constexpr int DPT = kBkScanN / NTH;  // buckets per thread
+  uint32_t cnt[DPT];
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int d = t + k * kBkThreads;
+  for (int k = 0; k < DPT; ++k) {
+    cnt[k] = 0u;
+    const int d = t + k * NTH;
     if (d < P) {
       uint32_t c[NW];
 #pragma unroll
@@ -112,11 +121,11 @@ __device__ void bk_tiles(const KeyFn& kf, int N, int ntiles, const SortBufs& sb,
     if (d < kBkScanN) loff[d] = cnt[k];
   }
   __syncthreads();
-  block_exclusive_scan<kBkThreads>(loff, kBkScanN, misc);
+  block_exclusive_scan_runs<NTH>(loff, kBkScanN, misc);
   uint32_t* col = sb.status;  // [P][ntiles]: (offset inside the tile << 16) | count
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int d = t + k * kBkThreads;
+  for (int k = 0; k < DPT; ++k) {
+    const int d = t + k * NTH;
     if (d < P) {
       col[(size_t)d * ntiles + tile] = (loff[d] << 16) | cnt[k];
       if (cnt[k]) atomicAdd(&sb.totals[d], cnt[k]);
@@ -258,7 +267,8 @@ struct BkLoc {
 // Workgroup j < kBkHashed orders hashed bucket kBkDedicated + j (known before
 // any load, so its column of (offset, count) words is read beside the
 // totals); the others copy the units of the dedicated buckets in order.
-__device__ void bk_buckets(int N, int ntiles, int key_bits, const SortBufs& sb, uint32_t* lds) {
+__device__ void bk_buckets(int N, int ntiles, int key_bits, const SortBufs& sb, uint32_t j,
+                           uint32_t* lds) {
   constexpr int NTH = kBkSortThreads, P = kBkBuckets;
   uint32_t* tot = lds + kBkLdsTot;
   uint32_t* uni = lds + kBkLdsUni;
@@ -267,7 +277,6 @@ __device__ void bk_buckets(int N, int ntiles, int key_bits, const SortBufs& sb, 
   uint32_t* misc = lds + kBkLdsMisc;
   uint32_t* sa = lds + kBkLdsSort;
   const int t = threadIdx.x;
-  const uint32_t j = blockIdx.x;
   const bool hashed = j < (uint32_t)kBkHashed;
   int b = kBkDedicated + (int)j;
   // bucket totals (and a hashed bucket's column), every load in flight at once

@@ -124,16 +124,15 @@ static hipError_t launch_tiled_sort(const KeyFn& kf, int N, const SortPlan& plan
 template <class KeyFn>
 __global__ __launch_bounds__(kBkThreads) void k_bk_tiles(KeyFn kf, int N, int ntiles, SortBufs sb) {
   extern __shared__ uint32_t lds[];
-  bk_tiles(kf, N, ntiles, sb, lds);
+  bk_tiles<kBkThreads>(kf, N, ntiles, sb, blockIdx.x, lds);
 }
 
 __global__ __launch_bounds__(kBkSortThreads) void k_bk_buckets(int N, int ntiles, int key_bits,
                                                                SortBufs sb) {
   extern __shared__ uint32_t lds[];
-  bk_buckets(N, ntiles, key_bits, sb, lds);
+  bk_buckets(N, ntiles, key_bits, sb, blockIdx.x, lds);
 }
 
-constexpr int kBkTilesLdsWords = kBkBuckets * (kBkThreads / kWave + 1) + kBkScanN + 32;
 
 template <class KeyFn>
 static hipError_t launch_sort(const KeyFn& kf, int N, const SortPlan& plan, const SortBufs& sb,
@@ -143,7 +142,7 @@ static hipError_t launch_sort(const KeyFn& kf, int N, const SortPlan& plan, cons
                      part_sort_lds_words(kPartSortThreads) * 4, L, kf, N, plan, sb);
   if (plan.bucket) {
     hipError_t e = pg_launch(k_bk_tiles<KeyFn>, dim3(plan.ntiles), dim3(kBkThreads),
-                             kBkTilesLdsWords * 4, L, kf, N, plan.ntiles, sb);
+                             bk_tiles_lds_words(kBkThreads) * 4, L, kf, N, plan.ntiles, sb);
     if (e == hipSuccess)
       e = pg_launch(k_bk_buckets, dim3(bk_grid(N)), dim3(kBkSortThreads), kBkLdsWords * 4, L, N,
                     plan.ntiles, plan.key_bits, sb);
@@ -207,6 +206,20 @@ static hipError_t launch_apply(const ApplyArgs& a, const KeyFn& kf, int grid, co
 
 hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, const Launch& L) {
   return launch_apply(a, kf, grid, L);
+}
+
+hipError_t launch_apply_step_next(const ApplyArgs& a, const StepKeys& kf, int grid,
+                                  const Launch& L) {
+  const uint32_t lds = a.nx.n_wg ? bk_tiles_lds_words(kBlock) * 4 : 0;
+  const int g = grid + a.nx.n_wg;
+  if (a.s.ch == 16) return pg_launch(k_apply<16, StepKeys>, dim3(g), dim3(kBlock), lds, L, a, kf);
+  return pg_launch(k_apply<64, StepKeys>, dim3(g), dim3(kBlock), lds, L, a, kf);
+}
+
+hipError_t launch_segfix_step(const SegArgs& a, const NextSort& nx, int n_fix, const Launch& L) {
+  const uint32_t lds = nx.n_wg ? kBkLdsWords * 4 : 0;
+  return pg_launch(k_segfix_step, dim3(n_fix + nx.n_wg), dim3(kSegfixThreads), lds, L, a, nx,
+                   n_fix);
 }
 
 hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, const Launch& L) {

@@ -101,9 +101,19 @@ struct DenseArgs {
   float lr, invB;
 };
 
+// The next training step's bucketed sort, run as extra workgroups of this
+// step's update (its tiles) and fix-up (its buckets) launches.  n_wg = 0:
+// none.
+struct NextSort {
+  StepKeys kf;
+  SortBufs sb;
+  int N, ntiles, key_bits;
+  int n_wg;
+};
+
 // One launch with roles: workgroups [0, n_e) update the table (sorted
-// segments or atomics); the rest run the dense SGD (if n_d > 0) and clear
-// the sort counters.
+// segments or atomics); the next ones run the dense SGD (if n_d > 0) and
+// clear the sort counters; the last nx.n_wg rank the next step's sort tiles.
 struct ApplyArgs {
   SegArgs s;
   int mode;  // 0 sorted segments, 1 atomic
@@ -113,6 +123,7 @@ struct ApplyArgs {
   int n_part;
   DenseArgs dn;
   ZeroRanges zero;
+  NextSort nx;
 };
 
 struct ScoreArgs {
@@ -157,6 +168,11 @@ hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const
 hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, const Launch& L);
 hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, const Launch& L);
 hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L);
+// the update of a training step with nx.n_wg extra workgroups for the next
+// step's sort tiles, and its fix-up with the buckets of that sort
+hipError_t launch_apply_step_next(const ApplyArgs& a, const StepKeys& kf, int grid,
+                                  const Launch& L);
+hipError_t launch_segfix_step(const SegArgs& a, const NextSort& nx, int n_fix, const Launch& L);
 
 // The general advanced-indexing op (any storage format, increment or
 // assignment) over a sorted entry list; pointers as in SegArgs, the table

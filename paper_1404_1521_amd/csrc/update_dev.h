@@ -77,12 +77,21 @@ __device__ void dense_sgd(const DenseArgs& a, int gid, int nthreads, bool bad) {
   }
 }
 
+// Workgroups [0, n_e) update the table; the next gridDim - n_e - nx.n_wg run
+// the dense SGD and clearing roles; the last nx.n_wg rank the tiles of the
+// next training step's bucketed sort (its ids only).
 template <int CH, class KeyFn>
 __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
   __shared__ float F[kWavesPerBlock][kMaxD];
   __shared__ float Lp[kWavesPerBlock][kMaxD];
   __shared__ int meta[kWavesPerBlock][5];
   const int t = threadIdx.x;
+  const int n_dz = (int)gridDim.x - a.n_e - a.nx.n_wg;
+  if ((int)blockIdx.x >= a.n_e + n_dz) {
+    extern __shared__ uint32_t lds_u[];
+    bk_tiles<kBlock>(a.nx.kf, a.nx.N, a.nx.ntiles, a.nx.sb, blockIdx.x - a.n_e - n_dz, lds_u);
+    return;
+  }
   if ((int)blockIdx.x < a.n_e) {
     // all-or-nothing: an out-of-range id voids the update.  The error words
     // were set (or not) by earlier launches: the workgroup leaves together
@@ -99,7 +108,7 @@ __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
   }
   const bool bad = void_bits(a.s) != 0u;
   const int gid = (blockIdx.x - a.n_e) * kBlock + t;
-  const int nthreads = (gridDim.x - a.n_e) * kBlock;
+  const int nthreads = n_dz * kBlock;
   if (a.n_d > 0) dense_sgd(a.dn, gid, nthreads, bad);
   zero_ranges(a.zero, gid, nthreads);
 }
@@ -133,21 +142,22 @@ __global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
 // by its wave, a heavy one is listed and then summed by the whole workgroup.
 // Every row is a different segment's, so the order in which heavy ones are
 // taken does not matter.
+// Workgroup wg of nwg: crossing segments listed in the range slots (see
+// k_segfix).  red, heavy and nheavy are the workgroup's LDS.
 template <class A>
-__global__ __launch_bounds__(kSegfixThreads) void k_segfix(A a) {
-  __shared__ float red[kSegfixWaves * kMaxD];
-  __shared__ int heavy[kSegfixWaves][3];  // (start chunk, row, partials)
-  __shared__ int nheavy;
+__device__ void segfix_wg(const A& a, int wg, int nwg, float* red, int (*heavy)[3],
+                          int* nheavy_p) {
+  int& nheavy = *nheavy_p;
   if (void_bits(a)) return;
   const uint32_t cnt = (uint32_t)((a.N + a.rg - 1) / a.rg);  // ranges of the apply
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
-  // slot li of a round goes to workgroup li % gridDim.x, so the segments of
-  // heavy rows that start in nearby chunks land in different workgroups
-  for (uint32_t base = 0; base + blockIdx.x < cnt; base += gridDim.x * kSegfixWaves) {
+  // slot li of a round goes to workgroup li % nwg, so the segments of heavy
+  // rows that start in nearby ranges land in different workgroups
+  for (uint32_t base = 0; base + wg < cnt; base += nwg * kSegfixWaves) {
     if (t == 0) nheavy = 0;
     __syncthreads();
-    const uint32_t li = base + (uint32_t)w * gridDim.x + blockIdx.x;
+    const uint32_t li = base + (uint32_t)w * nwg + wg;
     if (li < cnt) {
       const int2 rec = a.long_list[li];
       if (rec.x >= 0) {
@@ -165,6 +175,30 @@ __global__ __launch_bounds__(kSegfixThreads) void k_segfix(A a) {
     for (int h = 0; h < nh; ++h) seg_fix_row(a, heavy[h][0], heavy[h][1], heavy[h][2], red);
     __syncthreads();  // the heavy list is rewritten by the next round
   }
+}
+
+template <class A>
+__global__ __launch_bounds__(kSegfixThreads) void k_segfix(A a) {
+  __shared__ float red[kSegfixWaves * kMaxD];
+  __shared__ int heavy[kSegfixWaves][3];  // (start range, row, partials)
+  __shared__ int nheavy;
+  segfix_wg(a, blockIdx.x, gridDim.x, red, heavy, &nheavy);
+}
+
+// The fix-up of a training step and, in workgroups [n_fix, gridDim), the
+// bucket launch of the next step's bucketed sort (its tiles ran in the
+// update launch), which only reads that step's ids: no stream join needed.
+__global__ __launch_bounds__(kSegfixThreads) void k_segfix_step(SegArgs a, NextSort nx, int n_fix) {
+  __shared__ float red[kSegfixWaves * kMaxD];
+  __shared__ int heavy[kSegfixWaves][3];
+  __shared__ int nheavy;
+  extern __shared__ uint32_t lds_u[];
+  static_assert(kSegfixThreads == kBkSortThreads, "one workgroup size for both roles");
+  if ((int)blockIdx.x < n_fix) {
+    segfix_wg(a, blockIdx.x, n_fix, red, heavy, &nheavy);
+    return;
+  }
+  bk_buckets(nx.N, nx.ntiles, nx.key_bits, nx.sb, blockIdx.x - n_fix, lds_u);
 }
 
 }  // namespace pg

@@ -674,7 +674,8 @@ def test_sorted_mode_is_deterministic():
 
 GRAPH_CASES = [
     (PRESETS["sweep_1024"], 1024, 6),   # sort fused into the step kernel, partition-wise update
-    (PRESETS["sweep_1024"], 4096, 4),   # one-sweep sort on the side stream, fix-up launch
+    (PRESETS["sweep_1024"], 4096, 4),   # bucketed sort of the next step inside the update
+                                        # and fix-up launches
     (PRESETS["sweep_1024"], 8192, 3),   # two tiles per workgroup: the pipelined tile loop
     (LARGE_SHAPES[0], 100, 4),          # wide layers: partitioned sort on the side stream
     (LARGE_SHAPES[1], 1030, 3),         # wide layers, two dW1 slices
