@@ -77,37 +77,39 @@ __device__ void dense_sgd(const DenseArgs& a, int gid, int nthreads, bool bad) {
   }
 }
 
-// Workgroups [0, n_e) update the table; the next gridDim - n_e - nx.n_wg run
-// the dense SGD and clearing roles; the last nx.n_wg rank the tiles of the
-// next training step's bucketed sort (its ids only).
+// Workgroups [0, nx.n_wg) rank the tiles of the next training step's
+// bucketed sort (its ids only; first in the grid, so that they are dispatched
+// beside the table role, not after it); the next n_e update the table; the
+// rest run the dense SGD and clearing roles.
 template <int CH, class KeyFn>
 __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
   __shared__ float F[kWavesPerBlock][kMaxD];
   __shared__ float Lp[kWavesPerBlock][kMaxD];
   __shared__ int meta[kWavesPerBlock][5];
   const int t = threadIdx.x;
-  const int n_dz = (int)gridDim.x - a.n_e - a.nx.n_wg;
-  if ((int)blockIdx.x >= a.n_e + n_dz) {
+  if ((int)blockIdx.x < a.nx.n_wg) {
     extern __shared__ uint32_t lds_u[];
-    bk_tiles<kBlock>(a.nx.kf, a.nx.N, a.nx.ntiles, a.nx.sb, blockIdx.x - a.n_e - n_dz, lds_u);
+    bk_tiles<kBlock>(a.nx.kf, a.nx.N, a.nx.ntiles, a.nx.sb, blockIdx.x, lds_u);
     return;
   }
-  if ((int)blockIdx.x < a.n_e) {
+  const int wg = (int)blockIdx.x - a.nx.n_wg;  // index among the update's workgroups
+  const int n_dz = (int)gridDim.x - a.nx.n_wg - a.n_e;
+  if (wg < a.n_e) {
     // all-or-nothing: an out-of-range id voids the update.  The error words
     // were set (or not) by earlier launches: the workgroup leaves together
     if (a.mode == 0) {
       if (__builtin_amdgcn_readfirstlane(void_bits(a.s)) != 0u) return;
       const int nranges = ceil_div(a.s.N, CH * kWavesPerBlock);
-      for (int r = blockIdx.x; r < nranges; r += a.n_e)
+      for (int r = wg; r < nranges; r += a.n_e)
         seg_apply_range<CH, kWavesPerBlock>(a.s, r, F, Lp, meta);
     } else {
       if (void_bits(a.s)) return;
-      atomic_rows(a.s, kf, blockIdx.x, a.n_e);
+      atomic_rows(a.s, kf, wg, a.n_e);
     }
     return;
   }
   const bool bad = void_bits(a.s) != 0u;
-  const int gid = (blockIdx.x - a.n_e) * kBlock + t;
+  const int gid = (wg - a.n_e) * kBlock + t;
   const int nthreads = n_dz * kBlock;
   if (a.n_d > 0) dense_sgd(a.dn, gid, nthreads, bad);
   zero_ranges(a.zero, gid, nthreads);
@@ -185,20 +187,21 @@ __global__ __launch_bounds__(kSegfixThreads) void k_segfix(A a) {
   segfix_wg(a, blockIdx.x, gridDim.x, red, heavy, &nheavy);
 }
 
-// The fix-up of a training step and, in workgroups [n_fix, gridDim), the
-// bucket launch of the next step's bucketed sort (its tiles ran in the
-// update launch), which only reads that step's ids: no stream join needed.
+// The fix-up of a training step and, in workgroups [0, nx.n_wg) (first, so
+// that they are dispatched beside it), the bucket launch of the next step's
+// bucketed sort (its tiles ran in the update launch), which only reads that
+// step's ids: no stream join needed.
 __global__ __launch_bounds__(kSegfixThreads) void k_segfix_step(SegArgs a, NextSort nx, int n_fix) {
   __shared__ float red[kSegfixWaves * kMaxD];
   __shared__ int heavy[kSegfixWaves][3];
   __shared__ int nheavy;
   extern __shared__ uint32_t lds_u[];
   static_assert(kSegfixThreads == kBkSortThreads, "one workgroup size for both roles");
-  if ((int)blockIdx.x < n_fix) {
-    segfix_wg(a, blockIdx.x, n_fix, red, heavy, &nheavy);
+  if ((int)blockIdx.x < nx.n_wg) {
+    bk_buckets(nx.N, nx.ntiles, nx.key_bits, nx.sb, blockIdx.x, lds_u);
     return;
   }
-  bk_buckets(nx.N, nx.ntiles, nx.key_bits, nx.sb, blockIdx.x - n_fix, lds_u);
+  segfix_wg(a, (int)blockIdx.x - nx.n_wg, n_fix, red, heavy, &nheavy);
 }
 
 }  // namespace pg
