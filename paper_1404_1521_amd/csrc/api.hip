@@ -301,7 +301,7 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   hipError_t e = hipSuccess;
 
   LargeArgs la{};
-  int n_fb = 0;
+  int n_fb = 0, split = 1;
   if (ctx->large) {
     la.E = E;
     la.W1 = W1;
@@ -364,6 +364,11 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
     fa.tiles_per_wg = ceil_div(fa.ntiles, shape8 ? std::min(ctx->max_parts, kF8MaxWorkgroups)
                                                  : ctx->max_parts);
     n_fb = ceil_div(fa.ntiles, fa.tiles_per_wg);
+    // one tile per workgroup and CUs to spare: two workgroups per tile, each
+    // taking half of its backward (the forward runs in both)
+    fa.split = (shape8 && fa.tiles_per_wg == 1 && fa.n_sort + 2 * n_fb <= kF8MaxWorkgroups) ? 2 : 1;
+    n_fb *= fa.split;
+    split = fa.split;
     fa.part_stride = ctx->part_stride;
     fa.invB = 1.0f / (float)B;
     {
@@ -405,9 +410,11 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
   } else {
     aa.dn.n_parts = n_fb;
     aa.dn.part_stride = ctx->part_stride;
+    aa.dn.split = split;
+    // the vector partials: every slot, or the first of each pair when split
     aa.dn.vpart = ctx->ws.part + (size_t)ctx->Hp * ctx->K;
-    aa.dn.n_vparts = n_fb;
-    aa.dn.vstride = ctx->part_stride;
+    aa.dn.n_vparts = n_fb / split;
+    aa.dn.vstride = ctx->part_stride * split;
   }
   aa.dn.H = cf.H;
   aa.dn.Hp = ctx->Hp;
@@ -600,7 +607,9 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
       e = alloc(ctx, &ws.vpart, (size_t)ceil_div(c.max_batch, kLgRows) * (2 * c.H + 2));
     if (e == hipSuccess) e = alloc(ctx, &ws.vbuf, (size_t)c.max_batch * 3 * c.H);
   } else if (e == hipSuccess) {
-    e = alloc(ctx, &ws.part, (size_t)ctx->max_parts * ctx->part_stride);
+    // two slots per tile group: the split backward gives each workgroup of a
+    // pair its own
+    e = alloc(ctx, &ws.part, (size_t)2 * ctx->max_parts * ctx->part_stride);
   }
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_end, (size_t)std::max(c.V, c.max_rows));
   if (e == hipSuccess) e = alloc(ctx, &ws.seg_part, (size_t)ctx->max_chunks * 2 * ctx->seg_stride);

@@ -23,6 +23,10 @@
 //             16 columns) round-robin over the waves.
 // W1 is staged once per workgroup in LDS (row stride K + 4 floats, rows
 // >= H zero) and read from there as the B operand of the forward and of G.
+// Small batches (one tile per workgroup, CUs to spare) split the backward:
+// two workgroups take the same tile, both run the forward and the epilogue,
+// and each computes half of the dW1 and G output tiles, writing its own
+// dense-partial slot.
 // A workgroup with several tiles takes two barriers per tile: the tiles are
 // software-pipelined so that dW1 and G of one tile share a phase with the
 // forward of the next (a single tile takes three, in a plain sequence).
@@ -72,7 +76,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);  // wave-uniform
   const int n16 = lane & 15, g = lane >> 4;
-  const int nt_w = w % NT, kq = w / NT;  // this wave's hidden block and chunk set
+  const int nt_w = w % NT, kq = w / NT;  // forward: this wave's hidden block and chunk set
 
   float* w1s = lds;                       // [HP][K+4]
   float* xl = w1s + Sh::kW1;              // [2][W1P][QD][16] float4
@@ -80,13 +84,25 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   float* vt = zp + Sh::kZp;               // [3][16][HP+1]
   float* red = vt + Sh::kVt;              // [waves][2*HP+2]
 
-  const int tile0 = wg * a.tiles_per_wg;
+  // Split backward (a.split == 2): workgroups 2q and 2q+1 take the same
+  // tiles, both run the forward and the epilogue, and half h = wg & 1 takes
+  // every second dW1 output tile and every second G output tile (linear
+  // indices L = 2 (w + 16 i) + h); each writes its own partial slot, and the
+  // db1 / dw2 / loss sums come from half 0 only.
+  const int nh = a.split;
+  const int h = wg & (nh - 1);
+  const int tile0 = (wg / nh) * a.tiles_per_wg;
+  // dW1 output tiles L = kc NT + nt of this wave: L = nh (w + 16 i) + h, all
+  // in hidden block ntd
+  constexpr int NLT = NCH * NT;
+  const int ntd = (nh * w + h) % NT;
   const int ntl = min(a.tiles_per_wg, a.ntiles - tile0);  // tiles of this workgroup (>= 1)
 
   // ids of the X pieces of this thread in tile `tile`: piece pi = t + 512 p
   // covers window r = pi % 16, column quad (pi / 16) % QD, position
-  // pi / (16 QD) (position win: the corrupt id).  Rows >= B read row 0; an
-  // id outside [0, V) raises the flag and reads row 0.
+  // pi / (16 QD) (position win: the corrupt id).  Rows >= B read row 0.  The
+  // loads are only issued here: the range check waits for them, so it sits
+  // in load_x, where the rows' addresses need the ids anyway.
   auto load_ids = [&](int tile, int32_t (&id)[XPT]) {
 #pragma unroll
     for (int p = 0; p < XPT; ++p) {
@@ -96,22 +112,20 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       id[p] = 0;
       if (pi < XF4 && b < a.B) id[p] = (j < WIN) ? a.windows[(size_t)b * WIN + j] : a.corrupt[b];
     }
-    bool bad = false;
-#pragma unroll
-    for (int p = 0; p < XPT; ++p) {
-      const bool bk = (uint32_t)id[p] >= (uint32_t)a.V;
-      bad |= bk;
-      id[p] = bk ? 0 : id[p];
-    }
-    if (bad) atomicOr(a.flag, kFlagBadId);
   };
+  // the rows of one tile into registers; an id outside [0, V) reads row 0
+  // and raises the flag (after every load is issued)
   auto load_x = [&](const int32_t (&id)[XPT], f4 (&xr)[XPT]) {
+    bool bad = false;
 #pragma unroll
     for (int p = 0; p < XPT; ++p) {
       const int pi = t + kF8Threads * p;
       const int qq = (pi / kTileRows) % QD;
-      xr[p] = pi < XF4 ? ld4(a.E + (size_t)id[p] * D + 4 * qq) : kZero4;
+      const bool bk = (uint32_t)id[p] >= (uint32_t)a.V;
+      bad |= bk;
+      xr[p] = pi < XF4 ? ld4(a.E + (size_t)(bk ? 0 : id[p]) * D + 4 * qq) : kZero4;
     }
+    if (bad) atomicOr(a.flag, kFlagBadId);
   };
   auto store_x = [&](int buf, const f4 (&xr)[XPT]) {
 #pragma unroll
@@ -120,9 +134,11 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       if (pi < XF4) st4(xl + buf * Sh::kX + 4 * pi, xr[p]);
     }
   };
-
-  // ---- prologue: ids of the first two tiles, W1, the first tile's rows
+  // ---- prologue: ids of the first tile, W1 and the first tile's rows in
+  // flight together (the rows wait only for the ids), then the ids of the
+  // second tile
   int32_t ids[2][XPT];
+  f4 xr[XPT];
   load_ids(tile0, ids[0]);
   {  // W1 into LDS (rows >= H zero); loads batched before the stores
     constexpr int N4 = HP * (K / 4);
@@ -134,6 +150,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       const int n = i / (K / 4), k4 = i - n * (K / 4);
       v[u] = (i < N4 && n < a.H) ? ld4(a.W1 + (size_t)n * K + 4 * k4) : kZero4;
     }
+    load_x(ids[0], xr);
     if (ntl > 1) load_ids(tile0 + 1, ids[1]);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -142,8 +159,6 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       if (i < N4) st4(w1s + n * S + 4 * k4, v[u]);
     }
   }
-  f4 xr[XPT];
-  load_x(ids[0], xr);
   // epilogue lane map: hidden unit hn = lane % 32 of row 2w + lane / 32
   const int hn = lane & 31, rsel = lane >> 5;
   const float b1v = hn < a.H ? a.b1[hn] : 0.f;
@@ -155,156 +170,6 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   for (int ci = 0; ci < CPW; ++ci) accW[ci] = kZero4;
   float db1a = 0.f, dw2a = 0.f, lossa = 0.f;
 
-  if constexpr (!PIPE) {
-  // Tiles one after another, three barriers each (X staged, forward
-  // partials, V).  Used when a workgroup has a single tile: the pipelined
-  // form below measured 0.3 us slower there.
-  for (int tt = 0; tt < ntl; ++tt) {
-    const int tile = tile0 + tt;
-    const int row0 = tile * kTileRows;
-    const int buf = tt & 1;
-    const float* X = xl + buf * Sh::kX;
-    store_x(buf, xr);
-    __syncthreads();  // X of this tile (and W1) staged
-    if (tt + 1 < ntl) {
-      load_x(ids[(tt + 1) & 1], xr);                           // rows of the next tile
-      if (tt + 2 < ntl) load_ids(tile + 2, ids[tt & 1]);       // ids two tiles ahead
-    }
-
-    // ---- forward: wave (nt_w, kq) over chunks kc = kq + KW ci; common
-    // blocks, true centre and corrupt centre accumulate separately
-    f4 zc = kZero4, zctr = kZero4, zcor = kZero4;
-#pragma unroll
-    for (int ci = 0; ci < CPW; ++ci) {
-      const int kc = kq + KW * ci;
-      if (kc < NCH) {
-        const int j = kc / DQ, qq = 4 * (kc % DQ) + g;
-        const f4 xa = ld4(X + 4 * ((j * QD + qq) * kTileRows + n16));
-        const f4 wb = ld4(w1s + (nt_w * 16 + n16) * S + kc * 16 + 4 * g);
-        if (j != C) {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) zc = mfma16x4(xa[q], wb[q], zc);
-        } else {
-          const f4 xt = ld4(X + 4 * ((WIN * QD + qq) * kTileRows + n16));
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            zctr = mfma16x4(xa[q], wb[q], zctr);
-            zcor = mfma16x4(xt[q], wb[q], zcor);
-          }
-        }
-      }
-    }
-    // partials [kq][type][nt][component][lane] (component-major: a reader of
-    // one component of every lane touches consecutive words)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      zp[(((kq * 3 + 0) * NT + nt_w) * 4 + i) * kWave + lane] = zc[i];
-      zp[(((kq * 3 + 1) * NT + nt_w) * 4 + i) * kWave + lane] = zctr[i];
-      zp[(((kq * 3 + 2) * NT + nt_w) * 4 + i) * kWave + lane] = zcor[i];
-    }
-    __syncthreads();  // forward partials written
-
-    // ---- epilogue: lane (hn, rsel) of wave w < 8 takes hidden unit hn of
-    // row 2w + rsel
-    if (w < kTileRows / 2) {
-      const int r = 2 * w + rsel;
-      const int row = row0 + r;
-      const int nt = hn >> 4, src = (hn & 15) + 16 * (r >> 2), comp = r & 3;
-      float Zc = 0.f, Zctr = 0.f, Zcor = 0.f;
-      if (hn < HP) {
-#pragma unroll
-        for (int v = 0; v < KW; ++v) {
-          Zc += zp[(((v * 3 + 0) * NT + nt) * 4 + comp) * kWave + src];
-          Zctr += zp[(((v * 3 + 1) * NT + nt) * 4 + comp) * kWave + src];
-          Zcor += zp[(((v * 3 + 2) * NT + nt) * 4 + comp) * kWave + src];
-        }
-      }
-      const float z = b1v + (Zc + Zctr);
-      const float zt = b1v + (Zc + Zcor);
-      const float h = tanh_fast(z), ht = tanh_fast(zt);
-      // h - h~ = tanh(z - z~) (1 - h h~), z - z~ = zctr - zcor without
-      // cancellation against the common part
-      const float hmh = tanh_fast(Zctr - Zcor) * (1.f - h * ht);
-      float ps = w2v * h, pst = w2v * ht;
-#pragma unroll
-      for (int o = 1; o < 32; o <<= 1) {
-        ps += __shfl_xor(ps, o);
-        pst += __shfl_xor(pst, o);
-      }
-      const float mg = 1.f - (b2v + ps) + (b2v + pst);
-      const bool on = row < a.B && mg > 0.f;  // hinge active (derivative 0 at margin 0)
-      const float gst = on ? a.invB : 0.f;    // d loss/d s~ = m/B, d loss/d s = -m/B
-      const float gw = gst * w2v;
-      const float dz = -gw * (1.f - h * h);
-      const float dzt = gw * (1.f - ht * ht);
-      const float dsum = gw * hmh * (h + ht);  // dz + dz~ = g w2 (h - h~)(h + h~)
-      if (hn < HP) {
-        vt[(0 * kTileRows + r) * (HP + 1) + hn] = dsum;
-        vt[(1 * kTileRows + r) * (HP + 1) + hn] = dz;
-        vt[(2 * kTileRows + r) * (HP + 1) + hn] = dzt;
-      }
-      db1a += dsum;
-      dw2a -= gst * hmh;  // -(m/B) h + (m/B) h~
-      if (hn == 0) lossa += on ? mg : 0.f;
-    }
-    __syncthreads();  // V written
-
-    // ---- dW1 += V^T X for this wave's (nt, chunks).  A operand: lane (n16,
-    // g) holds V[4ii+g][nt*16 + n16]; B operand: X[4ii+g][16kc + n16].
-    {
-      float vc[3][4];
-#pragma unroll
-      for (int ty = 0; ty < 3; ++ty)
-#pragma unroll
-        for (int ii = 0; ii < 4; ++ii)
-          vc[ty][ii] = vt[(ty * kTileRows + 4 * ii + g) * (HP + 1) + nt_w * 16 + n16];
-#pragma unroll
-      for (int ci = 0; ci < CPW; ++ci) {
-        const int kc = kq + KW * ci;
-        if (kc < NCH) {
-          const int j = kc / DQ, qq = 4 * (kc % DQ) + (n16 >> 2);
-#pragma unroll
-          for (int ii = 0; ii < 4; ++ii) {
-            const float xb = X[4 * ((j * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
-            if (j != C) {
-              accW[ci] = mfma16x4(vc[0][ii], xb, accW[ci]);
-            } else {
-              const float xc = X[4 * ((WIN * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
-              accW[ci] = mfma16x4(vc[1][ii], xb, accW[ci]);
-              accW[ci] = mfma16x4(vc[2][ii], xc, accW[ci]);
-            }
-          }
-        }
-      }
-    }
-
-    // ---- G: output tiles ot = w + 16u (position j = ot / DQ, columns cb*16).
-    // A operand: lane (r = n16, g) holds V_ty[r][4q + g]; B operand: lane
-    // (col = n16, g) holds W1[4q + g][jj*D + cb*16 + col].
-#pragma unroll
-    for (int u = 0; u < GPW; ++u) {
-      const int ot = w + kF8Waves * u;
-      if (ot < NGT) {
-        const int j = ot / DQ, cb = ot - (ot / DQ) * DQ;
-        const int ty = (j == WIN) ? 2 : (j == C ? 1 : 0);
-        const int jj = (j == WIN) ? C : j;
-        f4 acc = kZero4;
-#pragma unroll
-        for (int q = 0; q < HP / 4; ++q) {
-          const float av = vt[(ty * kTileRows + n16) * (HP + 1) + 4 * q + g];
-          const float bv = w1s[(4 * q + g) * S + jj * D + cb * 16 + n16];
-          acc = mfma16x4(av, bv, acc);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = row0 + 4 * g + i;
-          if (row < a.B) __builtin_nontemporal_store(acc[i], &a.G[((size_t)row * W1P + j) * D + cb * 16 + n16]);
-        }
-      }
-    }
-  }
-
-  } else {
   // ---- forward of the tile in X: split-K partials into zp
   auto forward = [&](const float* X) {
     // ---- forward: wave (nt_w, kq) over chunks kc = kq + KW ci; common
@@ -388,19 +253,21 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   };
   // ---- dW1 and G of the tile in X starting at row0 (reads vt)
   auto backward = [&](const float* X, int row0) {
-    // ---- dW1 += V^T X for this wave's (nt, chunks).  A operand: lane (n16,
-    // g) holds V[4ii+g][nt*16 + n16]; B operand: X[4ii+g][16kc + n16].
+    // ---- dW1 += V^T X for this wave's output tiles (block ntd, chunks kc).
+    // A operand: lane (n16, g) holds V[4ii+g][ntd*16 + n16]; B operand:
+    // X[4ii+g][16kc + n16].
     {
       float vc[3][4];
 #pragma unroll
       for (int ty = 0; ty < 3; ++ty)
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii)
-          vc[ty][ii] = vt[(ty * kTileRows + 4 * ii + g) * (HP + 1) + nt_w * 16 + n16];
+          vc[ty][ii] = vt[(ty * kTileRows + 4 * ii + g) * (HP + 1) + ntd * 16 + n16];
 #pragma unroll
       for (int ci = 0; ci < CPW; ++ci) {
-        const int kc = kq + KW * ci;
-        if (kc < NCH) {
+        const int L = nh * (w + kF8Waves * ci) + h;
+        if (L < NLT) {
+          const int kc = L / NT;
           const int j = kc / DQ, qq = 4 * (kc % DQ) + (n16 >> 2);
 #pragma unroll
           for (int ii = 0; ii < 4; ++ii) {
@@ -417,12 +284,13 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       }
     }
 
-    // ---- G: output tiles ot = w + 16u (position j = ot / DQ, columns cb*16).
+    // ---- G: output tiles ot = nh (w + 16u) + h (position j = ot / DQ,
+    // columns cb*16).
     // A operand: lane (r = n16, g) holds V_ty[r][4q + g]; B operand: lane
     // (col = n16, g) holds W1[4q + g][jj*D + cb*16 + col].
 #pragma unroll
     for (int u = 0; u < GPW; ++u) {
-      const int ot = w + kF8Waves * u;
+      const int ot = nh * (w + kF8Waves * u) + h;
       if (ot < NGT) {
         const int j = ot / DQ, cb = ot - (ot / DQ) * DQ;
         const int ty = (j == WIN) ? 2 : (j == C ? 1 : 0);
@@ -443,38 +311,58 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
     }
   };
 
-  // Software pipeline, two barriers per tile: the epilogue of tile t runs
-  // beside the staging of tile t+1's rows (into the other X buffer), then
-  // dW1 and G of tile t run in one phase with the forward of tile t+1.
-  // Between a buffer's last reader and its next writer there is always a
-  // barrier: zp (forward t+1 after the epilogue of t), vt (epilogue t+1
-  // after dW1/G of t), X[t&1] (rows of t+2 after dW1 of t).
-  store_x(0, xr);
-  if (ntl > 1) {
-    load_x(ids[1], xr);                                  // rows of tile 1
-    if (ntl > 2) load_ids(tile0 + 2, ids[0]);            // ids of tile 2
-  }
-  __syncthreads();  // X of tile 0 and W1 staged
-  forward(xl);
-  __syncthreads();  // forward partials of tile 0 written
-  for (int tt = 0; tt < ntl; ++tt) {
-    const int row0 = (tile0 + tt) * kTileRows;
-    epilogue(row0);
-    if (tt + 1 < ntl) {
-      store_x((tt + 1) & 1, xr);                         // rows of tile tt+1
-      if (tt + 2 < ntl) {
-        load_x(ids[tt & 1], xr);                         // rows of tile tt+2
-        if (tt + 3 < ntl) load_ids(tile0 + tt + 3, ids[(tt + 1) & 1]);
+  if constexpr (!PIPE) {
+    // Tiles one after another, three barriers each (X staged, forward
+    // partials, V).  Used when a workgroup has a single tile: the pipelined
+    // form below measured 0.3 us slower there.
+    for (int tt = 0; tt < ntl; ++tt) {
+      const int tile = tile0 + tt;
+      const int buf = tt & 1;
+      const float* X = xl + buf * Sh::kX;
+      store_x(buf, xr);
+      __syncthreads();  // X of this tile (and W1) staged
+      if (tt + 1 < ntl) {
+        load_x(ids[(tt + 1) & 1], xr);                      // rows of the next tile
+        if (tt + 2 < ntl) load_ids(tile + 2, ids[tt & 1]);  // ids two tiles ahead
+      }
+      forward(X);
+      __syncthreads();  // forward partials written
+      epilogue(tile * kTileRows);
+      __syncthreads();  // V written
+      backward(X, tile * kTileRows);
+    }
+  } else {
+    // Software pipeline, two barriers per tile: the epilogue of tile t runs
+    // beside the staging of tile t+1's rows (into the other X buffer), then
+    // dW1 and G of tile t run in one phase with the forward of tile t+1.
+    // Between a buffer's last reader and its next writer there is always a
+    // barrier: zp (forward t+1 after the epilogue of t), vt (epilogue t+1
+    // after dW1/G of t), X[t&1] (rows of t+2 after dW1 of t).
+    store_x(0, xr);
+    if (ntl > 1) {
+      load_x(ids[1], xr);                                  // rows of tile 1
+      if (ntl > 2) load_ids(tile0 + 2, ids[0]);            // ids of tile 2
+    }
+    __syncthreads();  // X of tile 0 and W1 staged
+    forward(xl);
+    __syncthreads();  // forward partials of tile 0 written
+    for (int tt = 0; tt < ntl; ++tt) {
+      const int row0 = (tile0 + tt) * kTileRows;
+      epilogue(row0);
+      if (tt + 1 < ntl) {
+        store_x((tt + 1) & 1, xr);                         // rows of tile tt+1
+        if (tt + 2 < ntl) {
+          load_x(ids[tt & 1], xr);                         // rows of tile tt+2
+          if (tt + 3 < ntl) load_ids(tile0 + tt + 3, ids[(tt + 1) & 1]);
+        }
+      }
+      __syncthreads();  // V of tile tt and X of tile tt+1 written
+      backward(xl + (tt & 1) * Sh::kX, row0);
+      if (tt + 1 < ntl) {  // (uniform: every wave takes the same branch)
+        forward(xl + ((tt + 1) & 1) * Sh::kX);
+        __syncthreads();  // forward partials of tile tt+1 written; vt, X[tt&1] free
       }
     }
-    __syncthreads();  // V of tile tt and X of tile tt+1 written
-    backward(xl + (tt & 1) * Sh::kX, row0);
-    if (tt + 1 < ntl) {  // (uniform: every wave takes the same branch)
-      forward(xl + ((tt + 1) & 1) * Sh::kX);
-      __syncthreads();  // forward partials of tile tt+1 written; vt, X[tt&1] free
-    }
-  }
-
   }
 
   // ---- this workgroup's partial of the dense gradients (streaming stores,
@@ -483,10 +371,11 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   float* P = a.part + (size_t)wg * a.part_stride;
 #pragma unroll
   for (int ci = 0; ci < CPW; ++ci) {
-    const int kc = kq + KW * ci;
-    if (kc < NCH) {
+    const int L = nh * (w + kF8Waves * ci) + h;
+    if (L < NLT) {
+      const int kc = L / NT;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) __builtin_nontemporal_store(accW[ci][i], &P[(nt_w * 16 + 4 * g + i) * K + kc * 16 + n16]);
+      for (int i = 0; i < 4; ++i) __builtin_nontemporal_store(accW[ci][i], &P[(ntd * 16 + 4 * g + i) * K + kc * 16 + n16]);
     }
   }
   // db1, dw2 (per hidden unit: the two row halves of the wave, then the
@@ -505,7 +394,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
     rw[2 * HP + 1] = 0.f;
   }
   __syncthreads();
-  if (w == 0) {
+  if (w == 0 && h == 0) {
     for (int e = lane; e < 2 * HP + 2; e += kWave) {
       float s = red[e];
 #pragma unroll

@@ -54,7 +54,9 @@ struct FwdArgs {
   SortPlan plan;
   SortBufs sb;
   int ntiles;        // ceil(B / 16)
-  int tiles_per_wg;  // consecutive tiles per workgroup
+  int tiles_per_wg;  // consecutive tiles per workgroup (pair of workgroups when split)
+  int split;         // 16-wave kernel: 2 = two workgroups per tile group, each taking
+                     // half of the backward; 1 = one
   int part_stride;   // floats per dense partial slot: Hp*K + 2*Hp + 2
   float invB;
 };
@@ -98,6 +100,9 @@ struct DenseArgs {
   const float* part;   // dW1 partials: slot p at part + p * part_stride
   const float* vpart;  // db1, dw2, loss, db2 partials: slot p at vpart + p * vstride
   int n_parts, part_stride, n_vparts, vstride, H, Hp, K;
+  // 2: the partial slots come in pairs (2q, 2q+1) that each hold half of the
+  // dW1 output tiles (tile L = (k / 16) (Hp / 16) + n / 16 in slot 2q + L % 2)
+  int split;
   float lr, invB;
 };
 

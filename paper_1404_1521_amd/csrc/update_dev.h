@@ -44,8 +44,14 @@ __device__ void dense_sgd(const DenseArgs& a, int gid, int nthreads, bool bad) {
   for (int e0 = gid / SL; e0 < nel; e0 += nthreads / SL) {
     const bool mat = e0 < HK;
     const float* src = mat ? a.part + e0 : a.vpart + (e0 - HK);
-    const int np = mat ? a.n_parts : a.n_vparts;
-    const size_t stride = mat ? (size_t)a.part_stride : (size_t)a.vstride;
+    int np = mat ? a.n_parts : a.n_vparts;
+    size_t stride = mat ? (size_t)a.part_stride : (size_t)a.vstride;
+    if (mat && a.split == 2) {  // the slot of the pair that holds this element's tile
+      const int n = e0 / a.K, k = e0 - n * a.K;
+      src += (size_t)((((k >> 4) * (a.Hp >> 4)) + (n >> 4)) & 1) * a.part_stride;
+      np >>= 1;
+      stride *= 2;
+    }
     float s = 0.f;
     for (int p0 = sl; p0 < np; p0 += 8 * SL) {
       float v[8];
