@@ -67,7 +67,7 @@ struct F8Shape {
   static_assert(HP <= 32, "one hidden unit per lane of each 32-lane row half");
 };
 
-template <int D, int WIN, int NT, bool PIPE>
+template <int D, int WIN, int NT, bool PIPE, int NH>
 __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   using Sh = F8Shape<D, WIN, NT>;
   constexpr int HP = Sh::HP, K = Sh::K, C = Sh::C, W1P = Sh::W1P, DQ = Sh::DQ, QD = Sh::QD;
@@ -84,12 +84,13 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   float* vt = zp + Sh::kZp;               // [3][16][HP+1]
   float* red = vt + Sh::kVt;              // [waves][2*HP+2]
 
-  // Split backward (a.split == 2): workgroups 2q and 2q+1 take the same
+  // Split backward (NH == 2): workgroups 2q and 2q+1 take the same
   // tiles, both run the forward and the epilogue, and half h = wg & 1 takes
   // every second dW1 output tile and every second G output tile (linear
   // indices L = 2 (w + 16 i) + h); each writes its own partial slot, and the
   // db1 / dw2 / loss sums come from half 0 only.
-  const int nh = a.split;
+  static_assert(NH == 1 || (NH == 2 && !PIPE), "the split takes single-tile workgroups");
+  constexpr int nh = NH;
   const int h = wg & (nh - 1);
   const int tile0 = (wg / nh) * a.tiles_per_wg;
   // dW1 output tiles L = kc NT + nt of this wave: L = nh (w + 16 i) + h, all

@@ -63,8 +63,9 @@ __global__ __launch_bounds__(kBlock, (NT == 1 || (NT == 2 && CPW <= 5)) ? 2 : 1)
 
 // The same step for the compile-time shapes, 16 waves per workgroup (the
 // sort role of small batches too); PIPE: software-pipelined tiles, for
-// workgroups with more than one tile.
-template <int D, int WIN, int NT, bool PIPE>
+// workgroups with more than one tile; NH = 2: two workgroups per tile, each
+// taking half of the backward.
+template <int D, int WIN, int NT, bool PIPE, int NH>
 __global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {
   extern __shared__ float lds_f[];
   if ((int)blockIdx.x < a.n_sort) {
@@ -74,7 +75,7 @@ __global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {
                           reinterpret_cast<uint32_t*>(lds_f));
     return;
   }
-  fwdbwd8_wg<D, WIN, NT, PIPE>(a, blockIdx.x - a.n_sort, lds_f);
+  fwdbwd8_wg<D, WIN, NT, PIPE, NH>(a, blockIdx.x - a.n_sort, lds_f);
 }
 
 // =============================================================== sort
@@ -175,10 +176,12 @@ hipError_t launch_step_fwdbwd8(const FwdArgs& a, int shape, int grid, size_t lds
                                const Launch& L) {
   const dim3 g(grid), b(kF8Threads);
   if (shape == 1)
-    return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<64, 5, 2, true>, g, b, lds, L, a)
-                              : pg_launch(k_step_fwdbwd8<64, 5, 2, false>, g, b, lds, L, a);
-  return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<16, 5, 1, true>, g, b, lds, L, a)
-                            : pg_launch(k_step_fwdbwd8<16, 5, 1, false>, g, b, lds, L, a);
+    return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<64, 5, 2, true, 1>, g, b, lds, L, a)
+           : a.split == 2     ? pg_launch(k_step_fwdbwd8<64, 5, 2, false, 2>, g, b, lds, L, a)
+                              : pg_launch(k_step_fwdbwd8<64, 5, 2, false, 1>, g, b, lds, L, a);
+  return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<16, 5, 1, true, 1>, g, b, lds, L, a)
+         : a.split == 2     ? pg_launch(k_step_fwdbwd8<16, 5, 1, false, 2>, g, b, lds, L, a)
+                            : pg_launch(k_step_fwdbwd8<16, 5, 1, false, 1>, g, b, lds, L, a);
 }
 
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
