@@ -363,6 +363,8 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
     const int shape8 = fwdbwd8_shape(cf.d, cf.win, ctx->NT);
     fa.tiles_per_wg = ceil_div(fa.ntiles, shape8 ? std::min(ctx->max_parts, kF8MaxWorkgroups)
                                                  : ctx->max_parts);
+    // the pair form takes an even number of tiles per workgroup
+    if (shape8 && kF8MultiForm == 2 && fa.tiles_per_wg > 1) fa.tiles_per_wg += fa.tiles_per_wg & 1;
     n_fb = ceil_div(fa.ntiles, fa.tiles_per_wg);
     // one tile per workgroup and CUs to spare: two workgroups per tile, each
     // taking half of its backward (the forward runs in both)
@@ -374,7 +376,7 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
     {
       Timed tm(ctx, POLYGLOT_K_FWDBWD);
       if (shape8) {
-        size_t lds = fwdbwd8_lds_bytes(shape8);
+        size_t lds = fwdbwd8_lds_bytes(shape8, fa.tiles_per_wg);
         if (fa.n_sort) lds = std::max(lds, part_sort_lds_words(kF8Threads) * 4);
         e = launch_step_fwdbwd8(fa, shape8, fa.n_sort + n_fb, lds, tm.L);
       } else {

@@ -27,9 +27,12 @@
 // two workgroups take the same tile, both run the forward and the epilogue,
 // and each computes half of the dW1 and G output tiles, writing its own
 // dense-partial slot.
-// A workgroup with several tiles takes two barriers per tile: the tiles are
-// software-pipelined so that dW1 and G of one tile share a phase with the
-// forward of the next (a single tile takes three, in a plain sequence).
+// Three forms (FORM): 0, tiles one after another, three barriers each (a
+// workgroup with one tile); 1, tiles software-pipelined, two barriers each,
+// dW1 and G of one tile sharing a phase with the forward of the next; 2,
+// tiles in pairs, four barriers per pair: each phase holds the work of both
+// tiles (two independent MFMA chains per wave, and every wave busy in the
+// epilogue), at the price of a single X buffer.
 #pragma once
 #include "common.h"
 #include "launch.h"
@@ -40,7 +43,7 @@ __device__ __forceinline__ f4 mfma16x4(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-template <int D, int WIN, int NT>
+template <int D, int WIN, int NT, int TP>
 struct F8Shape {
   static constexpr int HP = NT * 16;         // hidden units, padded
   static constexpr int K = D * WIN;          // window vector length
@@ -49,39 +52,49 @@ struct F8Shape {
   static constexpr int DQ = D / 16;          // 16-column chunks per row
   static constexpr int QD = D / 4;           // column quads per row
   static constexpr int NCH = K / 16;         // K-chunks
-  static constexpr int KW = kF8Waves / NT;   // waves per hidden block
-  static constexpr int CPW = (NCH + KW - 1) / KW;  // chunks per wave
+  static constexpr int KW = kF8Waves / NT;   // dW1: waves per hidden block
+  static constexpr int CPW = (NCH + KW - 1) / KW;  // dW1: chunks per wave
+  static constexpr int KWF = kF8Waves / (TP * NT);  // forward: waves per output tile
+  static constexpr int CPWF = (NCH + KWF - 1) / KWF;  // forward: chunks per wave
   static constexpr int NGT = W1P * DQ;       // G output tiles per 16-window tile
-  static constexpr int GPW = (NGT + kF8Waves - 1) / kF8Waves;  // G tiles per wave
-  static constexpr int XF4 = W1P * QD * kTileRows;  // float4 pieces of X per tile
+  static constexpr int GPW = (TP * NGT + kF8Waves - 1) / kF8Waves;  // G tiles per wave
+  static constexpr int XF1 = W1P * QD * kTileRows;  // float4 pieces of X per tile
+  static constexpr int XF4 = TP * XF1;              // ... per group of TP tiles
   static constexpr int XPT = (XF4 + kF8Threads - 1) / kF8Threads;  // pieces per thread
   static constexpr int S = K + 4;            // W1 row stride in LDS
+  static constexpr int NXB = TP == 1 ? 2 : 1;  // X buffers
   // LDS, in floats
   static constexpr int kW1 = HP * S;
   static constexpr int kX = XF4 * 4;                       // one X buffer
   static constexpr int kZp = kF8Waves * 3 * 4 * kWave;     // forward split-K partials
-  static constexpr int kVt = 3 * kTileRows * (HP + 1);
+  static constexpr int kVt = TP * 3 * kTileRows * (HP + 1);
   static constexpr int kRed = kF8Waves * (2 * HP + 2);
-  static constexpr int kLds = kW1 + 2 * kX + kZp + kVt + kRed;
-  static_assert(D % 16 == 0 && WIN % 2 == 1 && kF8Waves % NT == 0, "shape");
+  static constexpr int kLds = kW1 + NXB * kX + kZp + kVt + kRed;
+  static_assert(D % 16 == 0 && WIN % 2 == 1 && kF8Waves % (TP * NT) == 0, "shape");
+  static_assert(kLds * 4 <= 160 * 1024, "LDS of one workgroup");
   static_assert(HP <= 32, "one hidden unit per lane of each 32-lane row half");
 };
 
-template <int D, int WIN, int NT, bool PIPE, int NH>
+template <int D, int WIN, int NT, int FORM, int NH>
 __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
-  using Sh = F8Shape<D, WIN, NT>;
+  constexpr int TP = FORM == 2 ? 2 : 1;  // tiles per phase
+  using Sh = F8Shape<D, WIN, NT, TP>;
   constexpr int HP = Sh::HP, K = Sh::K, C = Sh::C, W1P = Sh::W1P, DQ = Sh::DQ, QD = Sh::QD;
-  constexpr int NCH = Sh::NCH, KW = Sh::KW, CPW = Sh::CPW, NGT = Sh::NGT, GPW = Sh::GPW;
-  constexpr int XF4 = Sh::XF4, XPT = Sh::XPT, S = Sh::S;
+  constexpr int NCH = Sh::NCH, CPW = Sh::CPW, NGT = Sh::NGT, GPW = Sh::GPW;
+  constexpr int KWF = Sh::KWF, CPWF = Sh::CPWF;
+  constexpr int XF1 = Sh::XF1, XF4 = Sh::XF4, XPT = Sh::XPT, S = Sh::S;
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);  // wave-uniform
   const int n16 = lane & 15, g = lane >> 4;
-  const int nt_w = w % NT, kq = w / NT;  // forward: this wave's hidden block and chunk set
+  // forward: this wave's output tile otf (tile otf / NT of the group, hidden
+  // block otf % NT) and chunk set kqf
+  const int otf = w % (TP * NT), kqf = w / (TP * NT);
+  const int tpf = otf / NT, ntf = otf % NT;
 
   float* w1s = lds;                       // [HP][K+4]
-  float* xl = w1s + Sh::kW1;              // [2][W1P][QD][16] float4
-  float* zp = xl + 2 * Sh::kX;            // [kq][3][nt][4][64]
-  float* vt = zp + Sh::kZp;               // [3][16][HP+1]
+  float* xl = w1s + Sh::kW1;              // [NXB][TP][W1P][QD][16] float4
+  float* zp = xl + Sh::NXB * Sh::kX;      // [kqf][3][otf][4][64]
+  float* vt = zp + Sh::kZp;               // [TP][3][16][HP+1]
   float* red = vt + Sh::kVt;              // [waves][2*HP+2]
 
   // Split backward (NH == 2): workgroups 2q and 2q+1 take the same
@@ -89,7 +102,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   // every second dW1 output tile and every second G output tile (linear
   // indices L = 2 (w + 16 i) + h); each writes its own partial slot, and the
   // db1 / dw2 / loss sums come from half 0 only.
-  static_assert(NH == 1 || (NH == 2 && !PIPE), "the split takes single-tile workgroups");
+  static_assert(NH == 1 || (NH == 2 && FORM == 0), "the split takes single-tile workgroups");
   constexpr int nh = NH;
   const int h = wg & (nh - 1);
   const int tile0 = (wg / nh) * a.tiles_per_wg;
@@ -99,17 +112,19 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   const int ntd = (nh * w + h) % NT;
   const int ntl = min(a.tiles_per_wg, a.ntiles - tile0);  // tiles of this workgroup (>= 1)
 
-  // ids of the X pieces of this thread in tile `tile`: piece pi = t + 512 p
-  // covers window r = pi % 16, column quad (pi / 16) % QD, position
-  // pi / (16 QD) (position win: the corrupt id).  Rows >= B read row 0.  The
-  // loads are only issued here: the range check waits for them, so it sits
-  // in load_x, where the rows' addresses need the ids anyway.
+  // ids of the X pieces of this thread in the group of TP tiles starting at
+  // `tile`: piece pi = t + 512 p covers tile pi / XF1 of the group and,
+  // with q = pi % XF1, window r = q % 16, column quad (q / 16) % QD,
+  // position q / (16 QD) (position win: the corrupt id).  Rows >= B read
+  // row 0.  The loads are only issued here: the range check waits for them,
+  // so it sits in load_x, where the rows' addresses need the ids anyway.
   auto load_ids = [&](int tile, int32_t (&id)[XPT]) {
 #pragma unroll
     for (int p = 0; p < XPT; ++p) {
       const int pi = t + kF8Threads * p;
-      const int r = pi % kTileRows, j = pi / (kTileRows * QD);
-      const int b = tile * kTileRows + r;
+      const int tp = pi / XF1, q = pi - tp * XF1;
+      const int r = q % kTileRows, j = q / (kTileRows * QD);
+      const int b = (tile + tp) * kTileRows + r;
       id[p] = 0;
       if (pi < XF4 && b < a.B) id[p] = (j < WIN) ? a.windows[(size_t)b * WIN + j] : a.corrupt[b];
     }
@@ -121,7 +136,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
 #pragma unroll
     for (int p = 0; p < XPT; ++p) {
       const int pi = t + kF8Threads * p;
-      const int qq = (pi / kTileRows) % QD;
+      const int qq = ((pi % XF1) / kTileRows) % QD;
       const bool bk = (uint32_t)id[p] >= (uint32_t)a.V;
       bad |= bk;
       xr[p] = pi < XF4 ? ld4(a.E + (size_t)(bk ? 0 : id[p]) * D + 4 * qq) : kZero4;
@@ -152,7 +167,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       v[u] = (i < N4 && n < a.H) ? ld4(a.W1 + (size_t)n * K + 4 * k4) : kZero4;
     }
     load_x(ids[0], xr);
-    if (ntl > 1) load_ids(tile0 + 1, ids[1]);
+    if (ntl > TP) load_ids(tile0 + TP, ids[1]);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int i = u * kF8Threads + t;
@@ -171,18 +186,19 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   for (int ci = 0; ci < CPW; ++ci) accW[ci] = kZero4;
   float db1a = 0.f, dw2a = 0.f, lossa = 0.f;
 
-  // ---- forward of the tile in X: split-K partials into zp
-  auto forward = [&](const float* X) {
-    // ---- forward: wave (nt_w, kq) over chunks kc = kq + KW ci; common
+  // ---- forward of the tiles in X: split-K partials into zp
+  auto forward = [&](const float* Xg) {
+    // ---- forward: wave (otf, kqf) over chunks kc = kqf + KWF ci; common
     // blocks, true centre and corrupt centre accumulate separately
+    const float* X = Xg + 4 * XF1 * tpf;
     f4 zc = kZero4, zctr = kZero4, zcor = kZero4;
 #pragma unroll
-    for (int ci = 0; ci < CPW; ++ci) {
-      const int kc = kq + KW * ci;
+    for (int ci = 0; ci < CPWF; ++ci) {
+      const int kc = kqf + KWF * ci;
       if (kc < NCH) {
         const int j = kc / DQ, qq = 4 * (kc % DQ) + g;
         const f4 xa = ld4(X + 4 * ((j * QD + qq) * kTileRows + n16));
-        const f4 wb = ld4(w1s + (nt_w * 16 + n16) * S + kc * 16 + 4 * g);
+        const f4 wb = ld4(w1s + (ntf * 16 + n16) * S + kc * 16 + 4 * g);
         if (j != C) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) zc = mfma16x4(xa[q], wb[q], zc);
@@ -196,31 +212,32 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
         }
       }
     }
-    // partials [kq][type][nt][component][lane] (component-major: a reader of
-    // one component of every lane touches consecutive words)
+    // partials [kqf][type][otf][component][lane] (component-major: a
+    // reader of one component of every lane touches consecutive words)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      zp[(((kq * 3 + 0) * NT + nt_w) * 4 + i) * kWave + lane] = zc[i];
-      zp[(((kq * 3 + 1) * NT + nt_w) * 4 + i) * kWave + lane] = zctr[i];
-      zp[(((kq * 3 + 2) * NT + nt_w) * 4 + i) * kWave + lane] = zcor[i];
+      zp[(((kqf * 3 + 0) * (TP * NT) + otf) * 4 + i) * kWave + lane] = zc[i];
+      zp[(((kqf * 3 + 1) * (TP * NT) + otf) * 4 + i) * kWave + lane] = zctr[i];
+      zp[(((kqf * 3 + 2) * (TP * NT) + otf) * 4 + i) * kWave + lane] = zcor[i];
     }
   };
-  // ---- epilogue of the tile starting at row0: zp -> V (vt) and the
+  // ---- epilogue of the tiles starting at row0: zp -> V (vt) and the
   // accumulators
   auto epilogue = [&](int row0) {
-    // ---- epilogue: lane (hn, rsel) of wave w < 8 takes hidden unit hn of
-    // row 2w + rsel
-    if (w < kTileRows / 2) {
+    // ---- epilogue: lane (hn, rsel) of wave w < 8 TP takes hidden unit hn of
+    // row 2w + rsel of the group (tile tp = r / 16, row rr = r % 16 in it)
+    if (w < TP * kTileRows / 2) {
       const int r = 2 * w + rsel;
       const int row = row0 + r;
-      const int nt = hn >> 4, src = (hn & 15) + 16 * (r >> 2), comp = r & 3;
+      const int tp = r / kTileRows, rr = r % kTileRows;
+      const int ot = tp * NT + (hn >> 4), src = (hn & 15) + 16 * (rr >> 2), comp = rr & 3;
       float Zc = 0.f, Zctr = 0.f, Zcor = 0.f;
       if (hn < HP) {
 #pragma unroll
-        for (int v = 0; v < KW; ++v) {
-          Zc += zp[(((v * 3 + 0) * NT + nt) * 4 + comp) * kWave + src];
-          Zctr += zp[(((v * 3 + 1) * NT + nt) * 4 + comp) * kWave + src];
-          Zcor += zp[(((v * 3 + 2) * NT + nt) * 4 + comp) * kWave + src];
+        for (int v = 0; v < KWF; ++v) {
+          Zc += zp[(((v * 3 + 0) * (TP * NT) + ot) * 4 + comp) * kWave + src];
+          Zctr += zp[(((v * 3 + 1) * (TP * NT) + ot) * 4 + comp) * kWave + src];
+          Zcor += zp[(((v * 3 + 2) * (TP * NT) + ot) * 4 + comp) * kWave + src];
         }
       }
       const float z = b1v + (Zc + Zctr);
@@ -243,27 +260,29 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       const float dzt = gw * (1.f - ht * ht);
       const float dsum = gw * hmh * (h + ht);  // dz + dz~ = g w2 (h - h~)(h + h~)
       if (hn < HP) {
-        vt[(0 * kTileRows + r) * (HP + 1) + hn] = dsum;
-        vt[(1 * kTileRows + r) * (HP + 1) + hn] = dz;
-        vt[(2 * kTileRows + r) * (HP + 1) + hn] = dzt;
+        vt[((tp * 3 + 0) * kTileRows + rr) * (HP + 1) + hn] = dsum;
+        vt[((tp * 3 + 1) * kTileRows + rr) * (HP + 1) + hn] = dz;
+        vt[((tp * 3 + 2) * kTileRows + rr) * (HP + 1) + hn] = dzt;
       }
       db1a += dsum;
       dw2a -= gst * hmh;  // -(m/B) h + (m/B) h~
       if (hn == 0) lossa += on ? mg : 0.f;
     }
   };
-  // ---- dW1 and G of the tile in X starting at row0 (reads vt)
-  auto backward = [&](const float* X, int row0) {
-    // ---- dW1 += V^T X for this wave's output tiles (block ntd, chunks kc).
-    // A operand: lane (n16, g) holds V[4ii+g][ntd*16 + n16]; B operand:
-    // X[4ii+g][16kc + n16].
-    {
+  // ---- dW1 and G of the tiles in X starting at row0 (reads vt)
+  auto backward = [&](const float* Xg, int row0) {
+    // ---- dW1 += V^T X for this wave's output tiles (block ntd, chunks kc),
+    // the group's tiles in order.  A operand: lane (n16, g) holds
+    // V[4ii+g][ntd*16 + n16]; B operand: X[4ii+g][16kc + n16].
+#pragma unroll
+    for (int tp = 0; tp < TP; ++tp) {
+      const float* X = Xg + 4 * XF1 * tp;
       float vc[3][4];
 #pragma unroll
       for (int ty = 0; ty < 3; ++ty)
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii)
-          vc[ty][ii] = vt[(ty * kTileRows + 4 * ii + g) * (HP + 1) + ntd * 16 + n16];
+          vc[ty][ii] = vt[((tp * 3 + ty) * kTileRows + 4 * ii + g) * (HP + 1) + ntd * 16 + n16];
 #pragma unroll
       for (int ci = 0; ci < CPW; ++ci) {
         const int L = nh * (w + kF8Waves * ci) + h;
@@ -285,37 +304,38 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       }
     }
 
-    // ---- G: output tiles ot = nh (w + 16u) + h (position j = ot / DQ,
-    // columns cb*16).
+    // ---- G: output tiles ot = nh (w + 16u) + h of the group (tile
+    // ot / NGT, position j = (ot % NGT) / DQ, columns cb*16).
     // A operand: lane (r = n16, g) holds V_ty[r][4q + g]; B operand: lane
     // (col = n16, g) holds W1[4q + g][jj*D + cb*16 + col].
 #pragma unroll
     for (int u = 0; u < GPW; ++u) {
       const int ot = nh * (w + kF8Waves * u) + h;
-      if (ot < NGT) {
-        const int j = ot / DQ, cb = ot - (ot / DQ) * DQ;
+      if (ot < TP * NGT) {
+        const int tp = ot / NGT, o = ot - tp * NGT;
+        const int j = o / DQ, cb = o - (o / DQ) * DQ;
         const int ty = (j == WIN) ? 2 : (j == C ? 1 : 0);
         const int jj = (j == WIN) ? C : j;
         f4 acc = kZero4;
 #pragma unroll
         for (int q = 0; q < HP / 4; ++q) {
-          const float av = vt[(ty * kTileRows + n16) * (HP + 1) + 4 * q + g];
+          const float av = vt[((tp * 3 + ty) * kTileRows + n16) * (HP + 1) + 4 * q + g];
           const float bv = w1s[(4 * q + g) * S + jj * D + cb * 16 + n16];
           acc = mfma16x4(av, bv, acc);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int row = row0 + 4 * g + i;
+          const int row = row0 + tp * kTileRows + 4 * g + i;
           if (row < a.B) __builtin_nontemporal_store(acc[i], &a.G[((size_t)row * W1P + j) * D + cb * 16 + n16]);
         }
       }
     }
   };
 
-  if constexpr (!PIPE) {
+  if constexpr (FORM == 0) {
     // Tiles one after another, three barriers each (X staged, forward
     // partials, V).  Used when a workgroup has a single tile: the pipelined
-    // form below measured 0.3 us slower there.
+    // form measured 0.3 us slower there.
     for (int tt = 0; tt < ntl; ++tt) {
       const int tile = tile0 + tt;
       const int buf = tt & 1;
@@ -331,6 +351,27 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       epilogue(tile * kTileRows);
       __syncthreads();  // V written
       backward(X, tile * kTileRows);
+    }
+  } else if constexpr (FORM == 2) {
+    // Pairs of tiles, four barriers per pair (X staged, forward partials, V,
+    // and the end of the pair's dW1 before the next pair's rows overwrite
+    // the single X buffer).  tiles_per_wg is even, so the second tile of a
+    // pair is this workgroup's, or past the last tile (rows >= B).
+    const int ng = (ntl + 1) / 2;
+    for (int gi = 0; gi < ng; ++gi) {
+      const int row0 = (tile0 + 2 * gi) * kTileRows;
+      store_x(0, xr);
+      __syncthreads();  // X of this pair (and W1) staged
+      if (gi + 1 < ng) {
+        load_x(ids[(gi + 1) & 1], xr);                                // rows of the next pair
+        if (gi + 2 < ng) load_ids(tile0 + 2 * (gi + 2), ids[gi & 1]);  // ids two pairs ahead
+      }
+      forward(xl);
+      __syncthreads();  // forward partials written
+      epilogue(row0);
+      __syncthreads();  // V written
+      backward(xl, row0);
+      if (gi + 1 < ng) __syncthreads();  // X and vt free (uniform branch)
     }
   } else {
     // Software pipeline, two barriers per tile: the epilogue of tile t runs

@@ -62,10 +62,10 @@ __global__ __launch_bounds__(kBlock, (NT == 1 || (NT == 2 && CPW <= 5)) ? 2 : 1)
 }
 
 // The same step for the compile-time shapes, 16 waves per workgroup (the
-// sort role of small batches too); PIPE: software-pipelined tiles, for
-// workgroups with more than one tile; NH = 2: two workgroups per tile, each
-// taking half of the backward.
-template <int D, int WIN, int NT, bool PIPE, int NH>
+// sort role of small batches too); FORM: 0 single tile, 1 pipelined tiles, 2
+// tile pairs; NH = 2: two workgroups per tile, each taking half of the
+// backward.
+template <int D, int WIN, int NT, int FORM, int NH>
 __global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {
   extern __shared__ float lds_f[];
   if ((int)blockIdx.x < a.n_sort) {
@@ -75,7 +75,7 @@ __global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {
                           reinterpret_cast<uint32_t*>(lds_f));
     return;
   }
-  fwdbwd8_wg<D, WIN, NT, PIPE, NH>(a, blockIdx.x - a.n_sort, lds_f);
+  fwdbwd8_wg<D, WIN, NT, FORM, NH>(a, blockIdx.x - a.n_sort, lds_f);
 }
 
 // =============================================================== sort
@@ -168,20 +168,24 @@ int fwdbwd8_shape(int d, int win, int NT) {
   return 0;
 }
 
-size_t fwdbwd8_lds_bytes(int shape) {
-  return (shape == 1 ? F8Shape<64, 5, 2>::kLds : F8Shape<16, 5, 1>::kLds) * sizeof(float);
+size_t fwdbwd8_lds_bytes(int shape, int tiles_per_wg) {
+  constexpr int TP = kF8MultiForm == 2 ? 2 : 1;  // tiles per phase of the multi-tile form
+  if (tiles_per_wg > 1)
+    return (shape == 1 ? F8Shape<64, 5, 2, TP>::kLds : F8Shape<16, 5, 1, TP>::kLds) * sizeof(float);
+  return (shape == 1 ? F8Shape<64, 5, 2, 1>::kLds : F8Shape<16, 5, 1, 1>::kLds) * sizeof(float);
 }
 
 hipError_t launch_step_fwdbwd8(const FwdArgs& a, int shape, int grid, size_t lds,
                                const Launch& L) {
   const dim3 g(grid), b(kF8Threads);
+  constexpr int MF = kF8MultiForm;
   if (shape == 1)
-    return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<64, 5, 2, true, 1>, g, b, lds, L, a)
-           : a.split == 2     ? pg_launch(k_step_fwdbwd8<64, 5, 2, false, 2>, g, b, lds, L, a)
-                              : pg_launch(k_step_fwdbwd8<64, 5, 2, false, 1>, g, b, lds, L, a);
-  return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<16, 5, 1, true, 1>, g, b, lds, L, a)
-         : a.split == 2     ? pg_launch(k_step_fwdbwd8<16, 5, 1, false, 2>, g, b, lds, L, a)
-                            : pg_launch(k_step_fwdbwd8<16, 5, 1, false, 1>, g, b, lds, L, a);
+    return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<64, 5, 2, MF, 1>, g, b, lds, L, a)
+           : a.split == 2     ? pg_launch(k_step_fwdbwd8<64, 5, 2, 0, 2>, g, b, lds, L, a)
+                              : pg_launch(k_step_fwdbwd8<64, 5, 2, 0, 1>, g, b, lds, L, a);
+  return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<16, 5, 1, MF, 1>, g, b, lds, L, a)
+         : a.split == 2     ? pg_launch(k_step_fwdbwd8<16, 5, 1, 0, 2>, g, b, lds, L, a)
+                            : pg_launch(k_step_fwdbwd8<16, 5, 1, 0, 1>, g, b, lds, L, a);
 }
 
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,

@@ -156,9 +156,12 @@ struct GatherArgs {
 hipError_t launch_step_fwdbwd(const FwdArgs& a, int NT, int cpw, int grid, size_t lds,
                               const Launch& L);
 // 16-wave fused kernel for the compile-time shapes: fwdbwd8_shape() gives the
-// shape id (0: not covered), fwdbwd8_lds_bytes() its LDS.
+// shape id (0: not covered), fwdbwd8_lds_bytes() its LDS.  Workgroups with
+// more than one tile take form kF8MultiForm (2: tile pairs, tiles_per_wg
+// even; 1: software-pipelined single tiles).
 int fwdbwd8_shape(int d, int win, int NT);
-size_t fwdbwd8_lds_bytes(int shape);
+size_t fwdbwd8_lds_bytes(int shape, int tiles_per_wg);
+constexpr int kF8MultiForm = 2;
 constexpr int kF8Waves = 16;
 constexpr int kF8Threads = kF8Waves * kWave;  // 512
 constexpr int kF8MaxWorkgroups = 256;         // one workgroup per CU
