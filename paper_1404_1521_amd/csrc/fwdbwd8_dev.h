@@ -113,7 +113,7 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
   const int ntl = min(a.tiles_per_wg, a.ntiles - tile0);  // tiles of this workgroup (>= 1)
 
   // ids of the X pieces of this thread in the group of TP tiles starting at
-  // `tile`: piece pi = t + 512 p covers tile pi / XF1 of the group and,
+  // `tile`: piece pi = t + 1024 p covers tile pi / XF1 of the group and,
   // with q = pi % XF1, window r = q % 16, column quad (q / 16) % QD,
   // position q / (16 QD) (position win: the corrupt id).  Rows >= B read
   // row 0.  The loads are only issued here: the range check waits for them,

@@ -163,7 +163,7 @@ int fwdbwd8_shape(int d, int win, int NT);
 size_t fwdbwd8_lds_bytes(int shape, int tiles_per_wg);
 constexpr int kF8MultiForm = 2;
 constexpr int kF8Waves = 16;
-constexpr int kF8Threads = kF8Waves * kWave;  // 512
+constexpr int kF8Threads = kF8Waves * kWave;  // 1024
 constexpr int kF8MaxWorkgroups = 256;         // one workgroup per CU
 hipError_t launch_step_fwdbwd8(const FwdArgs& a, int shape, int grid, size_t lds,
                                const Launch& L);
