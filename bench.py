@@ -274,12 +274,16 @@ def time_events(torch, stream, fn, reps):
 
 
 def kernel_rooflines(torch, np, pg, workloads, stream, reps=20):
-    """Standalone gather (B=65536 windows) and scatter-add (327,680 Zipf(1.2)
-    rows into a 100k x 64 table) with their HBM rooflines.  Durations are the
-    library's per-kernel events (bound to the dispatch).  The scatter-add's
-    roofline covers its table-update kernels (the sort is reported separately,
-    as its bytes are not the operation's); whole calls are timed end to end on
-    the stream as well."""
+    """Standalone gather (B = 16,384 windows over the 1M x 128 stress table,
+    and B = 65,536 over the cache-resident 100k x 64 table), scatter-add
+    (327,680 Zipf(1.2) rows into a 100k x 64 table) and the general op
+    (bfloat16 increment with int64 ids, binary16 assignment with int32 ids,
+    same workload) with
+    their HBM rooflines.  Durations are the library's per-kernel events (bound
+    to the dispatch).  A scatter-add or general-op roofline covers the
+    table-update kernels (the sort is reported separately, as its bytes are
+    not the operation's); whole calls are timed end to end on the stream as
+    well."""
     out = {}
     # The gather, twice: over the stress table (1M x 128 floats, 512 MB,
     # twice the 256 MB Infinity Cache) and over the 100k x 64 table (25.6 MB,
