@@ -367,8 +367,11 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
     if (shape8 && kF8MultiForm == 2 && fa.tiles_per_wg > 1) fa.tiles_per_wg += fa.tiles_per_wg & 1;
     n_fb = ceil_div(fa.ntiles, fa.tiles_per_wg);
     // one tile per workgroup and CUs to spare: two workgroups per tile, each
-    // taking half of its backward (the forward runs in both)
-    fa.split = (shape8 && fa.tiles_per_wg == 1 && fa.n_sort + 2 * n_fb <= kF8MaxWorkgroups) ? 2 : 1;
+    // taking half of its backward (the forward runs in both).  Only the
+    // d 64 shape: the small one's backward is too short to pay for the
+    // second copy of the forward (B = 32 step 11.6 -> 11.8 us split).
+    fa.split = (shape8 == 1 && fa.tiles_per_wg == 1 && fa.n_sort + 2 * n_fb <= kF8MaxWorkgroups)
+                   ? 2 : 1;
     n_fb *= fa.split;
     split = fa.split;
     fa.part_stride = ctx->part_stride;

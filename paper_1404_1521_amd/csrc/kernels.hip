@@ -184,7 +184,6 @@ hipError_t launch_step_fwdbwd8(const FwdArgs& a, int shape, int grid, size_t lds
            : a.split == 2     ? pg_launch(k_step_fwdbwd8<64, 5, 2, 0, 2>, g, b, lds, L, a)
                               : pg_launch(k_step_fwdbwd8<64, 5, 2, 0, 1>, g, b, lds, L, a);
   return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<16, 5, 1, MF, 1>, g, b, lds, L, a)
-         : a.split == 2     ? pg_launch(k_step_fwdbwd8<16, 5, 1, 0, 2>, g, b, lds, L, a)
                             : pg_launch(k_step_fwdbwd8<16, 5, 1, 0, 1>, g, b, lds, L, a);
 }
 
