@@ -34,6 +34,8 @@
 // tiles (two independent MFMA chains per wave, and every wave busy in the
 // epilogue), at the price of a single X buffer.
 #pragma once
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
 
@@ -441,6 +443,370 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
       float s = red[e];
 #pragma unroll
       for (int v = 1; v < kF8Waves; ++v) s += red[v * (2 * HP + 2) + e];
+      P[HP * K + e] = s;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Role-specialised form for workgroups with many tiles (hidden layer of 32
+// units, NT = 2), 12 waves per workgroup.  The other forms keep all 16 waves
+// in step, so the epilogue (tanh, scores, shuffles: vector-ALU work) never
+// overlaps the matrix work.  Here the waves take roles:
+//   waves 0-3    staging and epilogue: the ids and rows of later tiles, the
+//                X tile into LDS, and the epilogue of tile k-1 (a lane per
+//                hidden unit of two rows);
+//   waves 4-7    forward of tile k: output block nt = (w-4) / 2, the K-half
+//                kh = (w-4) % 2 of the chunks, W1 operands held in
+//                registers for the whole launch;
+//   waves 8-11   dW1 of tile k-2: output block nt = (w-8) / 2, chunk half
+//                (w-8) % 2, accumulated in registers across the tiles;
+//   waves 4-11   G of tile k-2, three 16x16 output tiles each, their W1
+//                operands held in registers too.
+// Each SIMD thus runs a staging/epilogue wave beside two matrix waves, with
+// the registers of three waves per SIMD (the register-resident operands do
+// not fit four).
+// One barrier per phase: phase p runs forward(p), epilogue(p-1) and
+// dW1/G(p-2), with four X buffers (a tile's rows are written in phase k-1,
+// read by the forward in phase k and by dW1 in phase k+2) and two buffers
+// each of the split-K partials and of V.  W1 is not in LDS at all.
+template <int D, int WIN>
+struct F8WsShape {
+  static constexpr int NT = 2, HP = 32, K = D * WIN, C = WIN / 2, W1P = WIN + 1;
+  static constexpr int DQ = D / 16, QD = D / 4, NCH = K / 16;
+  static constexpr int NE = 4;                       // staging / epilogue waves
+  static constexpr int NW = 12;                      // waves per workgroup
+  static constexpr int NTH = NW * kWave;
+  static_assert(NTH == kF8WsThreads, "launch shape");
+  static constexpr int CF = NCH / 2;                 // chunks per forward or dW1 wave
+  static constexpr int NGT = W1P * DQ;               // G output tiles per tile
+  static constexpr int GPW = (NGT + 7) / 8;          // G tiles per matrix wave
+  static constexpr int XF1 = W1P * QD * kTileRows;   // float4 pieces of X per tile
+  static constexpr int XPE = (XF1 + NE * kWave - 1) / (NE * kWave);  // per staging lane
+  static constexpr int kX = XF1 * 4;                 // one X buffer, floats
+  static constexpr int kZp = 2 * 3 * NT * 4 * kWave; // one partial buffer: [kh][type][nt][4][64]
+  static constexpr int kVt = 3 * kTileRows * (HP + 1);
+  static constexpr int kRed = NE * (2 * HP + 2);
+  static constexpr int kLds = 4 * kX + 2 * kZp + 2 * kVt + kRed;
+  static_assert(NCH % 2 == 0 && D % 16 == 0 && WIN % 2 == 1, "shape");
+  static_assert(kLds * 4 <= 160 * 1024, "LDS of one workgroup");
+};
+
+template <int D, int WIN>
+__device__ void fwdbwd8_ws(const FwdArgs& a, int wg, float* lds) {
+  using Sh = F8WsShape<D, WIN>;
+  constexpr int NT = Sh::NT, HP = Sh::HP, K = Sh::K, C = Sh::C, W1P = Sh::W1P, DQ = Sh::DQ;
+  constexpr int QD = Sh::QD, NE = Sh::NE, CF = Sh::CF, NGT = Sh::NGT;
+  constexpr int GPW = Sh::GPW, XF1 = Sh::XF1, XPE = Sh::XPE;
+  const int t = threadIdx.x, lane = t & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);  // wave-uniform
+  const bool stager = w < NE;
+  float* xl = lds;                                 // [4][W1P][QD][16] float4
+  float* zp = xl + 4 * Sh::kX;                     // [2][kh][3][nt][4][64]
+  float* vt = zp + 2 * Sh::kZp;                    // [2][3][16][HP+1]
+  float* red = vt + 2 * Sh::kVt;                   // [NE][2*HP+2]
+  const int tile0 = wg * a.tiles_per_wg;
+  const int ntl = min(a.tiles_per_wg, a.ntiles - tile0);
+
+  // staging lanes: piece pi = t + 256 p of a tile covers window pi % 16,
+  // column quad (pi / 16) % QD, position pi / (16 QD); rows >= B read row 0
+  auto load_ids = [&](int tile, int32_t (&id)[XPE]) {
+#pragma unroll
+    for (int p = 0; p < XPE; ++p) {
+      const int pi = t + NE * kWave * p;
+      const int r = pi % kTileRows, j = pi / (kTileRows * QD);
+      const int b = tile * kTileRows + r;
+      id[p] = 0;
+      if (pi < XF1 && b < a.B) id[p] = (j < WIN) ? a.windows[(size_t)b * WIN + j] : a.corrupt[b];
+    }
+  };
+  auto load_x = [&](const int32_t (&id)[XPE], f4 (&xr)[XPE]) {
+    bool bad = false;
+#pragma unroll
+    for (int p = 0; p < XPE; ++p) {
+      const int pi = t + NE * kWave * p;
+      const int qq = (pi / kTileRows) % QD;
+      const bool bk = (uint32_t)id[p] >= (uint32_t)a.V;
+      bad |= bk;
+      xr[p] = pi < XF1 ? ld4(a.E + (size_t)(bk ? 0 : id[p]) * D + 4 * qq) : kZero4;
+    }
+    if (bad) atomicOr(a.flag, kFlagBadId);
+  };
+  auto store_x = [&](int buf, const f4 (&xr)[XPE]) {
+#pragma unroll
+    for (int p = 0; p < XPE; ++p) {
+      const int pi = t + NE * kWave * p;
+      if (pi < XF1) st4(xl + buf * Sh::kX + 4 * pi, xr[p]);
+    }
+  };
+
+  // Registers of the matrix waves.  rr: the forward waves' W1 operands (lane
+  // (n16, g) holds W1[nt*16 + n16][16kc + 4g .. +3] for its chunks kc =
+  // kh*CF + c), the dW1 waves' accumulators.  wg1: the G operands of the
+  // wave's output tiles ot = mi + 8u (lane (n16, g) holds W1[4q + g][jj*D +
+  // cb*16 + n16] at step q).
+  f4 rr[CF];
+  float wg1[GPW][HP / 4];
+#pragma unroll
+  for (int c = 0; c < CF; ++c) rr[c] = kZero4;
+#pragma unroll
+  for (int u = 0; u < GPW; ++u)
+#pragma unroll
+    for (int q = 0; q < HP / 4; ++q) wg1[u][q] = 0.f;
+
+  // The work of matrix wave MI = w - NE (a compile-time constant, so that
+  // every operand offset is an immediate): stage 0 loads its W1 operands;
+  // stage 1 runs phase p (forward of tile p for MI < 4; dW1 of tile p-2 for
+  // MI >= 4; G of tile p-2 for all).
+  auto matrix = [&](auto mic, int stage, int p, int n16, int g) {
+    constexpr int MI = decltype(mic)::value;
+    constexpr int nt = (MI & 3) >> 1, kh = MI & 1;
+    constexpr bool FWD = MI < 4;
+    if (stage == 0) {
+      if constexpr (FWD) {
+        const int n = nt * 16 + n16;
+#pragma unroll
+        for (int c = 0; c < CF; ++c)
+          rr[c] = n < a.H ? ld4(a.W1 + (size_t)n * K + (kh * CF + c) * 16 + 4 * g) : kZero4;
+      }
+#pragma unroll
+      for (int u = 0; u < GPW; ++u) {
+        const int ot = MI + 8 * u;
+        if (ot < NGT) {
+          const int j = ot / DQ, cb = ot % DQ, jj = (j == WIN) ? C : j;
+#pragma unroll
+          for (int q = 0; q < HP / 4; ++q) {
+            const int k = 4 * q + g;
+            wg1[u][q] = k < a.H ? a.W1[(size_t)k * K + jj * D + cb * 16 + n16] : 0.f;
+          }
+        }
+      }
+      return;
+    }
+    if constexpr (FWD) {
+      if (p < ntl) {
+        // ---- forward of tile p: split-K partials of half kh into zp[p % 2]
+        const float* X = xl + (p & 3) * Sh::kX;
+        f4 zc = kZero4, zctr = kZero4, zcor = kZero4;
+#pragma unroll
+        for (int c = 0; c < CF; ++c) {
+          __builtin_amdgcn_sched_barrier(0);  // one chunk's operands in flight at a time
+          const int kc = kh * CF + c;
+          const int j = kc / DQ, qq = 4 * (kc % DQ) + g;
+          const f4 xa = ld4(X + 4 * ((j * QD + qq) * kTileRows + n16));
+          if (j != C) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) zc = mfma16x4(xa[q], rr[c][q], zc);
+          } else {
+            const f4 xt = ld4(X + 4 * ((WIN * QD + qq) * kTileRows + n16));
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              zctr = mfma16x4(xa[q], rr[c][q], zctr);
+              zcor = mfma16x4(xt[q], rr[c][q], zcor);
+            }
+          }
+        }
+        float* Z = zp + (p & 1) * Sh::kZp;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          Z[(((kh * 3 + 0) * NT + nt) * 4 + i) * kWave + lane] = zc[i];
+          Z[(((kh * 3 + 1) * NT + nt) * 4 + i) * kWave + lane] = zctr[i];
+          Z[(((kh * 3 + 2) * NT + nt) * 4 + i) * kWave + lane] = zcor[i];
+        }
+      }
+    }
+    if (p >= 2) {
+      const int q2 = p - 2;  // the tile whose backward runs now
+      const float* X = xl + (q2 & 3) * Sh::kX;
+      const float* V = vt + (q2 & 1) * Sh::kVt;
+      const int row0 = (tile0 + q2) * kTileRows;
+      if constexpr (!FWD) {
+        // ---- dW1 += V^T X for block nt, chunks kc = kh*CF + c.  A operand:
+        // lane (n16, g) holds V[4ii+g][nt*16 + n16]; B operand:
+        // X[4ii+g][16kc + n16].
+        float vc[3][4];
+#pragma unroll
+        for (int ty = 0; ty < 3; ++ty)
+#pragma unroll
+          for (int ii = 0; ii < 4; ++ii)
+            vc[ty][ii] = V[(ty * kTileRows + 4 * ii + g) * (HP + 1) + nt * 16 + n16];
+#pragma unroll
+        for (int c = 0; c < CF; ++c) {
+          __builtin_amdgcn_sched_barrier(0);
+          const int kc = kh * CF + c;
+          const int j = kc / DQ, qq = 4 * (kc % DQ) + (n16 >> 2);
+#pragma unroll
+          for (int ii = 0; ii < 4; ++ii) {
+            const float xb = X[4 * ((j * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
+            if (j != C) {
+              rr[c] = mfma16x4(vc[0][ii], xb, rr[c]);
+            } else {
+              const float xc = X[4 * ((WIN * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
+              rr[c] = mfma16x4(vc[1][ii], xb, rr[c]);
+              rr[c] = mfma16x4(vc[2][ii], xc, rr[c]);
+            }
+          }
+        }
+      }
+      // ---- G: output tiles ot = MI + 8u (position j = ot / DQ, columns
+      // cb*16).  A operand: lane (r = n16, g) holds V_ty[r][4q + g].
+#pragma unroll
+      for (int u = 0; u < GPW; ++u) {
+        const int ot = MI + 8 * u;
+        if (ot < NGT) {
+          const int j = ot / DQ, cb = ot % DQ;
+          const int ty = (j == WIN) ? 2 : (j == C ? 1 : 0);
+          f4 acc = kZero4;
+#pragma unroll
+          for (int q = 0; q < HP / 4; ++q)
+            acc = mfma16x4(V[(ty * kTileRows + n16) * (HP + 1) + 4 * q + g], wg1[u][q], acc);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int row = row0 + 4 * g + i;
+            if (row < a.B) __builtin_nontemporal_store(acc[i], &a.G[((size_t)row * W1P + j) * D + cb * 16 + n16]);
+          }
+        }
+      }
+    }
+  };
+  auto run_matrix = [&](int stage, int p) {
+    // the lane's coordinates through an opaque copy, so that the compiler
+    // recomputes each role's operand offsets in the phase instead of
+    // hoisting all eight roles' offsets out of the loop into registers
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int n16 = ln & 15, g = ln >> 4;
+    switch (w - NE) {
+      case 0: matrix(std::integral_constant<int, 0>{}, stage, p, n16, g); break;
+      case 1: matrix(std::integral_constant<int, 1>{}, stage, p, n16, g); break;
+      case 2: matrix(std::integral_constant<int, 2>{}, stage, p, n16, g); break;
+      case 3: matrix(std::integral_constant<int, 3>{}, stage, p, n16, g); break;
+      case 4: matrix(std::integral_constant<int, 4>{}, stage, p, n16, g); break;
+      case 5: matrix(std::integral_constant<int, 5>{}, stage, p, n16, g); break;
+      case 6: matrix(std::integral_constant<int, 6>{}, stage, p, n16, g); break;
+      default: matrix(std::integral_constant<int, 7>{}, stage, p, n16, g); break;
+    }
+  };
+
+  // epilogue lane map (staging waves): hidden unit hn = lane % 32 of rows
+  // 2w + lane / 32 and 2w + lane / 32 + 8
+  const int hn = lane & 31, rsel = lane >> 5;
+  float b1v = 0.f, w2v = 0.f, b2v = 0.f;
+  float db1a = 0.f, dw2a = 0.f, lossa = 0.f;
+  // The staging waves' rows in flight live in rr, which they do not use
+  // otherwise, so that the union of the roles' registers stays small.  (Ids
+  // loaded a phase ahead and held there too measured 1 us slower per step.)
+  static_assert(XPE <= CF, "staging rows fit the matrix registers");
+  f4 (&xr)[XPE] = *reinterpret_cast<f4 (*)[XPE]>(&rr[0]);
+  if (stager) {
+    b1v = hn < a.H ? a.b1[hn] : 0.f;
+    w2v = hn < a.H ? a.w2[hn] : 0.f;
+    b2v = a.b2[0];
+    int32_t ids[XPE];
+    load_ids(tile0, ids);
+    load_x(ids, xr);
+    store_x(0, xr);
+    if (ntl > 1) {
+      load_ids(tile0 + 1, ids);
+      load_x(ids, xr);
+    }
+  } else {
+    run_matrix(0, 0);
+  }
+  __syncthreads();  // X of tile 0 staged
+
+  for (int p = 0; p < ntl + 2; ++p) {
+    if (stager) {
+      if (p >= 1 && p <= ntl) {
+        // ---- epilogue of tile p-1: zp[(p-1) % 2] -> vt[(p-1) % 2]
+        const float* Z = zp + ((p - 1) & 1) * Sh::kZp;
+        float* V = vt + ((p - 1) & 1) * Sh::kVt;
+#pragma unroll
+        for (int s8 = 0; s8 < 2; ++s8) {
+          const int r = 2 * w + rsel + 8 * s8;
+          const int row = (tile0 + p - 1) * kTileRows + r;
+          const int ntr = hn >> 4, src = (hn & 15) + 16 * (r >> 2), comp = r & 3;
+          float Zc = 0.f, Zctr = 0.f, Zcor = 0.f;
+#pragma unroll
+          for (int v = 0; v < 2; ++v) {
+            Zc += Z[(((v * 3 + 0) * NT + ntr) * 4 + comp) * kWave + src];
+            Zctr += Z[(((v * 3 + 1) * NT + ntr) * 4 + comp) * kWave + src];
+            Zcor += Z[(((v * 3 + 2) * NT + ntr) * 4 + comp) * kWave + src];
+          }
+          const float z = b1v + (Zc + Zctr);
+          const float zt = b1v + (Zc + Zcor);
+          const float h = tanh_fast(z), ht = tanh_fast(zt);
+          // h - h~ = tanh(z - z~) (1 - h h~), z - z~ = zctr - zcor without
+          // cancellation against the common part
+          const float hmh = tanh_fast(Zctr - Zcor) * (1.f - h * ht);
+          float ps = w2v * h, pst = w2v * ht;
+#pragma unroll
+          for (int o = 1; o < 32; o <<= 1) {
+            ps += __shfl_xor(ps, o);
+            pst += __shfl_xor(pst, o);
+          }
+          const float mg = 1.f - (b2v + ps) + (b2v + pst);
+          const bool on = row < a.B && mg > 0.f;  // hinge active (derivative 0 at margin 0)
+          const float gst = on ? a.invB : 0.f;    // d loss/d s~ = m/B, d loss/d s = -m/B
+          const float gw = gst * w2v;
+          const float dz = -gw * (1.f - h * h);
+          const float dzt = gw * (1.f - ht * ht);
+          const float dsum = gw * hmh * (h + ht);  // dz + dz~ = g w2 (h - h~)(h + h~)
+          V[(0 * kTileRows + r) * (HP + 1) + hn] = dsum;
+          V[(1 * kTileRows + r) * (HP + 1) + hn] = dz;
+          V[(2 * kTileRows + r) * (HP + 1) + hn] = dzt;
+          db1a += dsum;
+          dw2a -= gst * hmh;  // -(m/B) h + (m/B) h~
+          if (hn == 0) lossa += on ? mg : 0.f;
+        }
+      }
+      if (p + 1 < ntl) {
+        store_x((p + 1) & 3, xr);  // rows of tile p+1
+        if (p + 2 < ntl) {         // rows of tile p+2 (their ids first: the wait
+          int32_t ids[XPE];        // overlaps the matrix waves' work)
+          load_ids(tile0 + p + 2, ids);
+          load_x(ids, xr);
+        }
+      }
+    } else {
+      run_matrix(1, p);
+    }
+    __syncthreads();  // this phase's X, zp and vt writes visible; its reads done
+  }
+
+  // ---- this workgroup's partial slot: dW1 [Hp][K] from the dW1 waves, then
+  // db1 [Hp], dw2 [Hp], loss, db2 from the staging waves
+  float* P = a.part + (size_t)wg * a.part_stride;
+  if (w >= NE + 4) {
+    const int mi = w - NE, nt = (mi & 3) >> 1, kh = mi & 1;
+    const int n16 = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int c = 0; c < CF; ++c) {
+      const int kc = kh * CF + c;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) __builtin_nontemporal_store(rr[c][i], &P[(nt * 16 + 4 * g + i) * K + kc * 16 + n16]);
+    }
+  }
+  if (stager) {
+    db1a += __shfl_xor(db1a, 32);
+    dw2a += __shfl_xor(dw2a, 32);
+    for (int o = 1; o < kWave; o <<= 1) lossa += __shfl_xor(lossa, o);
+    float* rw = red + w * (2 * HP + 2);
+    if (rsel == 0) {
+      rw[hn] = db1a;
+      rw[HP + hn] = dw2a;
+    }
+    if (lane == 0) {
+      rw[2 * HP] = lossa;
+      rw[2 * HP + 1] = 0.f;
+    }
+  }
+  __syncthreads();
+  if (w == 0) {
+    for (int e = lane; e < 2 * HP + 2; e += kWave) {
+      float s = red[e];
+#pragma unroll
+      for (int v = 1; v < NE; ++v) s += red[v * (2 * HP + 2) + e];
       P[HP * K + e] = s;
     }
   }

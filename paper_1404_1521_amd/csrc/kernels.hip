@@ -78,6 +78,14 @@ __global__ __launch_bounds__(kF8Threads, 1) void k_step_fwdbwd8(FwdArgs a) {
   fwdbwd8_wg<D, WIN, NT, FORM, NH>(a, blockIdx.x - a.n_sort, lds_f);
 }
 
+// Role-specialised form for workgroups with many tiles (12 waves; never
+// with the sort role, which only small batches take).
+template <int D, int WIN>
+__global__ __launch_bounds__(kF8WsThreads, 1) void k_step_fwdbwd8_ws(FwdArgs a) {
+  extern __shared__ float lds_f[];
+  fwdbwd8_ws<D, WIN>(a, blockIdx.x, lds_f);
+}
+
 // =============================================================== sort
 
 // Partitioned sort of a small list, partition blockIdx.x.
@@ -169,6 +177,7 @@ int fwdbwd8_shape(int d, int win, int NT) {
 }
 
 size_t fwdbwd8_lds_bytes(int shape, int tiles_per_wg) {
+  if (shape == 1 && tiles_per_wg >= kF8WsMinTiles) return F8WsShape<64, 5>::kLds * sizeof(float);  // n_sort is 0 there
   constexpr int TP = kF8MultiForm == 2 ? 2 : 1;  // tiles per phase of the multi-tile form
   if (tiles_per_wg > 1)
     return (shape == 1 ? F8Shape<64, 5, 2, TP>::kLds : F8Shape<16, 5, 1, TP>::kLds) * sizeof(float);
@@ -180,7 +189,9 @@ hipError_t launch_step_fwdbwd8(const FwdArgs& a, int shape, int grid, size_t lds
   const dim3 g(grid), b(kF8Threads);
   constexpr int MF = kF8MultiForm;
   if (shape == 1)
-    return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<64, 5, 2, MF, 1>, g, b, lds, L, a)
+    return a.tiles_per_wg >= kF8WsMinTiles && a.n_sort == 0
+               ? pg_launch(k_step_fwdbwd8_ws<64, 5>, g, dim3(kF8WsThreads), lds, L, a)
+           : a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<64, 5, 2, MF, 1>, g, b, lds, L, a)
            : a.split == 2     ? pg_launch(k_step_fwdbwd8<64, 5, 2, 0, 2>, g, b, lds, L, a)
                               : pg_launch(k_step_fwdbwd8<64, 5, 2, 0, 1>, g, b, lds, L, a);
   return a.tiles_per_wg > 1 ? pg_launch(k_step_fwdbwd8<16, 5, 1, MF, 1>, g, b, lds, L, a)
