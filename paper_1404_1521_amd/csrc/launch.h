@@ -164,7 +164,7 @@ size_t fwdbwd8_lds_bytes(int shape, int tiles_per_wg);
 constexpr int kF8MultiForm = 2;
 // From this many tiles per workgroup the d 64 shape takes the role-specialised
 // form (form 3), whose three-stage pipeline fills and drains over two phases.
-constexpr int kF8WsMinTiles = 4;
+constexpr int kF8WsMinTiles = 8;  // at 4 (B = 16,384) tile pairs were 1 us faster
 constexpr int kF8WsThreads = 12 * kWave;  // its workgroup: 12 waves
 constexpr int kF8Waves = 16;
 constexpr int kF8Threads = kF8Waves * kWave;  // 1024
