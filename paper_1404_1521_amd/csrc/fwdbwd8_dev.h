@@ -469,7 +469,13 @@ __device__ void fwdbwd8_wg(const FwdArgs& a, int wg, float* lds) {
 // One barrier per phase: phase p runs forward(p), epilogue(p-1) and
 // dW1/G(p-2), with four X buffers (a tile's rows are written in phase k-1,
 // read by the forward in phase k and by dW1 in phase k+2) and two buffers
-// each of the split-K partials and of V.  W1 is not in LDS at all.
+// each of the split-K partials and of V.  W1 is not in LDS at all.  The X
+// tile is stored by column, [position][column][window] with the 16 windows
+// of a column padded to XS = 20 floats: a dW1 lane reads the four windows
+// its MFMA steps need in one 128-bit read (the contraction runs over the
+// windows in the order 4g + step, on both operands), and the forward's
+// operand reads (four columns of one window) and the staging stores are
+// 32-bit accesses on 64 distinct banks.
 template <int D, int WIN>
 struct F8WsShape {
   static constexpr int NT = 2, HP = 32, K = D * WIN, C = WIN / 2, W1P = WIN + 1;
@@ -482,7 +488,8 @@ struct F8WsShape {
   static constexpr int NGT = W1P * DQ;               // G output tiles per tile
   static constexpr int XF1 = W1P * QD * kTileRows;   // float4 pieces of X per tile
   static constexpr int XPE = (XF1 + NE * kWave - 1) / (NE * kWave);  // per staging lane
-  static constexpr int kX = XF1 * 4;                 // one X buffer, floats
+  static constexpr int XS = kTileRows + 4;           // floats per column of an X tile
+  static constexpr int kX = W1P * D * XS;            // one X buffer, floats
   static constexpr int kZp = 2 * 3 * NT * 4 * kWave; // one partial buffer: [kh][type][nt][4][64]
   static constexpr int kVt = 3 * kTileRows * (HP + 1);
   static constexpr int kRed = NE * (2 * HP + 2);
@@ -496,11 +503,11 @@ __device__ void fwdbwd8_ws(const FwdArgs& a, int wg, float* lds) {
   using Sh = F8WsShape<D, WIN>;
   constexpr int NT = Sh::NT, HP = Sh::HP, K = Sh::K, C = Sh::C, W1P = Sh::W1P, DQ = Sh::DQ;
   constexpr int QD = Sh::QD, NE = Sh::NE, CF = Sh::CF, NGT = Sh::NGT;
-  constexpr int XF1 = Sh::XF1, XPE = Sh::XPE;
+  constexpr int XF1 = Sh::XF1, XPE = Sh::XPE, XS = Sh::XS;
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);  // wave-uniform
   const bool stager = w < NE;
-  float* xl = lds;                                 // [4][W1P][QD][16] float4
+  float* xl = lds;                                 // [4][W1P][D][XS]
   float* zp = xl + 4 * Sh::kX;                     // [2][kh][3][nt][4][64]
   float* vt = zp + 2 * Sh::kZp;                    // [2][3][16][HP+1]
   float* red = vt + 2 * Sh::kVt;                   // [NE][2*HP+2]
@@ -531,11 +538,17 @@ __device__ void fwdbwd8_ws(const FwdArgs& a, int wg, float* lds) {
     }
     if (bad) atomicOr(a.flag, kFlagBadId);
   };
+  // piece pi (window r, column quad qq, position j) to its four columns
   auto store_x = [&](int buf, const f4 (&xr)[XPE]) {
 #pragma unroll
     for (int p = 0; p < XPE; ++p) {
       const int pi = t + NE * kWave * p;
-      if (pi < XF1) st4(xl + buf * Sh::kX + 4 * pi, xr[p]);
+      const int r = pi % kTileRows, qq = (pi / kTileRows) % QD, j = pi / (kTileRows * QD);
+      float* dst = xl + buf * Sh::kX + (j * D + 4 * qq) * XS + r;
+      if (pi < XF1) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) dst[c * XS] = xr[p][c];
+      }
     }
   };
 
@@ -595,13 +608,18 @@ __device__ void fwdbwd8_ws(const FwdArgs& a, int wg, float* lds) {
         for (int c = 0; c < CF; ++c) {
           __builtin_amdgcn_sched_barrier(0);  // one chunk's operands in flight at a time
           const int kc = kh * CF + c;
-          const int j = kc / DQ, qq = 4 * (kc % DQ) + g;
-          const f4 xa = ld4(X + 4 * ((j * QD + qq) * kTileRows + n16));
+          const int j = kc / DQ, col = 16 * (kc % DQ) + 4 * g;
+          // A operand: X[window n16][col + q], four columns of one window
+          float xa[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) xa[q] = X[(j * D + col + q) * XS + n16];
           if (j != C) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) zc = mfma16x4(xa[q], rr[c][q], zc);
           } else {
-            const f4 xt = ld4(X + 4 * ((WIN * QD + qq) * kTileRows + n16));
+            float xt[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) xt[q] = X[(WIN * D + col + q) * XS + n16];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               zctr = mfma16x4(xa[q], rr[c][q], zctr);
@@ -624,29 +642,31 @@ __device__ void fwdbwd8_ws(const FwdArgs& a, int wg, float* lds) {
       const float* V = vt + (q2 & 1) * Sh::kVt;
       const int row0 = (tile0 + q2) * kTileRows;
       if constexpr (!FWD) {
-        // ---- dW1 += V^T X for block nt, chunks kc = kh*CF + c.  A operand:
-        // lane (n16, g) holds V[4ii+g][nt*16 + n16]; B operand:
-        // X[4ii+g][16kc + n16].
+        // ---- dW1 += V^T X for block nt, chunks kc = kh*CF + c, over the
+        // windows in the order 4g + ii.  A operand: lane (n16, g) holds
+        // V[4g+ii][nt*16 + n16]; B operand: X[4g+ii][16kc + n16], the four
+        // of a lane from one 128-bit read.
         float vc[3][4];
 #pragma unroll
         for (int ty = 0; ty < 3; ++ty)
 #pragma unroll
           for (int ii = 0; ii < 4; ++ii)
-            vc[ty][ii] = V[(ty * kTileRows + 4 * ii + g) * (HP + 1) + nt * 16 + n16];
+            vc[ty][ii] = V[(ty * kTileRows + 4 * g + ii) * (HP + 1) + nt * 16 + n16];
 #pragma unroll
         for (int c = 0; c < CF; ++c) {
           __builtin_amdgcn_sched_barrier(0);
           const int kc = kh * CF + c;
-          const int j = kc / DQ, qq = 4 * (kc % DQ) + (n16 >> 2);
+          const int j = kc / DQ, col = 16 * (kc % DQ) + n16;
+          const f4 xb = ld4(X + (j * D + col) * XS + 4 * g);
+          if (j != C) {
 #pragma unroll
-          for (int ii = 0; ii < 4; ++ii) {
-            const float xb = X[4 * ((j * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
-            if (j != C) {
-              rr[c] = mfma16x4(vc[0][ii], xb, rr[c]);
-            } else {
-              const float xc = X[4 * ((WIN * QD + qq) * kTileRows + 4 * ii + g) + (n16 & 3)];
-              rr[c] = mfma16x4(vc[1][ii], xb, rr[c]);
-              rr[c] = mfma16x4(vc[2][ii], xc, rr[c]);
+            for (int ii = 0; ii < 4; ++ii) rr[c] = mfma16x4(vc[0][ii], xb[ii], rr[c]);
+          } else {
+            const f4 xc = ld4(X + (WIN * D + col) * XS + 4 * g);
+#pragma unroll
+            for (int ii = 0; ii < 4; ++ii) {
+              rr[c] = mfma16x4(vc[1][ii], xb[ii], rr[c]);
+              rr[c] = mfma16x4(vc[2][ii], xc[ii], rr[c]);
             }
           }
         }

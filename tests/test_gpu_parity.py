@@ -449,6 +449,21 @@ def test_pipelined_tiles_ragged(B):
     run_both(w, 2, B, 0)
 
 
+@pytest.mark.parametrize("B", [32653, 32773])
+def test_role_specialised_tiles_ragged(B):
+    """Eight or more tiles per workgroup take the role-specialised form
+    (staging, forward and dW1 waves pipelined one tile apart): 2041 tiles at
+    eight per workgroup leave the last workgroup one tile (the pipeline's
+    fill and drain with nothing between), 2049 tiles at ten per workgroup
+    leave it nine; the last tile holds 13 or 5 windows."""
+    ntiles = -(-B // 16)
+    per = -(-ntiles // 256)
+    per += per & 1
+    assert per >= 8 and ntiles % per in (1, 9) and B % 16 != 0
+    w = PRESETS["sweep_1024"].with_batch(B)
+    run_both(w, 2, B, 0)
+
+
 @pytest.mark.parametrize("mode", [0, 1])
 def test_full_size_batch_65536_one_step(mode):
     w = PRESETS["sweep_65536"]
