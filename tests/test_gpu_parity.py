@@ -438,12 +438,14 @@ def test_sweep_batches(B, steps):
 
 @pytest.mark.parametrize("B", [4100, 8215, 8231])
 def test_pipelined_tiles_ragged(B):
-    """More than 256 tiles, so workgroups take several tiles through the
-    pipelined loop, and the last workgroup fewer: 257 tiles at two per
-    workgroup (the last has one), 514 and 515 tiles at three per workgroup
-    (the last has one or two); the last tile holds 4, 7 or 7 windows."""
+    """More than 256 tiles, so workgroups take their tiles in pairs (an even
+    number per workgroup), and the last workgroup fewer: 257 tiles at two per
+    workgroup (the last has one: a pair whose second tile is past the batch),
+    514 and 515 tiles at four per workgroup (the last has two or three); the
+    last tile holds 4, 7 or 7 windows."""
     ntiles = -(-B // 16)
     per = -(-ntiles // 256)
+    per += per & 1
     assert per > 1 and ntiles % per != 0
     w = PRESETS["sweep_1024"].with_batch(B)
     run_both(w, 2, B, 0)
