@@ -130,7 +130,7 @@ __global__ __launch_bounds__(kBlock) void k_gen_apply(GenArgs<T> a, int n_e) {
   __shared__ float Lp[kWavesPerBlock][kMaxD];
   __shared__ int meta[kWavesPerBlock][5];
   if ((int)blockIdx.x < n_e) {
-    if (__builtin_amdgcn_readfirstlane(void_bits(a)) != 0u) return;
+    // (the error words are tested beside each chunk's keys)
     const int nranges = ceil_div(a.N, CH * kWavesPerBlock);
     for (int r = blockIdx.x; r < nranges; r += n_e)
       seg_apply_range<CH, kWavesPerBlock>(a, r, F, Lp, meta);
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(kPartApplyThreads) void k_gen_apply_part(GenArgs<T>
   __shared__ float F[kPartApplyWaves][kMaxD];
   __shared__ float Lp[kPartApplyWaves][kMaxD];
   __shared__ int meta[kPartApplyWaves][5];
-  if (__builtin_amdgcn_readfirstlane(void_bits(a)) != 0u) return;
+  // (the error words are tested beside each chunk's keys)
   const int p = blockIdx.x;
   seg_apply_partition<kPartApplyWaves>(a, a.part_off[p], a.part_off[p + 1], F, Lp, meta);
 }

@@ -132,16 +132,20 @@ __device__ __forceinline__ void seg_close(const SegArgs& a, size_t i, float v) {
 
 // One wave applies entries [i0, min(i0 + CH, end)) of the sorted list (see
 // the file comment).  A is SegArgs or another argument set with the same
-// fields and its own seg_load / seg_add.
+// fields and its own seg_load / seg_add.  Returns false, having written
+// nothing, when an earlier launch raised an error that voids the update (the
+// error words are loaded beside the chunk's keys, so the callers need no
+// round trip of their own to test them: every wave of the launch reads the
+// same value).
 template <int CH, class A>
-__device__ void seg_apply_rows(const A& a, int i0, int end, const ChunkSink& sink) {
+__device__ bool seg_apply_rows(const A& a, int i0, int end, const ChunkSink& sink) {
   static_assert(CH % 8 == 0 && CH <= kWave, "rows are walked in blocks of 8");
   const int lane = lane_id();
   // the error words (set by earlier launches) are read beside the chunk's
   // keys, and tested before any write
   const uint32_t flag = *a.flag | *a.flag2;
   const ChunkInfo ci = chunk_info(a.sk, a.sv, end, i0, CH);
-  if (__builtin_amdgcn_readfirstlane(flag) != 0u) return;  // a bad id voids the update
+  if (__builtin_amdgcn_readfirstlane(flag) != 0u) return false;  // a bad id voids the update
   const int nact = ci.nact;
   const uint64_t act = nact >= 64 ? ~0ull : ((1ull << nact) - 1ull);
   // piece ends: the lane before every later head, and the last active lane
@@ -219,6 +223,7 @@ __device__ void seg_apply_rows(const A& a, int i0, int end, const ChunkSink& sin
       if (starts_long) sink.last[col] = last_sum;
     }
   }
+  return true;
 }
 
 // Threads of a partition workgroup: 16 waves, so one round covers 1024
@@ -249,11 +254,12 @@ __device__ void seg_apply_partition(const A& a, int s, int e,
   for (int cb = 0; cb < CB; ++cb) open[cb] = 0.f;
   for (int r0 = 0; r0 < nch; r0 += NW) {
     const int c = r0 + w;
+    bool ok = true;  // (wave 0 always has a chunk: its own test covers the combine)
     if (c < nch)
-      seg_apply_rows<kPartApplyChunk>(a, s + c * kPartApplyChunk, e,
-                                      ChunkSink{F[w], Lp[w], meta[w]});
+      ok = seg_apply_rows<kPartApplyChunk>(a, s + c * kPartApplyChunk, e,
+                                           ChunkSink{F[w], Lp[w], meta[w]});
     __syncthreads();  // the round's open pieces are in LDS
-    if (w == 0) {
+    if (w == 0 && ok) {
       const int nc = min(NW, nch - r0);
       // every chunk's flags and keys at once (lane k reads chunk k), then
       // taken as wave-uniform values
@@ -318,10 +324,10 @@ __device__ void seg_apply_range(const A& a, int r, float (*F)[kMaxD], float (*Lp
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   const int s = r * NW * CH;
   const int nch = min(NW, (a.N - s + CH - 1) / CH);
-  if (w < nch)
-    seg_apply_rows<CH>(a, s + w * CH, a.N, ChunkSink{F[w], Lp[w], meta[w]});
+  bool ok = true;  // (wave 0 always has a chunk: its own test covers the combine)
+  if (w < nch) ok = seg_apply_rows<CH>(a, s + w * CH, a.N, ChunkSink{F[w], Lp[w], meta[w]});
   __syncthreads();  // the chunks' open pieces are in LDS
-  if (w == 0) {
+  if (w == 0 && ok) {
     int mk[5];
 #pragma unroll
     for (int x = 0; x < 5; ++x) mk[x] = lane < nch ? meta[lane][x] : 0;

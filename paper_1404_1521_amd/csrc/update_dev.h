@@ -102,9 +102,9 @@ __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
   const int n_dz = (int)gridDim.x - a.nx.n_wg - a.n_e;
   if (wg < a.n_e) {
     // all-or-nothing: an out-of-range id voids the update.  The error words
-    // were set (or not) by earlier launches: the workgroup leaves together
+    // were set (or not) by earlier launches, so every wave reads the same
+    // value (the sorted mode tests it beside each chunk's keys)
     if (a.mode == 0) {
-      if (__builtin_amdgcn_readfirstlane(void_bits(a.s)) != 0u) return;
       const int nranges = ceil_div(a.s.N, CH * kWavesPerBlock);
       for (int r = wg; r < nranges; r += a.n_e)
         seg_apply_range<CH, kWavesPerBlock>(a.s, r, F, Lp, meta);
@@ -130,9 +130,7 @@ __global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
   __shared__ int meta[kPartApplyWaves][5];
   const int t = threadIdx.x;
   if ((int)blockIdx.x < a.n_part) {
-    // the error words were set (or not) by earlier launches: every wave
-    // reads the same value, so the whole workgroup leaves together
-    if (__builtin_amdgcn_readfirstlane(void_bits(a.s)) != 0u) return;
+    // (the error words are tested beside each chunk's keys)
     const int p = blockIdx.x;
     seg_apply_partition<kPartApplyWaves>(a.s, a.part_off[p], a.part_off[p + 1], F, Lp, meta);
     return;
