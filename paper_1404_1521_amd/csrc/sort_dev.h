@@ -327,16 +327,27 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
 
   // The words (key bits above the partition bits, then the entry id) are
   // distinct, so a word's place in the sorted partition is the number of
-  // smaller words: up to kRankSortMax words are ranked by one pass of
-  // broadcast LDS reads, one thread per word (the same order as the stable
-  // radix passes, which larger partitions take).
+  // smaller words: up to kRankSortMax words are ranked by broadcast LDS
+  // reads (the same order as the stable radix passes, which larger
+  // partitions take).  Word i is counted by G threads, thread group g
+  // scanning its own share of the words, so the pass over a partition of
+  // M words costs about M / G compares per thread; the G counts meet in LDS.
   uint32_t* res;
   if (M <= kRankSortMax && M <= NTH) {
-    if (t < M) {
-      const uint32_t wv = bufA[t];
+    int S = 16;  // words padded to a power of two: thread t counts for word t % S
+    while (S < M) S <<= 1;
+    const int G = min(NTH / S, 16);
+    const int i = t & (S - 1), g = t / S;
+    uint32_t* cnt = reinterpret_cast<uint32_t*>(rank16);  // [G][S] partial counts
+    uint32_t wv = 0u;
+    if (g < G && i < M) {
+      wv = bufA[i];
+      // this group's share [lo, hi): whole 4-word steps except the last share
+      const int lo = ((g * M) / G) & ~3;
+      const int hi = g == G - 1 ? M : (((g + 1) * M) / G) & ~3;
       uint32_t r = 0u;
-      int j = 0;
-      for (; j + 16 <= M; j += 16) {  // four reads in flight per step
+      int j = lo;
+      for (; j + 16 <= hi; j += 16) {  // four reads in flight per step
         uint4 q[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) q[u] = *reinterpret_cast<const uint4*>(bufA + j + 4 * u);
@@ -345,12 +356,18 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
           r += (q[u].x < wv ? 1u : 0u) + (q[u].y < wv ? 1u : 0u) + (q[u].z < wv ? 1u : 0u) +
                (q[u].w < wv ? 1u : 0u);
       }
-      for (; j + 4 <= M; j += 4) {
+      for (; j + 4 <= hi; j += 4) {
         const uint4 q = *reinterpret_cast<const uint4*>(bufA + j);
         r += (q.x < wv ? 1u : 0u) + (q.y < wv ? 1u : 0u) + (q.z < wv ? 1u : 0u) +
              (q.w < wv ? 1u : 0u);
       }
-      for (; j < M; ++j) r += bufA[j] < wv ? 1u : 0u;
+      for (; j < hi; ++j) r += bufA[j] < wv ? 1u : 0u;
+      cnt[g * S + i] = r;
+    }
+    __syncthreads();
+    if (g == 0 && i < M) {
+      uint32_t r = 0u;
+      for (int gg = 0; gg < G; ++gg) r += cnt[gg * S + i];
       bufB[r] = wv;
     }
     __syncthreads();
