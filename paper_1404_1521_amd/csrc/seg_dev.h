@@ -49,6 +49,7 @@ struct SegArgs {
   float alpha;
   // completed pieces are added as they close (float atomics), not deferred
   static constexpr bool kDeferred = false;
+  struct Pre {};
 };
 
 // Piece structure of one chunk, computed by the whole wave (lanes < ch).
@@ -180,6 +181,10 @@ __device__ bool seg_apply_rows(const A& a, int i0, int end, const ChunkSink& sin
       const int ent = __builtin_amdgcn_readlane(ci.ent, r);
       v[r] = seg_load(a, (size_t)ent * a.d + colc);
     }
+    // (argument sets whose row update is a load and a store: the first
+    // block of old rows in flight beside the entries' rows)
+    typename A::Pre pre;
+    if constexpr (A::kDeferred) seg_prefetch_rows<CH>(a, ci, complete, colc, pre);
     // running sum in entry order, closed at every piece end (tail);
     // completed pieces go straight to their rows, or (argument sets whose
     // row update is a load and a store) replace their tail row's value and
@@ -217,7 +222,7 @@ __device__ bool seg_apply_rows(const A& a, int i0, int end, const ChunkSink& sin
         }
       }
     }
-    if constexpr (A::kDeferred) seg_add_rows<CH>(a, ci, complete, v, colc, cok);
+    if constexpr (A::kDeferred) seg_add_rows<CH>(a, ci, complete, v, colc, cok, pre);
     if (cok) {
       if (ci.cont_first) sink.first[col] = first_sum;
       if (starts_long) sink.last[col] = last_sum;
