@@ -180,7 +180,7 @@ __global__ __launch_bounds__(kPartApplyThreads) void k_gen_apply_part(GenArgs<T>
   seg_apply_partition<kPartApplyWaves>(a, a.part_off[p], a.part_off[p + 1], F, Lp, meta);
 }
 
-// Row access of the fix-up (seg_fix_row_wave / seg_fix_row, launched as
+// Row access of the fix-up (seg_fix_slot_wave / seg_fix_row, launched as
 // k_segfix<GenArgs<T>>): four consecutive columns at element i, n of them
 // inside the row, converted to and from float.  The fix-up is the row's only
 // writer.
@@ -197,6 +197,10 @@ __device__ __forceinline__ void seg_put4(const GenArgs<T>& a, size_t i, int n, f
 #pragma unroll
   for (int k = 0; k < 4; ++k)
     if (k < n) a.table[i + k] = Elem<T>::put(v[k]);
+}
+template <class T>
+__device__ __forceinline__ void seg_add4(const GenArgs<T>& a, size_t i, int n, f4 v) {
+  seg_put4(a, i, n, seg_row4(a, i, n) + v);
 }
 
 // Assignment: one wave per 64 sorted entries; an entry whose successor has

@@ -39,7 +39,8 @@ struct SegArgs {
   const int32_t* sv;        // entry ids in sorted order [N]
   float* seg_part;          // [chunks][2][seg_stride]
   int2* long_list;          // [ranges] by range: (range, row) if a segment that crosses
-                            // ranges starts in it, else (-1, 0); every range writes its slot
+                            // ranges starts in it, (-2, 0) if one segment runs through the
+                            // whole range, else (-1, 0); every range writes its slot
   int32_t* seg_end;         // [rows]: end range of a crossing segment, by key
   const uint32_t* flag;     // sticky error bits: nonzero voids the update
   const uint32_t* flag2;    // the error word of this list's sort (a training step's sort
@@ -387,7 +388,8 @@ __device__ void seg_apply_range(const A& a, int r, float (*F)[kMaxD], float (*Lp
     }
     if (lane == 0) {
       const bool starts_long = olL && !front_open;
-      a.long_list[r] = starts_long ? make_int2(r, okey) : make_int2(-1, 0);
+      const bool middle = cf0 && olL && front_open;  // one segment runs through the range
+      a.long_list[r] = starts_long ? make_int2(r, okey) : make_int2(middle ? -2 : -1, 0);
       if (cf0 && !(olL && front_open)) a.seg_end[key0] = r;
     }
   }
@@ -411,36 +413,70 @@ __device__ __forceinline__ f4 seg_row4(const SegArgs& a, size_t i, int n) {
 __device__ __forceinline__ void seg_put4(const SegArgs& a, size_t i, int n, f4 v) {
   if (n > 0) st4(a.table + i, v);
 }
+// A crossing segment's sum v (alpha applied) added to the row by its only
+// writer: float adds at the L2 (no read round trip; the same rounding as the
+// row's load, add and store).
+__device__ __forceinline__ void seg_add4(const SegArgs& a, size_t i, int n, f4 v) {
+  if (n > 0) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) unsafeAtomicAdd(a.table + i + k, v[k]);
+  }
+}
 
-// One wave finishes crossing segment (cs, key) when it has at most
-// kSegfixLight partials, m = seg_end[key] - cs + 1, and returns m; a heavier
-// segment is left alone (the caller hands it to the whole workgroup).  The
-// kSegfixLight candidate partials (chunks below nchunks) and the row are read
-// together with seg_end, then masked by m, so the segment costs one round of
-// loads after its slot.  Lane group gq = lane/16 sums partials gq, gq+4, ...
-// in order (each lane four consecutive columns), and the four group sums are
-// combined by a fixed butterfly.  Partial rows are read four columns at a
+// One wave takes range slot li of nchunks (ranges).  Lane k reads slot li + k
+// (k < kSegfixLight) and lane group gq = lane/16 the candidate partials gq,
+// gq+4, ... of a segment starting at li, all in one round of loads together
+// with the error words; the slots after li say where such a segment ends (a
+// run of middle ranges, then its end range), so m, its number of partials,
+// needs no second round.  A segment of at most kSegfixLight partials is
+// finished here: each lane sums four consecutive columns of its group's
+// partials in order, the four group sums meet by a fixed butterfly, and the
+// row takes the sum (seg_add4: float32 adds at the L2, else a load and a
+// store).  Returns 0 (no segment starts at li, or the update is void), m, or
+// kSegfixLight + 1 for a heavier segment, which the caller hands to the
+// whole workgroup with *key_out set.  Partial rows are read four columns at a
 // time up to the next multiple of 4 (inside the partial slot's stride); the
 // row access masks the columns past d.
 template <class A>
-__device__ int seg_fix_row_wave(const A& a, int cs, int32_t key, int nchunks) {
+__device__ int seg_fix_slot_wave(const A& a, int li, int nchunks, int32_t* key_out) {
   const int lane = lane_id(), q = lane & 15, gq = lane >> 4;
-  const int ce = a.seg_end[key];
+  const int2 rec = (lane < kSegfixLight && li + lane < nchunks) ? a.long_list[li + lane]
+                                                                 : make_int2(-1, 0);
+  const uint32_t flag = *a.flag | *a.flag2;
+  f4 x[kSegfixLight / 4];
+  {
+    const int col = 4 * q;
+    const bool cok = col < a.d;
+#pragma unroll
+    for (int u = 0; u < kSegfixLight / 4; ++u) {
+      const int i = 4 * u + gq;
+      const size_t slot = i == 0 ? (size_t)li * 2 + 1 : (size_t)(li + i) * 2;
+      x[u] = (li + i < nchunks && cok) ? ld4(a.seg_part + slot * a.seg_stride + col) : kZero4;
+    }
+  }
+  const int cs = __builtin_amdgcn_readlane(rec.x, 0);
+  if (cs < 0 || __builtin_amdgcn_readfirstlane(flag) != 0u) return 0;
+  const int32_t key = __builtin_amdgcn_readlane(rec.y, 0);
+  // the end range: the first slot after li that is not a middle range
+  const uint64_t ends = __ballot(lane >= 1 && lane < kSegfixLight && rec.x != -2);
+  if (ends == 0ull) {
+    *key_out = key;
+    return kSegfixLight + 1;
+  }
+  const int m = __ffsll((unsigned long long)ends);  // end slot j = m - 1
   for (int c0 = 0; c0 < a.d; c0 += 64) {
     const int col = c0 + 4 * q;
     const bool cok = col < a.d;
     const size_t tr = (size_t)key * a.d + col;
     const int nrow = (gq == 0 && cok) ? min(4, a.d - col) : 0;
-    const f4 row = seg_row4(a, tr, nrow);
-    f4 x[kSegfixLight / 4];
+    if (c0 > 0) {
 #pragma unroll
-    for (int u = 0; u < kSegfixLight / 4; ++u) {
-      const int i = 4 * u + gq;
-      const size_t slot = i == 0 ? (size_t)cs * 2 + 1 : (size_t)(cs + i) * 2;
-      x[u] = (cs + i < nchunks && cok) ? ld4(a.seg_part + slot * a.seg_stride + col) : kZero4;
+      for (int u = 0; u < kSegfixLight / 4; ++u) {
+        const int i = 4 * u + gq;
+        const size_t slot = i == 0 ? (size_t)cs * 2 + 1 : (size_t)(cs + i) * 2;
+        x[u] = (i < m && cok) ? ld4(a.seg_part + slot * a.seg_stride + col) : kZero4;
+      }
     }
-    const int m = __builtin_amdgcn_readfirstlane(ce) - cs + 1;
-    if (m > kSegfixLight) return m;
     f4 acc = kZero4;
 #pragma unroll
     for (int u = 0; u < kSegfixLight / 4; ++u)
@@ -450,9 +486,9 @@ __device__ int seg_fix_row_wave(const A& a, int cs, int32_t key, int nchunks) {
       acc[k] += __shfl_xor(acc[k], 16);
       acc[k] += __shfl_xor(acc[k], 32);
     }
-    seg_put4(a, tr, nrow, row + a.alpha * acc);
+    seg_add4(a, tr, nrow, a.alpha * acc);
   }
-  return __builtin_amdgcn_readfirstlane(ce) - cs + 1;
+  return m;
 }
 
 // The whole workgroup adds the m partials of crossing segment (cs, key) and
@@ -474,7 +510,10 @@ __device__ void seg_fix_row(const A& a, int cs, int32_t key, int m,
     const size_t tr = (size_t)key * a.d + col;
     const bool owner = w == 0 && gq == 0 && cok;
     const int nrow = owner ? min(4, a.d - col) : 0;
-    const f4 row = seg_row4(a, tr, nrow);  // in flight beside the partials
+    // a table whose row update is a load and a store: the row in flight
+    // beside the partials (float32 rows take the sum at the L2 instead)
+    f4 row = kZero4;
+    if constexpr (A::kDeferred) row = seg_row4(a, tr, nrow);
     f4 acc = kZero4;
     for (int base = 0; base < m; base += G * kSegfixUnroll) {
       f4 x[kSegfixUnroll];
@@ -499,7 +538,8 @@ __device__ void seg_fix_row(const A& a, int cs, int32_t key, int m,
       f4 s = ld4(red + 4 * q);
 #pragma unroll
       for (int v = 1; v < kSegfixWaves; ++v) s += ld4(red + v * kMaxD + 4 * q);
-      seg_put4(a, tr, nrow, row + a.alpha * s);
+      if constexpr (A::kDeferred) seg_put4(a, tr, nrow, row + a.alpha * s);
+      else seg_add4(a, tr, nrow, a.alpha * s);
     }
   }
 }

@@ -154,7 +154,7 @@ template <class A>
 __device__ void segfix_wg(const A& a, int wg, int nwg, float* red, int (*heavy)[3],
                           int* nheavy_p) {
   int& nheavy = *nheavy_p;
-  if (void_bits(a)) return;
+  // (the error words are tested beside each slot's loads)
   const uint32_t cnt = (uint32_t)((a.N + a.rg - 1) / a.rg);  // ranges of the apply
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -165,15 +165,13 @@ __device__ void segfix_wg(const A& a, int wg, int nwg, float* red, int (*heavy)[
     __syncthreads();
     const uint32_t li = base + (uint32_t)w * nwg + wg;
     if (li < cnt) {
-      const int2 rec = a.long_list[li];
-      if (rec.x >= 0) {
-        const int m = seg_fix_row_wave(a, rec.x, rec.y, (int)cnt);  // partials of the segment
-        if (m > kSegfixLight && lane == 0) {
-          const int h = atomicAdd(&nheavy, 1);
-          heavy[h][0] = rec.x;
-          heavy[h][1] = rec.y;
-          heavy[h][2] = m;
-        }
+      int32_t key = 0;
+      const int m = seg_fix_slot_wave(a, (int)li, (int)cnt, &key);
+      if (m > kSegfixLight && lane == 0) {  // a heavy row: its partials run to seg_end[key]
+        const int h = atomicAdd(&nheavy, 1);
+        heavy[h][0] = (int)li;
+        heavy[h][1] = key;
+        heavy[h][2] = a.seg_end[key] - (int)li + 1;
       }
     }
     __syncthreads();
