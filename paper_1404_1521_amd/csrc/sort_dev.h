@@ -243,6 +243,7 @@ constexpr int kPartBits = 7;
 // words (quadratic in the partition: measured faster than the two LDS radix
 // passes up to about 540 entries, slower at 720).
 constexpr int kRankSortMax = 512;
+constexpr int kRankSplitMin = 128;  // partitions above this place their smallest key first
 constexpr int kPartSortThreads = 1024;  // one workgroup of 16 waves per partition
 constexpr int kPartSortMisc = 32;       // scan scratch: wave sums, then the partition total
 __host__ __device__ constexpr size_t part_sort_lds_words(int nth) {
@@ -332,41 +333,73 @@ __device__ void part_sort(const KeyFn& kf, int N, const SortPlan& plan, int part
   // partitions take).  Word i is counted by G threads, thread group g
   // scanning its own share of the words, so the pass over a partition of
   // M words costs about M / G compares per thread; the G counts meet in LDS.
+  // In a frequency-ranked vocabulary the smallest key of a partition (key
+  // bits above the partition bits all zero) is by far its most frequent: in
+  // a partition of more than kRankSplitMin words those words, already in
+  // entry order in bufA, take the first places by a prefix count, and only
+  // the others are ranked by comparison.
   uint32_t* res;
   if (M <= kRankSortMax && M <= NTH) {
+    uint32_t* cnt = reinterpret_cast<uint32_t*>(rank16);  // [G][S] partial counts
+    uint32_t* rest = cnt + NTH;                           // the other words, compacted
+    const uint32_t* src = bufA;
+    int Mr = M, Z = 0;
+    if (M > kRankSplitMin) {
+      const int lane = t & (kWave - 1), w = t / kWave;
+      const uint32_t wv0 = t < M ? bufA[t] : 0u;
+      const bool z = t < M && (wv0 >> vb) == 0u;
+      const uint64_t zm = __ballot(z);
+      if (lane == 0) misc[w] = (uint32_t)__popcll(zm);
+      __syncthreads();
+      uint32_t zb = 0u, zt = 0u;
+#pragma unroll
+      for (int k = 0; k < NW; ++k) {
+        const uint32_t c = misc[k];
+        zb += k < w ? c : 0u;
+        zt += c;
+      }
+      zb += (uint32_t)__popcll(zm & lanemask_lt());  // zero-key words before word t
+      if (t < M) {
+        if (z) bufB[zb] = wv0;
+        else rest[t - zb] = wv0;
+      }
+      __syncthreads();
+      Z = (int)zt;
+      Mr = M - Z;
+      src = rest;
+    }
     int S = 16;  // words padded to a power of two: thread t counts for word t % S
-    while (S < M) S <<= 1;
+    while (S < Mr) S <<= 1;
     const int G = min(NTH / S, 16);
     const int i = t & (S - 1), g = t / S;
-    uint32_t* cnt = reinterpret_cast<uint32_t*>(rank16);  // [G][S] partial counts
     uint32_t wv = 0u;
-    if (g < G && i < M) {
-      wv = bufA[i];
+    if (g < G && i < Mr) {
+      wv = src[i];
       // this group's share [lo, hi): whole 4-word steps except the last share
-      const int lo = ((g * M) / G) & ~3;
-      const int hi = g == G - 1 ? M : (((g + 1) * M) / G) & ~3;
+      const int lo = ((g * Mr) / G) & ~3;
+      const int hi = g == G - 1 ? Mr : (((g + 1) * Mr) / G) & ~3;
       uint32_t r = 0u;
       int j = lo;
       for (; j + 16 <= hi; j += 16) {  // four reads in flight per step
         uint4 q[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) q[u] = *reinterpret_cast<const uint4*>(bufA + j + 4 * u);
+        for (int u = 0; u < 4; ++u) q[u] = *reinterpret_cast<const uint4*>(src + j + 4 * u);
 #pragma unroll
         for (int u = 0; u < 4; ++u)
           r += (q[u].x < wv ? 1u : 0u) + (q[u].y < wv ? 1u : 0u) + (q[u].z < wv ? 1u : 0u) +
                (q[u].w < wv ? 1u : 0u);
       }
       for (; j + 4 <= hi; j += 4) {
-        const uint4 q = *reinterpret_cast<const uint4*>(bufA + j);
+        const uint4 q = *reinterpret_cast<const uint4*>(src + j);
         r += (q.x < wv ? 1u : 0u) + (q.y < wv ? 1u : 0u) + (q.z < wv ? 1u : 0u) +
              (q.w < wv ? 1u : 0u);
       }
-      for (; j < hi; ++j) r += bufA[j] < wv ? 1u : 0u;
+      for (; j < hi; ++j) r += src[j] < wv ? 1u : 0u;
       cnt[g * S + i] = r;
     }
     __syncthreads();
-    if (g == 0 && i < M) {
-      uint32_t r = 0u;
+    if (g == 0 && i < Mr) {
+      uint32_t r = (uint32_t)Z;
       for (int gg = 0; gg < G; ++gg) r += cnt[gg * S + i];
       bufB[r] = wv;
     }
