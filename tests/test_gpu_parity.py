@@ -275,6 +275,63 @@ def test_scatter_add_partition_sizes_exact(M):
         assert np.array_equal(host(td), ref.astype(np.float32)), mode
 
 
+@pytest.mark.parametrize("M", [129, 300, 512])
+@pytest.mark.parametrize("case", ["absent", "only", "mixed"])
+def test_scatter_add_smallest_key_placement(M, case):
+    """A partition of more than 128 entries places the entries of its
+    smallest key (id 0 in partition 0) first by a prefix count and ranks only
+    the others: partition 0 here holds M entries with none of id 0, only id 0,
+    or id 0 among seven other multiples of 128, in shuffled entry order.
+    Integer Y and a zero table make every summation order exact, so the
+    result must equal the oracle's exactly."""
+    rng = np.random.default_rng(3000 + M + 7 * len(case))
+    rows, N, d = 1024, 6000, 24
+    mult = np.arange(0, rows, 128, dtype=np.int32)
+    pool = {"absent": mult[1:], "only": mult[:1], "mixed": mult}[case]
+    hot = rng.choice(pool, M)
+    if case == "mixed":
+        hot[: M // 3] = 0
+    other = rng.integers(0, rows, 4 * N).astype(np.int32)
+    other = other[other % 128 != 0][: N - M]
+    idx = rng.permutation(np.concatenate([hot, other])).astype(np.int32)
+    assert idx.size == N and np.count_nonzero(idx % 128 == 0) == M
+    Y = rng.integers(-8, 9, (N, d)).astype(np.float32)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    t0 = np.zeros((rows, d), np.float32)
+    ref = t0.astype(np.float64)
+    oracle.scatter_add(ref, idx, Y.astype(np.float64), 0.5)
+    td = dev(t0)
+    ctx.scatter_add(td, dev(idx), dev(Y), 0.5, pg().SCATTER_SORTED)
+    assert ctx.status() == pg().OK
+    assert np.array_equal(host(td), ref.astype(np.float32))
+
+
+@pytest.mark.parametrize("L", [64 * 15 + 1, 64 * 16, 64 * 16 + 1, 64 * 17 + 5])
+@pytest.mark.parametrize("lead", [0, 10])
+def test_scatter_add_segment_spans_fixup(L, lead):
+    """A 20,000-entry list (16-entry chunks, ranges of 64 entries): row 7
+    holds L entries that start at sorted position `lead` (after `lead`
+    entries of row 3; no other id below 100), so its segment runs through a
+    known number of ranges: up to 16 partials are finished by one fix-up
+    wave, which finds the segment's end from the ranges marked as run
+    through; more go to the whole workgroup.  Exact integer sums."""
+    rng = np.random.default_rng(5000 + L + lead)
+    rows, N, d = 4096, 20000, 24
+    head = np.concatenate([np.full(lead, 3, np.int32), np.full(L, 7, np.int32)])
+    other = rng.integers(100, rows, N - head.size).astype(np.int32)
+    idx = rng.permutation(np.concatenate([head, other])).astype(np.int32)
+    Y = rng.integers(-8, 9, (N, d)).astype(np.float32)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    t0 = np.zeros((rows, d), np.float32)
+    ref = t0.astype(np.float64)
+    oracle.scatter_add(ref, idx, Y.astype(np.float64), 0.25)
+    for mode in (pg().SCATTER_SORTED, pg().SCATTER_ATOMIC):
+        td = dev(t0)
+        ctx.scatter_add(td, dev(idx), dev(Y), 0.25, mode)
+        assert ctx.status() == pg().OK
+        assert np.array_equal(host(td), ref.astype(np.float32)), mode
+
+
 def test_small_vocabulary_step_partition_rounds():
     """A 64-word vocabulary at B = 1365 (8190 entries, the largest list the
     partitioned sort takes): each partition holds one word, the most frequent
