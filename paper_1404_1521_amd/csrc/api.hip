@@ -292,7 +292,8 @@ NextSort next_sort(polyglot_ctx* ctx, const int32_t* windows, const int32_t* cor
 // one step, on the main stream; sorted mode reads sort set `set`.
 int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,
                     const int32_t* windows, const int32_t* corrupt, int B, float lr,
-                    float* loss_dev, int set, hipEvent_t sorted_ev, const NextSort& nx) {
+                    float* loss_dev, int set, hipEvent_t sorted_ev, const NextSort& nx,
+                    const int32_t* next_windows, const int32_t* next_corrupt) {
   const polyglot_config& cf = ctx->cfg;
   const int N = B * (cf.win + 1);
   const bool sorted = cf.scatter_mode == POLYGLOT_SCATTER_SORTED;
@@ -397,6 +398,13 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
 
   ApplyArgs aa{};
   aa.s = seg_args(ctx, E, ctx->ws.G, plan, set, N, cf.d, -lr, true);
+  if (next_windows) {  // warm the memory-side cache with the next step's ids
+    aa.pf.p[0] = next_windows;
+    aa.pf.n[0] = B * cf.win;
+    aa.pf.p[1] = next_corrupt;
+    aa.pf.n[1] = B;
+    aa.pf.sink = ctx->ws.pf_sink;
+  }
   aa.mode = sorted ? 0 : 1;
   aa.n_e = table_workgroups(aa.s, aa.mode);
   aa.n_d = ceil_div(ctx->part_stride * kDenseSlices, kBlock);
@@ -507,10 +515,13 @@ int enqueue_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, 
         (fold && s + 1 < S)
             ? next_sort(ctx, windows + (s + 1) * wstride, corrupt + (size_t)(s + 1) * B, B, 1 - q)
             : NextSort{};
+    const bool more = s + 1 < S;
     const int r = enqueue_compute(ctx, E, W1, b1, w2, b2, windows + s * wstride,
                                   corrupt + (size_t)s * B, B, lr,
                                   losses_dev ? losses_dev + s : nullptr, q,
-                                  side_sort ? ctx->ev_sorted[q] : nullptr, nx);
+                                  side_sort ? ctx->ev_sorted[q] : nullptr, nx,
+                                  more ? windows + (s + 1) * wstride : nullptr,
+                                  more ? corrupt + (size_t)(s + 1) * B : nullptr);
     if (r) return r;
     if (side_sort) {
       e = hipEventRecord(ctx->ev_done[q], ctx->stream);
@@ -622,6 +633,7 @@ int polyglot_init(const polyglot_config* cfg, void* stream, polyglot_ctx** out) 
   if (e == hipSuccess) e = alloc(ctx, &ws.idx32, (size_t)c.max_scatter);
   if (e == hipSuccess) e = alloc(ctx, &ws.flag, 3);
   if (e == hipSuccess) e = alloc(ctx, &ws.scratch_loss, 1);
+  if (e == hipSuccess) e = alloc(ctx, &ws.pf_sink, 1);
   for (int k = 0; k < 2; ++k) {
     if (e == hipSuccess)
       e = hipMemset(ws.totals[k], 0, sizeof(uint32_t) * kMaxPasses * kMaxBins);

@@ -79,6 +79,7 @@ struct Workspace {
                             // training step's side-stream sort, word 1 + q by the side-stream
                             // sort of sort set q (read only by that set's update)
   float* scratch_loss;      // loss slot used when the caller passes no loss pointer
+  uint32_t* pf_sink;        // [1] written only by an unlikely prefetch sum (see Prefetch)
   int32_t* idx32;           // [max_scatter] int64 indices narrowed to int32 keys
 };
 

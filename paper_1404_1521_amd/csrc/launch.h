@@ -119,6 +119,17 @@ struct NextSort {
 // One launch with roles: workgroups [0, n_e) update the table (sorted
 // segments or atomics); the next ones run the dense SGD (if n_d > 0) and
 // clear the sort counters; the last nx.n_wg rank the next step's sort tiles.
+// The next step's ids in a multi-step call (or null): the dense workgroups
+// of this step's update read one word per 64-byte line of them, so that the
+// next fused kernel's first dependent loads find them in the memory-side
+// cache shared by every XCD.  The values are not used (sink: a word written
+// only if their sum takes one particular value, which keeps the loads).
+struct Prefetch {
+  const int32_t* p[2];
+  int n[2];
+  uint32_t* sink;
+};
+
 struct ApplyArgs {
   SegArgs s;
   int mode;  // 0 sorted segments, 1 atomic
@@ -129,6 +140,7 @@ struct ApplyArgs {
   DenseArgs dn;
   ZeroRanges zero;
   NextSort nx;
+  Prefetch pf;
 };
 
 struct ScoreArgs {
