@@ -20,9 +20,9 @@
 // heavy Zipf row) leaves one partial per spanned range (slot 1: the open
 // last piece of the range where it starts; slot 0: the first piece of every
 // later spanned range); the range where it starts records it in its own slot
-// of the segment list (no shared counter) and its end range is recorded by
-// key; the fix-up launch adds the partials in a fixed order and applies the
-// row.  After a partitioned sort, where no key spans two partitions, one
+// of the segment list (no shared counter), every range it runs through marks
+// its slot, and its end range is recorded by key; the fix-up launch adds the
+// partials in a fixed order and applies the row.  After a partitioned sort, where no key spans two partitions, one
 // workgroup per partition completes every segment itself
 // (seg_apply_partition).
 // Sums never depend on scheduling, no row is written twice and no wave
@@ -423,7 +423,8 @@ __device__ __forceinline__ void seg_add4(const SegArgs& a, size_t i, int n, f4 v
   }
 }
 
-// One wave takes range slot li of nchunks (ranges).  Lane k reads slot li + k
+// One wave takes range slot li of nchunks, the number of ranges (the
+// partial slots).  Lane k reads slot li + k
 // (k < kSegfixLight) and lane group gq = lane/16 the candidate partials gq,
 // gq+4, ... of a segment starting at li, all in one round of loads together
 // with the error words; the slots after li say where such a segment ends (a
