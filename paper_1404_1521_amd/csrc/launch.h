@@ -248,6 +248,6 @@ __host__ __device__ inline size_t fwdbwd_lds_floats(int Hp, int K) {
 }
 
 // Launch-shape constants shared with the host.
-constexpr int kDenseSlices = 8;  // lanes that share one element of the dense reduction
+constexpr int kDenseSlices = 8;  // slot groups of the dense reduction
 
 }  // namespace pg

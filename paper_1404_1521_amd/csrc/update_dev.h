@@ -43,54 +43,70 @@ __device__ __forceinline__ void zero_ranges(const ZeroRanges& z, size_t gid, siz
     for (size_t i = gid; i < z.n[r]; i += nthreads) z.p[r][i] = 0u;
 }
 
-// Dense SGD: kDenseSlices adjacent lanes share an element; lane s sums the
-// partial slots s, s+8, ... in order, then a fixed butterfly adds the eight
-// sums, so the reduction is deterministic.  Elements: dW1 [Hp][K] from the
-// dW1 partials, then db1 [Hp], dw2 [Hp], loss, db2 from the vector partials.
-__device__ void dense_sgd(const DenseArgs& a, int gid, int nthreads, bool bad) {
+// Dense SGD.  A workgroup of T threads takes T / 8 consecutive elements at a
+// time; its threads form kDenseSlices = 8 slot groups, group g summing the
+// partial slots g, g + 8, g + 16, ... in order, with adjacent threads on
+// adjacent elements of one slot (whole cache lines per load).  The eight
+// group sums meet in LDS in the fixed tree ((0 + 1) + (2 + 3)) + ((4 + 5) +
+// (6 + 7)), so the reduction is deterministic.  Elements: dW1 [Hp][K] from
+// the dW1 partials, then db1 [Hp], dw2 [Hp], loss, db2 from the vector
+// partials.  wg of nwg: this workgroup among the dense ones; red: T floats of
+// LDS.  Every thread of the workgroup takes part (it synchronises).
+template <int T>
+__device__ void dense_sgd(const DenseArgs& a, int wg, int nwg, bool bad, float* red) {
+  constexpr int SL = kDenseSlices;
+  constexpr int EW = T / SL;
+  static_assert(SL == 8 && T % SL == 0, "the combining tree adds eight group sums");
   const int HK = a.Hp * a.K;
   const int nel = HK + 2 * a.Hp + 2;
-  constexpr int SL = kDenseSlices;
-  const int sl = gid % SL;
-  for (int e0 = gid / SL; e0 < nel; e0 += nthreads / SL) {
-    const bool mat = e0 < HK;
-    const float* src = mat ? a.part + e0 : a.vpart + (e0 - HK);
-    int np = mat ? a.n_parts : a.n_vparts;
-    size_t stride = mat ? (size_t)a.part_stride : (size_t)a.vstride;
-    if (mat && a.split == 2) {  // the slot of the pair that holds this element's tile
-      const int n = e0 / a.K, k = e0 - n * a.K;
-      src += (size_t)((((k >> 4) * (a.Hp >> 4)) + (n >> 4)) & 1) * a.part_stride;
-      np >>= 1;
-      stride *= 2;
-    }
+  const int t = threadIdx.x;
+  const int g = t / EW, j = t - g * EW;
+  for (int base = wg * EW; base < nel; base += nwg * EW) {
+    const int e = base + j;
     float s = 0.f;
-    for (int p0 = sl; p0 < np; p0 += 8 * SL) {
-      float v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int p = p0 + u * SL;
-        v[u] = p < np ? src[(size_t)p * stride] : 0.f;
+    if (e < nel) {
+      const bool mat = e < HK;
+      const float* src = mat ? a.part + e : a.vpart + (e - HK);
+      int np = mat ? a.n_parts : a.n_vparts;
+      size_t stride = mat ? (size_t)a.part_stride : (size_t)a.vstride;
+      if (mat && a.split == 2) {  // the slot of the pair that holds this element's tile
+        const int n = e / a.K, k = e - n * a.K;
+        src += (size_t)((((k >> 4) * (a.Hp >> 4)) + (n >> 4)) & 1) * a.part_stride;
+        np >>= 1;
+        stride *= 2;
       }
+      for (int p0 = g; p0 < np; p0 += 8 * SL) {
+        float v[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) s += v[u];
-    }
+        for (int u = 0; u < 8; ++u) {
+          const int p = p0 + u * SL;
+          v[u] = p < np ? src[(size_t)p * stride] : 0.f;
+        }
 #pragma unroll
-    for (int o = 1; o < SL; o <<= 1) s += __shfl_xor(s, o);
-    if (sl != 0) continue;
-    const int e = e0;
-    if (e < HK) {
-      if (!bad && e / a.K < a.H) a.W1[e] = a.W1[e] - a.lr * s;
-    } else if (e < HK + a.Hp) {
-      const int n = e - HK;
-      if (!bad && n < a.H) a.b1[n] = a.b1[n] - a.lr * s;
-    } else if (e < HK + 2 * a.Hp) {
-      const int n = e - HK - a.Hp;
-      if (!bad && n < a.H) a.w2[n] = a.w2[n] - a.lr * s;
-    } else if (e == HK + 2 * a.Hp) {
-      a.loss_out[0] = bad ? __builtin_nanf("") : s * a.invB;
-    } else {
-      if (!bad) a.b2[0] = a.b2[0] - a.lr * s;
+        for (int u = 0; u < 8; ++u) s += v[u];
+      }
     }
+    red[t] = s;
+    __syncthreads();
+    if (g == 0 && e < nel) {
+      const float* r = red + j;
+      s = ((r[0] + r[EW]) + (r[2 * EW] + r[3 * EW])) +
+          ((r[4 * EW] + r[5 * EW]) + (r[6 * EW] + r[7 * EW]));
+      if (e < HK) {
+        if (!bad && e / a.K < a.H) a.W1[e] = a.W1[e] - a.lr * s;
+      } else if (e < HK + a.Hp) {
+        const int n = e - HK;
+        if (!bad && n < a.H) a.b1[n] = a.b1[n] - a.lr * s;
+      } else if (e < HK + 2 * a.Hp) {
+        const int n = e - HK - a.Hp;
+        if (!bad && n < a.H) a.w2[n] = a.w2[n] - a.lr * s;
+      } else if (e == HK + 2 * a.Hp) {
+        a.loss_out[0] = bad ? __builtin_nanf("") : s * a.invB;
+      } else {
+        if (!bad) a.b2[0] = a.b2[0] - a.lr * s;
+      }
+    }
+    __syncthreads();  // red is rewritten by the next pass
   }
 }
 
@@ -129,7 +145,7 @@ __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
   const int nthreads = n_dz * kBlock;
   const uint32_t pfa = prefetch_lines(a.pf, gid, nthreads);
   const bool bad = void_bits(a.s) != 0u;
-  if (a.n_d > 0) dense_sgd(a.dn, gid, nthreads, bad);
+  if (a.n_d > 0) dense_sgd<kBlock>(a.dn, wg - a.n_e, n_dz, bad, &F[0][0]);
   zero_ranges(a.zero, gid, nthreads);
   prefetch_keep(a.pf, pfa);
 }
@@ -152,7 +168,8 @@ __global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
   const int nthreads = (gridDim.x - a.n_part) * kPartApplyThreads;
   const uint32_t pfa = prefetch_lines(a.pf, gid, nthreads);
   const bool bad = void_bits(a.s) != 0u;
-  if (a.n_d > 0) dense_sgd(a.dn, gid, nthreads, bad);
+  if (a.n_d > 0)
+    dense_sgd<kPartApplyThreads>(a.dn, blockIdx.x - a.n_part, gridDim.x - a.n_part, bad, &F[0][0]);
   zero_ranges(a.zero, gid, nthreads);
   prefetch_keep(a.pf, pfa);
 }
