@@ -890,6 +890,8 @@ int polyglot_scatter_update(polyglot_ctx* ctx, void* table, int32_t dtype, int32
   c.part_off = ctx->ws.part_off[0];
   c.partitioned = plan.small;
   c.n_part = 1 << plan.part_bits;  // the partitions this sort wrote
+  c.packed = dtype != POLYGLOT_F32 && d % 2 == 0 && reinterpret_cast<uintptr_t>(table) % 4 == 0 &&
+             reinterpret_cast<uintptr_t>(Y) % 4 == 0;
   if (e == hipSuccess) {
     Timed tm(ctx, POLYGLOT_K_SCATTER);
     e = launch_gen_update(c, tm.L);

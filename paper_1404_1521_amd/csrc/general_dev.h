@@ -84,6 +84,17 @@ struct GenArgs {
   struct Pre {
     T old[kPre];
   };
+  static constexpr bool kPacked = false;
+  using elem = T;
+};
+
+// The same arguments for a 16-bit format whose rows are whole 32-bit words
+// (d even, table and Y 4-byte aligned): the walk reads and writes two rows
+// per word (seg_walk_packed).
+template <class T>
+struct GenArgsP : GenArgs<T> {
+  static_assert(sizeof(T) == 2, "two elements per word");
+  static constexpr bool kPacked = true;
 };
 
 template <class T>
@@ -149,10 +160,124 @@ __device__ void seg_add_rows(const GenArgs<T>& a, const ChunkInfo& ci, uint64_t 
   }
 }
 
+// Packed walk.  For pair i of a chunk (rows 2i, 2i + 1), lanes < 32 read
+// row 2i and lanes >= 32 row 2i + 1, one 32-bit word (two columns) per lane:
+// lane l holds columns 2w, 2w + 1 of its row, w = c0 / 2 + l % 32.  Swapping
+// the upper half-wave of the first-column values with the lower half-wave of
+// the second-column values (v_permlane32_swap) leaves row 2i in one register
+// and row 2i + 1 in the other, lane l on column 2w + l / 32 of both; the same
+// swap turns two such rows back into words.  The old values of every row the
+// chunk completes are loaded beside the entries' rows, one word per lane per
+// pair, so a chunk takes one round of loads and writes each row as its piece
+// closes: half the registers per row in flight of the one-row walk, and half
+// the load and store instructions.  Same sums, same order, same rounding
+// (once per row) as seg_apply_rows.  (bfloat16, 327,680 entries into
+// 100000 x 64 in 32-entry chunks: apply 19.6 -> 18.1 us; 16- and 64-entry
+// chunks measured 21.2 and 23.4 us.)
+__device__ __forceinline__ void swap_halves(float& x, float& y) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false,
+                                                  false);
+  x = __uint_as_float(r[0]);
+  y = __uint_as_float(r[1]);
+}
+template <class T>
+__device__ __forceinline__ void unpack2(uint32_t w, float& x, float& y) {
+  x = Elem<T>::get(T{(uint16_t)(w & 0xffffu)});
+  y = Elem<T>::get(T{(uint16_t)(w >> 16)});
+}
+template <class T>
+__device__ __forceinline__ uint32_t pack2(float x, float y) {
+  return (uint32_t)Elem<T>::put(x).bits | ((uint32_t)Elem<T>::put(y).bits << 16);
+}
+
+template <int CH, class A>
+__device__ void seg_walk_packed(const A& a, const ChunkInfo& ci, uint64_t tails, uint64_t complete,
+                                int first_tail, bool starts_long, const ChunkSink& sink) {
+  using T = typename A::elem;
+  constexpr int NP = CH / 2;
+  const int lane = lane_id(), h = lane >> 5;
+  const int nact = ci.nact;
+  const uint32_t* Yw = reinterpret_cast<const uint32_t*>(a.Y);
+  uint32_t* Tw = reinterpret_cast<uint32_t*>(a.table);
+  const int dw = a.d >> 1;  // words per row
+  for (int c0 = 0; c0 < a.d; c0 += kWave) {
+    const int w = (c0 >> 1) + (lane & 31);
+    const bool wok = w < dw;
+    const int wc = wok ? w : dw - 1;  // lanes past the row end read its last word
+    // every pair's entries (rows past the chunk's end read entry 0's row,
+    // which no piece uses) and the old words of its complete rows
+    uint32_t y[NP], o[NP];
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      const int e0 = __builtin_amdgcn_readlane(ci.ent, 2 * i);
+      const int e1 = __builtin_amdgcn_readlane(ci.ent, 2 * i + 1);
+      y[i] = Yw[(size_t)(h ? e1 : e0) * dw + wc];
+    }
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      uint32_t c2 = (uint32_t)(complete >> (2 * i)) & 3u;
+      asm volatile("" : "+s"(c2));
+      o[i] = 0u;
+      if (c2 != 0u) {
+        const int k0 = __builtin_amdgcn_readlane(ci.key, 2 * i);
+        const int k1 = __builtin_amdgcn_readlane(ci.key, 2 * i + 1);
+        if ((c2 >> h) & 1u) o[i] = Tw[(size_t)(h ? k1 : k0) * dw + wc];
+      }
+    }
+    float acc = 0.f, first_sum = 0.f, last_sum = 0.f;
+#pragma unroll
+    for (int r0 = 0; r0 < CH; r0 += 8) {
+      uint32_t tw = (uint32_t)(tails >> r0) & 0xffu, cw = (uint32_t)(complete >> r0) & 0xffu;
+      int ft = first_tail - r0, lt = nact - 1 - r0;
+      asm volatile("" : "+s"(tw), "+s"(cw), "+s"(ft), "+s"(lt));
+      float v[8];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        unpack2<T>(y[r0 / 2 + p], v[2 * p], v[2 * p + 1]);
+        swap_halves(v[2 * p], v[2 * p + 1]);
+      }
+      if (tw == 0u) {  // no piece ends in these rows
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc += v[u];
+        continue;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        acc += v[u];
+        if ((tw >> u) & 1u) {
+          if (u == ft) first_sum = acc;
+          if (u == lt) last_sum = acc;
+          if ((cw >> u) & 1u) v[u] = a.alpha * acc;
+          acc = 0.f;
+        }
+      }
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const uint32_t c2 = (cw >> (2 * p)) & 3u;
+        if (c2 == 0u) continue;
+        float x, z;
+        unpack2<T>(o[r0 / 2 + p], x, z);
+        swap_halves(x, z);  // old values of rows r0 + 2p (x) and r0 + 2p + 1 (z)
+        x += v[2 * p];
+        z += v[2 * p + 1];
+        swap_halves(x, z);  // back to words: columns 2w, 2w + 1 of this lane's row
+        const int k0 = __builtin_amdgcn_readlane(ci.key, r0 + 2 * p);
+        const int k1 = __builtin_amdgcn_readlane(ci.key, r0 + 2 * p + 1);
+        if (((c2 >> h) & 1u) && wok) Tw[(size_t)(h ? k1 : k0) * dw + w] = pack2<T>(x, z);
+      }
+    }
+    if (wok) {
+      const int col = 2 * w + h;
+      if (ci.cont_first) sink.first[col] = first_sum;
+      if (starts_long) sink.last[col] = last_sum;
+    }
+  }
+}
+
 // Increment: one wave per chunk of CH sorted entries (seg_apply_rows), the
-// extra workgroups clear the sort counters.
-template <int CH, class T>
-__global__ __launch_bounds__(kBlock) void k_gen_apply(GenArgs<T> a, int n_e) {
+// extra workgroups clear the sort counters.  A: GenArgs<T> or GenArgsP<T>.
+template <int CH, class A>
+__global__ __launch_bounds__(kBlock) void k_gen_apply(A a, int n_e) {
   __shared__ float F[kWavesPerBlock][kMaxD];
   __shared__ float Lp[kWavesPerBlock][kMaxD];
   __shared__ int meta[kWavesPerBlock][5];
@@ -170,8 +295,8 @@ __global__ __launch_bounds__(kBlock) void k_gen_apply(GenArgs<T> a, int n_e) {
 // Increment after a partitioned sort (N <= kSmallSortN): workgroup p applies
 // partition p, whose segments never leave it, so no fix-up follows; the
 // extra workgroups clear nothing (the small sort keeps no counters).
-template <class T>
-__global__ __launch_bounds__(kPartApplyThreads) void k_gen_apply_part(GenArgs<T> a) {
+template <class A>
+__global__ __launch_bounds__(kPartApplyThreads) void k_gen_apply_part(A a) {
   __shared__ float F[kPartApplyWaves][kMaxD];
   __shared__ float Lp[kPartApplyWaves][kMaxD];
   __shared__ int meta[kPartApplyWaves][5];

@@ -274,15 +274,22 @@ static GenArgs<T> gen_args(const GenCall& c) {
   return a;
 }
 
+template <class A>
+static hipError_t launch_gen_inc(const GenCall& c, const A& a, const Launch& L) {
+  if (c.partitioned)
+    return pg_launch(k_gen_apply_part<A>, dim3(c.n_part), dim3(kPartApplyThreads), 0, L, a);
+  const dim3 grid(c.n_e + c.n_z), block(kBlock);
+  if (c.ch == 16) return pg_launch(k_gen_apply<16, A>, grid, block, 0, L, a, c.n_e);
+  return pg_launch(k_gen_apply<32, A>, grid, block, 0, L, a, c.n_e);
+}
+
 template <class T>
 static hipError_t launch_gen_update_t(const GenCall& c, const Launch& L) {
   const dim3 grid(c.n_e + c.n_z), block(kBlock);
   if (c.op == 1) return pg_launch(k_gen_set<T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
-  if (c.partitioned)
-    return pg_launch(k_gen_apply_part<T>, dim3(c.n_part), dim3(kPartApplyThreads), 0, L,
-                     gen_args<T>(c));
-  if (c.ch == 16) return pg_launch(k_gen_apply<16, T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
-  return pg_launch(k_gen_apply<32, T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
+  if constexpr (sizeof(T) == 2)
+    if (c.packed) return launch_gen_inc(c, GenArgsP<T>{gen_args<T>(c)}, L);
+  return launch_gen_inc(c, gen_args<T>(c), L);
 }
 
 hipError_t launch_gen_update(const GenCall& c, const Launch& L) {

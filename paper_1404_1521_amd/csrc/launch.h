@@ -223,6 +223,9 @@ struct GenCall {
   const int32_t* part_off;
   bool partitioned;
   int n_part;
+  // a 16-bit increment whose rows are whole 32-bit words (d even, table and
+  // Y 4-byte aligned): the packed walk, two rows per load and store
+  bool packed;
 };
 hipError_t launch_gen_update(const GenCall& c, const Launch& L);
 hipError_t launch_gen_fix(const GenCall& c, int grid, const Launch& L);

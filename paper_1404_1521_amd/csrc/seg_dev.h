@@ -50,6 +50,7 @@ struct SegArgs {
   float alpha;
   // completed pieces are added as they close (float atomics), not deferred
   static constexpr bool kDeferred = false;
+  static constexpr bool kPacked = false;  // one row per load, not the packed walk
   struct Pre {};
 };
 
@@ -132,6 +133,12 @@ __device__ __forceinline__ void seg_close(const SegArgs& a, size_t i, float v) {
   unsafeAtomicAdd(a.table + i, v);
 }
 
+// The walk of argument sets whose rows are 16-bit elements read and written
+// two rows per 32-bit word (kPacked; defined with those formats).
+template <int CH, class A>
+__device__ void seg_walk_packed(const A& a, const ChunkInfo& ci, uint64_t tails, uint64_t complete,
+                                int first_tail, bool starts_long, const ChunkSink& sink);
+
 // One wave applies entries [i0, min(i0 + CH, end)) of the sorted list (see
 // the file comment).  A is SegArgs or another argument set with the same
 // fields and its own seg_load / seg_add.  Returns false, having written
@@ -164,6 +171,10 @@ __device__ bool seg_apply_rows(const A& a, int i0, int end, const ChunkSink& sin
     sink.meta[2] = single;
     sink.meta[3] = ci.key;  // lane 0 holds the first piece's key
     sink.meta[4] = ci.last_key;
+  }
+  if constexpr (A::kPacked) {
+    seg_walk_packed<CH>(a, ci, tails, complete, first_tail, starts_long, sink);
+    return true;
   }
   for (int c0 = 0; c0 < a.d; c0 += kWave) {
     const int col = c0 + lane;

@@ -1101,3 +1101,39 @@ def test_scatter_update_widest_rows_long_list(fmt):
     assert np.all(np.abs(gv - rv) <= _format_bound(fmt, t0, idx, Y, 0.5, rv))
     untouched = np.setdiff1d(np.arange(rows), idx)
     assert np.array_equal(got[untouched], t0[untouched])
+
+
+def _offset_view(a, fmt):
+    """The array on the device one element past a 4-byte boundary: rows are
+    no longer whole 32-bit words, so 16-bit increments take the one-row walk
+    instead of the packed one."""
+    flat = np.concatenate([np.zeros(1, a.dtype), np.ascontiguousarray(a).reshape(-1)])
+    t = _to_dev(flat, fmt)[1:].view(a.shape)
+    assert t.data_ptr() % 4 == 2
+    return t
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "f16"])
+@pytest.mark.parametrize("rows,d,N", [(100_000, 64, 327_680), (3000, 128, 20_000), (500, 2, 6000)])
+def test_scatter_update_packed_and_one_row_walks(fmt, rows, d, N):
+    """Even widths from 4-byte aligned pointers (two rows per load and store)
+    and the same inputs one element off that alignment (one row per load),
+    chunked and partition-sorted lists: both against the oracle."""
+    rng = np.random.default_rng(d * 31 + N)
+    t0, Y, idx = _format_inputs(rng, fmt, rows, d, N, 1.2, np.int32)
+    ref = t0.copy()
+    oracle.scatter_add_ex(ref, idx, Y, -0.5, 0, bf16=fmt == "bf16")
+    code = _FMT[fmt][1]
+    rv = oracle.decode(ref, code) if fmt == "bf16" else ref.astype(np.float64)
+    bound = _format_bound(fmt, t0, idx, Y, -0.5, rv)
+    untouched = np.setdiff1d(np.arange(rows), idx)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    for aligned in (True, False):
+        td = _to_dev(t0, fmt) if aligned else _offset_view(t0, fmt)
+        Yd = _to_dev(Y, fmt) if aligned else _offset_view(Y, fmt)
+        ctx.scatter_update(td, dev(idx), Yd, -0.5)
+        assert ctx.status() == pg().OK
+        got = _to_host(td.contiguous(), fmt)
+        gv = oracle.decode(got, code) if fmt == "bf16" else got.astype(np.float64)
+        assert np.all(np.abs(gv - rv) <= bound), aligned
+        assert np.array_equal(got[untouched], t0[untouched]), aligned
