@@ -892,6 +892,13 @@ int polyglot_scatter_update(polyglot_ctx* ctx, void* table, int32_t dtype, int32
   c.n_part = 1 << plan.part_bits;  // the partitions this sort wrote
   c.packed = dtype != POLYGLOT_F32 && d % 2 == 0 && reinterpret_cast<uintptr_t>(table) % 4 == 0 &&
              reinterpret_cast<uintptr_t>(Y) % 4 == 0;
+  c.set_word = (int)es;
+  for (int wb = 16; wb > (int)es; wb /= 2)
+    if (((size_t)d * es) % wb == 0 && reinterpret_cast<uintptr_t>(table) % wb == 0 &&
+        reinterpret_cast<uintptr_t>(Y) % wb == 0) {
+      c.set_word = wb;
+      break;
+    }
   if (e == hipSuccess) {
     Timed tm(ctx, POLYGLOT_K_SCATTER);
     e = launch_gen_update(c, tm.L);

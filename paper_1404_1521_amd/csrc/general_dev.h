@@ -330,11 +330,21 @@ __device__ __forceinline__ void seg_add4(const GenArgs<T>& a, size_t i, int n, f
 
 // Assignment: one wave per 64 sorted entries; an entry whose successor has
 // another key (or that is the last) ends its row's segment, so it is the
-// row's last entry in index order, and its Y row is copied (lane = column),
-// 16 rows at a time.
-// The extra workgroups clear the sort counters.
-template <class T>
+// row's last entry in index order, and its Y row is copied.  The error words
+// are read beside the keys.  Each such entry's (entry, row) goes to the
+// wave's LDS slots by its rank among them, and the rows are copied as words
+// of W bytes (the widest that divides a row and the pointers' alignment):
+// word f of the group's copy is word f % dw of the (f / dw)-th row, dw words
+// per row, 8 or 16 words per lane in flight at once, so a group of short
+// rows takes one round of loads however many rows it ends (binary16, d 64:
+// four rows per load).  The extra workgroups clear the sort counters.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // a 16-byte word
+template <class W>
+constexpr int set_words() { return sizeof(W) >= 16 ? 8 : 16; }  // per lane, in flight
+template <class T, class W>
 __global__ __launch_bounds__(kBlock) void k_gen_set(GenArgs<T> a, int n_e) {
+  constexpr int kSetWords = set_words<W>();
+  __shared__ int2 tl[kWavesPerBlock][kWave];  // (entry, row) of the group's row ends, by rank
   const int lane = lane_id();
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if ((int)blockIdx.x >= n_e) {
@@ -342,42 +352,44 @@ __global__ __launch_bounds__(kBlock) void k_gen_set(GenArgs<T> a, int n_e) {
                 (size_t)(gridDim.x - n_e) * kBlock);
     return;
   }
-  if (__builtin_amdgcn_readfirstlane(void_bits(a)) != 0u) return;
+  const W* Yw = reinterpret_cast<const W*>(a.Y);
+  W* Tw = reinterpret_cast<W*>(a.table);
+  const int dw = (int)((size_t)a.d * sizeof(T) / sizeof(W));
   const int ngroups = ceil_div(a.N, kWave);
-  constexpr int RB = 16;  // rows copied together, their loads in flight at once
   for (int gi = blockIdx.x * kWavesPerBlock + w; gi < ngroups; gi += n_e * kWavesPerBlock) {
     const int i = gi * kWave + lane;
     const bool act = i < a.N;
+    const uint32_t flag = *a.flag | *a.flag2;
     const int32_t key = act ? a.sk[i] : -1;
     const int32_t nxt = (i + 1 < a.N) ? a.sk[i + 1] : -2;
     const int32_t ent = act ? a.sv[i] : 0;
-    uint64_t tails = __ballot(act && key != nxt);
-    while (tails) {
-      int src[RB];
-      int n = 0;
+    const bool tail = act && key != nxt;
+    const uint64_t tails = __ballot(tail);
+    if (__builtin_amdgcn_readfirstlane(flag) != 0u) return;  // a bad id voids the call
+    const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(tails >> 32),
+                                               __builtin_amdgcn_mbcnt_lo((uint32_t)tails, 0u));
+    if (tail) tl[w][rank] = make_int2(ent, key);
+    __builtin_amdgcn_wave_barrier();
+    const int total = __popcll((unsigned long long)tails) * dw;  // words to copy
+    for (int f0 = 0; f0 < total; f0 += kSetWords * kWave) {
+      W v[kSetWords];
+      size_t dst[kSetWords];
 #pragma unroll
-      for (int j = 0; j < RB; ++j) {
-        src[j] = 0;
-        if (tails) {
-          src[j] = __ffsll((unsigned long long)tails) - 1;
-          tails &= tails - 1;
-          n = j + 1;
+      for (int u = 0; u < kSetWords; ++u) {
+        const int f = f0 + u * kWave + lane;
+        dst[u] = ~(size_t)0;
+        if (f < total) {
+          const int j = f / dw, x = f - j * dw;
+          const int2 r = tl[w][j];
+          v[u] = Yw[(size_t)r.x * dw + x];
+          dst[u] = (size_t)r.y * dw + x;
         }
       }
-      for (int c0 = 0; c0 < a.d; c0 += kWave) {
-        const int col = c0 + lane;
-        const bool cok = col < a.d;
-        T v[RB];
 #pragma unroll
-        for (int j = 0; j < RB; ++j)
-          if (j < n && cok)
-            v[j] = a.Y[(size_t)__builtin_amdgcn_readlane(ent, src[j]) * a.d + col];
-#pragma unroll
-        for (int j = 0; j < RB; ++j)
-          if (j < n && cok)
-            a.table[(size_t)__builtin_amdgcn_readlane(key, src[j]) * a.d + col] = v[j];
-      }
+      for (int u = 0; u < kSetWords; ++u)
+        if (dst[u] != ~(size_t)0) Tw[dst[u]] = v[u];
     }
+    __builtin_amdgcn_wave_barrier();  // the slots are rewritten by the next group
   }
 }
 

@@ -286,7 +286,14 @@ static hipError_t launch_gen_inc(const GenCall& c, const A& a, const Launch& L) 
 template <class T>
 static hipError_t launch_gen_update_t(const GenCall& c, const Launch& L) {
   const dim3 grid(c.n_e + c.n_z), block(kBlock);
-  if (c.op == 1) return pg_launch(k_gen_set<T>, grid, block, 0, L, gen_args<T>(c), c.n_e);
+  if (c.op == 1) {  // copies in the widest words the rows and pointers allow
+    const GenArgs<T> a = gen_args<T>(c);
+    if (c.set_word == 16) return pg_launch(k_gen_set<T, u32x4>, grid, block, 0, L, a, c.n_e);
+    if (c.set_word == 8) return pg_launch(k_gen_set<T, uint64_t>, grid, block, 0, L, a, c.n_e);
+    if (c.set_word == 4) return pg_launch(k_gen_set<T, uint32_t>, grid, block, 0, L, a, c.n_e);
+    if constexpr (sizeof(T) == 2) return pg_launch(k_gen_set<T, uint16_t>, grid, block, 0, L, a, c.n_e);
+    return hipErrorInvalidValue;  // a float32 row is whole 4-byte words
+  }
   if constexpr (sizeof(T) == 2)
     if (c.packed) return launch_gen_inc(c, GenArgsP<T>{gen_args<T>(c)}, L);
   return launch_gen_inc(c, gen_args<T>(c), L);

@@ -226,6 +226,9 @@ struct GenCall {
   // a 16-bit increment whose rows are whole 32-bit words (d even, table and
   // Y 4-byte aligned): the packed walk, two rows per load and store
   bool packed;
+  // bytes per word of the assignment's row copies (2, 4, 8 or 16): the
+  // widest that divides a row and both pointers' alignment
+  int set_word;
 };
 hipError_t launch_gen_update(const GenCall& c, const Launch& L);
 hipError_t launch_gen_fix(const GenCall& c, int grid, const Launch& L);

@@ -1137,3 +1137,29 @@ def test_scatter_update_packed_and_one_row_walks(fmt, rows, d, N):
         gv = oracle.decode(got, code) if fmt == "bf16" else got.astype(np.float64)
         assert np.all(np.abs(gv - rv) <= bound), aligned
         assert np.array_equal(got[untouched], t0[untouched]), aligned
+
+
+def _shifted(a, fmt, k):
+    """The array on the device k elements past a 256-byte boundary."""
+    flat = np.concatenate([np.zeros(k, a.dtype), np.ascontiguousarray(a).reshape(-1)])
+    return _to_dev(flat, fmt)[k:].view(a.shape)
+
+
+@pytest.mark.parametrize("fmt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("rows,d,N", [(100_000, 64, 327_680), (700, 6, 3000), (5000, 24, 40_000)])
+def test_scatter_update_assignment_word_widths(fmt, rows, d, N):
+    """The assignment copies rows in the widest words that divide a row and
+    both pointers' alignment: pointers 0, 1, 2 and 4 elements past a 256-byte
+    boundary give 16-, 2-, 4- and 8-byte words (16-bit formats) or 16-, 4-,
+    8- and 16-byte words (float32), the last entry of each row winning,
+    bit-exact against the oracle."""
+    rng = np.random.default_rng(d * 7 + N)
+    t0, Y, idx = _format_inputs(rng, fmt, rows, d, N, 1.2, np.int32)
+    ref = t0.copy()
+    oracle.scatter_add_ex(ref, idx, Y, 1.0, 1, bf16=fmt == "bf16")
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    for k in (0, 1, 2, 4):
+        td, Yd = _shifted(t0, fmt, k), _shifted(Y, fmt, k)
+        ctx.scatter_update(td, dev(idx), Yd, 1.0, pg().OP_SET)
+        assert ctx.status() == pg().OK
+        assert np.array_equal(_to_host(td.contiguous(), fmt), ref), k
