@@ -204,7 +204,11 @@ int polyglot_scatter_add_noalloc(float* table, int32_t rows, int32_t d, const in
  *   op POLYGLOT_OP_SET: for every k in order, table[idx[k]] = Y[k]; for a
  *     repeated index the largest k wins (sorted mode only).
  * N <= max_scatter and rows <= max_rows of the context.  Float32 increments
- * take the same kernels as polyglot_scatter_add.  The caller owns every
+ * take the same kernels as polyglot_scatter_add.  Faster forms, with the
+ * same results: 16-bit increments whose rows are whole 4-byte words (d even,
+ * table and Y 4-byte aligned) read and write two rows per word; assignments
+ * copy rows in the widest words (up to 16 bytes) that divide a row and both
+ * pointers' alignment.  The caller owns every
  * buffer; the call is asynchronous on the context stream.  Returns
  * POLYGLOT_EINVAL for a bad format, op, mode, width or alignment or an
  * unsupported mode combination, POLYGLOT_ENULL, POLYGLOT_EBATCH; an index
