@@ -845,25 +845,31 @@ int polyglot_scatter_update(polyglot_ctx* ctx, void* table, int32_t dtype, int32
   if (mode == POLYGLOT_SCATTER_ATOMIC && (dtype != POLYGLOT_F32 || op != POLYGLOT_OP_INC))
     return fail(ctx, POLYGLOT_EINVAL, "scatter_update: the atomic mode takes float32 increments only");
   hipError_t e = hipSuccess;
-  const int32_t* keys = static_cast<const int32_t*>(idx);
-  if (idx_bytes == 8) {  // narrowed (and range-checked) into the context's key buffer
-    Timed tm(ctx, POLYGLOT_K_SORT);
-    e = launch_keys_from_i64(static_cast<const int64_t*>(idx), N, rows, ctx->ws.idx32,
-                             ctx->ws.flag, tm.L);
-    if (e != hipSuccess) return hip_fail(ctx, e, "scatter_update: key launch");
-    keys = ctx->ws.idx32;
-  }
   // float32 increments take the scatter-add kernels (their fix-up reads rows
   // as 16-byte vectors, so the sorted mode wants d % 4 == 0 and aligned rows)
   if (dtype == POLYGLOT_F32 && op == POLYGLOT_OP_INC &&
-      (mode == POLYGLOT_SCATTER_ATOMIC || (d % 4 == 0 && aligned16(table) && aligned16(Y))))
+      (mode == POLYGLOT_SCATTER_ATOMIC || (d % 4 == 0 && aligned16(table) && aligned16(Y)))) {
+    const int32_t* keys = static_cast<const int32_t*>(idx);
+    if (idx_bytes == 8) {  // narrowed (and range-checked) into the context's key buffer
+      Timed tm(ctx, POLYGLOT_K_SORT);
+      e = launch_keys_from_i64(static_cast<const int64_t*>(idx), N, rows, ctx->ws.idx32,
+                               ctx->ws.flag, tm.L);
+      if (e != hipSuccess) return hip_fail(ctx, e, "scatter_update: key launch");
+      keys = ctx->ws.idx32;
+    }
     return scatter_add_f32(ctx, static_cast<float*>(table), rows, d, keys,
                            static_cast<const float*>(Y), N, alpha, mode);
+  }
+  // the other calls sort the ids as they are (int64 ids narrowed and
+  // range-checked by the sort's own key loads)
   const SortPlan plan = make_plan(rows, N);
-  const IdxKeys kf{keys, rows};
   {
     Timed tm(ctx, POLYGLOT_K_SORT);
-    e = launch_sort_idx(kf, N, plan, sort_bufs(ctx, 0), tm.L);
+    e = idx_bytes == 8
+            ? launch_sort_i64(I64Keys{static_cast<const int64_t*>(idx), rows}, N, plan,
+                              sort_bufs(ctx, 0), tm.L)
+            : launch_sort_idx(IdxKeys{static_cast<const int32_t*>(idx), rows}, N, plan,
+                              sort_bufs(ctx, 0), tm.L);
   }
   GenCall c{};
   c.table = table;

@@ -215,6 +215,11 @@ hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const
   return launch_sort(kf, N, plan, sb, L);
 }
 
+hipError_t launch_sort_i64(const I64Keys& kf, int N, const SortPlan& plan, const SortBufs& sb,
+                           const Launch& L) {
+  return launch_sort(kf, N, plan, sb, L);
+}
+
 template <class KeyFn>
 static hipError_t launch_apply(const ApplyArgs& a, const KeyFn& kf, int grid, const Launch& L) {
   if (a.s.ch == 16) return pg_launch(k_apply<16, KeyFn>, dim3(grid), dim3(kBlock), 0, L, a, kf);

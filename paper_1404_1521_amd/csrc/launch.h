@@ -189,6 +189,8 @@ hipError_t launch_sort_step(const StepKeys& kf, int N, const SortPlan& plan, con
                             const Launch& L);
 hipError_t launch_sort_idx(const IdxKeys& kf, int N, const SortPlan& plan, const SortBufs& sb,
                            const Launch& L);
+hipError_t launch_sort_i64(const I64Keys& kf, int N, const SortPlan& plan, const SortBufs& sb,
+                           const Launch& L);
 hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, const Launch& L);
 hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, const Launch& L);
 hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L);

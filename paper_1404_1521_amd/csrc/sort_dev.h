@@ -53,6 +53,17 @@ struct IdxKeys {  // entries of the standalone scatter-add
   int range;        // table rows
   __device__ int32_t load(int e) const { return idx[e]; }
 };
+// int64 entries of the general op, narrowed as they are loaded: an id
+// outside [0, range) loads as 0xffffffff, which the sort's range check turns
+// into key 0 and the sticky error flag (no narrowing launch of its own).
+struct I64Keys {
+  const int64_t* idx;
+  int range;        // table rows
+  __device__ int32_t load(int e) const {
+    const int64_t v = idx[e];
+    return (v < 0 || v >= (int64_t)range) ? -1 : (int32_t)v;
+  }
+};
 
 // Loads U keys per thread with all loads in flight before any check; ids
 // outside [0, range) become 0 and raise the sticky flag once.
