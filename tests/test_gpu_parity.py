@@ -1163,3 +1163,34 @@ def test_scatter_update_assignment_word_widths(fmt, rows, d, N):
         ctx.scatter_update(td, dev(idx), Yd, 1.0, pg().OP_SET)
         assert ctx.status() == pg().OK
         assert np.array_equal(_to_host(td.contiguous(), fmt), ref), k
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "f16"])
+def test_scatter_update_int64_ids_lookback_sort(fmt):
+    """int64 ids are narrowed and range-checked by the sort's own key loads
+    in every sort form; 1,200,000 entries take the look-back sort (beyond the
+    bucketed sort's 1,048,576): against the oracle, then the same call with
+    one id out of range (past the first tile) leaves the table untouched."""
+    rows, d, N = 200_000, 8, 1_200_000
+    rng = np.random.default_rng(1200)
+    t0, Y, idx = _format_inputs(rng, fmt, rows, d, N, 1.1, np.int64)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    td = _to_dev(t0, fmt)
+    ctx.scatter_update(td, dev(idx), _to_dev(Y, fmt), -0.5)
+    assert ctx.status() == pg().OK
+    got = _to_host(td, fmt)
+    ref = t0.copy()
+    oracle.scatter_add_ex(ref, idx, Y, -0.5, 0, bf16=fmt == "bf16")
+    code = _FMT[fmt][1]
+    gv = oracle.decode(got, code) if fmt == "bf16" else got.astype(np.float64)
+    rv = oracle.decode(ref, code) if fmt == "bf16" else ref.astype(np.float64)
+    assert np.all(np.abs(gv - rv) <= _format_bound(fmt, t0, idx, Y, -0.5, rv))
+    untouched = np.setdiff1d(np.arange(rows), idx)
+    assert np.array_equal(got[untouched], t0[untouched])
+    bad = idx.copy()
+    bad[N - 7] = rows
+    td = _to_dev(t0, fmt)
+    ctx.scatter_update(td, dev(bad), _to_dev(Y, fmt), -0.5)
+    assert ctx.status() == pg().EID
+    assert np.array_equal(_to_host(td, fmt), t0)
+    assert ctx.status() == pg().OK
