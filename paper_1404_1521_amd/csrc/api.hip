@@ -478,7 +478,7 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
 // update and fix-up launches, beside their work, with no second stream (the
 // fused kernel holds every CU, so a side-stream sort could not overlap it,
 // and the cross-queue joins cost time of their own).  Other lists (above
-// 1,048,576 entries, or the small sort of wide layers): the sort of step s+1
+// 786,432 entries, or the small sort of wide layers): the sort of step s+1
 // runs on the side stream while step s computes; it waits for step s-1, the
 // last reader of the same sort set.
 int enqueue_steps(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2, float* b2,

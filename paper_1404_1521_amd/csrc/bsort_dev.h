@@ -44,9 +44,14 @@ constexpr int kBkDigitBits = 10;                    // bucket ids fit 10 bits
 static_assert(kBkBuckets <= (1 << kBkDigitBits), "bucket ids");
 constexpr int kBkScanN = 1024;                      // padded length of the per-bucket scans
 constexpr int kBkThreads = 512;                     // k_bk_tiles workgroup
-constexpr int kBkTileKeys = 2048;                   // keys per tile
+// keys per tile: 1536 (214 tiles of the 327,680-entry list, more CUs than
+// 160 of 2048) measured faster than 2048 from B = 4096 up (B = 16,384 step
+// 59.9 -> 58.4-59.4 us, B = 32,768 85.8 -> 84.0 us) and the same on the
+// 327,680-entry scatter-add; 1024 slowed the bucket launch, which reads one
+// word per tile for each bucket
+constexpr int kBkTileKeys = 1536;
 constexpr int kBkMaxTiles = 512;
-constexpr int kBkMaxN = kBkTileKeys * kBkMaxTiles;  // 1,048,576
+constexpr int kBkMaxN = kBkTileKeys * kBkMaxTiles;  // 786,432
 constexpr int kBkMaxKeyBits = 30;                   // hashed words pack (key >> 9) and 11 index bits
 constexpr int kBkSortThreads = 512;                 // k_bk_buckets workgroup
 constexpr int kBkUnit = 2048;                       // entries per unit of a dedicated bucket

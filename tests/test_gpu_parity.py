@@ -401,7 +401,7 @@ def _bucket_case(kind):
     elif kind == "uniform_mid":   # hashed buckets of 513..2048 entries: LDS radix passes
         rows, d, N = 5_000, 8, 700_000
         idx = rng.integers(0, rows, N).astype(np.int32)
-    else:                         # above 1,048,576 entries: the multi-tile look-back sort
+    else:                         # above 786,432 entries: the multi-tile look-back sort
         rows, d, N = 100_000, 4, 1_200_000
         idx = workloads.zipf_ids(rng, rows, 1.0, N)
     t0 = rng.normal(0, 0.01, (rows, d)).astype(np.float32)
@@ -412,13 +412,13 @@ def _bucket_case(kind):
 @pytest.mark.parametrize("kind", ["permuted_zipf", "one_key", "wide_keys", "few_keys",
                                   "one_key_per_bucket", "uniform_mid", "look_back"])
 def test_scatter_add_sort_paths(kind):
-    """Lists of 8,192 < N <= 1,048,576 entries take the bucketed sort (64
+    """Lists of 8,192 < N <= 786,432 entries take the bucketed sort (64
     dedicated buckets for the smallest ids, 512 hashed ones for the rest);
     these inputs reach its less common paths: heavy rows at random ids
     (hashed buckets above 2,048 entries, ordered through global memory),
     one key for every entry, 24-bit keys, key ranges inside the dedicated
     buckets, buckets of one key, and hashed buckets sorted by LDS radix
-    passes; above 1,048,576 entries the multi-tile look-back sort.  Against
+    passes; above 786,432 entries the multi-tile look-back sort.  Against
     the oracle, the touched rows, and two calls bit-identical."""
     t0, idx, Y = _bucket_case(kind)
     rows, d = t0.shape
@@ -1169,7 +1169,7 @@ def test_scatter_update_assignment_word_widths(fmt, rows, d, N):
 def test_scatter_update_int64_ids_lookback_sort(fmt):
     """int64 ids are narrowed and range-checked by the sort's own key loads
     in every sort form; 1,200,000 entries take the look-back sort (beyond the
-    bucketed sort's 1,048,576): against the oracle, then the same call with
+    bucketed sort's 786,432): against the oracle, then the same call with
     one id out of range (past the first tile) leaves the table untouched."""
     rows, d, N = 200_000, 8, 1_200_000
     rng = np.random.default_rng(1200)
