@@ -223,8 +223,7 @@ hipError_t launch_sort_i64(const I64Keys& kf, int N, const SortPlan& plan, const
 template <class KeyFn>
 static hipError_t launch_apply(const ApplyArgs& a, const KeyFn& kf, int grid, const Launch& L) {
   if (a.s.ch == 16) return pg_launch(k_apply<16, KeyFn>, dim3(grid), dim3(kBlock), 0, L, a, kf);
-  if (a.s.ch == 32) return pg_launch(k_apply<32, KeyFn>, dim3(grid), dim3(kBlock), 0, L, a, kf);
-  return pg_launch(k_apply<64, KeyFn>, dim3(grid), dim3(kBlock), 0, L, a, kf);
+  return pg_launch(k_apply<32, KeyFn>, dim3(grid), dim3(kBlock), 0, L, a, kf);
 }
 
 hipError_t launch_apply_step(const ApplyArgs& a, const StepKeys& kf, int grid, const Launch& L) {
@@ -236,8 +235,7 @@ hipError_t launch_apply_step_next(const ApplyArgs& a, const StepKeys& kf, int gr
   const uint32_t lds = a.nx.n_wg ? bk_tiles_lds_words(kBlock) * 4 : 0;
   const int g = grid + a.nx.n_wg;
   if (a.s.ch == 16) return pg_launch(k_apply<16, StepKeys>, dim3(g), dim3(kBlock), lds, L, a, kf);
-  if (a.s.ch == 32) return pg_launch(k_apply<32, StepKeys>, dim3(g), dim3(kBlock), lds, L, a, kf);
-  return pg_launch(k_apply<64, StepKeys>, dim3(g), dim3(kBlock), lds, L, a, kf);
+  return pg_launch(k_apply<32, StepKeys>, dim3(g), dim3(kBlock), lds, L, a, kf);
 }
 
 hipError_t launch_segfix_step(const SegArgs& a, const NextSort& nx, int n_fix, const Launch& L) {

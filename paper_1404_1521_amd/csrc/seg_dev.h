@@ -4,8 +4,8 @@
 // The training step uses it with Y = the per-entry embedding gradients and
 // alpha = -lr; polyglot_scatter_add with the caller's Y and alpha.
 //
-// The sorted entry list is cut into chunks of CH entries (16 or 64), one per
-// wave.  A wave loads the Y rows of its whole chunk at once (lane = column)
+// The sorted entry list is cut into chunks of CH entries (16 or 32; 64 in the
+// partition-wise apply), one per wave.  A wave loads the Y rows of its whole chunk at once (lane = column)
 // and walks them with a running sum that closes at each piece end (a
 // "piece" is a maximal run of equal keys inside the chunk).  Pieces whose
 // segment lies wholly inside the chunk are added to their table rows by that
@@ -107,9 +107,11 @@ __device__ __forceinline__ uint32_t void_bits(const A& a) {
 // batches over more waves; long chunks keep partials few for large ones.
 // Measured on training steps (same box, alternating, 16 -> 32 entries):
 // B = 2048 26.5 -> 27.7 us, B = 4096 35.7 -> 35.3, B = 8192 43.6 -> 42.2,
-// B = 16,384 58.6 -> 58.9; so 32 between 16,384 and 65,536 entries.
+// B = 16,384 58.6 -> 58.9; and 64 -> 32 above 131,072 entries: B = 32,768
+// 84.4 -> 83.8 us, B = 65,536 126.9 -> 126.2, stress and the 327,680-entry
+// scatter-add unchanged.
 __host__ __device__ inline int seg_chunk_size(int N) {
-  return (N > 16384 && N <= 65536) ? 32 : (N <= 131072 ? 16 : 64);
+  return (N <= 16384 || (N > 65536 && N <= 131072)) ? 16 : 32;
 }
 // The general op's typed increments defer their row updates past the walk
 // (a load and a store per row, 16 rows per round of loads), so shorter

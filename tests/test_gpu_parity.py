@@ -176,8 +176,8 @@ def test_scatter_add_matches_oracle(mode, rows, d, N, s):
 
 def _run_lengths_covering_every_lane(rng, N):
     """Keys whose sorted runs have every length 1..70 (shuffled), so piece
-    heads fall on every lane of a 64-entry chunk, runs cross chunk ends, and
-    a run starting at lane 31 continues past lane 32."""
+    heads fall on every lane of a chunk (32 or 64 entries), runs cross chunk
+    ends, and a run starting at lane 31 continues past lane 32."""
     lens = []
     while sum(lens) < N:
         lens.extend(rng.permutation(np.arange(1, 71)).tolist())
@@ -188,9 +188,11 @@ def _run_lengths_covering_every_lane(rng, N):
 @pytest.mark.parametrize("pattern", ["every_lane", "head_at_lane_31"])
 @pytest.mark.parametrize("d", [64, 80])
 def test_scatter_add_long_chunks_piece_structure(pattern, d):
-    """Lists above 131072 entries use 64-entry chunks; these key layouts put
-    piece boundaries on each lane (including both halves of the 64-bit lane
-    masks) and rows of 80 floats take a second, partial column block."""
+    """A 140,000-entry list (32-entry chunks, ranges of 128 entries); these
+    key layouts put piece boundaries on each lane of a chunk, runs across
+    chunk and range ends, and rows of 80 floats take a second, partial
+    column block.  (Both halves of the 64-bit lane masks are covered by the
+    partition-wise apply's 64-entry chunks: test_scatter_add_partition_every_lane.)"""
     rng = np.random.default_rng(7)
     N = 140_000
     if pattern == "every_lane":
@@ -199,6 +201,33 @@ def test_scatter_add_long_chunks_piece_structure(pattern, d):
         keys = ((np.arange(N) + 33) // 64).astype(np.int32)
     rows = int(keys.max()) + 5
     idx = keys[rng.permutation(N)]  # the sort regroups the runs
+    t0 = rng.normal(0, 0.01, (rows, d)).astype(np.float32)
+    Y = rng.normal(0, 1e-3, (N, d)).astype(np.float32)
+    ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
+    td = dev(t0)
+    ctx.scatter_add(td, dev(idx), dev(Y), -0.5, pg().SCATTER_SORTED)
+    assert ctx.status() == pg().OK
+    got = host(td)
+    ref = t0.copy()
+    oracle.scatter_add(ref, idx, Y, -0.5)
+    err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    assert np.all(err <= scatter_bound(t0, idx, Y, -0.5))
+    untouched = np.setdiff1d(np.arange(rows), idx)
+    assert np.array_equal(got[untouched], t0[untouched])
+
+
+@pytest.mark.parametrize("d", [64, 80])
+def test_scatter_add_partition_every_lane(d):
+    """8,192 entries whose ids are all multiples of 128 fall into one
+    partition of the partitioned sort, with runs of every length 1..70: the
+    partition-wise update's 64-entry chunks get piece heads on every lane,
+    both halves of the 64-bit lane masks, and runs across chunk and round
+    ends."""
+    rng = np.random.default_rng(17)
+    N = 8192
+    idx = (_run_lengths_covering_every_lane(rng, N) * 128).astype(np.int32)
+    rows = int(idx.max()) + 1
+    idx = idx[rng.permutation(N)]
     t0 = rng.normal(0, 0.01, (rows, d)).astype(np.float32)
     Y = rng.normal(0, 1e-3, (N, d)).astype(np.float32)
     ctx = pg().Context(1000, 16, 5, 8, max_batch=1, max_scatter=N, max_rows=rows)
@@ -623,7 +652,7 @@ def test_stress_full_size_parity(mode, steps):
     B 16384, lr 0.005) against the oracle: per-step losses, W1, b1, w2, b2
     and the touched rows of E under the parameter and delta bars, the other
     rows bit-identical.  This is the one shape that runs the wide-layer
-    backward with 16 dW1 slices, the multi-tile sort and 64-entry chunks
+    backward with 16 dW1 slices, the multi-tile sort and 32-entry chunks
     together."""
     w = PRESETS["stress"]
     run_both(w, steps, w.B, mode, touched_only=True)
@@ -973,7 +1002,7 @@ def _format_bound(fmt, t0, idx, Y, alpha, ref_vals):
 def test_scatter_update_matches_oracle(fmt, op, rows, d, N, s, idx_dtype):
     """Every storage format and op, int32 and int64 indices, widths that are
     not multiples of 4, the partition-sorted (N <= 8192) and the chunked list
-    (64-entry chunks above 131072, with heavy rows in the fix-up)."""
+    (32-entry chunks above 131072, with heavy rows in the fix-up)."""
     rng = np.random.default_rng(rows * 7 + N + d)
     t0, Y, idx = _format_inputs(rng, fmt, rows, d, N, s, idx_dtype)
     alpha = -0.75
