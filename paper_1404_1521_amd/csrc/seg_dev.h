@@ -251,10 +251,15 @@ __device__ bool seg_apply_rows(const A& a, int i0, int end, const ChunkSink& sin
 }
 
 // Threads of a partition workgroup: 16 waves, so one round covers 1024
-// entries in 64-entry chunks.
+// entries in 64-entry chunks.  Lists of at most kPartShortN entries take
+// 32-entry chunks instead: more waves share a partition's rows.  Training
+// steps, 64 -> 32 (same box, alternating): tiny (192 entries) 11.09 -> 10.59
+// us, poly256 (1,536) 13.21 -> 12.82, B = 512 14.85 -> 14.66, B = 768
+// (4,608) 16.02 -> 15.82; B = 1024 (6,144) 17.05 -> 17.25 us.
 constexpr int kPartApplyThreads = 1024;
 constexpr int kPartApplyWaves = kPartApplyThreads / kWave;
 constexpr int kPartApplyChunk = 64;
+constexpr int kPartShortN = 5120;
 
 // Segmented apply of one partition of a partitioned sort (NW waves per
 // workgroup), entries [s, e):
@@ -265,13 +270,13 @@ constexpr int kPartApplyChunk = 64;
 // segment (carried over from earlier rounds when it started there) and
 // applying the row once the segment closes.  The order of every sum is
 // fixed, so the result does not depend on scheduling.
-template <int NW, class A>
+template <int NW, class A, int PC = kPartApplyChunk>
 __device__ void seg_apply_partition(const A& a, int s, int e,
                                     float (*F)[kMaxD], float (*Lp)[kMaxD], int (*meta)[5]) {
   const int t = threadIdx.x, lane = t & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
   constexpr int CB = kMaxD / kWave;  // column blocks of the widest row
-  const int nch = (e - s + kPartApplyChunk - 1) / kPartApplyChunk;
+  const int nch = (e - s + PC - 1) / PC;
   float open[CB];                    // wave 0: the segment still open, by column block
   int open_key = 0, open_key_next = 0;
 #pragma unroll
@@ -280,7 +285,7 @@ __device__ void seg_apply_partition(const A& a, int s, int e,
     const int c = r0 + w;
     bool ok = true;  // (wave 0 always has a chunk: its own test covers the combine)
     if (c < nch)
-      ok = seg_apply_rows<kPartApplyChunk>(a, s + c * kPartApplyChunk, e,
+      ok = seg_apply_rows<PC>(a, s + c * PC, e,
                                            ChunkSink{F[w], Lp[w], meta[w]});
     __syncthreads();  // the round's open pieces are in LDS
     if (w == 0 && ok) {

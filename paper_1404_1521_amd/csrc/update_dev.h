@@ -152,7 +152,9 @@ __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
 
 // Sorted update of a partition-sorted list: workgroup p < n_part applies
 // partition p, whose segments never leave it, so no fix-up launch follows;
-// the remaining workgroups run the dense SGD and clearing roles.
+// the remaining workgroups run the dense SGD and clearing roles.  PC:
+// entries per chunk (32 for lists of at most kPartShortN entries, else 64).
+template <int PC>
 __global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
   __shared__ float F[kPartApplyWaves][kMaxD];
   __shared__ float Lp[kPartApplyWaves][kMaxD];
@@ -161,7 +163,8 @@ __global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
   if ((int)blockIdx.x < a.n_part) {
     // (the error words are tested beside each chunk's keys)
     const int p = blockIdx.x;
-    seg_apply_partition<kPartApplyWaves>(a.s, a.part_off[p], a.part_off[p + 1], F, Lp, meta);
+    seg_apply_partition<kPartApplyWaves, SegArgs, PC>(a.s, a.part_off[p], a.part_off[p + 1], F, Lp,
+                                                      meta);
     return;
   }
   const int gid = (blockIdx.x - a.n_part) * kPartApplyThreads + t;
