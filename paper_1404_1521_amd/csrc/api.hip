@@ -440,7 +440,7 @@ int enqueue_compute(polyglot_ctx* ctx, float* E, float* W1, float* b1, float* w2
     // so no fix-up launch follows
     aa.part_off = ctx->ws.part_off[set];
     aa.n_part = 1 << plan.part_bits;
-    aa.n_d = ceil_div(aa.n_d * kBlock, kPartApplyThreads);
+    aa.n_d = ceil_div(aa.n_d * kBlock, part_apply_threads(N));
     Timed tm(ctx, POLYGLOT_K_UPDATE);
     e = launch_apply_part(aa, aa.n_part + aa.n_d, tm.L);
   } else {

@@ -249,9 +249,15 @@ hipError_t launch_apply_idx(const ApplyArgs& a, const IdxKeys& kf, int grid, con
 }
 
 hipError_t launch_apply_part(const ApplyArgs& a, int grid, const Launch& L) {
+  static_assert(kPartTinyN <= kPartShortN, "the 8-wave form takes 32-entry chunks");
+  if (part_apply_threads(a.s.N) == kPartShortThreads)
+    return pg_launch(k_apply_part<32, kPartShortThreads>, dim3(grid), dim3(kPartShortThreads), 0, L,
+                     a);
   if (a.s.N <= kPartShortN)
-    return pg_launch(k_apply_part<32>, dim3(grid), dim3(kPartApplyThreads), 0, L, a);
-  return pg_launch(k_apply_part<kPartApplyChunk>, dim3(grid), dim3(kPartApplyThreads), 0, L, a);
+    return pg_launch(k_apply_part<32, kPartApplyThreads>, dim3(grid), dim3(kPartApplyThreads), 0, L,
+                     a);
+  return pg_launch(k_apply_part<kPartApplyChunk, kPartApplyThreads>, dim3(grid),
+                   dim3(kPartApplyThreads), 0, L, a);
 }
 
 hipError_t launch_segfix(const SegArgs& a, int grid, const Launch& L) {

@@ -260,6 +260,15 @@ constexpr int kPartApplyThreads = 1024;
 constexpr int kPartApplyWaves = kPartApplyThreads / kWave;
 constexpr int kPartApplyChunk = 64;
 constexpr int kPartShortN = 5120;
+// Lists of at most kPartTinyN entries take workgroups of 8 waves instead
+// of 16 (poly256 step, 1,536 entries: 12.83 -> 12.65 us, tiny 10.52 ->
+// 10.39 us); from B = 768 (4,608 entries) a heavy partition then needs a
+// second round of chunks (15.8 -> 17.3 us).
+constexpr int kPartTinyN = 2048;
+constexpr int kPartShortThreads = 512;
+__host__ __device__ constexpr int part_apply_threads(int N) {
+  return N <= kPartTinyN ? kPartShortThreads : kPartApplyThreads;
+}
 
 // Segmented apply of one partition of a partitioned sort (NW waves per
 // workgroup), entries [s, e):

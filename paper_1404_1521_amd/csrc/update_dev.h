@@ -153,26 +153,26 @@ __global__ __launch_bounds__(kBlock, 5) void k_apply(ApplyArgs a, KeyFn kf) {
 // Sorted update of a partition-sorted list: workgroup p < n_part applies
 // partition p, whose segments never leave it, so no fix-up launch follows;
 // the remaining workgroups run the dense SGD and clearing roles.  PC:
-// entries per chunk (32 for lists of at most kPartShortN entries, else 64).
-template <int PC>
-__global__ __launch_bounds__(kPartApplyThreads) void k_apply_part(ApplyArgs a) {
-  __shared__ float F[kPartApplyWaves][kMaxD];
-  __shared__ float Lp[kPartApplyWaves][kMaxD];
-  __shared__ int meta[kPartApplyWaves][5];
+// entries per chunk (32 for lists of at most kPartShortN entries, else 64),
+// NTH: threads per workgroup (part_apply_threads).
+template <int PC, int NTH>
+__global__ __launch_bounds__(NTH) void k_apply_part(ApplyArgs a) {
+  constexpr int NW = NTH / kWave;
+  __shared__ float F[NW][kMaxD];
+  __shared__ float Lp[NW][kMaxD];
+  __shared__ int meta[NW][5];
   const int t = threadIdx.x;
   if ((int)blockIdx.x < a.n_part) {
     // (the error words are tested beside each chunk's keys)
     const int p = blockIdx.x;
-    seg_apply_partition<kPartApplyWaves, SegArgs, PC>(a.s, a.part_off[p], a.part_off[p + 1], F, Lp,
-                                                      meta);
+    seg_apply_partition<NW, SegArgs, PC>(a.s, a.part_off[p], a.part_off[p + 1], F, Lp, meta);
     return;
   }
-  const int gid = (blockIdx.x - a.n_part) * kPartApplyThreads + t;
-  const int nthreads = (gridDim.x - a.n_part) * kPartApplyThreads;
+  const int gid = (blockIdx.x - a.n_part) * NTH + t;
+  const int nthreads = (gridDim.x - a.n_part) * NTH;
   const uint32_t pfa = prefetch_lines(a.pf, gid, nthreads);
   const bool bad = void_bits(a.s) != 0u;
-  if (a.n_d > 0)
-    dense_sgd<kPartApplyThreads>(a.dn, blockIdx.x - a.n_part, gridDim.x - a.n_part, bad, &F[0][0]);
+  if (a.n_d > 0) dense_sgd<NTH>(a.dn, blockIdx.x - a.n_part, gridDim.x - a.n_part, bad, &F[0][0]);
   zero_ranges(a.zero, gid, nthreads);
   prefetch_keep(a.pf, pfa);
 }
