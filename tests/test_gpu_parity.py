@@ -522,6 +522,18 @@ def test_sweep_batches(B, steps):
     run_both(w, steps, B, 0)
 
 
+@pytest.mark.parametrize("B", [341, 342, 853, 854, 2730, 2731, 10922, 10923, 21845, 21846])
+def test_update_forms_at_their_limits(B):
+    """Batches on both sides of each switch of the update's form (N = 6B
+    entries): 8- or 16-wave partition workgroups at 2,048 entries, 32- or
+    64-entry partition chunks at 5,120, and the chunked update's 16- or
+    32-entry chunks at 16,384, 65,536 and 131,072 entries."""
+    N = 6 * B
+    assert any(lim - 6 < N <= lim + 6 for lim in (2048, 5120, 16384, 65536, 131072))
+    w = PRESETS["sweep_1024"].with_batch(B)
+    run_both(w, 2, B, 0)
+
+
 @pytest.mark.parametrize("B", [4100, 8215, 8231])
 def test_pipelined_tiles_ragged(B):
     """More than 256 tiles, so workgroups take their tiles in pairs (an even
